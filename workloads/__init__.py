@@ -1,0 +1,248 @@
+"""Seeded synthetic span-query workloads.
+
+This module only *draws inputs*: token ids, the span structure of each query
+(shared prefix, commuting fragments, trailing cross segment) and the per-row
+q/k/v activations that a projection of random hidden states produces.  It holds
+none of the attention method's arithmetic (no masks, positions, RoPE, hashing
+or softmax), so both the HIP path and the oracle can consume it without
+sharing any of the method's code.
+
+Row convention: every span owns a contiguous run of rows in the q/k/v arrays,
+starting at ``Span.row``.  A fragment that several queries draw owns one run
+of rows, shared by all of them (the same content always has the same
+activations, as it would in the first layer of a model).
+
+Randomness: numpy ``Generator(PCG64)`` seeded through ``SeedSequence`` with a
+spawn key ``(kind, index)`` per object, so every object (a fragment's tokens,
+a token's hidden state, a weight matrix, a query's draw) is reproducible on
+its own.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+KIND_PREFIX = 1
+KIND_FRAG = 2
+KIND_CROSS = 3
+KIND_EMBED = 4
+KIND_WEIGHT = 5
+KIND_DRAW = 6
+KIND_DIRECT = 7
+KIND_LEN = 8
+
+VOCAB = 128256
+
+
+def rng(seed: int, kind: int, index: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed, spawn_key=(kind, index))))
+
+
+def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even (storage format only)."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return rounded.astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@dataclass
+class Span:
+    tokens: np.ndarray  # int32
+    row: int            # first row of this span's q/k/v/out rows
+
+    @property
+    def n(self) -> int:
+        return int(self.tokens.shape[0])
+
+
+@dataclass
+class Query:
+    prefix: Span
+    frags: List[Span]
+    cross: Span
+
+
+@dataclass
+class Workload:
+    name: str
+    dtype: str                 # "f32" or "bf16"
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rope_theta: float
+    page_size: int
+    batches: List[List[Query]]  # each batch is one span_plan call
+    q: np.ndarray              # [rows, Hq, d] float32 (exactly representable in dtype)
+    k: np.ndarray              # [rows, Hkv, d]
+    v: np.ndarray              # [rows, Hkv, d]
+    q_bits: Optional[np.ndarray] = None  # bf16 bit patterns when dtype == "bf16"
+    k_bits: Optional[np.ndarray] = None
+    v_bits: Optional[np.ndarray] = None
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def rows(self) -> int:
+        return int(self.q.shape[0])
+
+    def device_arrays(self):
+        """The arrays a GPU caller uploads: bf16 bit patterns or fp32 values."""
+        if self.dtype == "bf16":
+            return self.q_bits, self.k_bits, self.v_bits
+        return self.q, self.k, self.v
+
+
+def _tokens(seed: int, kind: int, index: int, n: int) -> np.ndarray:
+    return rng(seed, kind, index).integers(0, VOCAB, size=n, dtype=np.int64).astype(np.int32)
+
+
+class _RowBook:
+    """Assigns contiguous row runs to distinct spans."""
+
+    def __init__(self):
+        self.next = 0
+        self.token_runs: List[np.ndarray] = []
+
+    def add(self, tokens: np.ndarray) -> Span:
+        s = Span(tokens=tokens, row=self.next)
+        self.next += tokens.shape[0]
+        self.token_runs.append(tokens)
+        return s
+
+    def all_tokens(self) -> np.ndarray:
+        if not self.token_runs:
+            return np.zeros((0,), np.int32)
+        return np.concatenate(self.token_runs)
+
+
+def _project(seed: int, tokens: np.ndarray, hidden: int, hq: int, hkv: int, d: int,
+             x_std: float, w_std: float, mode: str):
+    """Per-row q/k/v (float32) for the given token ids.
+
+    mode "proj": x = E[token] ~ N(0, x_std^2) per distinct token id, weights
+    W_q, W_k, W_v ~ N(0, w_std^2); rows = x @ W.
+    mode "direct": q/k/v drawn directly ~ N(0, 1) per distinct token id.
+    """
+    uniq, inv = np.unique(tokens, return_inverse=True)
+    width = (hq + 2 * hkv) * d
+    out = np.empty((uniq.shape[0], width), np.float32)
+    if mode == "direct":
+        for i, t in enumerate(uniq):
+            out[i] = rng(seed, KIND_DIRECT, int(t)).standard_normal(width, dtype=np.float32)
+    else:
+        w = rng(seed, KIND_WEIGHT, 0).standard_normal((hidden, width), dtype=np.float32) * np.float32(w_std)
+        chunk = 4096
+        for c0 in range(0, uniq.shape[0], chunk):
+            c1 = min(uniq.shape[0], c0 + chunk)
+            x = np.empty((c1 - c0, hidden), np.float32)
+            for i in range(c0, c1):
+                x[i - c0] = rng(seed, KIND_EMBED, int(uniq[i])).standard_normal(hidden, dtype=np.float32)
+            x *= np.float32(x_std)
+            out[c0:c1] = x @ w
+    rows = out[inv]
+    q = rows[:, : hq * d].reshape(-1, hq, d)
+    k = rows[:, hq * d: (hq + hkv) * d].reshape(-1, hkv, d)
+    v = rows[:, (hq + hkv) * d:].reshape(-1, hkv, d)
+    return np.ascontiguousarray(q), np.ascontiguousarray(k), np.ascontiguousarray(v)
+
+
+def _finish(name, dtype, hq, hkv, d, theta, batches, book, seed, hidden, x_std, w_std, mode, meta):
+    q, k, v = _project(seed, book.all_tokens(), hidden, hq, hkv, d, x_std, w_std, mode)
+    wl = Workload(name=name, dtype=dtype, n_q_heads=hq, n_kv_heads=hkv, head_dim=d,
+                  rope_theta=theta, page_size=16, batches=batches, q=q, k=k, v=v, meta=meta)
+    if dtype == "bf16":
+        wl.q_bits, wl.k_bits, wl.v_bits = (round_to_bf16_bits(a) for a in (q, k, v))
+        wl.q, wl.k, wl.v = (bf16_bits_to_f32(b) for b in (wl.q_bits, wl.k_bits, wl.v_bits))
+    return wl
+
+
+def rag_workload(name: str = "rag", *, seed: int = 0, dtype: str = "bf16", n_q_heads: int = 32,
+                 n_kv_heads: int = 8, head_dim: int = 128, hidden: int = 4096,
+                 prefix_len: int = 256, pool_size: int = 64, frag_lens: Sequence[int] | int = 512,
+                 frags_per_query: int = 16, n_queries: int = 8, cross_len: int = 128,
+                 x_std: float = 1.0, w_std: float = 0.02, mode: str = "proj",
+                 rope_theta: float = 1e4, batch_split: Optional[Sequence[int]] = None,
+                 orders: Optional[Sequence[Sequence[int]]] = None) -> Workload:
+    """A shared prefix, a pool of fragments, queries drawing fragments in random order.
+
+    ``orders`` overrides the random draw with explicit fragment orders per query.
+    ``batch_split`` groups queries into successive span_plan calls (default: one batch).
+    """
+    book = _RowBook()
+    prefix = book.add(_tokens(seed, KIND_PREFIX, 0, prefix_len))
+    if isinstance(frag_lens, int):
+        frag_lens = [frag_lens] * pool_size
+    frags = [book.add(_tokens(seed, KIND_FRAG, f, int(frag_lens[f]))) for f in range(pool_size)]
+    queries = []
+    for qi in range(n_queries):
+        if orders is not None:
+            order = [int(x) for x in orders[qi]]
+        else:
+            order = [int(x) for x in rng(seed, KIND_DRAW, qi).choice(pool_size, size=frags_per_query, replace=False)]
+        cross = book.add(_tokens(seed, KIND_CROSS, qi, cross_len))
+        queries.append(Query(prefix=prefix, frags=[frags[f] for f in order], cross=cross))
+    if batch_split is None:
+        batches = [queries]
+    else:
+        batches, at = [], 0
+        for n in batch_split:
+            batches.append(queries[at: at + n])
+            at += n
+    meta = dict(prefix_len=prefix_len, pool_size=pool_size, frags_per_query=frags_per_query,
+                n_queries=n_queries, cross_len=cross_len, hidden=hidden, mode=mode, seed=seed)
+    return _finish(name, dtype, n_q_heads, n_kv_heads, head_dim, rope_theta, batches, book,
+                   seed, hidden, x_std, w_std, mode, meta)
+
+
+def config_c1(seed: int = 0, mode: str = "proj") -> Workload:
+    """fp32 MHA 4x64, hidden 256, prefix 32 + 4 fragments x 64 + cross 16.
+
+    Batch 0: query A, fragments in order (0,1,2,3), cold.  Batch 1: query B,
+    a seeded permutation of the same fragments (every fragment page a hit).
+    Projection: hidden N(0, 0.02^2), weights N(0, 1).  ``mode="direct"``
+    draws q/k/v ~ N(0,1) instead, so the softmax is far from flat.
+    """
+    perm = [int(x) for x in rng(seed, KIND_DRAW, 1000).permutation(4)]
+    if perm == [0, 1, 2, 3]:
+        perm = [3, 2, 1, 0]
+    wl = rag_workload("c1", seed=seed, dtype="f32", n_q_heads=4, n_kv_heads=4, head_dim=64, hidden=256,
+                      prefix_len=32, pool_size=4, frag_lens=64, frags_per_query=4, n_queries=2,
+                      cross_len=16, x_std=0.02, w_std=1.0, mode=mode, orders=[[0, 1, 2, 3], perm],
+                      batch_split=[1, 1])
+    return wl
+
+
+def config_c2(seed: int = 0, n_queries: int = 8, mode: str = "proj") -> Workload:
+    """Llama-3-8B attention layer shape, bf16, GQA 32/8, d 128, hidden 4096.
+
+    Prefix 256 + 16 fragments x 512 drawn from a pool of 64 in random order,
+    cross (question) 128 per query, 8 queries in one batch.
+    """
+    return rag_workload("c2", seed=seed, dtype="bf16", n_q_heads=32, n_kv_heads=8, head_dim=128,
+                        hidden=4096, prefix_len=256, pool_size=64, frag_lens=512, frags_per_query=16,
+                        n_queries=n_queries, cross_len=128, x_std=1.0, w_std=0.02, mode=mode)
+
+
+def config_c3(seed: int = 0, mode: str = "proj") -> Workload:
+    """Judge pattern: 2048-token shared prompt, 32 candidates x 256, judge cross 256."""
+    return rag_workload("c3", seed=seed, dtype="bf16", n_q_heads=32, n_kv_heads=8, head_dim=128,
+                        hidden=4096, prefix_len=2048, pool_size=32, frag_lens=256, frags_per_query=32,
+                        n_queries=1, cross_len=256, x_std=1.0, w_std=0.02, mode=mode,
+                        orders=[list(range(32))])
+
+
+def small_workload(name: str = "small", *, seed: int = 0, dtype: str = "bf16", n_q_heads: int = 8,
+                   n_kv_heads: int = 2, head_dim: int = 128, prefix_len: int = 40,
+                   frag_lens: Sequence[int] = (37, 64, 5, 100), n_queries: int = 3,
+                   frags_per_query: int = 3, cross_len: int = 23, mode: str = "direct",
+                   orders=None, batch_split=None) -> Workload:
+    """Small ragged case for parity: lengths off page boundaries, several tiles."""
+    return rag_workload(name, seed=seed, dtype=dtype, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
+                        head_dim=head_dim, hidden=64, prefix_len=prefix_len, pool_size=len(frag_lens),
+                        frag_lens=list(frag_lens), frags_per_query=frags_per_query, n_queries=n_queries,
+                        cross_len=cross_len, mode=mode, orders=orders, batch_split=batch_split)
