@@ -1,0 +1,258 @@
+/*
+ * spanq.h - span-query prefill attention over a paged KV cache (MI355X, gfx950).
+ *
+ * A span query (Castro et al., "Using Span Queries to Optimize for Cache and
+ * Attention Locality", Def. 2-3) of the RAG / judge form
+ *     G( cross-join( prefix, plus(F_1, ..., F_n), cross ) )
+ * presents a shared prefix, n commuting fragments (the children of the
+ * commutative join, section 4.3) in some order, and a non-commuting cross
+ * segment (question, judge prompt).  This library executes its prefill:
+ *
+ *   span_plan              hash every page of every span, look each span up in
+ *                          the page cache (stop at the first miss), deduplicate
+ *                          fragments across the batch, allocate or evict pages,
+ *                          and build the device work lists (sections 2, 5.4).
+ *   span_prefill_fragments rotate and write the keys/values of every new prefix
+ *                          and fragment token into its page, then run span-prefill
+ *                          attention: a fragment token attends to the whole prefix
+ *                          and causally to its own fragment, at canonical
+ *                          positions (section 5.6; section 5.1 footnote).
+ *   span_cross_attend      write the cross tokens' pages, then run cross
+ *                          attention: a cross token attends to the prefix, to all
+ *                          fragments in this query's order, and causally to the
+ *                          cross segment, with every cached page repositioned to
+ *                          its place in this query (section 5.5).
+ *   kv_lookup              the longest cached run of a chain of page hashes
+ *                          (section 2).
+ *
+ * Conventions
+ * - Every function returns an int status: SPAN_OK (0) or a negative SPAN_E*
+ *   code; none throws or aborts.  span_last_error() gives a thread-local message
+ *   for the most recent failure on the calling thread.
+ * - Tokens are int32.  A page holds 16 tokens (page_size, device pools); every
+ *   span starts on a fresh page and its last page may be partial.
+ * - Activations are row-major arrays in the caller's row numbering:
+ *       q, out: [rows][num_q_heads][head_dim]     k, v: [rows][num_kv_heads][head_dim]
+ *   element type = the pool dtype (SPAN_F32: float, SPAN_BF16: bfloat16 bits).
+ *   Token j of a span lives in row span.row + j.  q and k are BEFORE rotary
+ *   encoding.  Only rows of tokens the plan computes (new prefix/fragment tokens
+ *   and all cross tokens) are read or written.
+ * - Query head h reads kv head floor(h * num_kv_heads / num_q_heads).
+ * - Rotary encoding: rotate-half pairs (i, i + d/2), inverse frequency
+ *   rope_theta^(-2i/d).
+ * - Device work is enqueued asynchronously on the caller's HIP stream (void* =
+ *   hipStream_t; NULL = the null stream).  Caller buffers and the plan must stay
+ *   alive until that work completes.
+ * - A pool is not thread-safe; use one thread per pool.
+ */
+#ifndef SPANQ_H
+#define SPANQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPAN_OK 0
+#define SPAN_EINVAL (-1)  /* bad argument or unsupported shape */
+#define SPAN_ENOMEM (-2)  /* pool exhausted: more pages needed than free or evictable */
+#define SPAN_EHIP (-3)    /* a HIP runtime call failed */
+#define SPAN_ESTATE (-4)  /* call-order violation (e.g. attention after commit) */
+
+#define SPAN_F32 0
+#define SPAN_BF16 1
+
+#define SPAN_HASH_SPAN 0  /* per-span chains: fragments hit in any order (section 5.4) */
+#define SPAN_HASH_STOCK 1 /* one chain over the whole prompt, partial tail page never
+                             cached (section 2); prefix-only queries, host-only pools */
+
+#define SPAN_KERNEL_AUTO 0    /* bf16 MFMA kernel where the shape allows, else generic */
+#define SPAN_KERNEL_GENERIC 1 /* vector-ALU kernel, any supported shape / dtype */
+#define SPAN_KERNEL_MFMA 2    /* bf16 MFMA kernel (SPAN_EINVAL if the shape does not fit) */
+
+typedef struct span_pool span_pool;
+typedef struct span_plan span_plan;
+
+typedef struct {
+  int32_t num_layers;   /* >= 1; each layer has its own page slab */
+  int32_t num_q_heads;  /* multiple of num_kv_heads */
+  int32_t num_kv_heads;
+  int32_t head_dim;     /* 64 or 128 */
+  int32_t page_size;    /* 16 for device pools; any >= 1 for host-only pools */
+  int32_t dtype;        /* SPAN_F32 or SPAN_BF16 */
+  int32_t hash_mode;    /* SPAN_HASH_SPAN or SPAN_HASH_STOCK */
+  int32_t kernel;       /* SPAN_KERNEL_* */
+  int32_t device;       /* HIP device ordinal, or -1 for a host-only pool (no device
+                           memory: planning and lookup only) */
+  int32_t reserved;
+  float rope_theta;
+  int64_t num_pages;    /* pages per layer */
+  void* device_buf;     /* optional caller-owned device buffer of span_pool_bytes();
+                           NULL = the library allocates (and frees) it */
+  size_t device_bytes;
+} span_pool_config;
+
+/* Bytes of device memory a pool with this config needs:
+ *   num_layers * num_pages * 2 * num_kv_heads * page_size * head_dim * elem_size.
+ * Page layout (one layer): K as [kv_head][slot][head_dim], then V as
+ * [kv_head][head_dim][slot] (transposed so the P.V contraction reads it directly). */
+int span_pool_bytes(const span_pool_config* cfg, size_t* bytes);
+
+/* Create a pool.  With device >= 0 the page memory is device memory (allocated
+ * here unless device_buf is given).  *out receives the handle. */
+int span_pool_create(const span_pool_config* cfg, span_pool** out);
+
+/* Destroy a pool and every plan still attached to it.  Frees library-owned memory. */
+int span_pool_destroy(span_pool* pool);
+
+/* Forget every cached page (all pages free, LRU clock unchanged).  SPAN_ESTATE if
+ * a plan is alive. */
+int span_pool_reset(span_pool* pool);
+
+typedef struct {
+  int64_t num_pages;
+  int64_t free_pages;
+  int64_t cached_pages;    /* published pages */
+  int64_t pinned_pages;    /* pages held by live plans */
+  int64_t tick;            /* LRU clock: number of successful span_plan calls */
+  int64_t total_evictions;
+} span_pool_info;
+int span_pool_get_info(const span_pool* pool, span_pool_info* info);
+
+/* Base device address of the page memory and the element offset of (layer, page):
+ * K of kv head h, slot s, dim i at base + off + (h*page_size + s)*head_dim + i;
+ * V at base + off + num_kv_heads*page_size*head_dim + (h*head_dim + i)*page_size + s. */
+int span_pool_page_address(const span_pool* pool, int32_t layer, int32_t page_id,
+                           void** base, int64_t* elem_offset);
+
+/* ---------------------------------------------------------------- hashing */
+
+/* Chain seeds of the page hash (section 5.4: a fragment's chain starts from the
+ * prefix, never from its left siblings).
+ *   prefix chain seed      = SPAN_HASH_ROOT
+ *   fragment chain seed    = mix(last prefix page hash, or SPAN_HASH_ROOT if the
+ *                                prefix is empty, XOR SPAN_HASH_FRAG_TAG)
+ * mix = SplitMix64 (Steele, Lea, Flood 2014): x + 0x9E3779B97F4A7C15, then
+ * xor-shift 30 / multiply 0xBF58476D1CE4E5B9 / xor-shift 27 / multiply
+ * 0x94D049BB133111EB / xor-shift 31.
+ * Page i of a chain: h = previous page's hash (or the seed); h = mix(h ^ t) for
+ * each token t (as uint32); page hash = mix(h ^ (n << 32) ^ i), n = tokens in page. */
+#define SPAN_HASH_ROOT 0x243F6A8885A308D3ull
+#define SPAN_HASH_FRAG_TAG 0x13198A2E03707344ull
+uint64_t span_hash_mix(uint64_t x);
+
+/* Hashes of the pages of one chain.  out must hold ceil(n / page_size) values;
+ * with include_partial == 0 a trailing partial page is not hashed.  *n_pages
+ * receives the number written. */
+int span_hash_pages(uint64_t seed, const int32_t* tokens, int32_t n, int32_t page_size,
+                    int32_t include_partial, uint64_t* out, int32_t* n_pages);
+
+/* Section 2 lookup: page_ids[i] = cached page holding hash i or -1; *n_leading_hits
+ * = number of leading hits (lookup stops at the first miss).  Pure: no LRU touch,
+ * no content check (span_plan also compares the stored tokens). */
+int kv_lookup(const span_pool* pool, const uint64_t* hashes, int32_t n, int32_t* page_ids,
+              int32_t* n_leading_hits);
+
+/* ---------------------------------------------------------------- planning */
+
+typedef struct {
+  const int32_t* tokens;  /* host memory, n tokens */
+  int32_t n;              /* >= 0 */
+  int32_t reserved;
+  int64_t row;            /* caller row of token 0 in q/k/v/out */
+} span_tokens;
+
+typedef struct {
+  span_tokens prefix;       /* shared prefix (may be empty) */
+  const span_tokens* frags; /* n_frags commuting children, in this query's order */
+  int32_t n_frags;
+  int32_t reserved;
+  span_tokens cross;        /* trailing non-commuting segment (may be empty) */
+} span_query;
+
+/* Plan a batch of queries (sections 2 and 5.4).  Pages of the prefix and of each
+ * fragment are hashed per span and looked up, stopping at each span's first miss;
+ * a span already scheduled earlier in the batch is a hit for later ones.  Missing
+ * pages and the cross pages are allocated (lowest free id first; with no free page
+ * the least recently used unpinned cached page is evicted, a span's tail pages
+ * first).  All pages the plan uses are pinned until commit (cache pages) or destroy
+ * (cross pages).  The device work lists are copied once, on `stream`.
+ * SPAN_ENOMEM (pool unchanged) if the batch needs more pages than are free or
+ * evictable.  Host-only pools plan but cannot run attention. */
+int span_plan_create(span_pool* pool, const span_query* queries, int32_t n_queries, void* stream,
+                     span_plan** out);
+
+typedef struct {
+  int64_t pages_hit;        /* prefix/fragment pages served from cache (incl. batch dedup) */
+  int64_t pages_new;        /* prefix/fragment pages to compute */
+  int64_t pages_cross;      /* transient cross pages */
+  int64_t pages_evicted;
+  int64_t tokens_hit;
+  int64_t tokens_new;       /* prefix/fragment tokens to compute */
+  int64_t tokens_cross;
+  int64_t prefill_pairs;    /* (query, key) pairs the span mask allows, prefill rows */
+  int64_t cross_pairs;      /* same, cross rows */
+  int64_t prefill_tiles;
+  int64_t cross_tiles;      /* work items including KV splits */
+  int64_t kv_splits;        /* KV splits per cross row tile */
+  int64_t cross_kv_pages;   /* page reads of the cross pass per kv head */
+} span_stats;
+int span_plan_stats(const span_plan* plan, span_stats* stats);
+
+/* Block table of one span: span = -1 prefix, 0..n_frags-1 fragment children,
+ * n_frags cross.  Writes up to cap page ids; *n = pages of the span, *n_hit =
+ * leading pages that were hits. */
+int span_plan_block_table(const span_plan* plan, int32_t query, int32_t span, int32_t* page_ids,
+                          int32_t cap, int32_t* n, int32_t* n_hit);
+
+/* Page ids evicted by this plan, in eviction order. */
+int span_plan_evicted(const span_plan* plan, int32_t* page_ids, int32_t cap, int32_t* n);
+
+/* Caller rows the plan reads (q, k, v) and writes (out): the new prefix/fragment
+ * token rows (prefill) then the cross rows, in work order. */
+int span_plan_rows(const span_plan* plan, int64_t* rows, int64_t cap, int64_t* n_prefill,
+                   int64_t* n_cross);
+
+/* ---------------------------------------------------------------- attention */
+
+/* Prefill of the new prefix and fragment tokens for one layer (sections 5.1, 5.6):
+ * rotate each new key at its canonical position (prefix token t at t, fragment
+ * token j at P + j), write keys and values into their pages, then write out[row] =
+ * softmax over the span mask of q.k / sqrt(d) times V, with the query also at its
+ * canonical position.  No-op when every page hit. */
+int span_prefill_fragments(span_plan* plan, int32_t layer, const void* q, const void* k,
+                           const void* v, void* out, void* stream);
+
+/* Cross attention for one layer (sections 5.5, 5.6): write the cross tokens' keys
+ * and values into the plan's transient pages, then for every cross row attend to the
+ * prefix, to every fragment in this query's order and causally to the cross segment,
+ * all at final positions (index in prefix | F_s1 | ... | F_sn | cross).  Cached
+ * fragment keys are rotated by (final - canonical) position as they are read; pages
+ * are never rewritten.  Must follow span_prefill_fragments for the same layer. */
+int span_cross_attend(span_plan* plan, int32_t layer, const void* q, const void* k, const void* v,
+                      void* out, void* stream);
+
+/* Publish the plan's new prefix/fragment pages in the cache index, unpin its pages
+ * and free its cross pages.  Call after the last layer's kernels are enqueued; pages
+ * released here may be reused by the next plan's kernels, so a next plan on another
+ * stream must be ordered after this plan's work by the caller. */
+int span_plan_commit(span_plan* plan);
+
+/* Free the plan.  Without a prior commit its new pages are freed unpublished and its
+ * hits unpinned.  Device metadata is released on the plan's stream. */
+int span_plan_destroy(span_plan* plan);
+
+/* ---------------------------------------------------------------- debug */
+
+const char* span_last_error(void);
+
+/* Copy one page (K then V, page layout above) of one layer to host memory; synchronous. */
+int span_pool_read_page(const span_pool* pool, int32_t layer, int32_t page_id, void* host_dst,
+                        size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPANQ_H */

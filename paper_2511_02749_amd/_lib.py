@@ -1,0 +1,300 @@
+"""ctypes binding of libspanq.so.  Argument marshalling only."""
+from __future__ import annotations
+
+import ctypes
+import os
+import weakref
+from typing import Iterable, List, Optional, Sequence
+
+import numpy as np
+
+try:  # bind to torch's HIP runtime when torch is present (one runtime per process)
+    import torch  # noqa: F401
+except ImportError:  # pragma: no cover
+    torch = None
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+SPAN_OK, SPAN_EINVAL, SPAN_ENOMEM, SPAN_EHIP, SPAN_ESTATE = 0, -1, -2, -3, -4
+SPAN_F32, SPAN_BF16 = 0, 1
+SPAN_HASH_SPAN, SPAN_HASH_STOCK = 0, 1
+SPAN_KERNEL = {"auto": 0, "generic": 1, "mfma": 2}
+SPAN_HASH_ROOT = 0x243F6A8885A308D3
+SPAN_HASH_FRAG_TAG = 0x13198A2E03707344
+
+EXPORTS = [
+    "span_last_error", "span_hash_mix", "span_pool_bytes", "span_pool_create", "span_pool_destroy",
+    "span_pool_reset", "span_pool_get_info", "span_pool_page_address", "span_pool_read_page",
+    "span_hash_pages", "kv_lookup", "span_plan_create", "span_plan_stats", "span_plan_block_table",
+    "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
+    "span_plan_commit", "span_plan_destroy",
+]
+
+
+class SpanError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class PoolConfig(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("hash_mode", ctypes.c_int32), ("kernel", ctypes.c_int32), ("device", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("num_pages", ctypes.c_int64),
+                ("device_buf", ctypes.c_void_p), ("device_bytes", ctypes.c_size_t)]
+
+
+class PoolInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in
+                ("num_pages", "free_pages", "cached_pages", "pinned_pages", "tick", "total_evictions")]
+
+
+class SpanTokens(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.POINTER(ctypes.c_int32)), ("n", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("row", ctypes.c_int64)]
+
+
+class SpanQuery(ctypes.Structure):
+    _fields_ = [("prefix", SpanTokens), ("frags", ctypes.POINTER(SpanTokens)), ("n_frags", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("cross", SpanTokens)]
+
+
+STAT_FIELDS = ("pages_hit", "pages_new", "pages_cross", "pages_evicted", "tokens_hit", "tokens_new", "tokens_cross",
+               "prefill_pairs", "cross_pairs", "prefill_tiles", "cross_tiles", "kv_splits", "cross_kv_pages")
+
+
+class SpanStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS]
+
+
+_LIB = None
+
+
+def library_path() -> str:
+    return os.environ.get("SPANQ_LIB", os.path.join(HERE, "libspanq.so"))
+
+
+def load():
+    """Load libspanq.so (built by ``paper_2511_02749_amd/build.py``); raise if missing."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} not built: run python -m paper_2511_02749_amd.build")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, U64, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p
+    sig = {
+        "span_last_error": (ctypes.c_char_p, []),
+        "span_hash_mix": (U64, [U64]),
+        "span_pool_bytes": (I32, [P(PoolConfig), P(ctypes.c_size_t)]),
+        "span_pool_create": (I32, [P(PoolConfig), P(VP)]),
+        "span_pool_destroy": (I32, [VP]),
+        "span_pool_reset": (I32, [VP]),
+        "span_pool_get_info": (I32, [VP, P(PoolInfo)]),
+        "span_pool_page_address": (I32, [VP, I32, I32, P(VP), P(I64)]),
+        "span_pool_read_page": (I32, [VP, I32, I32, VP, ctypes.c_size_t]),
+        "span_hash_pages": (I32, [U64, P(I32), I32, I32, I32, P(U64), P(I32)]),
+        "kv_lookup": (I32, [VP, P(U64), I32, P(I32), P(I32)]),
+        "span_plan_create": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
+        "span_plan_stats": (I32, [VP, P(SpanStats)]),
+        "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
+        "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
+        "span_plan_rows": (I32, [VP, P(I64), I64, P(I64), P(I64)]),
+        "span_prefill_fragments": (I32, [VP, I32, VP, VP, VP, VP, VP]),
+        "span_cross_attend": (I32, [VP, I32, VP, VP, VP, VP, VP]),
+        "span_plan_commit": (I32, [VP]),
+        "span_plan_destroy": (I32, [VP]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    _LIB = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != SPAN_OK:
+        raise SpanError(rc, load().span_last_error().decode())
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _ptr(x) -> Optional[int]:
+    """Device pointer of a torch tensor (or an int address); None stays None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        if torch is not None and torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def hash_mix(x: int) -> int:
+    return int(load().span_hash_mix(x))
+
+
+def hash_pages(seed: int, tokens: Sequence[int], page_size: int = 16, include_partial: bool = True) -> List[int]:
+    lib = load()
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    out = np.zeros(max(1, (t.size + page_size - 1) // page_size), np.uint64)
+    n = ctypes.c_int32()
+    _check(lib.span_hash_pages(seed, _i32p(t), t.size, page_size, int(include_partial),
+                               out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), ctypes.byref(n)))
+    return [int(x) for x in out[: n.value]]
+
+
+class Pool:
+    """A paged KV pool and its cache index.  device=-1 gives a host-only pool."""
+
+    def __init__(self, *, num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str = "bf16",
+                 num_layers: int = 1, rope_theta: float = 1e4, page_size: int = 16, device: int = 0,
+                 hash_mode: str = "span", kernel: str = "auto"):
+        lib = load()
+        self.cfg = PoolConfig(num_layers=num_layers, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                              head_dim=head_dim, page_size=page_size,
+                              dtype=SPAN_BF16 if dtype == "bf16" else SPAN_F32,
+                              hash_mode=SPAN_HASH_STOCK if hash_mode == "stock" else SPAN_HASH_SPAN,
+                              kernel=SPAN_KERNEL[kernel], device=device, reserved=0, rope_theta=rope_theta,
+                              num_pages=num_pages, device_buf=None, device_bytes=0)
+        self.dtype = dtype
+        self._plans = weakref.WeakSet()
+        self._h = ctypes.c_void_p()
+        _check(lib.span_pool_create(ctypes.byref(self.cfg), ctypes.byref(self._h)))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def page_bytes(self) -> int:
+        es = 2 if self.dtype == "bf16" else 4
+        return 2 * self.cfg.num_kv_heads * self.cfg.page_size * self.cfg.head_dim * es
+
+    def close(self):
+        if self._h:
+            for p in list(self._plans):
+                p.destroy()
+            _check(load().span_pool_destroy(self._h))
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reset(self):
+        _check(load().span_pool_reset(self._h))
+
+    def info(self) -> dict:
+        i = PoolInfo()
+        _check(load().span_pool_get_info(self._h, ctypes.byref(i)))
+        return {n: int(getattr(i, n)) for n, _ in PoolInfo._fields_}
+
+    def lookup(self, hashes: Sequence[int]):
+        h = np.ascontiguousarray(hashes, dtype=np.uint64)
+        ids = np.zeros(max(1, h.size), np.int32)
+        lead = ctypes.c_int32()
+        _check(load().kv_lookup(self._h, h.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), h.size, _i32p(ids),
+                                ctypes.byref(lead)))
+        return [int(x) for x in ids[: h.size]], lead.value
+
+    def read_page(self, layer: int, page_id: int) -> np.ndarray:
+        """Raw page (K then V) as uint16 (bf16 bits) or float32 values."""
+        buf = np.zeros(self.page_bytes() // (2 if self.dtype == "bf16" else 4),
+                       np.uint16 if self.dtype == "bf16" else np.float32)
+        _check(load().span_pool_read_page(self._h, layer, page_id, buf.ctypes.data, buf.nbytes))
+        return buf
+
+    def plan(self, queries: Iterable, stream=None) -> "Plan":
+        """queries: objects with .prefix, .frags, .cross; each span has .tokens (int32) and .row."""
+        return Plan(self, list(queries), stream)
+
+
+def _span(s, keep: list) -> SpanTokens:
+    t = np.ascontiguousarray(s.tokens, dtype=np.int32)
+    keep.append(t)
+    return SpanTokens(tokens=_i32p(t), n=t.size, reserved=0, row=int(s.row))
+
+
+class Plan:
+    def __init__(self, pool: Pool, queries: list, stream=None):
+        lib = load()
+        self.pool = pool
+        keep: list = []
+        arr = (SpanQuery * max(1, len(queries)))()
+        for i, q in enumerate(queries):
+            fr = (SpanTokens * max(1, len(q.frags)))(*[_span(f, keep) for f in q.frags])
+            keep.append(fr)
+            arr[i] = SpanQuery(prefix=_span(q.prefix, keep), frags=fr, n_frags=len(q.frags), reserved=0,
+                               cross=_span(q.cross, keep))
+        self.n_queries = len(queries)
+        self.n_frags = [len(q.frags) for q in queries]
+        self._h = ctypes.c_void_p()
+        self._stream = _stream(stream)
+        _check(lib.span_plan_create(pool.handle, arr, len(queries), self._stream, ctypes.byref(self._h)))
+        pool._plans.add(self)
+
+    def stats(self) -> dict:
+        s = SpanStats()
+        _check(load().span_plan_stats(self._h, ctypes.byref(s)))
+        return {n: int(getattr(s, n)) for n in STAT_FIELDS}
+
+    def block_table(self, query: int, span: int):
+        """span: -1 prefix, 0..n-1 fragment children, n cross.  Returns (page ids, n_hit)."""
+        n, nh = ctypes.c_int32(), ctypes.c_int32()
+        _check(load().span_plan_block_table(self._h, query, span, None, 0, ctypes.byref(n), ctypes.byref(nh)))
+        ids = np.zeros(max(1, n.value), np.int32)
+        _check(load().span_plan_block_table(self._h, query, span, _i32p(ids), n.value, ctypes.byref(n),
+                                            ctypes.byref(nh)))
+        return [int(x) for x in ids[: n.value]], nh.value
+
+    def evicted(self) -> List[int]:
+        n = ctypes.c_int32()
+        _check(load().span_plan_evicted(self._h, None, 0, ctypes.byref(n)))
+        ids = np.zeros(max(1, n.value), np.int32)
+        _check(load().span_plan_evicted(self._h, _i32p(ids), n.value, ctypes.byref(n)))
+        return [int(x) for x in ids[: n.value]]
+
+    def rows(self):
+        """(prefill rows, cross rows) the plan computes."""
+        npf, ncr = ctypes.c_int64(), ctypes.c_int64()
+        _check(load().span_plan_rows(self._h, None, 0, ctypes.byref(npf), ctypes.byref(ncr)))
+        buf = np.zeros(max(1, npf.value + ncr.value), np.int64)
+        _check(load().span_plan_rows(self._h, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), buf.size,
+                                     ctypes.byref(npf), ctypes.byref(ncr)))
+        return buf[: npf.value].copy(), buf[npf.value: npf.value + ncr.value].copy()
+
+    def prefill(self, layer: int, q, k, v, out, stream=None):
+        _check(load().span_prefill_fragments(self._h, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                             _stream(stream) if stream is not None else self._stream))
+
+    def cross(self, layer: int, q, k, v, out, stream=None):
+        _check(load().span_cross_attend(self._h, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                        _stream(stream) if stream is not None else self._stream))
+
+    def commit(self):
+        _check(load().span_plan_commit(self._h))
+
+    def destroy(self):
+        if self._h:
+            _check(load().span_plan_destroy(self._h))
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass

@@ -1,0 +1,447 @@
+// C-ABI of the span-query prefill library: pools, plans, attention entry points.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/spanq.h"
+#include "kernels.h"
+#include "planner.h"
+
+using namespace spanq;
+
+namespace {
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SPAN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t elem_size(int32_t dtype) { return dtype == SPAN_BF16 ? 2 : 4; }
+
+}  // namespace
+
+struct span_pool {
+  span_pool_config cfg{};
+  PoolIndex* index = nullptr;
+  void* dev = nullptr;
+  bool owns_dev = false;
+  bool use_mfma = false;
+  std::set<span_plan*> plans;
+};
+
+struct span_plan {
+  span_pool* pool = nullptr;
+  Plan plan;
+  hipStream_t stream = nullptr;
+  std::vector<unsigned char> host_meta;
+  unsigned char* dev_meta = nullptr;
+  float* part = nullptr;  // partial O then partial (m, l)
+  size_t part_o_elems = 0;
+  // device views
+  const KvPage* kv = nullptr;
+  const NewPage* k3p = nullptr;
+  const NewPage* k3c = nullptr;
+  const WorkTile* tp = nullptr;
+  const WorkTile* tc = nullptr;
+  const CombineTile* cb = nullptr;
+  const double* inv_freq = nullptr;
+  int bm = kGenericBM;
+  bool mfma = false;
+  bool committed = false;
+};
+
+static int check_span(const span_tokens& s, const char* what) {
+  if (s.n < 0 || (s.n > 0 && !s.tokens)) return fail(SPAN_EINVAL, std::string("span_plan_create: bad ") + what);
+  if (s.n > 0 && (s.row < 0 || s.row + s.n > std::numeric_limits<int32_t>::max()))
+    return fail(SPAN_EINVAL, std::string("span_plan_create: ") + what + " rows must lie in [0, 2^31)");
+  return SPAN_OK;
+}
+
+template <typename T>
+static size_t put(std::vector<unsigned char>& buf, const std::vector<T>& v) {
+  size_t at = (buf.size() + 255) & ~static_cast<size_t>(255);
+  buf.resize(at + v.size() * sizeof(T));
+  if (!v.empty()) std::memcpy(buf.data() + at, v.data(), v.size() * sizeof(T));
+  return at;
+}
+
+extern "C" {
+
+const char* span_last_error(void) { return g_last_error.c_str(); }
+
+uint64_t span_hash_mix(uint64_t x) { return mix64(x); }
+
+int span_pool_bytes(const span_pool_config* c, size_t* bytes) {
+  if (!c || !bytes) return fail(SPAN_EINVAL, "span_pool_bytes: null argument");
+  if (c->num_layers < 1 || c->num_pages < 1 || c->num_kv_heads < 1 || c->head_dim < 1 || c->page_size < 1)
+    return fail(SPAN_EINVAL, "span_pool_bytes: sizes must be positive");
+  *bytes = static_cast<size_t>(c->num_layers) * static_cast<size_t>(c->num_pages) * 2 *
+           static_cast<size_t>(c->num_kv_heads) * static_cast<size_t>(c->page_size) *
+           static_cast<size_t>(c->head_dim) * elem_size(c->dtype);
+  return SPAN_OK;
+}
+
+int span_pool_create(const span_pool_config* c, span_pool** out) {
+  if (!c || !out) return fail(SPAN_EINVAL, "span_pool_create: null argument");
+  *out = nullptr;
+  if (c->dtype != SPAN_F32 && c->dtype != SPAN_BF16) return fail(SPAN_EINVAL, "span_pool_create: dtype");
+  if (c->num_layers < 1 || c->num_pages < 1 || c->num_pages > std::numeric_limits<int32_t>::max())
+    return fail(SPAN_EINVAL, "span_pool_create: num_layers >= 1 and 1 <= num_pages < 2^31 required");
+  if (c->num_q_heads < 1 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads != 0)
+    return fail(SPAN_EINVAL, "span_pool_create: num_q_heads must be a positive multiple of num_kv_heads");
+  if (c->hash_mode != SPAN_HASH_SPAN && c->hash_mode != SPAN_HASH_STOCK)
+    return fail(SPAN_EINVAL, "span_pool_create: hash_mode");
+  if (c->page_size < 1) return fail(SPAN_EINVAL, "span_pool_create: page_size");
+  if (c->device >= 0) {
+    if (c->page_size != kPage) return fail(SPAN_EINVAL, "span_pool_create: device pools use 16-token pages");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(SPAN_EINVAL, "span_pool_create: head_dim 64 or 128");
+    if (c->hash_mode != SPAN_HASH_SPAN) return fail(SPAN_EINVAL, "span_pool_create: stock hashing is host-only");
+    if (!(c->rope_theta > 0.f)) return fail(SPAN_EINVAL, "span_pool_create: rope_theta must be positive");
+    if (c->kernel == SPAN_KERNEL_MFMA && !mfma_supported(c->num_q_heads, c->num_kv_heads, c->head_dim, c->dtype))
+      return fail(SPAN_EINVAL, "span_pool_create: the MFMA kernel does not support this dtype/shape");
+  }
+  if (c->kernel < SPAN_KERNEL_AUTO || c->kernel > SPAN_KERNEL_MFMA) return fail(SPAN_EINVAL, "span_pool_create: kernel");
+  span_pool* p = new (std::nothrow) span_pool();
+  if (!p) return fail(SPAN_ENOMEM, "span_pool_create: host allocation");
+  p->cfg = *c;
+  if (c->device >= 0) {
+    size_t need = 0;
+    span_pool_bytes(c, &need);
+    hipError_t e = hipSetDevice(c->device);
+    if (e != hipSuccess) {
+      delete p;
+      return hip_fail(e, "span_pool_create: hipSetDevice");
+    }
+    if (c->device_buf) {
+      if (c->device_bytes < need) {
+        delete p;
+        return fail(SPAN_EINVAL, "span_pool_create: device_buf smaller than span_pool_bytes()");
+      }
+      p->dev = c->device_buf;
+    } else {
+      e = hipMalloc(&p->dev, need);
+      if (e != hipSuccess) {
+        delete p;
+        return hip_fail(e, "span_pool_create: hipMalloc of page memory");
+      }
+      p->owns_dev = true;
+    }
+    p->use_mfma = c->kernel == SPAN_KERNEL_MFMA ||
+                  (c->kernel == SPAN_KERNEL_AUTO && mfma_supported(c->num_q_heads, c->num_kv_heads, c->head_dim, c->dtype));
+  }
+  p->index = new (std::nothrow) PoolIndex(c->num_pages, c->page_size, c->hash_mode);
+  if (!p->index) {
+    if (p->owns_dev) (void)hipFree(p->dev);
+    delete p;
+    return fail(SPAN_ENOMEM, "span_pool_create: host allocation");
+  }
+  *out = p;
+  return SPAN_OK;
+}
+
+int span_plan_destroy(span_plan* plan);
+
+int span_pool_destroy(span_pool* p) {
+  if (!p) return fail(SPAN_EINVAL, "span_pool_destroy: null pool");
+  std::vector<span_plan*> live(p->plans.begin(), p->plans.end());
+  for (span_plan* pl : live) span_plan_destroy(pl);
+  if (p->owns_dev && p->dev) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(p->dev);
+  }
+  delete p->index;
+  delete p;
+  return SPAN_OK;
+}
+
+int span_pool_reset(span_pool* p) {
+  if (!p) return fail(SPAN_EINVAL, "span_pool_reset: null pool");
+  if (!p->plans.empty()) return fail(SPAN_ESTATE, "span_pool_reset: plans are alive");
+  p->index->reset();
+  return SPAN_OK;
+}
+
+int span_pool_get_info(const span_pool* p, span_pool_info* info) {
+  if (!p || !info) return fail(SPAN_EINVAL, "span_pool_get_info: null argument");
+  info->num_pages = p->index->num_pages();
+  info->free_pages = p->index->free_count();
+  info->cached_pages = p->index->cached_count();
+  info->pinned_pages = p->index->pinned_count();
+  info->tick = p->index->tick();
+  info->total_evictions = p->index->total_evictions();
+  return SPAN_OK;
+}
+
+int span_pool_page_address(const span_pool* p, int32_t layer, int32_t page_id, void** base, int64_t* off) {
+  if (!p || !base || !off) return fail(SPAN_EINVAL, "span_pool_page_address: null argument");
+  if (p->cfg.device < 0) return fail(SPAN_ESTATE, "span_pool_page_address: host-only pool");
+  if (layer < 0 || layer >= p->cfg.num_layers || page_id < 0 || page_id >= p->cfg.num_pages)
+    return fail(SPAN_EINVAL, "span_pool_page_address: layer or page out of range");
+  const int64_t page_elems = 2ll * p->cfg.num_kv_heads * p->cfg.page_size * p->cfg.head_dim;
+  *base = p->dev;
+  *off = (static_cast<int64_t>(layer) * p->cfg.num_pages + page_id) * page_elems;
+  return SPAN_OK;
+}
+
+int span_pool_read_page(const span_pool* p, int32_t layer, int32_t page_id, void* host_dst, size_t bytes) {
+  void* base = nullptr;
+  int64_t off = 0;
+  int rc = span_pool_page_address(p, layer, page_id, &base, &off);
+  if (rc) return rc;
+  const size_t es = elem_size(p->cfg.dtype);
+  const size_t page_bytes = 2ull * p->cfg.num_kv_heads * p->cfg.page_size * p->cfg.head_dim * es;
+  if (!host_dst || bytes < page_bytes) return fail(SPAN_EINVAL, "span_pool_read_page: destination too small");
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "span_pool_read_page: hipDeviceSynchronize");
+  e = hipMemcpy(host_dst, static_cast<unsigned char*>(base) + off * es, page_bytes, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "span_pool_read_page: hipMemcpy");
+  return SPAN_OK;
+}
+
+int span_hash_pages(uint64_t seed, const int32_t* tok, int32_t n, int32_t page_size, int32_t include_partial,
+                    uint64_t* out, int32_t* n_pages) {
+  if ((!tok && n > 0) || n < 0 || page_size < 1 || !n_pages || (!out && n > 0))
+    return fail(SPAN_EINVAL, "span_hash_pages: bad argument");
+  uint64_t h = seed;
+  int32_t w = 0;
+  for (int32_t p = 0; p * page_size < n; ++p) {
+    int32_t cnt = std::min(page_size, n - p * page_size);
+    if (cnt < page_size && !include_partial) break;
+    h = page_hash(h, tok + static_cast<int64_t>(p) * page_size, cnt, p);
+    out[w++] = h;
+  }
+  *n_pages = w;
+  return SPAN_OK;
+}
+
+int kv_lookup(const span_pool* p, const uint64_t* hashes, int32_t n, int32_t* page_ids, int32_t* n_leading) {
+  if (!p || n < 0 || (n > 0 && (!hashes || !page_ids)) || !n_leading)
+    return fail(SPAN_EINVAL, "kv_lookup: bad argument");
+  int32_t lead = 0;
+  bool run = true;
+  for (int32_t i = 0; i < n; ++i) {
+    page_ids[i] = static_cast<int32_t>(p->index->lookup(hashes[i]));
+    if (run && page_ids[i] >= 0) {
+      ++lead;
+    } else {
+      run = false;
+    }
+  }
+  *n_leading = lead;
+  return SPAN_OK;
+}
+
+int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan** out) {
+  if (!pool || !out || nq < 0 || (nq > 0 && !qs)) return fail(SPAN_EINVAL, "span_plan_create: bad argument");
+  *out = nullptr;
+  std::vector<QueryIn> in(static_cast<size_t>(nq));
+  for (int32_t i = 0; i < nq; ++i) {
+    const span_query& q = qs[i];
+    int rc = check_span(q.prefix, "prefix");
+    if (!rc) rc = check_span(q.cross, "cross");
+    if (rc) return rc;
+    if (q.n_frags < 0 || (q.n_frags > 0 && !q.frags)) return fail(SPAN_EINVAL, "span_plan_create: bad fragment list");
+    if (pool->cfg.hash_mode == SPAN_HASH_STOCK && (q.n_frags != 0 || q.cross.n != 0))
+      return fail(SPAN_EINVAL, "span_plan_create: stock hashing takes prefix-only queries");
+    in[i].prefix = SpanIn{q.prefix.tokens, q.prefix.n, q.prefix.row};
+    in[i].cross = SpanIn{q.cross.tokens, q.cross.n, q.cross.row};
+    for (int32_t f = 0; f < q.n_frags; ++f) {
+      rc = check_span(q.frags[f], "fragment");
+      if (rc) return rc;
+      in[i].frags.push_back(SpanIn{q.frags[f].tokens, q.frags[f].n, q.frags[f].row});
+    }
+  }
+  span_plan* pl = new (std::nothrow) span_plan();
+  if (!pl) return fail(SPAN_ENOMEM, "span_plan_create: host allocation");
+  pl->pool = pool;
+  pl->stream = static_cast<hipStream_t>(stream);
+  const bool device = pool->cfg.device >= 0;
+  pl->mfma = device && pool->use_mfma;
+  pl->bm = pl->mfma ? kMfmaBM : kGenericBM;
+  Tiling t;
+  t.bm_prefill = pl->bm;
+  t.bm_cross = pl->bm;
+  t.kv_heads = pl->mfma ? pool->cfg.num_kv_heads : pool->cfg.num_q_heads;
+  std::string msg;
+  int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
+  if (rc) {
+    delete pl;
+    return fail(rc, msg);
+  }
+  pool->plans.insert(pl);
+  if (device) {
+    Plan& P = pl->plan;
+    const int d = pool->cfg.head_dim;
+    std::vector<double> inv(static_cast<size_t>(d / 2));
+    for (int i = 0; i < d / 2; ++i)
+      inv[i] = std::pow(static_cast<double>(pool->cfg.rope_theta), -2.0 * i / d);
+    auto& hb = pl->host_meta;
+    size_t o_kv = put(hb, P.kv), o_k3p = put(hb, P.k3_prefill), o_k3c = put(hb, P.k3_cross);
+    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine), o_inv = put(hb, inv);
+    hipError_t e = hipSetDevice(pool->cfg.device);
+    if (e == hipSuccess) e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
+    if (e == hipSuccess && P.n_parts > 0) {
+      pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
+      size_t ml = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2;
+      e = hipMallocAsync(reinterpret_cast<void**>(&pl->part), (pl->part_o_elems + ml) * sizeof(float), pl->stream);
+    }
+    if (e != hipSuccess) {
+      span_plan_destroy(pl);
+      return hip_fail(e, "span_plan_create: device metadata");
+    }
+    pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
+    pl->k3p = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3p);
+    pl->k3c = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3c);
+    pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
+    pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
+    pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
+    pl->inv_freq = reinterpret_cast<const double*>(pl->dev_meta + o_inv);
+  }
+  *out = pl;
+  return SPAN_OK;
+}
+
+int span_plan_stats(const span_plan* pl, span_stats* s) {
+  if (!pl || !s) return fail(SPAN_EINVAL, "span_plan_stats: null argument");
+  const Plan& P = pl->plan;
+  s->pages_hit = P.pages_hit;
+  s->pages_new = P.pages_new;
+  s->pages_cross = static_cast<int64_t>(P.cross_pages.size());
+  s->pages_evicted = static_cast<int64_t>(P.evicted.size());
+  s->tokens_hit = P.tokens_hit;
+  s->tokens_new = P.tokens_new;
+  s->tokens_cross = P.tokens_cross;
+  s->prefill_pairs = P.prefill_pairs;
+  s->cross_pairs = P.cross_pairs;
+  s->prefill_tiles = static_cast<int64_t>(P.t_prefill.size());
+  s->cross_tiles = static_cast<int64_t>(P.t_cross.size());
+  s->kv_splits = P.kv_splits;
+  s->cross_kv_pages = P.cross_kv_pages;
+  return SPAN_OK;
+}
+
+int span_plan_block_table(const span_plan* pl, int32_t query, int32_t span, int32_t* ids, int32_t cap, int32_t* n,
+                          int32_t* n_hit) {
+  if (!pl || !n || !n_hit || cap < 0 || (cap > 0 && !ids)) return fail(SPAN_EINVAL, "span_plan_block_table: bad argument");
+  const Plan& P = pl->plan;
+  if (query < 0 || query >= static_cast<int32_t>(P.query_spans.size()))
+    return fail(SPAN_EINVAL, "span_plan_block_table: query out of range");
+  const auto& sp = P.query_spans[query];
+  const int32_t nfr = static_cast<int32_t>(sp.size()) - 2;
+  if (span < -1 || span > nfr) return fail(SPAN_EINVAL, "span_plan_block_table: span out of range");
+  const SpanPlan& s = P.spans[sp[span + 1]];
+  *n = static_cast<int32_t>(s.pages.size());
+  *n_hit = s.n_hit;
+  for (int32_t i = 0; i < std::min(cap, *n); ++i) ids[i] = s.pages[i];
+  return SPAN_OK;
+}
+
+int span_plan_evicted(const span_plan* pl, int32_t* ids, int32_t cap, int32_t* n) {
+  if (!pl || !n || cap < 0 || (cap > 0 && !ids)) return fail(SPAN_EINVAL, "span_plan_evicted: bad argument");
+  const auto& ev = pl->plan.evicted;
+  *n = static_cast<int32_t>(ev.size());
+  for (int32_t i = 0; i < std::min(cap, *n); ++i) ids[i] = ev[i];
+  return SPAN_OK;
+}
+
+int span_plan_rows(const span_plan* pl, int64_t* rows, int64_t cap, int64_t* n_prefill, int64_t* n_cross) {
+  if (!pl || !n_prefill || !n_cross || cap < 0 || (cap > 0 && !rows)) return fail(SPAN_EINVAL, "span_plan_rows: bad argument");
+  const Plan& P = pl->plan;
+  *n_prefill = static_cast<int64_t>(P.rows_prefill.size());
+  *n_cross = static_cast<int64_t>(P.rows_cross.size());
+  int64_t w = 0;
+  for (int64_t r : P.rows_prefill)
+    if (w < cap) rows[w++] = r;
+  for (int64_t r : P.rows_cross)
+    if (w < cap) rows[w++] = r;
+  return SPAN_OK;
+}
+
+static int attention_common(span_plan* pl, int32_t layer, const char* who) {
+  if (!pl) return fail(SPAN_EINVAL, std::string(who) + ": null plan");
+  if (pl->pool->cfg.device < 0) return fail(SPAN_ESTATE, std::string(who) + ": host-only pool");
+  if (pl->committed) return fail(SPAN_ESTATE, std::string(who) + ": plan already committed");
+  if (layer < 0 || layer >= pl->pool->cfg.num_layers) return fail(SPAN_EINVAL, std::string(who) + ": layer out of range");
+  return SPAN_OK;
+}
+
+static PoolGeom geom(const span_plan* pl, int32_t layer) {
+  const span_pool_config& c = pl->pool->cfg;
+  const int64_t page_elems = 2ll * c.num_kv_heads * c.page_size * c.head_dim;
+  return PoolGeom{pl->pool->dev, static_cast<int64_t>(layer) * c.num_pages * page_elems, c.num_q_heads,
+                  c.num_kv_heads, c.head_dim, c.dtype};
+}
+
+int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
+                           void* stream) {
+  int rc = attention_common(pl, layer, "span_prefill_fragments");
+  if (rc) return rc;
+  const Plan& P = pl->plan;
+  if (P.k3_prefill.empty() && P.t_prefill.empty()) return SPAN_OK;
+  if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_prefill_fragments: null activation pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  PoolGeom g = geom(pl, layer);
+  hipError_t e = launch_rope_write(g, pl->k3p, static_cast<int>(P.k3_prefill.size()), k, v, pl->inv_freq, s);
+  if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
+  const int nt = static_cast<int>(P.t_prefill.size());
+  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s)
+               : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s);
+  if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
+  return SPAN_OK;
+}
+
+int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
+                      void* stream) {
+  int rc = attention_common(pl, layer, "span_cross_attend");
+  if (rc) return rc;
+  const Plan& P = pl->plan;
+  if (P.t_cross.empty()) return SPAN_OK;
+  if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_cross_attend: null activation pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  PoolGeom g = geom(pl, layer);
+  hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->inv_freq, s);
+  if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
+  float* po = pl->part;
+  float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
+  const int nt = static_cast<int>(P.t_cross.size());
+  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s)
+               : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s);
+  if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
+  e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);
+  if (e != hipSuccess) return hip_fail(e, "span_cross_attend: combine");
+  return SPAN_OK;
+}
+
+int span_plan_commit(span_plan* pl) {
+  if (!pl) return fail(SPAN_EINVAL, "span_plan_commit: null plan");
+  if (pl->committed) return fail(SPAN_ESTATE, "span_plan_commit: already committed");
+  pl->pool->index->commit(&pl->plan);
+  pl->committed = true;
+  return SPAN_OK;
+}
+
+int span_plan_destroy(span_plan* pl) {
+  if (!pl) return fail(SPAN_EINVAL, "span_plan_destroy: null plan");
+  if (!pl->committed) pl->pool->index->release(&pl->plan);
+  if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
+  if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
+  pl->pool->plans.erase(pl);
+  delete pl;
+  return SPAN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,37 @@
+// Device helpers shared by the HIP kernels: bf16 storage and rotary angles.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace spanq {
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float(static_cast<uint32_t>(x) << 16); }
+
+// float -> bfloat16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>(0x7fc0u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
+
+// sin/cos of pos * inv_freq: the product and its reduction to [-pi, pi] in
+// double precision, the trigonometric evaluation in single precision.
+__device__ __forceinline__ void rope_angle(int pos, double inv_freq, float* sn, float* cs) {
+  const double a = static_cast<double>(pos) * inv_freq;
+  const double r = a - 6.283185307179586476925 * rint(a * 0.15915494309189533577);
+  sincosf(static_cast<float>(r), sn, cs);
+}
+
+}  // namespace spanq

@@ -1,0 +1,39 @@
+// Launchers of the HIP kernels (kernels.hip, attn_mfma.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "work.h"
+
+namespace spanq {
+
+struct PoolGeom {
+  void* base;          // page memory
+  int64_t layer_off;   // element offset of the layer slab
+  int32_t hq, hkv, d;
+  int32_t dtype;       // SPAN_F32 / SPAN_BF16
+};
+
+// K3: rotate keys at their positions and write keys/values of new pages.
+hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n_pages, const void* k,
+                             const void* v, const double* inv_freq, hipStream_t s);
+
+// Generic (vector ALU) span attention over work tiles of up to 64 rows.
+constexpr int kGenericBM = 64;
+hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
+                               const void* q, void* out, float* part_o, float* part_ml,
+                               const double* inv_freq, hipStream_t s);
+
+// bf16 MFMA span attention; tiles of kMfmaBM rows, one work-group per (tile, kv head).
+constexpr int kMfmaBM = 64;
+bool mfma_supported(int hq, int hkv, int d, int dtype);
+hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
+                            const void* q, void* out, float* part_o, float* part_ml,
+                            const double* inv_freq, hipStream_t s);
+
+// K4: merge KV-split partials (bm = rows per tile of the producing kernel).
+hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,
+                          const float* part_ml, int bm, void* out, hipStream_t s);
+
+}  // namespace spanq

@@ -1,0 +1,264 @@
+// Page writer (K3), generic span attention and KV-split combine for gfx950.
+//
+// Rotary encoding (section 5.5 cites RoFormer): rotate-half pairs (i, i + d/2)
+// at angle pos * theta^(-2i/d).  Angles are formed in double precision, reduced
+// to [-pi, pi] and evaluated in single precision.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/spanq.h"
+#include "dev_common.h"
+#include "kernels.h"
+
+namespace spanq {
+
+// ------------------------------------------------------------------ K3
+// One work-group per new page.  K goes to [kv_head][slot][d] rotated at its
+// position; V goes transposed to [kv_head][d][slot].  Unfilled slots are zeroed
+// so that masked keys never feed a NaN into the P.V product.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restrict__ pages,
+                                                         const T* __restrict__ k, const T* __restrict__ v,
+                                                         T* __restrict__ pool, int64_t layer_off, int hkv,
+                                                         const double* __restrict__ inv_freq) {
+  const NewPage pg = pages[blockIdx.x];
+  const int64_t page_elems = 2ll * hkv * kPage * D;
+  T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems;
+  T* vp = kp + static_cast<int64_t>(hkv) * kPage * D;
+  constexpr int H = D / 2;
+  for (int e = threadIdx.x; e < hkv * kPage * H; e += blockDim.x) {
+    const int h = e / (kPage * H);
+    const int rem = e - h * (kPage * H);
+    const int s = rem / H;
+    const int i = rem - s * H;
+    float y0 = 0.f, y1 = 0.f;
+    if (s < pg.n_valid) {
+      const int64_t src = (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D;
+      const float x0 = to_f32(k[src + i]);
+      const float x1 = to_f32(k[src + i + H]);
+      float sn, cs;
+      rope_angle(pg.pos0 + s, inv_freq[i], &sn, &cs);
+      y0 = x0 * cs - x1 * sn;
+      y1 = x1 * cs + x0 * sn;
+    }
+    T* dst = kp + (static_cast<int64_t>(h) * kPage + s) * D;
+    dst[i] = from_f32<T>(y0);
+    dst[i + H] = from_f32<T>(y1);
+  }
+  for (int e = threadIdx.x; e < hkv * D * kPage; e += blockDim.x) {
+    const int h = e / (D * kPage);
+    const int rem = e - h * (D * kPage);
+    const int dd = rem / kPage;
+    const int s = rem - dd * kPage;
+    T val = from_f32<T>(0.f);
+    if (s < pg.n_valid) val = v[(static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + dd];
+    vp[(static_cast<int64_t>(h) * D + dd) * kPage + s] = val;
+  }
+}
+
+template <typename T, int D>
+static hipError_t rope_write_t(const PoolGeom& g, const NewPage* pages, int n, const void* k, const void* v,
+                               const double* inv_freq, hipStream_t s) {
+  hipLaunchKernelGGL((rope_write_kernel<T, D>), dim3(n), dim3(256), 0, s, pages, static_cast<const T*>(k),
+                     static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv, inv_freq);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, const void* k, const void* v,
+                             const double* inv_freq, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (g.dtype == SPAN_BF16) {
+    if (g.d == 128) return rope_write_t<bf16_t, 128>(g, pages, n, k, v, inv_freq, s);
+    return rope_write_t<bf16_t, 64>(g, pages, n, k, v, inv_freq, s);
+  }
+  if (g.d == 128) return rope_write_t<float, 128>(g, pages, n, k, v, inv_freq, s);
+  return rope_write_t<float, 64>(g, pages, n, k, v, inv_freq, s);
+}
+
+// ------------------------------------------------------------------ generic attention
+// One wave per (tile, query head); lane r owns query row r of the tile.  Each
+// key page is staged in LDS (rotated by the page's delta when it is read from a
+// different position than it was written at), then every lane scores its row
+// against the 16 slots and folds them into an online softmax (base 2).
+template <typename T, int D>
+__global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __restrict__ tiles,
+                                                          const KvPage* __restrict__ kv,
+                                                          const T* __restrict__ q, T* __restrict__ out,
+                                                          const T* __restrict__ pool, int64_t layer_off, int hq,
+                                                          int hkv, float scale_log2,
+                                                          const double* __restrict__ inv_freq,
+                                                          float* __restrict__ part_o, float* __restrict__ part_ml) {
+  constexpr int H = D / 2;
+  __shared__ float ks[kPage][D + 1];
+  __shared__ float vs[D][kPage + 1];
+  const WorkTile t = tiles[blockIdx.x];
+  const int h = blockIdx.y;
+  const int g = (h * hkv) / hq;
+  const int lane = threadIdx.x;
+  const bool active = lane < t.n_rows;
+  const int qpos = t.q_pos0 + lane;
+  const int64_t page_elems = 2ll * hkv * kPage * D;
+
+  float qv[D];
+  float acc[D];
+#pragma unroll
+  for (int i = 0; i < D; ++i) acc[i] = 0.f;
+  if (active) {
+    const T* qr = q + (static_cast<int64_t>(t.q_row0 + lane) * hq + h) * D;
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      float sn, cs;
+      rope_angle(qpos, inv_freq[i], &sn, &cs);
+      const float x0 = to_f32(qr[i]);
+      const float x1 = to_f32(qr[i + H]);
+      qv[i] = x0 * cs - x1 * sn;
+      qv[i + H] = x1 * cs + x0 * sn;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < D; ++i) qv[i] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int pi = t.kv_begin; pi < t.kv_end; ++pi) {
+    const KvPage pg = kv[pi];
+    const T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems + static_cast<int64_t>(g) * kPage * D;
+    const T* vp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems +
+                  static_cast<int64_t>(hkv) * kPage * D + static_cast<int64_t>(g) * D * kPage;
+    __syncthreads();
+    for (int e = lane; e < kPage * H; e += 64) {
+      const int s = e / H;
+      const int i = e - s * H;
+      float x0 = to_f32(kp[s * D + i]);
+      float x1 = to_f32(kp[s * D + i + H]);
+      if (pg.delta != 0) {
+        float sn, cs;
+        rope_angle(pg.delta, inv_freq[i], &sn, &cs);
+        const float y0 = x0 * cs - x1 * sn;
+        x1 = x1 * cs + x0 * sn;
+        x0 = y0;
+      }
+      ks[s][i] = x0;
+      ks[s][i + H] = x1;
+    }
+    for (int e = lane; e < D * kPage; e += 64) vs[e / kPage][e % kPage] = to_f32(vp[e]);
+    __syncthreads();
+    if (!active) continue;
+    float sc[kPage];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kPage; ++s) {
+      const bool ok = s < pg.n_valid && pg.pos0 + s <= qpos;
+      float dot = 0.f;
+#pragma unroll
+      for (int i = 0; i < D; ++i) dot += qv[i] * ks[s][i];
+      sc[s] = ok ? dot * scale_log2 : -INFINITY;
+      mx = fmaxf(mx, sc[s]);
+    }
+    if (mx == -INFINITY) continue;
+    const float m_new = fmaxf(m, mx);
+    const float corr = exp2f(m - m_new);  // m == -inf gives 0
+    l *= corr;
+#pragma unroll
+    for (int i = 0; i < D; ++i) acc[i] *= corr;
+#pragma unroll
+    for (int s = 0; s < kPage; ++s) {
+      const float p = exp2f(sc[s] - m_new);
+      l += p;
+#pragma unroll
+      for (int i = 0; i < D; ++i) acc[i] += p * vs[i][s];
+    }
+    m = m_new;
+  }
+  if (!active) return;
+  const int64_t orow = static_cast<int64_t>(t.q_row0 + lane);
+  if (t.part < 0) {
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    T* o = out + (orow * hq + h) * D;
+#pragma unroll
+    for (int i = 0; i < D; ++i) o[i] = from_f32<T>(acc[i] * inv);
+  } else {
+    const int64_t slot = (static_cast<int64_t>(t.part) * hq + h) * kGenericBM + lane;
+    float* po = part_o + slot * D;
+#pragma unroll
+    for (int i = 0; i < D; ++i) po[i] = acc[i];
+    part_ml[slot * 2 + 0] = m;
+    part_ml[slot * 2 + 1] = l;
+  }
+}
+
+template <typename T, int D>
+static hipError_t attn_generic_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
+                                 void* out, float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+  const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  hipLaunchKernelGGL((attn_generic_kernel<T, D>), dim3(n, g.hq), dim3(64), 0, s, tiles, kv,
+                     static_cast<const T*>(q), static_cast<T*>(out), static_cast<const T*>(g.base), g.layer_off,
+                     g.hq, g.hkv, scale_log2, inv_freq, part_o, part_ml);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
+                               void* out, float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (g.dtype == SPAN_BF16) {
+    if (g.d == 128) return attn_generic_t<bf16_t, 128>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+    return attn_generic_t<bf16_t, 64>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+  }
+  if (g.d == 128) return attn_generic_t<float, 128>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+  return attn_generic_t<float, 64>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+}
+
+// ------------------------------------------------------------------ K4 combine
+// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restrict__ tiles,
+                                                      const float* __restrict__ part_o,
+                                                      const float* __restrict__ part_ml, int bm, int hq,
+                                                      T* __restrict__ out) {
+  const CombineTile t = tiles[blockIdx.x];
+  const int h = blockIdx.y;
+  for (int e = threadIdx.x; e < t.n_rows * D; e += blockDim.x) {
+    const int r = e / D;
+    const int i = e - r * D;
+    float M = -INFINITY;
+    for (int p = 0; p < t.n_parts; ++p)
+      M = fmaxf(M, part_ml[((static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r) * 2]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+      for (int p = 0; p < t.n_parts; ++p) {
+        const int64_t slot = (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r;
+        const float mp = part_ml[slot * 2];
+        if (mp == -INFINITY) continue;
+        const float w = exp2f(mp - M);
+        L += part_ml[slot * 2 + 1] * w;
+        O += part_o[slot * D + i] * w;
+      }
+    }
+    out[(static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + i] = from_f32<T>(L > 0.f ? O / L : 0.f);
+  }
+}
+
+hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n, const float* part_o,
+                          const float* part_ml, int bm, void* out, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dim3 grid(n, g.hq);
+  if (g.dtype == SPAN_BF16) {
+    if (g.d == 128)
+      hipLaunchKernelGGL((combine_kernel<bf16_t, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+                         static_cast<bf16_t*>(out));
+    else
+      hipLaunchKernelGGL((combine_kernel<bf16_t, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+                         static_cast<bf16_t*>(out));
+  } else {
+    if (g.d == 128)
+      hipLaunchKernelGGL((combine_kernel<float, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+                         static_cast<float*>(out));
+    else
+      hipLaunchKernelGGL((combine_kernel<float, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+                         static_cast<float*>(out));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace spanq

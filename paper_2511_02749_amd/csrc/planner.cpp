@@ -1,0 +1,426 @@
+// Page cache index and span planner.
+//
+// Hashing follows sections 2 and 5.4 of the paper: pages are hashed in chains
+// (each page folds in the previous page's hash), a lookup stops at a chain's
+// first miss, and at each commuting child the chain restarts from a seed that
+// depends on the shared prefix only.  Allocation, deduplication and eviction
+// rules are this library's (the paper leaves them to vLLM's block pool):
+// lowest free page id; a span already scheduled in the same plan is a hit;
+// LRU victim by (last use, -index in span, page id), so tail pages go first.
+#include "planner.h"
+
+#include <algorithm>
+#include <cstring>
+
+#include "../../include/spanq.h"
+
+namespace spanq {
+
+uint64_t mix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+uint64_t page_hash(uint64_t prev, const int32_t* tok, int32_t n, int32_t page_idx) {
+  uint64_t h = prev;
+  for (int32_t i = 0; i < n; ++i) h = mix64(h ^ static_cast<uint64_t>(static_cast<uint32_t>(tok[i])));
+  return mix64(h ^ (static_cast<uint64_t>(static_cast<uint32_t>(n)) << 32) ^
+               static_cast<uint64_t>(static_cast<uint32_t>(page_idx)));
+}
+
+uint64_t fragment_seed(uint64_t prefix_last_or_root) { return mix64(prefix_last_or_root ^ SPAN_HASH_FRAG_TAG); }
+
+PoolIndex::PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode)
+    : num_pages_(num_pages), page_size_(page_size), hash_mode_(hash_mode) {
+  pages_.resize(static_cast<size_t>(num_pages));
+  page_tokens_.resize(static_cast<size_t>(num_pages) * page_size);
+  reset();
+}
+
+void PoolIndex::reset() {
+  index_.clear();
+  evictable_.clear();
+  free_.clear();
+  for (int64_t i = 0; i < num_pages_; ++i) {
+    pages_[i] = PageRec{};
+    free_.insert(free_.end(), static_cast<int32_t>(i));
+  }
+}
+
+int64_t PoolIndex::pinned_count() const {
+  int64_t n = 0;
+  for (const auto& p : pages_) n += (p.used && p.pins > 0) ? 1 : 0;
+  return n;
+}
+
+int64_t PoolIndex::lookup(uint64_t h) const {
+  auto it = index_.find(h);
+  return it == index_.end() ? -1 : it->second;
+}
+
+bool PoolIndex::content_equal(int32_t pid, const Spec& s) const {
+  const PageRec& p = pages_[pid];
+  if (p.idx != s.idx || p.n_tok != s.n_tok || p.parent != s.parent) return false;
+  return std::memcmp(&page_tokens_[static_cast<size_t>(pid) * page_size_], s.tok,
+                     sizeof(int32_t) * s.n_tok) == 0;
+}
+
+bool PoolIndex::spec_equal(const Spec& a, const Spec& b) const {
+  return a.idx == b.idx && a.n_tok == b.n_tok && a.parent == b.parent &&
+         std::memcmp(a.tok, b.tok, sizeof(int32_t) * a.n_tok) == 0;
+}
+
+int32_t PoolIndex::pop_free() {
+  auto it = free_.begin();
+  int32_t pid = *it;
+  free_.erase(it);
+  return pid;
+}
+
+void PoolIndex::push_free(int32_t pid) {
+  pages_[pid] = PageRec{};
+  free_.insert(pid);
+}
+
+void PoolIndex::evict_one(Plan* p) {
+  auto it = evictable_.begin();
+  int32_t pid = std::get<2>(*it);
+  evictable_.erase(it);
+  index_.erase(pages_[pid].hash);
+  p->evicted.push_back(pid);
+  ++total_evictions_;
+  push_free(pid);
+}
+
+namespace {
+struct Entry {
+  bool hit;     // page served by a published page
+  bool dup;     // page scheduled earlier in this plan
+  int32_t x;    // page id (hit) or slot (new)
+};
+}  // namespace
+
+int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& tiling, Plan* out,
+                    std::string* msg) {
+  const int32_t ps = page_size_;
+  std::vector<Spec> specs;
+  std::unordered_map<uint64_t, int32_t> pending;
+  struct SpanWalk {
+    int kind, query, child;
+    SpanIn in;
+    std::vector<Entry> entries;
+  };
+  std::vector<SpanWalk> walk;
+  std::vector<std::vector<int>> query_spans(qs.size());
+
+  for (size_t qi = 0; qi < qs.size(); ++qi) {
+    const QueryIn& q = qs[qi];
+    struct Src { uint64_t seed; SpanIn in; int kind, child; bool partial_ok; };
+    std::vector<Src> srcs;
+    if (hash_mode_ == SPAN_HASH_STOCK) {
+      srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, false});
+    } else {
+      uint64_t h = SPAN_HASH_ROOT;
+      for (int32_t p = 0; p * ps < q.prefix.n; ++p) {
+        int32_t n = std::min(ps, q.prefix.n - p * ps);
+        h = page_hash(h, q.prefix.tok + p * ps, n, p);
+      }
+      uint64_t fs = fragment_seed(h);
+      srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, true});
+      for (size_t c = 0; c < q.frags.size(); ++c) srcs.push_back({fs, q.frags[c], 1, static_cast<int>(c), true});
+    }
+    for (const Src& s : srcs) {
+      SpanWalk w{s.kind, static_cast<int>(qi), s.child, s.in, {}};
+      uint64_t h = s.seed;
+      bool missed = false;
+      for (int32_t p = 0; p * ps < s.in.n; ++p) {
+        int32_t n = std::min(ps, s.in.n - p * ps);
+        Spec sp{page_hash(h, s.in.tok + p * ps, n, p), h, p, n, s.in.tok + p * ps,
+                n == ps || s.partial_ok, false};
+        h = sp.hash;
+        if (!missed && sp.cacheable) {
+          auto it = pending.find(sp.hash);
+          if (it != pending.end() && spec_equal(specs[it->second], sp)) {
+            w.entries.push_back({false, true, it->second});
+            continue;
+          }
+          auto jt = index_.find(sp.hash);
+          if (jt != index_.end() && content_equal(jt->second, sp)) {
+            w.entries.push_back({true, false, jt->second});
+            continue;
+          }
+        }
+        missed = true;
+        int32_t slot = static_cast<int32_t>(specs.size());
+        specs.push_back(sp);
+        if (sp.cacheable && pending.find(sp.hash) == pending.end()) pending[sp.hash] = slot;
+        w.entries.push_back({false, false, slot});
+      }
+      query_spans[qi].push_back(static_cast<int>(walk.size()));
+      walk.push_back(std::move(w));
+    }
+    // cross segment: transient pages, never looked up
+    SpanWalk w{2, static_cast<int>(qi), 0, q.cross, {}};
+    if (hash_mode_ != SPAN_HASH_STOCK) {
+      for (int32_t p = 0; p * ps < q.cross.n; ++p) {
+        int32_t n = std::min(ps, q.cross.n - p * ps);
+        int32_t slot = static_cast<int32_t>(specs.size());
+        specs.push_back(Spec{0, 0, p, n, q.cross.tok + p * ps, false, true});
+        w.entries.push_back({false, false, slot});
+      }
+    }
+    query_spans[qi].push_back(static_cast<int>(walk.size()));
+    walk.push_back(std::move(w));
+  }
+
+  // distinct published pages this plan hits, in walk order
+  std::vector<int32_t> hit_pids;
+  {
+    std::vector<char> seen(static_cast<size_t>(num_pages_), 0);
+    for (const auto& w : walk)
+      for (const auto& e : w.entries)
+        if (e.hit && !seen[e.x]) {
+          seen[e.x] = 1;
+          hit_pids.push_back(e.x);
+        }
+  }
+  int64_t need = static_cast<int64_t>(specs.size());
+  int64_t evictable = static_cast<int64_t>(evictable_.size());
+  for (int32_t pid : hit_pids)
+    if (pages_[pid].published && pages_[pid].pins == 0) --evictable;
+  if (need > free_count() + evictable) {
+    *msg = "pool exhausted: plan needs " + std::to_string(need) + " pages, " +
+           std::to_string(free_count()) + " free, " + std::to_string(evictable) + " evictable";
+    return SPAN_ENOMEM;
+  }
+
+  // ---- mutate
+  Plan& P = *out;
+  P.pool = this;
+  P.tick = ++tick_;
+  for (int32_t pid : hit_pids) {
+    PageRec& r = pages_[pid];
+    if (r.published && r.pins == 0) evictable_.erase(std::make_tuple(r.last_use, -r.idx, pid));
+    r.pins += 1;
+    r.last_use = P.tick;
+  }
+  P.hits = hit_pids;
+  std::vector<int32_t> slot_pid(specs.size(), -1);
+  auto alloc = [&](int32_t slot) {
+    if (free_.empty()) evict_one(&P);
+    int32_t pid = pop_free();
+    const Spec& s = specs[slot];
+    PageRec& r = pages_[pid];
+    r = PageRec{};
+    r.hash = s.hash;
+    r.parent = s.parent;
+    r.idx = s.idx;
+    r.n_tok = s.n_tok;
+    r.last_use = P.tick;
+    r.pins = 1;
+    r.used = true;
+    r.published = false;
+    r.cacheable = s.cacheable && !s.cross;
+    std::memcpy(&page_tokens_[static_cast<size_t>(pid) * ps], s.tok, sizeof(int32_t) * s.n_tok);
+    slot_pid[slot] = pid;
+    P.new_pages.push_back(pid);
+    if (s.cross) P.cross_pages.push_back(pid);
+  };
+  for (size_t qi = 0; qi < qs.size(); ++qi)
+    for (int wi : query_spans[qi])
+      for (const Entry& e : walk[wi].entries)
+        if (!e.hit && !e.dup) alloc(e.x);
+
+  P.query_spans = query_spans;
+  P.spans.resize(walk.size());
+  for (size_t wi = 0; wi < walk.size(); ++wi) {
+    const SpanWalk& w = walk[wi];
+    SpanPlan& sp = P.spans[wi];
+    sp.kind = w.kind;
+    sp.query = w.query;
+    sp.child = w.child;
+    sp.n_tok = w.in.n;
+    sp.row = w.in.row;
+    sp.n_hit = 0;
+    bool leading = true;
+    for (const Entry& e : w.entries) {
+      sp.pages.push_back(e.hit ? e.x : slot_pid[e.x]);
+      if (leading && (e.hit || e.dup)) {
+        ++sp.n_hit;
+      } else {
+        leading = false;
+      }
+    }
+    if (w.kind != 2) {
+      int64_t np = static_cast<int64_t>(sp.pages.size());
+      P.pages_hit += sp.n_hit;
+      int64_t new_here = 0;
+      for (size_t i = sp.n_hit; i < w.entries.size(); ++i) new_here += (!w.entries[i].dup) ? 1 : 0;
+      P.pages_new += new_here;
+      int64_t hit_tok = std::min<int64_t>(w.in.n, static_cast<int64_t>(sp.n_hit) * ps);
+      P.tokens_hit += hit_tok;
+      P.tokens_new += (np > sp.n_hit) ? (w.in.n - hit_tok) : 0;
+    } else {
+      P.tokens_cross += w.in.n;
+    }
+  }
+  if (build) build_work(&P, tiling);
+  ++live_plans;
+  return SPAN_OK;
+}
+
+void PoolIndex::build_work(Plan* p, const Tiling& t) {
+  const int32_t ps = page_size_;
+  p->bm_cross = t.bm_cross;
+  for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
+    const auto& ids = p->query_spans[qi];
+    SpanPlan& prefix = p->spans[ids[0]];
+    SpanPlan& cross = p->spans[ids.back()];
+    const int32_t P = prefix.n_tok;
+    prefix.canon0 = 0;
+    prefix.final0 = 0;
+    int32_t at = P;
+    for (size_t c = 1; c + 1 < ids.size(); ++c) {
+      SpanPlan& f = p->spans[ids[c]];
+      f.canon0 = P;
+      f.final0 = at;
+      at += f.n_tok;
+    }
+    cross.canon0 = at;
+    cross.final0 = at;
+  }
+  // ---- prefill: new pages and row tiles of every span that computes pages
+  for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
+    const auto& ids = p->query_spans[qi];
+    const SpanPlan& prefix = p->spans[ids[0]];
+    for (size_t c = 0; c + 1 < ids.size(); ++c) {
+      const SpanPlan& s = p->spans[ids[c]];
+      const int32_t np = static_cast<int32_t>(s.pages.size());
+      if (s.n_hit >= np) continue;
+      for (int32_t pg = s.n_hit; pg < np; ++pg)
+        p->k3_prefill.push_back(NewPage{s.pages[pg], std::min(ps, s.n_tok - pg * ps),
+                                        static_cast<int32_t>(s.row + pg * ps), s.canon0 + pg * ps});
+      const int32_t kv0 = static_cast<int32_t>(p->kv.size());
+      if (s.kind == 1)
+        for (size_t pg = 0; pg < prefix.pages.size(); ++pg)
+          p->kv.push_back(KvPage{prefix.pages[pg], std::min<int32_t>(ps, prefix.n_tok - static_cast<int32_t>(pg) * ps),
+                                 static_cast<int32_t>(pg) * ps, 0});
+      for (int32_t pg = 0; pg < np; ++pg)
+        p->kv.push_back(KvPage{s.pages[pg], std::min(ps, s.n_tok - pg * ps), s.canon0 + pg * ps, 0});
+      const int32_t kv1 = static_cast<int32_t>(p->kv.size());
+      const int32_t pre = (s.kind == 1) ? prefix.n_tok : 0;
+      for (int32_t j0 = s.n_hit * ps; j0 < s.n_tok; j0 += t.bm_prefill) {
+        int32_t n = std::min(t.bm_prefill, s.n_tok - j0);
+        int32_t last_pos = s.canon0 + j0 + n - 1;
+        int32_t end = kv0;
+        while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
+        p->t_prefill.push_back(WorkTile{static_cast<int32_t>(s.row + j0), n, s.canon0 + j0, kv0, end, -1, 0, 0});
+        for (int32_t j = j0; j < j0 + n; ++j) {
+          p->rows_prefill.push_back(s.row + j);
+          p->prefill_pairs += pre + j + 1;
+        }
+      }
+    }
+  }
+  // ---- cross: pages, key list in query order, split-KV row tiles
+  struct CrossTile { int32_t row0, n, pos0, kv0, kv1; };
+  std::vector<CrossTile> ct;
+  int32_t max_pages = 0;
+  for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
+    const auto& ids = p->query_spans[qi];
+    const SpanPlan& cross = p->spans[ids.back()];
+    if (cross.n_tok == 0) continue;
+    for (size_t pg = 0; pg < cross.pages.size(); ++pg)
+      p->k3_cross.push_back(NewPage{cross.pages[pg], std::min<int32_t>(ps, cross.n_tok - static_cast<int32_t>(pg) * ps),
+                                    static_cast<int32_t>(cross.row + pg * ps), cross.final0 + static_cast<int32_t>(pg) * ps});
+    const int32_t kv0 = static_cast<int32_t>(p->kv.size());
+    for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
+      const SpanPlan& s = p->spans[ids[c]];
+      for (size_t pg = 0; pg < s.pages.size(); ++pg)
+        p->kv.push_back(KvPage{s.pages[pg], std::min<int32_t>(ps, s.n_tok - static_cast<int32_t>(pg) * ps),
+                               s.final0 + static_cast<int32_t>(pg) * ps, s.final0 - s.canon0});
+    }
+    for (size_t pg = 0; pg < cross.pages.size(); ++pg)
+      p->kv.push_back(KvPage{cross.pages[pg], std::min<int32_t>(ps, cross.n_tok - static_cast<int32_t>(pg) * ps),
+                             cross.final0 + static_cast<int32_t>(pg) * ps, 0});
+    const int32_t kv1 = static_cast<int32_t>(p->kv.size());
+    p->cross_kv_pages += kv1 - kv0;
+    for (int32_t j0 = 0; j0 < cross.n_tok; j0 += t.bm_cross) {
+      int32_t n = std::min(t.bm_cross, cross.n_tok - j0);
+      int32_t last_pos = cross.final0 + j0 + n - 1;
+      int32_t end = kv0;
+      while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
+      ct.push_back(CrossTile{static_cast<int32_t>(cross.row + j0), n, cross.final0 + j0, kv0, end});
+      max_pages = std::max(max_pages, end - kv0);
+      for (int32_t j = j0; j < j0 + n; ++j) {
+        p->rows_cross.push_back(cross.row + j);
+        p->cross_pairs += cross.final0 + j + 1;
+      }
+    }
+  }
+  int32_t splits = 1;
+  if (!ct.empty()) {
+    int64_t items = static_cast<int64_t>(ct.size()) * t.kv_heads;
+    int64_t want = (t.target_items + items - 1) / items;
+    int64_t cap = std::max<int64_t>(1, max_pages / t.min_split_pages);
+    splits = static_cast<int32_t>(std::max<int64_t>(1, std::min(want, cap)));
+  }
+  p->kv_splits = splits;
+  for (const CrossTile& c : ct) {
+    int32_t n_pages = c.kv1 - c.kv0;
+    int32_t chunk = (n_pages + splits - 1) / splits;
+    int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
+    if (parts <= 1) {
+      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});
+      continue;
+    }
+    int32_t part0 = p->n_parts;
+    for (int32_t s = 0; s < parts; ++s) {
+      int32_t b = c.kv0 + s * chunk;
+      int32_t e = std::min(c.kv1, b + chunk);
+      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, b, e, p->n_parts++, 0, 0});
+    }
+    p->combine.push_back(CombineTile{c.row0, c.n, part0, parts});
+  }
+}
+
+void PoolIndex::commit(Plan* p) {
+  for (int32_t pid : p->new_pages) {
+    PageRec& r = pages_[pid];
+    if (!r.cacheable || index_.count(r.hash)) continue;
+    index_[r.hash] = pid;
+    r.published = true;
+  }
+  for (int32_t pid : p->new_pages) {
+    PageRec& r = pages_[pid];
+    r.pins -= 1;
+    if (!r.published) {
+      push_free(pid);
+    } else if (r.pins == 0) {
+      evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+    }
+  }
+  for (int32_t pid : p->hits) {
+    PageRec& r = pages_[pid];
+    r.pins -= 1;
+    if (r.published && r.pins == 0) evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+  }
+  p->committed = true;
+  --live_plans;
+}
+
+void PoolIndex::release(Plan* p) {
+  if (p->committed) return;
+  for (int32_t pid : p->new_pages) push_free(pid);
+  for (int32_t pid : p->hits) {
+    PageRec& r = pages_[pid];
+    r.pins -= 1;
+    if (r.published && r.pins == 0) evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+  }
+  p->committed = true;
+  --live_plans;
+}
+
+}  // namespace spanq

@@ -1,0 +1,134 @@
+// Host-side page cache index and span planner (no HIP dependency).
+#pragma once
+#include <cstdint>
+#include <set>
+#include <string>
+#include <tuple>
+#include <unordered_map>
+#include <vector>
+
+#include "work.h"
+
+namespace spanq {
+
+uint64_t mix64(uint64_t x);
+uint64_t page_hash(uint64_t prev, const int32_t* tok, int32_t n, int32_t page_idx);
+uint64_t fragment_seed(uint64_t prefix_last_or_root);
+
+struct PageRec {
+  uint64_t hash = 0;
+  uint64_t parent = 0;
+  int32_t idx = 0;
+  int32_t n_tok = 0;
+  int64_t last_use = 0;
+  int32_t pins = 0;
+  bool used = false;
+  bool published = false;
+  bool cacheable = false;
+};
+
+struct SpanIn {
+  const int32_t* tok;
+  int32_t n;
+  int64_t row;
+};
+
+struct QueryIn {
+  SpanIn prefix;
+  std::vector<SpanIn> frags;
+  SpanIn cross;
+};
+
+// Planned span of one query.
+struct SpanPlan {
+  int kind = 0;  // 0 prefix, 1 fragment, 2 cross
+  int query = 0;
+  int child = 0;
+  int32_t n_tok = 0;
+  int64_t row = 0;
+  int32_t canon0 = 0;  // canonical position of token 0
+  int32_t final0 = 0;  // final position of token 0 in its query
+  std::vector<int32_t> pages;
+  int32_t n_hit = 0;
+};
+
+struct Tiling {
+  int bm_prefill = 64;   // rows per prefill tile
+  int bm_cross = 64;     // rows per cross tile
+  int kv_heads = 1;      // work items per tile (one per kv head)
+  int target_items = 2048;
+  int min_split_pages = 8;
+};
+
+class PoolIndex;
+
+struct Plan {
+  PoolIndex* pool = nullptr;
+  int64_t tick = 0;
+  std::vector<SpanPlan> spans;
+  std::vector<std::vector<int>> query_spans;  // per query: prefix, fragments..., cross
+  std::vector<int32_t> evicted, new_pages, cross_pages, hits;
+  bool committed = false;
+
+  // work lists
+  std::vector<KvPage> kv;
+  std::vector<NewPage> k3_prefill, k3_cross;
+  std::vector<WorkTile> t_prefill, t_cross;
+  std::vector<CombineTile> combine;
+  std::vector<int64_t> rows_prefill, rows_cross;
+  int32_t n_parts = 0;
+  int32_t kv_splits = 1;
+  int bm_cross = 64;
+
+  int64_t pages_hit = 0, pages_new = 0, tokens_hit = 0, tokens_new = 0, tokens_cross = 0;
+  int64_t prefill_pairs = 0, cross_pairs = 0, cross_kv_pages = 0;
+};
+
+class PoolIndex {
+ public:
+  PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode);
+
+  // Returns 0, or -2 (pool full, unchanged), -1 (bad input) with msg set.
+  int plan(const std::vector<QueryIn>& qs, bool build_work, const Tiling& tiling, Plan* out,
+           std::string* msg);
+  void commit(Plan* p);
+  void release(Plan* p);  // destroy without commit
+  void reset();
+  int64_t lookup(uint64_t h) const;  // page id or -1
+
+  int64_t num_pages() const { return num_pages_; }
+  int64_t free_count() const { return static_cast<int64_t>(free_.size()); }
+  int64_t cached_count() const { return static_cast<int64_t>(index_.size()); }
+  int64_t pinned_count() const;
+  int64_t tick() const { return tick_; }
+  int64_t total_evictions() const { return total_evictions_; }
+  int32_t page_size() const { return page_size_; }
+  int live_plans = 0;
+
+ private:
+  struct Spec {
+    uint64_t hash, parent;
+    int32_t idx, n_tok;
+    const int32_t* tok;
+    bool cacheable, cross;
+  };
+  bool content_equal(int32_t pid, const Spec& s) const;
+  bool spec_equal(const Spec& a, const Spec& b) const;
+  int32_t pop_free();
+  void push_free(int32_t pid);
+  void evict_one(Plan* p);
+  void build_work(Plan* p, const Tiling& tiling);
+
+  int64_t num_pages_;
+  int32_t page_size_;
+  int32_t hash_mode_;
+  std::vector<PageRec> pages_;
+  std::vector<int32_t> page_tokens_;
+  std::unordered_map<uint64_t, int32_t> index_;
+  std::set<int32_t> free_;
+  std::set<std::tuple<int64_t, int32_t, int32_t>> evictable_;  // (last_use, -idx, id)
+  int64_t tick_ = 0;
+  int64_t total_evictions_ = 0;
+};
+
+}  // namespace spanq

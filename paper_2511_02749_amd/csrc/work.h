@@ -1,0 +1,51 @@
+// Device work-list records shared by the planner (host) and the kernels.
+// Plain 16/32-byte PODs so one host buffer can be copied to the device as is.
+#pragma once
+#include <cstdint>
+
+namespace spanq {
+
+constexpr int kPage = 16;  // tokens per page on device pools
+
+// One page of a query's key/value list.  Key slot s of the page sits at position
+// pos0 + s in the frame of the rows reading it; the page stores keys rotated at
+// position (pos0 - delta) + s, so a reader rotates them by `delta` more.
+struct KvPage {
+  int32_t page_id;
+  int32_t n_valid;  // filled slots (a span's last page may be partial)
+  int32_t pos0;
+  int32_t delta;
+};
+
+// One page to fill from caller rows: slots 0..n_valid-1 come from rows
+// src_row.., keys rotated at positions pos0...
+struct NewPage {
+  int32_t page_id;
+  int32_t n_valid;
+  int32_t src_row;
+  int32_t pos0;
+};
+
+// A tile of up to BM consecutive query rows of one span, against the key pages
+// kv[kv_begin, kv_end).  part < 0: write the normalised output; else write the
+// unnormalised partial (one KV split) into partial slot `part`.
+struct WorkTile {
+  int32_t q_row0;
+  int32_t n_rows;
+  int32_t q_pos0;
+  int32_t kv_begin;
+  int32_t kv_end;
+  int32_t part;
+  int32_t pad0;
+  int32_t pad1;
+};
+
+// Merge partial slots part0..part0+n_parts-1 into output rows q_row0...
+struct CombineTile {
+  int32_t q_row0;
+  int32_t n_rows;
+  int32_t part0;
+  int32_t n_parts;
+};
+
+}  // namespace spanq

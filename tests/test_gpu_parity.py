@@ -1,0 +1,199 @@
+"""GPU parity: the HIP path through the C-ABI against the oracle, element by element.
+
+Tolerances (max abs error against the float64 oracle run on the same rounded
+inputs): 2e-2 for bf16 pools, 1e-4 for fp32 pools.  Page ids / hits are
+checked bit-exactly elsewhere (host tests); here the page *contents* and the
+attention outputs are checked, plus the two bit-identity invariants: a
+fragment's cached KV does not depend on the order it was first seen in, and
+cross output over reused pages equals a cold recompute.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import attention as OA
+from tests.helpers import TOL, GpuRun, max_err, oracle_rows, query_layout, query_rows
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    print(flush=True)
+
+
+def _computed_rows(plan):
+    pre, cross = plan.rows()
+    return np.concatenate([pre, cross])
+
+
+def _check_rows(run, batch, rows, tol, limit=None):
+    """Compare GPU output rows with the oracle; each row is evaluated in the first
+    query of the batch that contains it."""
+    rows = np.asarray(rows, np.int64)
+    if limit is not None and rows.size > limit:
+        rows = rows[np.linspace(0, rows.size - 1, limit).astype(np.int64)]
+    remaining = set(int(r) for r in rows)
+    worst = 0.0
+    for q in batch:
+        mine = [r for r in query_rows(q) if int(r) in remaining]
+        if not mine:
+            continue
+        ref = oracle_rows(run.wl, q, mine)
+        got = run.out_rows(mine)
+        for i, r in enumerate(mine):
+            worst = max(worst, max_err(got[i], ref[int(r)]))
+            remaining.discard(int(r))
+    assert not remaining
+    assert worst <= tol, f"max abs err {worst} > {tol}"
+    return worst
+
+
+@pytest.mark.parametrize("mode", ["proj", "direct"])
+def test_c1_cold_then_permuted_hits(mode):
+    wl = W.config_c1(mode=mode)
+    run = GpuRun(wl)
+    a = run.run_batch(wl.batches[0])
+    sa = a.stats()
+    assert sa["tokens_hit"] == 0 and sa["tokens_new"] == 32 + 4 * 64
+    _check_rows(run, wl.batches[0], _computed_rows(a), TOL["f32"])
+    b = run.run_batch(wl.batches[1])
+    sb = b.stats()
+    assert sb["tokens_new"] == 0 and sb["tokens_hit"] == 32 + 4 * 64 and sb["tokens_cross"] == 16
+    pre, cross = b.rows()
+    assert pre.size == 0 and cross.size == 16
+    _check_rows(run, wl.batches[1], cross, TOL["f32"])
+    run.close()
+
+
+SMALL = [
+    dict(name="ragged", head_dim=128, n_q_heads=8, n_kv_heads=2),
+    dict(name="d64", head_dim=64, n_q_heads=8, n_kv_heads=2),
+    dict(name="mha", head_dim=128, n_q_heads=4, n_kv_heads=4),
+    dict(name="noprefix", prefix_len=0, frag_lens=(16, 1, 77, 130), cross_len=40),
+    dict(name="nocross", cross_len=0),
+    dict(name="bigtiles", prefix_len=100, frag_lens=(300, 129, 64), frags_per_query=3, cross_len=150),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kernel", ["generic", "auto"])
+@pytest.mark.parametrize("case", SMALL, ids=[c["name"] for c in SMALL])
+def test_small_ragged(case, dtype, kernel):
+    case = dict(case)
+    case.pop("name")
+    wl = W.small_workload(dtype=dtype, **case)
+    run = GpuRun(wl, kernel=kernel)
+    plan = run.run_batch(wl.batches[0])
+    _check_rows(run, wl.batches[0], _computed_rows(plan), TOL[dtype])
+    run.close()
+
+
+def test_duplicate_fragment_in_one_query():
+    wl = W.small_workload(orders=[[0, 1, 0], [2, 1, 3], [1, 1, 2]], n_queries=3)
+    run = GpuRun(wl)
+    plan = run.run_batch(wl.batches[0])
+    st = plan.stats()
+    assert st["tokens_new"] == 40 + 37 + 64 + 5 + 100
+    _check_rows(run, wl.batches[0], _computed_rows(plan), TOL["bf16"])
+    run.close()
+
+
+def _page_kv(run, page_id, wl):
+    raw = run.pool.read_page(0, page_id)
+    if wl.dtype == "bf16":
+        raw = (raw.astype(np.uint32) << 16).view(np.float32)
+    hkv, d = wl.n_kv_heads, wl.head_dim
+    k = raw[: hkv * 16 * d].reshape(hkv, 16, d)
+    v = raw[hkv * 16 * d:].reshape(hkv, d, 16).transpose(0, 2, 1)
+    return k, v
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pages_hold_canonical_kv(dtype):
+    wl = W.small_workload(dtype=dtype)
+    run = GpuRun(wl)
+    q0 = wl.batches[0][0]
+    plan = run.run_batch([q0])
+    lay = query_layout(q0)
+    rows = query_rows(q0)
+    for child, f in enumerate(q0.frags):
+        ids, _ = plan.block_table(0, child)
+        kc, vc = OA.cached_fragment_kv(wl.k[rows], wl.v[rows], lay, child, wl.rope_theta)
+        for p, pid in enumerate(ids):
+            k, v = _page_kv(run, pid, wl)
+            n = min(16, f.n - 16 * p)
+            kr, vr = kc[16 * p: 16 * p + n].transpose(1, 0, 2), vc[16 * p: 16 * p + n].transpose(1, 0, 2)
+            rtol = 2.0 ** -8 if dtype == "bf16" else 1e-6
+            np.testing.assert_allclose(k[:, :n], kr, rtol=rtol, atol=1e-5)
+            np.testing.assert_array_equal(v[:, :n], vr.astype(np.float32))
+            assert not np.any(k[:, n:]) and not np.any(v[:, n:])   # unfilled slots are zero
+    run.close()
+
+
+def test_permutation_keeps_pages_and_rows_bit_identical():
+    wl = W.small_workload(orders=[[0, 1, 2, 3], [3, 1, 0, 2]], n_queries=2, frags_per_query=4,
+                          batch_split=[1, 1])
+    runs = [GpuRun(wl), GpuRun(wl)]
+    plans = [runs[0].run_batch(wl.batches[0]), runs[1].run_batch(wl.batches[1])]
+    orders = [[0, 1, 2, 3], [3, 1, 0, 2]]
+    for f in range(4):
+        tabs = [plans[i].block_table(0, orders[i].index(f))[0] for i in range(2)]
+        for pa, pb in zip(*tabs):
+            assert np.array_equal(runs[0].pool.read_page(0, pa), runs[1].pool.read_page(0, pb))
+        frow = wl.batches[0][0].frags[f]
+        rows = np.arange(frow.row, frow.row + frow.n)
+        assert np.array_equal(runs[0].out_rows(rows), runs[1].out_rows(rows))
+    for r in runs:
+        r.close()
+
+
+@pytest.mark.parametrize("kernel", ["generic", "auto"])
+def test_cache_hit_equals_recompute(kernel):
+    wl = W.small_workload(orders=[[0, 1, 2, 3], [3, 1, 0, 2]], n_queries=2, frags_per_query=4,
+                          batch_split=[1, 1])
+    warm = GpuRun(wl, kernel=kernel)
+    warm.run_batch(wl.batches[0])
+    pw = warm.run_batch(wl.batches[1])
+    assert pw.stats()["tokens_new"] == 0
+    cold = GpuRun(wl, kernel=kernel)
+    pc = cold.run_batch(wl.batches[1])
+    assert pc.stats()["tokens_hit"] == 0
+    _, cross = pw.rows()
+    assert np.array_equal(warm.out_rows(cross), cold.out_rows(cross))
+    _check_rows(warm, wl.batches[1], cross, TOL["bf16"])
+    warm.close()
+    cold.close()
+
+
+def test_c2_full_size_sampled():
+    wl = W.config_c2()
+    run = GpuRun(wl)
+    batch = wl.batches[0]
+    plan = run.run_batch(batch)
+    st = plan.stats()
+    assert st["tokens_cross"] == 8 * 128
+    pre, cross = plan.rows()
+    _check_rows(run, batch, pre, TOL["bf16"], limit=96)
+    _check_rows(run, batch, cross, TOL["bf16"], limit=96)
+    # second pass, every query reversed: all prefix/fragment pages hit
+    rev = [W.Query(prefix=q.prefix, frags=q.frags[::-1], cross=q.cross) for q in batch]
+    p2 = run.run_batch(rev)
+    assert p2.stats()["tokens_new"] == 0
+    _, cross2 = p2.rows()
+    _check_rows(run, rev, cross2, TOL["bf16"], limit=96)
+    run.close()
+
+
+def test_c3_full_size_sampled():
+    wl = W.config_c3()
+    run = GpuRun(wl)
+    batch = wl.batches[0]
+    plan = run.run_batch(batch)
+    pre, cross = plan.rows()
+    _check_rows(run, batch, pre, TOL["bf16"], limit=64)
+    _check_rows(run, batch, cross, TOL["bf16"], limit=64)
+    run.close()

@@ -1,0 +1,193 @@
+"""The C-ABI library on the CPU: exported symbols, hashing and planning.
+
+No GPU: pools are host-only (device = -1), so only hashing, lookup, planning,
+commit and eviction run.  Page ids, hit counts and eviction lists must equal
+the oracle's replay bit for bit.
+"""
+import ctypes
+import os
+import random
+import re
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+
+from oracle import hashing as OH
+from oracle.pool import PoolFull, PoolReplay
+
+spanq = pytest.importorskip("paper_2511_02749_amd")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    try:
+        return spanq.load()
+    except FileNotFoundError:
+        pytest.skip("libspanq.so not built")
+
+
+def test_every_declared_symbol_is_exported(lib):
+    header = open(os.path.join(ROOT, "include", "spanq.h")).read()
+    header = re.sub(r"/\*.*?\*/", "", header, flags=re.S)
+    names = set(re.findall(r"^\s*(?:int|uint64_t|const char\*)\s+(\w+)\s*\(", header, flags=re.M))
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(spanq._lib.EXPORTS) == names
+
+
+def test_hash_matches_oracle(lib):
+    rnd = np.random.default_rng(0)
+    assert spanq.hash_mix(0) == OH.splitmix64(0)
+    for n in [0, 1, 15, 16, 17, 33, 100]:
+        toks = rnd.integers(-2**31, 2**31 - 1, size=n).astype(np.int32)
+        for seed in [OH.ROOT_SEED, 12345, 2**64 - 1]:
+            for partial in [True, False]:
+                got = spanq.hash_pages(seed, toks, 16, partial)
+                want = OH.chain(seed, [int(t) for t in toks], 16, include_partial=partial)
+                assert got == want
+    assert spanq.SPAN_HASH_ROOT == OH.ROOT_SEED and spanq.SPAN_HASH_FRAG_TAG == OH.FRAG_TAG
+
+
+def _span(tokens, row=0):
+    return SimpleNamespace(tokens=np.asarray(tokens, np.int32), row=row)
+
+
+def _q(prefix, frags, cross):
+    return SimpleNamespace(prefix=_span(prefix), frags=[_span(f) for f in frags], cross=_span(cross))
+
+
+def _compare(plan, res, queries):
+    for qi, (pre, frags, cross) in enumerate(queries):
+        qr = res.queries[qi]
+        ids, nh = plan.block_table(qi, -1)
+        assert (ids, nh) == (qr.prefix.page_ids, qr.prefix.n_hit)
+        for c in range(len(frags)):
+            ids, nh = plan.block_table(qi, c)
+            assert (ids, nh) == (qr.frags[c].page_ids, qr.frags[c].n_hit)
+        ids, nh = plan.block_table(qi, len(frags))
+        assert ids == qr.cross.page_ids and nh == 0
+    assert plan.evicted() == res.evicted
+
+
+def test_paper_chat_example(lib):
+    HELLO, HOW, ARE, YOU, Q, I, AM, FINE = range(1, 9)
+    pool = spanq.Pool(num_q_heads=1, num_kv_heads=1, head_dim=64, num_pages=16, page_size=2, device=-1,
+                      hash_mode="stock", dtype="f32")
+    p1 = pool.plan([_q([HELLO, HOW, ARE, YOU, Q], [], [])])
+    p1.commit()
+    assert pool.info()["cached_pages"] == 2
+    p2 = pool.plan([_q([HELLO, HOW, ARE, YOU, Q, I, AM, FINE], [], [])])
+    ids, nh = p2.block_table(0, -1)
+    assert nh * 2 == 4                              # 4 of 5 context tokens hit (80%)
+    assert ids[:2] == p1.block_table(0, -1)[0][:2]
+    hashes = spanq.hash_pages(spanq.SPAN_HASH_ROOT, [HELLO, HOW, ARE, YOU, Q, I, AM, FINE], 2, False)
+    looked, lead = pool.lookup(hashes)
+    assert lead == 2 and looked[2:] == [-1, -1]
+    p1.destroy(); p2.destroy(); pool.close()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_planner_matches_oracle_replay(lib, seed):
+    rnd = random.Random(100 + seed)
+    ps = 16
+    vocab = 40 if seed % 2 else 128256   # small vocab: many equal pages, exercises verification/dedup
+    prefixes = [[rnd.randrange(vocab) for _ in range(rnd.randrange(0, 40))] for _ in range(3)]
+    frags = [[rnd.randrange(vocab) for _ in range(rnd.randrange(1, 70))] for _ in range(10)]
+    num_pages = rnd.randrange(12, 60)
+    pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=num_pages, device=-1, dtype="f32")
+    ref = PoolReplay(num_pages=num_pages, page_size=ps)
+    live = []
+    for step in range(60):
+        qs = []
+        for _ in range(rnd.randrange(1, 4)):
+            chosen = rnd.sample(range(10), rnd.randrange(0, 5))
+            if rnd.random() < 0.2 and chosen:
+                chosen.append(chosen[0])          # the same fragment twice in one query
+            qs.append((prefixes[rnd.randrange(3)], [frags[i] for i in chosen],
+                       [rnd.randrange(vocab) for _ in range(rnd.randrange(0, 40))]))
+        try:
+            res = ref.plan(qs)
+        except PoolFull:
+            with pytest.raises(spanq.SpanError) as ei:
+                pool.plan([_q(*x) for x in qs])
+            assert ei.value.code == -2
+            continue
+        plan = pool.plan([_q(*x) for x in qs])
+        _compare(plan, res, qs)
+        info = pool.info()
+        assert info["tick"] == ref.tick
+        live.append((plan, res))
+        # retire plans in a random order, mostly by commit
+        while live and (len(live) > 2 or rnd.random() < 0.6):
+            p, r = live.pop(rnd.randrange(len(live)))
+            if rnd.random() < 0.85:
+                p.commit(); ref.commit(r)
+            else:
+                ref.destroy(r)
+            p.destroy()
+            info = pool.info()
+            assert info["free_pages"] == len(ref.free)
+            assert info["cached_pages"] == len(ref.index)
+    for p, r in live:
+        p.commit(); ref.commit(r); p.destroy()
+    assert pool.info()["cached_pages"] == len(ref.index)
+    pool.close()
+
+
+def test_enomem_leaves_pool_unchanged(lib):
+    pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=4, device=-1, dtype="f32")
+    a = pool.plan([_q(list(range(40)), [], [])])        # 3 pages
+    before = pool.info()
+    with pytest.raises(spanq.SpanError) as ei:
+        pool.plan([_q(list(range(100, 140)), [], [])])
+    assert ei.value.code == -2 and pool.info() == before
+    a.commit(); a.destroy()
+    b = pool.plan([_q(list(range(100, 140)), [], [])])  # evicts the committed pages, tail first
+    assert b.evicted() == [2, 1]
+    b.destroy()
+    pool.reset()
+    assert pool.info()["free_pages"] == 4
+    pool.close()
+
+
+def test_state_errors(lib):
+    pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=8, device=-1, dtype="f32")
+    p = pool.plan([_q([1, 2, 3], [[4, 5]], [6])])
+    with pytest.raises(spanq.SpanError) as ei:
+        pool.reset()
+    assert ei.value.code == -4
+    with pytest.raises(spanq.SpanError) as ei:
+        p.prefill(0, 1, 1, 1, 1)
+    assert ei.value.code == -4                          # host-only pool
+    p.commit()
+    with pytest.raises(spanq.SpanError):
+        p.commit()
+    p.destroy()
+    pool.reset()
+    assert pool.info()["cached_pages"] == 0
+    with pytest.raises(spanq.SpanError) as ei:
+        spanq.Pool(num_q_heads=3, num_kv_heads=2, head_dim=64, num_pages=8, device=-1)
+    assert ei.value.code == -1
+    pool.close()
+
+
+def test_plan_rows_and_pair_counts(lib):
+    pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=64, device=-1, dtype="f32")
+    pre = SimpleNamespace(tokens=np.arange(20, dtype=np.int32), row=0)
+    f0 = SimpleNamespace(tokens=np.arange(100, 137, dtype=np.int32), row=20)
+    f1 = SimpleNamespace(tokens=np.arange(200, 205, dtype=np.int32), row=57)
+    cr = SimpleNamespace(tokens=np.arange(300, 309, dtype=np.int32), row=62)
+    q = SimpleNamespace(prefix=pre, frags=[f1, f0], cross=cr)
+    p = pool.plan([q])
+    s = p.stats()
+    assert s["tokens_new"] == 20 + 37 + 5 and s["tokens_cross"] == 9 and s["tokens_hit"] == 0
+    assert s["pages_new"] == 2 + 3 + 1 and s["pages_cross"] == 1
+    P, L0, L1, Q = 20, 5, 37, 9
+    assert s["prefill_pairs"] == P * (P + 1) // 2 + sum(L * P + L * (L + 1) // 2 for L in (L0, L1))
+    assert s["cross_pairs"] == Q * (P + L0 + L1) + Q * (Q + 1) // 2
+    p.destroy()
+    pool.close()
