@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Span-prefill attention throughput and cache-hit TTFT on one MI355X.
+
+Workload (default): one Llama-3-8B-shaped attention layer in bf16 (32 query
+heads, 8 kv heads, head_dim 128, hidden 4096, random weights N(0, 0.02^2)),
+a 256-token shared prefix, a pool of 64 fragments x 512 tokens, 8 queries each
+drawing 16 fragments in random order, a 128-token cross segment (question) per
+query.  Synthetic, seeded inputs (no dataset, no trained weights).
+
+A timed step is one cold batch through the whole hot path: pool reset, span
+planning (hashing, lookup, dedup, allocation), page writes, span-prefill
+attention, cross attention with repositioning, KV-split merge and commit.
+q/k/v of every row are resident in HBM before timing starts.
+
+Printed JSON (last stdout line):
+  value      algorithmic attention TFLOP/s of the cold batch step
+             (4 * head_dim * q_heads * allowed (query, key) pairs / step time)
+  ttft       single-query time to first token of the attention layer (plan call to
+             stream sync after cross attention): cold, warm (all fragments cached, new
+             order) and a dense causal run of the same sequence, p50/p99
+  roofline   span-prefill attention kernel: algorithmic FLOPs per launch / mean launch
+             duration (HIP events on the launch stream) against the bf16 dense MFMA peak
+  cpu_baseline  the float64 oracle on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "span-prefill attention TFLOP/s + cache-hit TTFT (ms), 16×512-tok fragments"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def _pct(xs, p):
+    import numpy as np
+    return float(np.percentile(np.asarray(xs), p)) if xs else None
+
+
+def _flops(wl, pairs):
+    return 4.0 * wl.head_dim * wl.n_q_heads * pairs
+
+
+def cpu_baseline(wl, query, seconds):
+    """The oracle timed on this host's cores over sampled rows of one query."""
+    import numpy as np
+
+    from oracle import attention as OA
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    lay = OA.layout(query.prefix.n, [f.n for f in query.frags], query.cross.n)
+    rows = np.concatenate([np.arange(query.prefix.row, query.prefix.row + query.prefix.n)] +
+                          [np.arange(f.row, f.row + f.n) for f in query.frags] +
+                          [np.arange(query.cross.row, query.cross.row + query.cross.n)])
+    q, k, v = wl.q[rows], wl.k[rows], wl.v[rows]
+    rng = np.random.default_rng(0)
+    order = rng.permutation(lay.n)
+    done, pairs = 0, 0
+    t0 = time.perf_counter()
+    while done < lay.n and time.perf_counter() - t0 < seconds:
+        sel = np.sort(order[done: done + 64])
+        OA.attention_rows(q, k, v, lay, sel, wl.rope_theta)
+        pairs += int(OA.mask_rows(lay, sel).sum())
+        done += sel.size
+    dt = time.perf_counter() - t0
+    return {"value": _flops(wl, pairs) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{done} random rows of one query ({lay.n} tokens), float64, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c2", choices=["c2", "c3"])
+    ap.add_argument("--kernel", default="auto", choices=["auto", "generic", "mfma"])
+    ap.add_argument("--ttft-reps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the span-query path here is a single-GPU build "
+              "(no sharding or collectives); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2511_02749_amd as spanq
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    wl = W.config_c2() if args.config == "c2" else W.config_c3()
+    batch = wl.batches[0]
+    print(f"[bench] workload {wl.name}: {wl.rows} rows generated in {time.perf_counter() - t_gen:.1f} s",
+          file=sys.stderr, flush=True)
+    qa, ka, va = wl.device_arrays()
+    q, k, v = (torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda() for a in (qa, ka, va))
+    out = torch.zeros_like(q)
+    per_query_pages = max((qq.prefix.n + 15) // 16 + sum((f.n + 15) // 16 for f in qq.frags) +
+                          (qq.cross.n + 15) // 16 for qq in batch)
+    distinct_pages = sum((s.n + 15) // 16 for s in {id(x): x for qq in batch for x in [qq.prefix, *qq.frags]}.values())
+    num_pages = distinct_pages + len(batch) * 64 + 4 * per_query_pages
+    pool = spanq.Pool(num_q_heads=wl.n_q_heads, num_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                      num_pages=num_pages, dtype=wl.dtype, rope_theta=wl.rope_theta, kernel=args.kernel,
+                      timing=True, device=0)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pool.reset()
+        plan = pool.plan(batch, stream)
+        plan.prefill(0, q, k, v, out)
+        plan.cross(0, q, k, v, out)
+        plan.commit()
+        return plan
+
+    for _ in range(args.warmup):
+        step().destroy()
+    torch.cuda.synchronize()
+    plans = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        plans.append(step())
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = plans[0].stats()
+    times = [p.kernel_times() for p in plans]
+    for p in plans:
+        p.destroy()
+    ms_step = wall * 1e3 / args.steps
+    flops_step = _flops(wl, st["prefill_pairs"] + st["cross_pairs"])
+    k1_flops = _flops(wl, st["prefill_pairs"])
+    k2_flops = _flops(wl, st["cross_pairs"])
+    mean = {n: float(np.mean([t[n] for t in times])) for n in spanq._lib.TIME_FIELDS}
+    k1_tflops = k1_flops / (mean["prefill_attention_ms"] * 1e-3) / 1e12
+    k2_tflops = k2_flops / (mean["cross_attention_ms"] * 1e-3) / 1e12
+    kv_bytes_page = 2 * wl.n_kv_heads * 16 * wl.head_dim * 2
+    print(f"[bench] step {ms_step:.3f} ms; K1 {mean['prefill_attention_ms']:.3f} ms {k1_tflops:.1f} TFLOP/s; "
+          f"K2 {mean['cross_attention_ms']:.3f} ms {k2_tflops:.1f} TFLOP/s", file=sys.stderr, flush=True)
+
+    # ---------------- single-query TTFT: cold, warm (cached fragments, new order), dense causal
+    ttft = {}
+    if args.ttft_reps > 0:
+        q0 = batch[0]
+        rev = W.Query(prefix=q0.prefix, frags=q0.frags[::-1], cross=q0.cross)
+
+        def one(query, qq, kk, vv, oo):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            p = pool.plan([query], stream)
+            p.prefill(0, qq, kk, vv, oo)
+            p.cross(0, qq, kk, vv, oo)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t) * 1e3
+            p.commit()
+            p.destroy()
+            return dt
+
+        cold, warm, dense = [], [], []
+        for _ in range(args.ttft_reps + 2):
+            pool.reset()
+            cold.append(one(q0, q, k, v, out))
+            warm.append(one(rev, q, k, v, out))
+        rows = np.concatenate([np.arange(s.row, s.row + s.n) for s in [q0.prefix, *q0.frags, q0.cross]])
+        ridx = torch.as_tensor(rows, device="cuda")
+        qd, kd, vd = q[ridx].contiguous(), k[ridx].contiguous(), v[ridx].contiguous()
+        od = torch.zeros_like(qd)
+        toks = np.concatenate([s.tokens for s in [q0.prefix, *q0.frags, q0.cross]])
+        whole = W.Query(prefix=W.Span(tokens=toks, row=0), frags=[], cross=W.Span(tokens=toks[:0], row=0))
+        for _ in range(max(3, args.ttft_reps // 4) + 1):
+            pool.reset()
+            dense.append(one(whole, qd, kd, vd, od))
+        cold, warm, dense = cold[2:], warm[2:], dense[1:]
+        ttft = {"cold_ms_p50": _pct(cold, 50), "cold_ms_p99": _pct(cold, 99), "warm_ms_p50": _pct(warm, 50),
+                "warm_ms_p99": _pct(warm, 99), "dense_causal_ms_p50": _pct(dense, 50),
+                "warm_speedup_vs_cold": _pct(cold, 50) / _pct(warm, 50),
+                "warm_speedup_vs_dense": _pct(dense, 50) / _pct(warm, 50), "reps": len(cold),
+                "query": f"prefix {q0.prefix.n} + {len(q0.frags)} x {q0.frags[0].n} + cross {q0.cross.n}"}
+        print(f"[bench] ttft {json.dumps(ttft)}", file=sys.stderr, flush=True)
+    pool.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, batch[0], args.cpu_seconds)
+        print(f"[bench] cpu baseline {json.dumps(cpu)}", file=sys.stderr, flush=True)
+
+    result = {
+        "metric": METRIC,
+        "value": flops_step / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded tokens, random-init projection weights)",
+        "config": {
+            "workload": ("C2 span-query batch: Llama-3-8B-shaped attention layer (32/8 heads, d 128, hidden 4096), "
+                         "prefix 256 + 16 of 64 fragments x 512 in random order + cross 128, 8 queries, cold"
+                         if args.config == "c2" else
+                         "C3 judge pattern: prompt 2048 + 32 candidates x 256 + judge 256, one query, cold"),
+            "queries": len(batch),
+            "tokens_new": st["tokens_new"],
+            "tokens_cross": st["tokens_cross"],
+            "allowed_pairs": st["prefill_pairs"] + st["cross_pairs"],
+            "kernel": args.kernel,
+        },
+        "kernels": {
+            "span_prefill_attention": {"ms": mean["prefill_attention_ms"], "tflops": k1_tflops},
+            "cross_attention": {"ms": mean["cross_attention_ms"], "tflops": k2_tflops,
+                                "kv_splits": st["kv_splits"]},
+            "page_write_prefill": {"ms": mean["page_write_prefill_ms"],
+                                   "gbs": (st["pages_new"] * kv_bytes_page * 2) / (mean["page_write_prefill_ms"] * 1e-3) / 1e9
+                                   if mean["page_write_prefill_ms"] > 0 else None},
+            "page_write_cross_ms": mean["page_write_cross_ms"],
+            "combine_ms": mean["combine_ms"],
+        },
+        "roofline": {"kernel": "span_prefill_attention", "bound": "mfma", "achieved": k1_tflops,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": k1_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": None},
+        "ttft": ttft,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -72,6 +72,8 @@ extern "C" {
 #define SPAN_KERNEL_GENERIC 1 /* vector-ALU kernel, any supported shape / dtype */
 #define SPAN_KERNEL_MFMA 2    /* bf16 MFMA kernel (SPAN_EINVAL if the shape does not fit) */
 
+#define SPAN_FLAG_TIMING 1    /* bracket every kernel launch with HIP events (span_plan_kernel_times) */
+
 typedef struct span_pool span_pool;
 typedef struct span_plan span_plan;
 
@@ -86,7 +88,7 @@ typedef struct {
   int32_t kernel;       /* SPAN_KERNEL_* */
   int32_t device;       /* HIP device ordinal, or -1 for a host-only pool (no device
                            memory: planning and lookup only) */
-  int32_t reserved;
+  int32_t flags;        /* SPAN_FLAG_* */
   float rope_theta;
   int64_t num_pages;    /* pages per layer */
   void* device_buf;     /* optional caller-owned device buffer of span_pool_bytes();
@@ -108,7 +110,7 @@ int span_pool_create(const span_pool_config* cfg, span_pool** out);
 int span_pool_destroy(span_pool* pool);
 
 /* Forget every cached page (all pages free, LRU clock unchanged).  SPAN_ESTATE if
- * a plan is alive. */
+ * an uncommitted plan is alive (committed plans hold no pages). */
 int span_pool_reset(span_pool* pool);
 
 typedef struct {
@@ -245,6 +247,20 @@ int span_plan_commit(span_plan* plan);
 int span_plan_destroy(span_plan* plan);
 
 /* ---------------------------------------------------------------- debug */
+
+/* Kernel durations of a plan's launches on a pool created with SPAN_FLAG_TIMING,
+ * measured with HIP events recorded on the launch stream, summed over every layer
+ * call so far; launches counts the attention calls timed.  Waits for the events. */
+typedef struct {
+  float page_write_prefill_ms;  /* K3 over new prefix/fragment pages */
+  float prefill_attention_ms;   /* span-prefill attention */
+  float page_write_cross_ms;    /* K3 over cross pages */
+  float cross_attention_ms;     /* cross attention (all KV splits) */
+  float combine_ms;             /* KV-split merge */
+  int32_t prefill_calls;
+  int32_t cross_calls;
+} span_kernel_times;
+int span_plan_kernel_times(const span_plan* plan, span_kernel_times* times);
 
 const char* span_last_error(void);
 

@@ -27,8 +27,9 @@ EXPORTS = [
     "span_pool_reset", "span_pool_get_info", "span_pool_page_address", "span_pool_read_page",
     "span_hash_pages", "kv_lookup", "span_plan_create", "span_plan_stats", "span_plan_block_table",
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
-    "span_plan_commit", "span_plan_destroy",
+    "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times",
 ]
+SPAN_FLAG_TIMING = 1
 
 
 class SpanError(RuntimeError):
@@ -41,7 +42,7 @@ class PoolConfig(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("hash_mode", ctypes.c_int32), ("kernel", ctypes.c_int32), ("device", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("num_pages", ctypes.c_int64),
+                ("flags", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("num_pages", ctypes.c_int64),
                 ("device_buf", ctypes.c_void_p), ("device_bytes", ctypes.c_size_t)]
 
 
@@ -66,6 +67,15 @@ STAT_FIELDS = ("pages_hit", "pages_new", "pages_cross", "pages_evicted", "tokens
 
 class SpanStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS]
+
+
+TIME_FIELDS = ("page_write_prefill_ms", "prefill_attention_ms", "page_write_cross_ms", "cross_attention_ms",
+               "combine_ms")
+
+
+class KernelTimes(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in TIME_FIELDS] + [("prefill_calls", ctypes.c_int32),
+                                                            ("cross_calls", ctypes.c_int32)]
 
 
 _LIB = None
@@ -106,6 +116,7 @@ def load():
         "span_cross_attend": (I32, [VP, I32, VP, VP, VP, VP, VP]),
         "span_plan_commit": (I32, [VP]),
         "span_plan_destroy": (I32, [VP]),
+        "span_plan_kernel_times": (I32, [VP, P(KernelTimes)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -161,13 +172,14 @@ class Pool:
 
     def __init__(self, *, num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str = "bf16",
                  num_layers: int = 1, rope_theta: float = 1e4, page_size: int = 16, device: int = 0,
-                 hash_mode: str = "span", kernel: str = "auto"):
+                 hash_mode: str = "span", kernel: str = "auto", timing: bool = False):
         lib = load()
         self.cfg = PoolConfig(num_layers=num_layers, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                               head_dim=head_dim, page_size=page_size,
                               dtype=SPAN_BF16 if dtype == "bf16" else SPAN_F32,
                               hash_mode=SPAN_HASH_STOCK if hash_mode == "stock" else SPAN_HASH_SPAN,
-                              kernel=SPAN_KERNEL[kernel], device=device, reserved=0, rope_theta=rope_theta,
+                              kernel=SPAN_KERNEL[kernel], device=device,
+                              flags=SPAN_FLAG_TIMING if timing else 0, rope_theta=rope_theta,
                               num_pages=num_pages, device_buf=None, device_bytes=0)
         self.dtype = dtype
         self._plans = weakref.WeakSet()
@@ -284,6 +296,13 @@ class Plan:
     def cross(self, layer: int, q, k, v, out, stream=None):
         _check(load().span_cross_attend(self._h, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                         _stream(stream) if stream is not None else self._stream))
+
+    def kernel_times(self) -> dict:
+        t = KernelTimes()
+        _check(load().span_plan_kernel_times(self._h, ctypes.byref(t)))
+        d = {n: float(getattr(t, n)) for n in TIME_FIELDS}
+        d["prefill_calls"], d["cross_calls"] = int(t.prefill_calls), int(t.cross_calls)
+        return d
 
     def commit(self):
         _check(load().span_plan_commit(self._h))

@@ -61,7 +61,32 @@ struct span_plan {
   int bm = kGenericBM;
   bool mfma = false;
   bool committed = false;
+  // timing: groups of events recorded around each launch (SPAN_FLAG_TIMING)
+  std::vector<std::vector<hipEvent_t>> ev_prefill, ev_cross;
 };
+
+namespace {
+// Records n+1 events around n launches; returns an empty vector if timing is off.
+struct Timer {
+  std::vector<hipEvent_t> ev;
+  hipStream_t s;
+  Timer(bool on, int n, hipStream_t st) : s(st) {
+    if (!on) return;
+    ev.resize(n + 1, nullptr);
+    for (auto& e : ev)
+      if (hipEventCreate(&e) != hipSuccess) e = nullptr;
+  }
+  void mark(int i) {
+    if (!ev.empty() && ev[i]) (void)hipEventRecord(ev[i], s);
+  }
+};
+void destroy_events(std::vector<std::vector<hipEvent_t>>& groups) {
+  for (auto& g : groups)
+    for (auto e : g)
+      if (e) (void)hipEventDestroy(e);
+  groups.clear();
+}
+}  // namespace
 
 static int check_span(const span_tokens& s, const char* what) {
   if (s.n < 0 || (s.n > 0 && !s.tokens)) return fail(SPAN_EINVAL, std::string("span_plan_create: bad ") + what);
@@ -169,7 +194,8 @@ int span_pool_destroy(span_pool* p) {
 
 int span_pool_reset(span_pool* p) {
   if (!p) return fail(SPAN_EINVAL, "span_pool_reset: null pool");
-  if (!p->plans.empty()) return fail(SPAN_ESTATE, "span_pool_reset: plans are alive");
+  for (const span_plan* pl : p->plans)
+    if (!pl->committed) return fail(SPAN_ESTATE, "span_pool_reset: an uncommitted plan is alive");
   p->index->reset();
   return SPAN_OK;
 }
@@ -395,12 +421,17 @@ int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const vo
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_prefill_fragments: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
   PoolGeom g = geom(pl, layer);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 2, s);
+  tm.mark(0);
   hipError_t e = launch_rope_write(g, pl->k3p, static_cast<int>(P.k3_prefill.size()), k, v, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
+  tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
   e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s)
                : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
+  tm.mark(2);
+  if (!tm.ev.empty()) pl->ev_prefill.push_back(tm.ev);
   return SPAN_OK;
 }
 
@@ -413,16 +444,45 @@ int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_cross_attend: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
   PoolGeom g = geom(pl, layer);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s);
+  tm.mark(0);
   hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
+  tm.mark(1);
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
   e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s)
                : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
+  tm.mark(2);
   e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: combine");
+  tm.mark(3);
+  if (!tm.ev.empty()) pl->ev_cross.push_back(tm.ev);
+  return SPAN_OK;
+}
+
+static float elapsed(hipEvent_t a, hipEvent_t b) {
+  float ms = 0.f;
+  if (!a || !b || hipEventSynchronize(b) != hipSuccess || hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.f;
+  return ms;
+}
+
+int span_plan_kernel_times(const span_plan* pl, span_kernel_times* t) {
+  if (!pl || !t) return fail(SPAN_EINVAL, "span_plan_kernel_times: null argument");
+  std::memset(t, 0, sizeof(*t));
+  for (const auto& ev : pl->ev_prefill) {
+    t->page_write_prefill_ms += elapsed(ev[0], ev[1]);
+    t->prefill_attention_ms += elapsed(ev[1], ev[2]);
+    t->prefill_calls += 1;
+  }
+  for (const auto& ev : pl->ev_cross) {
+    t->page_write_cross_ms += elapsed(ev[0], ev[1]);
+    t->cross_attention_ms += elapsed(ev[1], ev[2]);
+    t->combine_ms += elapsed(ev[2], ev[3]);
+    t->cross_calls += 1;
+  }
   return SPAN_OK;
 }
 
@@ -437,6 +497,8 @@ int span_plan_commit(span_plan* pl) {
 int span_plan_destroy(span_plan* pl) {
   if (!pl) return fail(SPAN_EINVAL, "span_plan_destroy: null plan");
   if (!pl->committed) pl->pool->index->release(&pl->plan);
+  destroy_events(pl->ev_prefill);
+  destroy_events(pl->ev_cross);
   if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
   if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
   pl->pool->plans.erase(pl);
