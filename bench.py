@@ -135,6 +135,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = plans[0].stats()
+    host_plan_us = float(np.mean([p.stats()["host_plan_us"] for p in plans]))
+    host_upload_us = float(np.mean([p.stats()["host_upload_us"] for p in plans]))
     times = [p.kernel_times() for p in plans]
     for p in plans:
         p.destroy()
@@ -147,7 +149,8 @@ def main():
     k2_tflops = k2_flops / (mean["cross_attention_ms"] * 1e-3) / 1e12
     kv_bytes_page = 2 * wl.n_kv_heads * 16 * wl.head_dim * 2
     print(f"[bench] step {ms_step:.3f} ms; K1 {mean['prefill_attention_ms']:.3f} ms {k1_tflops:.1f} TFLOP/s; "
-          f"K2 {mean['cross_attention_ms']:.3f} ms {k2_tflops:.1f} TFLOP/s", file=sys.stderr, flush=True)
+          f"K2 {mean['cross_attention_ms']:.3f} ms {k2_tflops:.1f} TFLOP/s; combine {mean['combine_ms']:.3f} ms; "
+          f"host plan {host_plan_us:.0f} us upload {host_upload_us:.0f} us", file=sys.stderr, flush=True)
 
     # ---------------- single-query TTFT: cold, warm (cached fragments, new order), dense causal
     ttft = {}
@@ -155,7 +158,9 @@ def main():
         q0 = batch[0]
         rev = W.Query(prefix=q0.prefix, frags=q0.frags[::-1], cross=q0.cross)
 
-        def one(query, qq, kk, vv, oo):
+        host = {"cold": [], "warm": [], "dense": []}
+
+        def one(query, qq, kk, vv, oo, kind):
             torch.cuda.synchronize()
             t = time.perf_counter()
             p = pool.plan([query], stream)
@@ -164,14 +169,19 @@ def main():
             torch.cuda.synchronize()
             dt = (time.perf_counter() - t) * 1e3
             p.commit()
+            s1 = p.stats()
+            kt = p.kernel_times()
+            host[kind].append((s1["host_plan_us"], s1["host_upload_us"],
+                               kt["prefill_attention_ms"] + kt["page_write_prefill_ms"],
+                               kt["cross_attention_ms"] + kt["page_write_cross_ms"] + kt["combine_ms"]))
             p.destroy()
             return dt
 
         cold, warm, dense = [], [], []
         for _ in range(args.ttft_reps + 2):
             pool.reset()
-            cold.append(one(q0, q, k, v, out))
-            warm.append(one(rev, q, k, v, out))
+            cold.append(one(q0, q, k, v, out, "cold"))
+            warm.append(one(rev, q, k, v, out, "warm"))
         rows = np.concatenate([np.arange(s.row, s.row + s.n) for s in [q0.prefix, *q0.frags, q0.cross]])
         ridx = torch.as_tensor(rows, device="cuda")
         qd, kd, vd = q[ridx].contiguous(), k[ridx].contiguous(), v[ridx].contiguous()
@@ -180,13 +190,17 @@ def main():
         whole = W.Query(prefix=W.Span(tokens=toks, row=0), frags=[], cross=W.Span(tokens=toks[:0], row=0))
         for _ in range(max(3, args.ttft_reps // 4) + 1):
             pool.reset()
-            dense.append(one(whole, qd, kd, vd, od))
+            dense.append(one(whole, qd, kd, vd, od, "dense"))
         cold, warm, dense = cold[2:], warm[2:], dense[1:]
         ttft = {"cold_ms_p50": _pct(cold, 50), "cold_ms_p99": _pct(cold, 99), "warm_ms_p50": _pct(warm, 50),
                 "warm_ms_p99": _pct(warm, 99), "dense_causal_ms_p50": _pct(dense, 50),
                 "warm_speedup_vs_cold": _pct(cold, 50) / _pct(warm, 50),
                 "warm_speedup_vs_dense": _pct(dense, 50) / _pct(warm, 50), "reps": len(cold),
-                "query": f"prefix {q0.prefix.n} + {len(q0.frags)} x {q0.frags[0].n} + cross {q0.cross.n}"}
+                "query": f"prefix {q0.prefix.n} + {len(q0.frags)} x {q0.frags[0].n} + cross {q0.cross.n}",
+                "breakdown_us": {kind: dict(zip(("host_plan", "host_upload", "prefill_gpu", "cross_gpu"),
+                                                [float(np.median([x[i] for x in v])) * (1 if i < 2 else 1e3)
+                                                 for i in range(4)]))
+                                 for kind, v in host.items() if v}}
         print(f"[bench] ttft {json.dumps(ttft)}", file=sys.stderr, flush=True)
     pool.close()
 
@@ -228,6 +242,8 @@ def main():
                                    if mean["page_write_prefill_ms"] > 0 else None},
             "page_write_cross_ms": mean["page_write_cross_ms"],
             "combine_ms": mean["combine_ms"],
+            "host_plan_us": host_plan_us,
+            "host_upload_us": host_upload_us,
         },
         "roofline": {"kernel": "span_prefill_attention", "bound": "mfma", "achieved": k1_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": k1_tflops / PEAK_BF16_TFLOPS,

@@ -70,7 +70,8 @@ extern "C" {
 
 #define SPAN_KERNEL_AUTO 0    /* bf16 MFMA kernel where the shape allows, else generic */
 #define SPAN_KERNEL_GENERIC 1 /* vector-ALU kernel, any supported shape / dtype */
-#define SPAN_KERNEL_MFMA 2    /* bf16 MFMA kernel (SPAN_EINVAL if the shape does not fit) */
+#define SPAN_KERNEL_MFMA 2    /* bf16 MFMA kernel: bf16 pools, head_dim 64 or 128, num_q_heads /
+                                 num_kv_heads in {1, 2, 4} (SPAN_EINVAL otherwise) */
 
 #define SPAN_FLAG_TIMING 1    /* bracket every kernel launch with HIP events (span_plan_kernel_times) */
 
@@ -200,6 +201,8 @@ typedef struct {
   int64_t cross_tiles;      /* work items including KV splits */
   int64_t kv_splits;        /* KV splits per cross row tile */
   int64_t cross_kv_pages;   /* page reads of the cross pass per kv head */
+  double host_plan_us;      /* host time of hashing, lookup, allocation and work lists */
+  double host_upload_us;    /* host time of device metadata allocation + copy enqueue */
 } span_stats;
 int span_plan_stats(const span_plan* plan, span_stats* stats);
 

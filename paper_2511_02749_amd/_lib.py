@@ -52,7 +52,7 @@ class PoolInfo(ctypes.Structure):
 
 
 class SpanTokens(ctypes.Structure):
-    _fields_ = [("tokens", ctypes.POINTER(ctypes.c_int32)), ("n", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    _fields_ = [("tokens", ctypes.c_void_p), ("n", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("row", ctypes.c_int64)]
 
 
@@ -66,7 +66,8 @@ STAT_FIELDS = ("pages_hit", "pages_new", "pages_cross", "pages_evicted", "tokens
 
 
 class SpanStats(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS]
+    _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS] + [("host_plan_us", ctypes.c_double),
+                                                            ("host_upload_us", ctypes.c_double)]
 
 
 TIME_FIELDS = ("page_write_prefill_ms", "prefill_attention_ms", "page_write_cross_ms", "cross_attention_ms",
@@ -236,9 +237,11 @@ class Pool:
 
 
 def _span(s, keep: list) -> SpanTokens:
-    t = np.ascontiguousarray(s.tokens, dtype=np.int32)
-    keep.append(t)
-    return SpanTokens(tokens=_i32p(t), n=t.size, reserved=0, row=int(s.row))
+    t = s.tokens
+    if not (isinstance(t, np.ndarray) and t.dtype == np.int32 and t.flags.c_contiguous):
+        t = np.ascontiguousarray(t, dtype=np.int32)
+        keep.append(t)
+    return SpanTokens(t.ctypes.data if t.size else None, t.size, 0, int(s.row))
 
 
 class Plan:
@@ -262,7 +265,9 @@ class Plan:
     def stats(self) -> dict:
         s = SpanStats()
         _check(load().span_plan_stats(self._h, ctypes.byref(s)))
-        return {n: int(getattr(s, n)) for n in STAT_FIELDS}
+        d = {n: int(getattr(s, n)) for n in STAT_FIELDS}
+        d["host_plan_us"], d["host_upload_us"] = float(s.host_plan_us), float(s.host_upload_us)
+        return d
 
     def block_table(self, query: int, span: int):
         """span: -1 prefix, 0..n-1 fragment children, n cross.  Returns (page ids, n_hit)."""

@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -40,6 +41,7 @@ struct span_pool {
   bool owns_dev = false;
   bool use_mfma = false;
   std::set<span_plan*> plans;
+  std::vector<hipEvent_t> event_cache;  // reusable timing events
 };
 
 struct span_plan {
@@ -61,6 +63,8 @@ struct span_plan {
   int bm = kGenericBM;
   bool mfma = false;
   bool committed = false;
+  double host_plan_us = 0.0;    // hashing, lookup, allocation, work lists
+  double host_upload_us = 0.0;  // device metadata allocation and copy enqueue
   // timing: groups of events recorded around each launch (SPAN_FLAG_TIMING)
   std::vector<std::vector<hipEvent_t>> ev_prefill, ev_cross;
 };
@@ -70,20 +74,26 @@ namespace {
 struct Timer {
   std::vector<hipEvent_t> ev;
   hipStream_t s;
-  Timer(bool on, int n, hipStream_t st) : s(st) {
+  Timer(bool on, int n, hipStream_t st, std::vector<hipEvent_t>& cache) : s(st) {
     if (!on) return;
     ev.resize(n + 1, nullptr);
-    for (auto& e : ev)
-      if (hipEventCreate(&e) != hipSuccess) e = nullptr;
+    for (auto& e : ev) {
+      if (!cache.empty()) {
+        e = cache.back();
+        cache.pop_back();
+      } else if (hipEventCreate(&e) != hipSuccess) {
+        e = nullptr;
+      }
+    }
   }
   void mark(int i) {
     if (!ev.empty() && ev[i]) (void)hipEventRecord(ev[i], s);
   }
 };
-void destroy_events(std::vector<std::vector<hipEvent_t>>& groups) {
+void release_events(std::vector<std::vector<hipEvent_t>>& groups, std::vector<hipEvent_t>& cache) {
   for (auto& g : groups)
     for (auto e : g)
-      if (e) (void)hipEventDestroy(e);
+      if (e) cache.push_back(e);
   groups.clear();
 }
 }  // namespace
@@ -164,6 +174,13 @@ int span_pool_create(const span_pool_config* c, span_pool** out) {
       }
       p->owns_dev = true;
     }
+    // Plans take their metadata and split-KV partials from the device's stream-ordered
+    // pool; keep freed blocks cached there instead of returning them at each sync.
+    hipMemPool_t mp = nullptr;
+    if (hipDeviceGetDefaultMemPool(&mp, c->device) == hipSuccess && mp) {
+      uint64_t keep = UINT64_MAX;
+      (void)hipMemPoolSetAttribute(mp, hipMemPoolAttrReleaseThreshold, &keep);
+    }
     p->use_mfma = c->kernel == SPAN_KERNEL_MFMA ||
                   (c->kernel == SPAN_KERNEL_AUTO && mfma_supported(c->num_q_heads, c->num_kv_heads, c->head_dim, c->dtype));
   }
@@ -183,10 +200,9 @@ int span_pool_destroy(span_pool* p) {
   if (!p) return fail(SPAN_EINVAL, "span_pool_destroy: null pool");
   std::vector<span_plan*> live(p->plans.begin(), p->plans.end());
   for (span_plan* pl : live) span_plan_destroy(pl);
-  if (p->owns_dev && p->dev) {
-    (void)hipDeviceSynchronize();
-    (void)hipFree(p->dev);
-  }
+  if (p->cfg.device >= 0) (void)hipDeviceSynchronize();
+  for (hipEvent_t e : p->event_cache) (void)hipEventDestroy(e);
+  if (p->owns_dev && p->dev) (void)hipFree(p->dev);
   delete p->index;
   delete p;
   return SPAN_OK;
@@ -301,8 +317,14 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
   t.bm_prefill = pl->bm;
   t.bm_cross = pl->bm;
   t.kv_heads = pl->mfma ? pool->cfg.num_kv_heads : pool->cfg.num_q_heads;
+  // The MFMA kernel runs one 8-wave work-group per CU: aim the cross launch at one
+  // work-group per CU (256 on MI355X); the generic kernel is latency-bound and wants more.
+  t.target_items = pl->mfma ? 256 : 1024;
   std::string msg;
+  const auto t_plan0 = std::chrono::steady_clock::now();
   int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
+  const auto t_plan1 = std::chrono::steady_clock::now();
+  pl->host_plan_us = std::chrono::duration<double, std::micro>(t_plan1 - t_plan0).count();
   if (rc) {
     delete pl;
     return fail(rc, msg);
@@ -329,6 +351,7 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
       span_plan_destroy(pl);
       return hip_fail(e, "span_plan_create: device metadata");
     }
+    pl->host_upload_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t_plan1).count();
     pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
     pl->k3p = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3p);
     pl->k3c = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3c);
@@ -357,6 +380,8 @@ int span_plan_stats(const span_plan* pl, span_stats* s) {
   s->cross_tiles = static_cast<int64_t>(P.t_cross.size());
   s->kv_splits = P.kv_splits;
   s->cross_kv_pages = P.cross_kv_pages;
+  s->host_plan_us = pl->host_plan_us;
+  s->host_upload_us = pl->host_upload_us;
   return SPAN_OK;
 }
 
@@ -387,13 +412,14 @@ int span_plan_evicted(const span_plan* pl, int32_t* ids, int32_t cap, int32_t* n
 int span_plan_rows(const span_plan* pl, int64_t* rows, int64_t cap, int64_t* n_prefill, int64_t* n_cross) {
   if (!pl || !n_prefill || !n_cross || cap < 0 || (cap > 0 && !rows)) return fail(SPAN_EINVAL, "span_plan_rows: bad argument");
   const Plan& P = pl->plan;
-  *n_prefill = static_cast<int64_t>(P.rows_prefill.size());
-  *n_cross = static_cast<int64_t>(P.rows_cross.size());
+  *n_prefill = 0;
+  *n_cross = 0;
+  for (const auto& rr : P.rows_prefill) *n_prefill += rr.n;
+  for (const auto& rr : P.rows_cross) *n_cross += rr.n;
   int64_t w = 0;
-  for (int64_t r : P.rows_prefill)
-    if (w < cap) rows[w++] = r;
-  for (int64_t r : P.rows_cross)
-    if (w < cap) rows[w++] = r;
+  for (const auto* runs : {&P.rows_prefill, &P.rows_cross})
+    for (const auto& rr : *runs)
+      for (int32_t j = 0; j < rr.n && w < cap; ++j) rows[w++] = rr.row0 + j;
   return SPAN_OK;
 }
 
@@ -421,7 +447,7 @@ int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const vo
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_prefill_fragments: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
   PoolGeom g = geom(pl, layer);
-  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 2, s);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 2, s, pl->pool->event_cache);
   tm.mark(0);
   hipError_t e = launch_rope_write(g, pl->k3p, static_cast<int>(P.k3_prefill.size()), k, v, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
@@ -444,7 +470,7 @@ int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_cross_attend: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
   PoolGeom g = geom(pl, layer);
-  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s, pl->pool->event_cache);
   tm.mark(0);
   hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->inv_freq, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
@@ -497,8 +523,8 @@ int span_plan_commit(span_plan* pl) {
 int span_plan_destroy(span_plan* pl) {
   if (!pl) return fail(SPAN_EINVAL, "span_plan_destroy: null plan");
   if (!pl->committed) pl->pool->index->release(&pl->plan);
-  destroy_events(pl->ev_prefill);
-  destroy_events(pl->ev_cross);
+  release_events(pl->ev_prefill, pl->pool->event_cache);
+  release_events(pl->ev_cross, pl->pool->event_cache);
   if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
   if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
   pl->pool->plans.erase(pl);

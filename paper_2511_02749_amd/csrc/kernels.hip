@@ -210,7 +210,8 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, 
 }
 
 // ------------------------------------------------------------------ K4 combine
-// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.
+// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.  One
+// work-group per (tile, query head); a thread merges 8 consecutive dims of a row.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restrict__ tiles,
                                                       const float* __restrict__ part_o,
@@ -218,13 +219,17 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restr
                                                       T* __restrict__ out) {
   const CombineTile t = tiles[blockIdx.x];
   const int h = blockIdx.y;
-  for (int e = threadIdx.x; e < t.n_rows * D; e += blockDim.x) {
-    const int r = e / D;
-    const int i = e - r * D;
+  constexpr int C8 = D / 8;
+  for (int e = threadIdx.x; e < t.n_rows * C8; e += blockDim.x) {
+    const int r = e / C8;
+    const int c = e - r * C8;
     float M = -INFINITY;
     for (int p = 0; p < t.n_parts; ++p)
       M = fmaxf(M, part_ml[((static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r) * 2]);
-    float L = 0.f, O = 0.f;
+    float L = 0.f;
+    float acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
     if (M != -INFINITY) {
       for (int p = 0; p < t.n_parts; ++p) {
         const int64_t slot = (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r;
@@ -232,10 +237,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restr
         if (mp == -INFINITY) continue;
         const float w = exp2f(mp - M);
         L += part_ml[slot * 2 + 1] * w;
-        O += part_o[slot * D + i] * w;
+        const float4 a = *reinterpret_cast<const float4*>(part_o + slot * D + 8 * c);
+        const float4 b = *reinterpret_cast<const float4*>(part_o + slot * D + 8 * c + 4);
+        acc[0] += a.x * w; acc[1] += a.y * w; acc[2] += a.z * w; acc[3] += a.w * w;
+        acc[4] += b.x * w; acc[5] += b.y * w; acc[6] += b.z * w; acc[7] += b.w * w;
       }
     }
-    out[(static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + i] = from_f32<T>(L > 0.f ? O / L : 0.f);
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    T* dst = out + (static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + 8 * c;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dst[i] = from_f32<T>(acc[i] * inv);
   }
 }
 

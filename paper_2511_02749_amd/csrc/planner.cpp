@@ -36,22 +36,22 @@ PoolIndex::PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode)
     : num_pages_(num_pages), page_size_(page_size), hash_mode_(hash_mode) {
   pages_.resize(static_cast<size_t>(num_pages));
   page_tokens_.resize(static_cast<size_t>(num_pages) * page_size);
+  index_.reserve(static_cast<size_t>(std::min<int64_t>(num_pages, 1 << 20)));
   reset();
 }
 
 void PoolIndex::reset() {
+  // Records of ids >= watermark_ are rewritten when they are allocated again.
+  for (int64_t i = 0; i < watermark_; ++i) pages_[i] = PageRec{};
   index_.clear();
   evictable_.clear();
-  free_.clear();
-  for (int64_t i = 0; i < num_pages_; ++i) {
-    pages_[i] = PageRec{};
-    free_.insert(free_.end(), static_cast<int32_t>(i));
-  }
+  freed_.clear();
+  watermark_ = 0;
 }
 
 int64_t PoolIndex::pinned_count() const {
   int64_t n = 0;
-  for (const auto& p : pages_) n += (p.used && p.pins > 0) ? 1 : 0;
+  for (int64_t i = 0; i < watermark_; ++i) n += (pages_[i].used && pages_[i].pins > 0) ? 1 : 0;
   return n;
 }
 
@@ -73,15 +73,26 @@ bool PoolIndex::spec_equal(const Spec& a, const Spec& b) const {
 }
 
 int32_t PoolIndex::pop_free() {
-  auto it = free_.begin();
-  int32_t pid = *it;
-  free_.erase(it);
-  return pid;
+  if (!freed_.empty()) {
+    auto it = freed_.begin();
+    int32_t pid = *it;
+    freed_.erase(it);
+    return pid;
+  }
+  return static_cast<int32_t>(watermark_++);
 }
 
 void PoolIndex::push_free(int32_t pid) {
   pages_[pid] = PageRec{};
-  free_.insert(pid);
+  if (pid + 1 == watermark_) {
+    --watermark_;
+    while (!freed_.empty() && *freed_.rbegin() + 1 == watermark_) {
+      freed_.erase(std::prev(freed_.end()));
+      --watermark_;
+    }
+  } else {
+    freed_.insert(pid);
+  }
 }
 
 void PoolIndex::evict_one(Plan* p) {
@@ -107,6 +118,15 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   const int32_t ps = page_size_;
   std::vector<Spec> specs;
   std::unordered_map<uint64_t, int32_t> pending;
+  {
+    size_t pages_in = 0;
+    for (const QueryIn& q : qs) {
+      pages_in += (q.prefix.n + ps - 1) / ps + (q.cross.n + ps - 1) / ps;
+      for (const SpanIn& f : q.frags) pages_in += (f.n + ps - 1) / ps;
+    }
+    specs.reserve(pages_in);
+    pending.reserve(pages_in);
+  }
   struct SpanWalk {
     int kind, query, child;
     SpanIn in;
@@ -114,6 +134,32 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   };
   std::vector<SpanWalk> walk;
   std::vector<std::vector<int>> query_spans(qs.size());
+  // A span given twice in one call (same tokens pointer, length and chain seed) has
+  // the same page chain: hash it once.
+  struct MemoKey {
+    const int32_t* tok;
+    int32_t n;
+    uint64_t seed;
+    bool operator==(const MemoKey& o) const { return tok == o.tok && n == o.n && seed == o.seed; }
+  };
+  struct MemoHash {
+    size_t operator()(const MemoKey& k) const {
+      return static_cast<size_t>(mix64(reinterpret_cast<uintptr_t>(k.tok) ^ mix64(k.seed ^ static_cast<uint32_t>(k.n))));
+    }
+  };
+  std::unordered_map<MemoKey, std::vector<uint64_t>, MemoHash> memo;
+  auto chain_of = [&](uint64_t seed, const SpanIn& in) -> const std::vector<uint64_t>& {
+    auto it = memo.find(MemoKey{in.tok, in.n, seed});
+    if (it != memo.end()) return it->second;
+    std::vector<uint64_t> hs;
+    uint64_t h = seed;
+    for (int32_t p = 0; p * ps < in.n; ++p) {
+      const int32_t n = std::min(ps, in.n - p * ps);
+      h = page_hash(h, in.tok + p * ps, n, p);
+      hs.push_back(h);
+    }
+    return memo.emplace(MemoKey{in.tok, in.n, seed}, std::move(hs)).first->second;
+  };
 
   for (size_t qi = 0; qi < qs.size(); ++qi) {
     const QueryIn& q = qs[qi];
@@ -122,24 +168,18 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     if (hash_mode_ == SPAN_HASH_STOCK) {
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, false});
     } else {
-      uint64_t h = SPAN_HASH_ROOT;
-      for (int32_t p = 0; p * ps < q.prefix.n; ++p) {
-        int32_t n = std::min(ps, q.prefix.n - p * ps);
-        h = page_hash(h, q.prefix.tok + p * ps, n, p);
-      }
-      uint64_t fs = fragment_seed(h);
+      const std::vector<uint64_t>& ph = chain_of(SPAN_HASH_ROOT, q.prefix);
+      uint64_t fs = fragment_seed(ph.empty() ? SPAN_HASH_ROOT : ph.back());
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, true});
       for (size_t c = 0; c < q.frags.size(); ++c) srcs.push_back({fs, q.frags[c], 1, static_cast<int>(c), true});
     }
     for (const Src& s : srcs) {
       SpanWalk w{s.kind, static_cast<int>(qi), s.child, s.in, {}};
-      uint64_t h = s.seed;
+      const std::vector<uint64_t>& hs = chain_of(s.seed, s.in);
       bool missed = false;
       for (int32_t p = 0; p * ps < s.in.n; ++p) {
         int32_t n = std::min(ps, s.in.n - p * ps);
-        Spec sp{page_hash(h, s.in.tok + p * ps, n, p), h, p, n, s.in.tok + p * ps,
-                n == ps || s.partial_ok, false};
-        h = sp.hash;
+        Spec sp{hs[p], p == 0 ? s.seed : hs[p - 1], p, n, s.in.tok + p * ps, n == ps || s.partial_ok, false};
         if (!missed && sp.cacheable) {
           auto it = pending.find(sp.hash);
           if (it != pending.end() && spec_equal(specs[it->second], sp)) {
@@ -177,15 +217,13 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
 
   // distinct published pages this plan hits, in walk order
   std::vector<int32_t> hit_pids;
-  {
-    std::vector<char> seen(static_cast<size_t>(num_pages_), 0);
-    for (const auto& w : walk)
-      for (const auto& e : w.entries)
-        if (e.hit && !seen[e.x]) {
-          seen[e.x] = 1;
-          hit_pids.push_back(e.x);
-        }
-  }
+  const int64_t stamp = ++stamp_;
+  for (const auto& w : walk)
+    for (const auto& e : w.entries)
+      if (e.hit && pages_[e.x].seen_stamp != stamp) {
+        pages_[e.x].seen_stamp = stamp;
+        hit_pids.push_back(e.x);
+      }
   int64_t need = static_cast<int64_t>(specs.size());
   int64_t evictable = static_cast<int64_t>(evictable_.size());
   for (int32_t pid : hit_pids)
@@ -209,7 +247,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   P.hits = hit_pids;
   std::vector<int32_t> slot_pid(specs.size(), -1);
   auto alloc = [&](int32_t slot) {
-    if (free_.empty()) evict_one(&P);
+    if (free_count() == 0) evict_one(&P);
     int32_t pid = pop_free();
     const Spec& s = specs[slot];
     PageRec& r = pages_[pid];
@@ -317,13 +355,16 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
         int32_t end = kv0;
         while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
         p->t_prefill.push_back(WorkTile{static_cast<int32_t>(s.row + j0), n, s.canon0 + j0, kv0, end, -1, 0, 0});
-        for (int32_t j = j0; j < j0 + n; ++j) {
-          p->rows_prefill.push_back(s.row + j);
-          p->prefill_pairs += pre + j + 1;
-        }
+        p->rows_prefill.push_back(Plan::RowRun{s.row + j0, n});
+        // rows j0..j0+n-1 see pre + j + 1 keys each
+        p->prefill_pairs += static_cast<int64_t>(n) * (pre + 1) + static_cast<int64_t>(n) * (2 * j0 + n - 1) / 2;
       }
     }
   }
+  // longest key lists first, so the tail of the launch is short tiles
+  std::stable_sort(p->t_prefill.begin(), p->t_prefill.end(), [](const WorkTile& a, const WorkTile& b) {
+    return (a.kv_end - a.kv_begin) > (b.kv_end - b.kv_begin);
+  });
   // ---- cross: pages, key list in query order, split-KV row tiles
   struct CrossTile { int32_t row0, n, pos0, kv0, kv1; };
   std::vector<CrossTile> ct;
@@ -354,10 +395,8 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
       while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
       ct.push_back(CrossTile{static_cast<int32_t>(cross.row + j0), n, cross.final0 + j0, kv0, end});
       max_pages = std::max(max_pages, end - kv0);
-      for (int32_t j = j0; j < j0 + n; ++j) {
-        p->rows_cross.push_back(cross.row + j);
-        p->cross_pairs += cross.final0 + j + 1;
-      }
+      p->rows_cross.push_back(Plan::RowRun{cross.row + j0, n});
+      p->cross_pairs += static_cast<int64_t>(n) * (cross.final0 + 1) + static_cast<int64_t>(n) * (2 * j0 + n - 1) / 2;
     }
   }
   int32_t splits = 1;

@@ -25,6 +25,7 @@ struct PageRec {
   bool used = false;
   bool published = false;
   bool cacheable = false;
+  int64_t seen_stamp = 0;  // last plan() call that listed this page among its hits
 };
 
 struct SpanIn {
@@ -56,8 +57,8 @@ struct Tiling {
   int bm_prefill = 64;   // rows per prefill tile
   int bm_cross = 64;     // rows per cross tile
   int kv_heads = 1;      // work items per tile (one per kv head)
-  int target_items = 2048;
-  int min_split_pages = 8;
+  int target_items = 512;     // work-groups the cross launch aims for (KV splits x tiles x heads)
+  int min_split_pages = 16;   // at least 256 keys per KV split
 };
 
 class PoolIndex;
@@ -75,7 +76,11 @@ struct Plan {
   std::vector<NewPage> k3_prefill, k3_cross;
   std::vector<WorkTile> t_prefill, t_cross;
   std::vector<CombineTile> combine;
-  std::vector<int64_t> rows_prefill, rows_cross;
+  struct RowRun {
+    int64_t row0;
+    int32_t n;
+  };
+  std::vector<RowRun> rows_prefill, rows_cross;  // one run per row tile, in work order
   int32_t n_parts = 0;
   int32_t kv_splits = 1;
   int bm_cross = 64;
@@ -97,7 +102,7 @@ class PoolIndex {
   int64_t lookup(uint64_t h) const;  // page id or -1
 
   int64_t num_pages() const { return num_pages_; }
-  int64_t free_count() const { return static_cast<int64_t>(free_.size()); }
+  int64_t free_count() const { return static_cast<int64_t>(freed_.size()) + (num_pages_ - watermark_); }
   int64_t cached_count() const { return static_cast<int64_t>(index_.size()); }
   int64_t pinned_count() const;
   int64_t tick() const { return tick_; }
@@ -125,9 +130,12 @@ class PoolIndex {
   std::vector<PageRec> pages_;
   std::vector<int32_t> page_tokens_;
   std::unordered_map<uint64_t, int32_t> index_;
-  std::set<int32_t> free_;
+  // Free page ids: every id >= watermark_, plus the ids in freed_ (all < watermark_).
+  std::set<int32_t> freed_;
+  int64_t watermark_ = 0;
   std::set<std::tuple<int64_t, int32_t, int32_t>> evictable_;  // (last_use, -idx, id)
   int64_t tick_ = 0;
+  int64_t stamp_ = 0;  // counts plan() calls, successful or not
   int64_t total_evictions_ = 0;
 };
 
