@@ -1,9 +1,11 @@
 // bf16 MFMA span attention for gfx950 (CDNA4).
 //
-// One work-group per (row tile of up to 64 query tokens, kv head).  The G query
-// heads that share the kv head are packed into the work-group: wave w handles
-// head (w mod G) and token rows 32*(w div G) .. +31, so every K/V tile staged in
-// LDS feeds 2G waves.
+// One work-group of four waves per (row tile of 128/G query tokens, kv head).  The
+// G query heads that share the kv head are packed into the work-group: wave w
+// handles head (w mod G) and token rows 32*(w div G) .. +31, so every K/V tile
+// staged in LDS feeds all four waves.  Two work-groups fit a CU (registers: two
+// waves per SIMD; LDS: 2 x 68 KB), and having two independent work-groups, each
+// with its own barrier, lets one group's softmax overlap the other's MFMAs.
 //
 // Scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 //   A = K tile (32 keys x 16 dims, from LDS), B = Q^T (16 dims x 32 rows, kept in
@@ -37,6 +39,8 @@ namespace spanq {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
@@ -44,8 +48,9 @@ namespace {
 
 constexpr int kBN = 64;  // keys per tile (4 pages)
 
+// Two floats to packed bfloat16, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
@@ -53,7 +58,9 @@ __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w 
 
 template <int D, int G>
 struct Cfg {
-  static constexpr int NW = 2 * G;           // waves
+  static constexpr int RB = 4 / G;           // 32-row blocks per work-group
+  static constexpr int BM = 32 * RB;         // query tokens per tile
+  static constexpr int NW = 4;               // waves
   static constexpr int NT = 64 * NW;         // threads
   static constexpr int KS = D / 16;          // 16-dim steps of the QK contraction
   static constexpr int DB = D / 32;          // 32-dim blocks of the output
@@ -106,6 +113,10 @@ struct Stage {
   u32x4_t v[Cfg<D, G>::VPT];
 };
 
+// Global -> register staging of one key tile.  Every staging task of a wave lies
+// in one page (a page holds 16 * D/16 K tasks and 2 * D V tasks, both multiples of
+// the wave size), so the page index is made wave-uniform and the page base address
+// lives in scalar registers; each lane only adds a fixed 32-bit offset.
 template <int D, int G>
 __device__ __forceinline__ void fetch(const bf16_t* __restrict__ pool, int64_t layer_off, int hkv, int kvh,
                                       const TilePages& tp, Stage<D, G>& st) {
@@ -119,12 +130,13 @@ __device__ __forceinline__ void fetch(const bf16_t* __restrict__ pool, int64_t l
     if (task < C::KTASK) {
       const int key = task / C::KCH;
       const int c = task - key * C::KCH;
-      const int slot = key & 15;
-      const int pid = pick4(tp.id, key >> 4);
+      const int p = __builtin_amdgcn_readfirstlane(key >> 4);
+      const int pid = pick4(tp.id, p);
       if (pid >= 0) {
-        const bf16_t* src = pool + layer_off + pid * page_elems + (static_cast<int64_t>(kvh) * kPage + slot) * D;
-        st.klo[t] = *reinterpret_cast<const u32x4_t*>(src + 8 * c);
-        st.khi[t] = *reinterpret_cast<const u32x4_t*>(src + D / 2 + 8 * c);
+        const bf16_t* base = pool + (layer_off + pid * page_elems + static_cast<int64_t>(kvh) * kPage * D);
+        const uint32_t off = static_cast<uint32_t>((key & 15) * D + 8 * c);
+        st.klo[t] = *reinterpret_cast<const u32x4_t*>(base + off);
+        st.khi[t] = *reinterpret_cast<const u32x4_t*>(base + off + D / 2);
       }
     }
   }
@@ -133,15 +145,14 @@ __device__ __forceinline__ void fetch(const bf16_t* __restrict__ pool, int64_t l
     const int task = threadIdx.x + t * C::NT;
     st.v[t] = u32x4_t{0, 0, 0, 0};
     if (task < C::VTASK) {
-      const int p = task / (2 * D);
+      const int p = __builtin_amdgcn_readfirstlane(task / (2 * D));
       const int rem = task - p * (2 * D);
-      const int drow = rem >> 1;
-      const int half = rem & 1;
       const int pid = pick4(tp.id, p);
       if (pid >= 0) {
-        const bf16_t* src = pool + layer_off + pid * page_elems + static_cast<int64_t>(hkv) * kPage * D +
-                            (static_cast<int64_t>(kvh) * D + drow) * kPage + 8 * half;
-        st.v[t] = *reinterpret_cast<const u32x4_t*>(src);
+        const bf16_t* base = pool + (layer_off + pid * page_elems + static_cast<int64_t>(hkv) * kPage * D +
+                                     static_cast<int64_t>(kvh) * D * kPage);
+        const uint32_t off = static_cast<uint32_t>((rem >> 1) * kPage + 8 * (rem & 1));
+        st.v[t] = *reinterpret_cast<const u32x4_t*>(base + off);
       }
     }
   }
@@ -150,12 +161,12 @@ __device__ __forceinline__ void fetch(const bf16_t* __restrict__ pool, int64_t l
 // Rotate a staged chunk pair (dims 8c..8c+7 and D/2+8c..) by `delta` positions.
 template <int D>
 __device__ __forceinline__ void rotate_pair(u32x4_t& lo, u32x4_t& hi, int c, int delta,
-                                            const double* __restrict__ inv_freq) {
+                                            const float2* __restrict__ rope) {
+  const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(delta) * (D / 2) + 8 * c);
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    float s0, c0, s1, c1;
-    rope_angle(delta, inv_freq[8 * c + 2 * w], &s0, &c0);
-    rope_angle(delta, inv_freq[8 * c + 2 * w + 1], &s1, &c1);
+    const float4 v = cs4[w];  // (cos, sin) of frequencies 8c + 2w and 8c + 2w + 1
+    const float c0 = v.x, s0 = v.y, c1 = v.z, s1 = v.w;
     const float a0 = lo_bf16(lo[w]), a1 = hi_bf16(lo[w]);
     const float b0 = lo_bf16(hi[w]), b1 = hi_bf16(hi[w]);
     lo[w] = pack_bf16x2(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
@@ -165,7 +176,7 @@ __device__ __forceinline__ void rotate_pair(u32x4_t& lo, u32x4_t& hi, int c, int
 
 template <int D, int G>
 __device__ __forceinline__ void store(bf16_t* __restrict__ k_lds, bf16_t* __restrict__ v_lds, const TilePages& tp,
-                                      Stage<D, G>& st, const double* __restrict__ inv_freq) {
+                                      Stage<D, G>& st, const float2* __restrict__ rope) {
   using C = Cfg<D, G>;
 #pragma unroll
   for (int t = 0; t < C::KPT; ++t) {
@@ -174,7 +185,7 @@ __device__ __forceinline__ void store(bf16_t* __restrict__ k_lds, bf16_t* __rest
       const int key = task / C::KCH;
       const int c = task - key * C::KCH;
       const int delta = pick4(tp.delta, key >> 4);
-      if (delta != 0) rotate_pair<D>(st.klo[t], st.khi[t], c, delta, inv_freq);
+      if (delta != 0) rotate_pair<D>(st.klo[t], st.khi[t], c, delta, rope);
       *reinterpret_cast<u32x4_t*>(k_lds + key * C::KROW + 8 * c) = st.klo[t];
       *reinterpret_cast<u32x4_t*>(k_lds + key * C::KROW + D / 2 + 8 * c) = st.khi[t];
     }
@@ -197,12 +208,12 @@ __device__ __forceinline__ void store(bf16_t* __restrict__ k_lds, bf16_t* __rest
 }  // namespace
 
 template <int D, int G>
-__global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __restrict__ tiles,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(const WorkTile* __restrict__ tiles,
                                                             const KvPage* __restrict__ kv,
                                                             const bf16_t* __restrict__ q, bf16_t* __restrict__ out,
                                                             const bf16_t* __restrict__ pool, int64_t layer_off,
                                                             int hq, int hkv, float scale_log2,
-                                                            const double* __restrict__ inv_freq,
+                                                            const float2* __restrict__ rope,
                                                             float* __restrict__ part_o, float* __restrict__ part_ml) {
   using C = Cfg<D, G>;
   __shared__ __attribute__((aligned(16))) bf16_t k_lds[2][C::LDS_K];
@@ -221,6 +232,16 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
   const int qpos = t.q_pos0 + row;
   const int wave_min_pos = t.q_pos0 + 32 * rb;
 
+  const int n_pages = t.kv_end - t.kv_begin;
+  const int n_tiles = (n_pages + 3) >> 2;
+  TilePages cur, nxt;
+  Stage<D, G> st;
+  // first key tile in flight while the query rows are loaded and rotated
+  if (n_tiles > 0) {
+    read_pages(kv, t.kv_begin, t.kv_end, cur);
+    fetch<D, G>(pool, layer_off, hkv, kvh, cur, st);
+  }
+
   // ---- Q^T operand, rotated at the row's position and pre-scaled by log2(e)/sqrt(d)
   bf16x8_t qf[C::KS];
   {
@@ -238,13 +259,20 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
       }
 #pragma unroll
       for (int s = 0; s < C::KS / 2; ++s) {
+        // frequencies 16s + 8h2 .. +7: 8 consecutive (cos, sin) pairs, 64 bytes
+        const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(qpos) * (D / 2) + 16 * s + 8 * h2);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float sn, cs;
-          rope_angle(qpos, inv_freq[16 * s + 8 * h2 + e], &sn, &cs);
-          const float a = x[s][e], b = x[s + C::KS / 2][e];
-          x[s][e] = (a * cs - b * sn) * scale_log2;
-          x[s + C::KS / 2][e] = (b * cs + a * sn) * scale_log2;
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const float4 v = cs4[e2];  // (cos, sin) of frequencies 2*e2 and 2*e2 + 1
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int e = 2 * e2 + u;
+            const float cs = u ? v.z : v.x;
+            const float sn = u ? v.w : v.y;
+            const float a = x[s][e], b = x[s + C::KS / 2][e];
+            x[s][e] = (a * cs - b * sn) * scale_log2;
+            x[s + C::KS / 2][e] = (b * cs + a * sn) * scale_log2;
+          }
         }
       }
     } else {
@@ -254,9 +282,12 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
         for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
     }
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s)
+    for (int s = 0; s < C::KS; ++s) {
+      u32x4_t w;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qf[s][e] = __builtin_bit_cast(__bf16, f32_to_bf16(x[s][e]));
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(x[s][2 * e], x[s][2 * e + 1]);
+      qf[s] = __builtin_bit_cast(bf16x8_t, w);
+    }
   }
 
   f32x16_t o[C::DB];
@@ -267,15 +298,7 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
   float m = -INFINITY;
   float l = 0.f;
 
-  const int n_pages = t.kv_end - t.kv_begin;
-  const int n_tiles = (n_pages + 3) >> 2;
-  TilePages cur, nxt;
-  Stage<D, G> st;
-  if (n_tiles > 0) {
-    read_pages(kv, t.kv_begin, t.kv_end, cur);
-    fetch<D, G>(pool, layer_off, hkv, kvh, cur, st);
-    store<D, G>(k_lds[0], v_lds[0], cur, st, inv_freq);
-  }
+  if (n_tiles > 0) store<D, G>(k_lds[0], v_lds[0], cur, st, rope);
   __syncthreads();
 
   for (int j = 0; j < n_tiles; ++j) {
@@ -291,15 +314,16 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
     // ---- S^T = K Q^T over 64 keys (two 32-key blocks)
     f32x16_t s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
+    for (int ks = 0; ks < C::KS; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {  // two independent accumulator chains, interleaved
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kl + (32 * kb + r) * C::KROW + 16 * ks + 8 * h2);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[kb], 0, 0, 0);
       }
-    }
 
     // ---- mask: causal positions, partial pages, missing pages (wave-uniform test)
     bool need = false;
@@ -318,7 +342,7 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
         }
     }
 
-    // ---- online softmax (base 2; scores already scaled)
+    // ---- online softmax (base 2; scores already scaled), one max per 64-key tile
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -327,32 +351,43 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m, mx);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = exp2f(m - m_use);
+    const float corr = __builtin_amdgcn_exp2f(m - m_use);
     m = m_new;
-    bf16x8_t pk[2][2];
-    float psum = 0.f;
+    // the running max moves on few tiles once it has settled: rescale only then
+    if (__any(corr != 1.f)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = exp2f(s[kb][i] - m_use);
-        psum += pv;
-        pk[kb][i >> 3][i & 7] = __builtin_bit_cast(__bf16, f32_to_bf16(pv));
-      }
-    l = l * corr + psum;
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+    }
+    l *= corr;
 
-    // ---- O^T += V^T P^T
+    // ---- P = 2^(S - m) to bf16, and O^T += V^T P^T.  Block 0's exponentials are
+    // computed first; block 1's are interleaved with block 0's MFMAs, so the
+    // transcendental unit and the matrix core work at the same time.
+    bf16x8_t pk[2][2];
+    auto exp_block = [&](int kb) {
+      float psum = 0.f;
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db) {
-      const bf16_t* vrow = vl + (32 * db + r) * C::VROW + 4 * h2;
+      for (int half = 0; half < 2; ++half) {
+        u32x4_t w;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(s[kb][8 * half + 2 * e] - m_use);
+          const float p1 = __builtin_amdgcn_exp2f(s[kb][8 * half + 2 * e + 1] - m_use);
+          psum += p0 + p1;
+          w[e] = pack_bf16x2(p0, p1);
+        }
+        pk[kb][half] = __builtin_bit_cast(bf16x8_t, w);
+      }
+      l += psum;
+    };
+    auto pv_block = [&](int kb) {
 #pragma unroll
-        for (int stp = 0; stp < 2; ++stp) {
+      for (int stp = 0; stp < 2; ++stp)
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {  // DB independent accumulator chains, interleaved
+          const bf16_t* vrow = vl + (32 * db + r) * C::VROW + 4 * h2;
           const int k0 = 32 * kb + 16 * stp;
           const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow + k0);
           const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + k0 + 8);
@@ -360,10 +395,21 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
           const bf16x8_t a = __builtin_bit_cast(bf16x8_t, w);
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[kb][stp], o[db], 0, 0, 0);
         }
+    };
+    exp_block(0);
+    pv_block(0);
+    exp_block(1);
+#pragma unroll
+    for (int i = 0; i < 2 * C::DB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // its two LDS reads (next V operand)
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // block-1 softmax VALU
+      __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);  // block-1 exponentials
     }
+    pv_block(1);
 
     if (more) {
-      store<D, G>(k_lds[buf ^ 1], v_lds[buf ^ 1], nxt, st, inv_freq);
+      store<D, G>(k_lds[buf ^ 1], v_lds[buf ^ 1], nxt, st, rope);
       cur = nxt;
     }
     __syncthreads();
@@ -386,7 +432,7 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
         *reinterpret_cast<u32x2_t*>(dst + d0) = w;
       }
   } else {
-    const int64_t slot = (static_cast<int64_t>(t.part) * hq + head) * kMfmaBM + row;
+    const int64_t slot = (static_cast<int64_t>(t.part) * hq + head) * C::BM + row;
     float* po = part_o + slot * D;
 #pragma unroll
     for (int db = 0; db < C::DB; ++db)
@@ -403,6 +449,8 @@ __global__ __launch_bounds__(128 * G) void attn_mfma_kernel(const WorkTile* __re
   }
 }
 
+int mfma_bm(int g) { return 128 / g; }
+
 bool mfma_supported(int hq, int hkv, int d, int dtype) {
   if (dtype != SPAN_BF16 || hkv <= 0 || hq % hkv != 0) return false;
   const int g = hq / hkv;
@@ -412,17 +460,17 @@ bool mfma_supported(int hq, int hkv, int d, int dtype) {
 
 template <int D, int G>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
-                           float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+                           float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(n, g.hkv), dim3(128 * G), 0, s, tiles, kv,
+  hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(n, g.hkv), dim3(256), 0, s, tiles, kv,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
-                     g.layer_off, g.hq, g.hkv, scale_log2, inv_freq, part_o, part_ml);
+                     g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
-                           float* po, float* pml, const double* inv, hipStream_t s) {
+                           float* po, float* pml, const float2* inv, hipStream_t s) {
   switch (g.hq / g.hkv) {
     case 1: return launch_t<D, 1>(g, tiles, n, kv, q, out, po, pml, inv, s);
     case 2: return launch_t<D, 2>(g, tiles, n, kv, q, out, po, pml, inv, s);
@@ -432,11 +480,11 @@ static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, cons
 }
 
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                            void* out, float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+                            void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype)) return hipErrorInvalidValue;
-  if (g.d == 128) return launch_d<128>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
-  return launch_d<64>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+  if (g.d == 128) return launch_d<128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
+  return launch_d<64>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
 }
 
 }  // namespace spanq

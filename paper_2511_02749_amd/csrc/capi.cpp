@@ -42,7 +42,43 @@ struct span_pool {
   bool use_mfma = false;
   std::set<span_plan*> plans;
   std::vector<hipEvent_t> event_cache;  // reusable timing events
+  float2* rope_tab = nullptr;           // (cos, sin) per [position][head_dim / 2]
+  int64_t rope_n = 0;                   // positions in rope_tab
 };
+
+namespace {
+// Make the rotary table cover positions [0, need).  Computed on the host in double
+// precision (angle reduced to [-pi, pi] before cos/sin), rounded once to float.
+// Growth synchronises the device, since kernels of other plans may read the old table.
+int ensure_rope_table(span_pool* p, int64_t need) {
+  if (need <= p->rope_n) return SPAN_OK;
+  int64_t n = 4096;
+  while (n < need) n *= 2;
+  const int half = p->cfg.head_dim / 2;
+  std::vector<float2> tab(static_cast<size_t>(n) * half);
+  const double two_pi = 6.283185307179586476925;
+  for (int i = 0; i < half; ++i) {
+    const double f = std::pow(static_cast<double>(p->cfg.rope_theta), -2.0 * i / p->cfg.head_dim);
+    for (int64_t pos = 0; pos < n; ++pos) {
+      double a = static_cast<double>(pos) * f;
+      a -= two_pi * std::nearbyint(a / two_pi);
+      tab[static_cast<size_t>(pos) * half + i] = float2{static_cast<float>(std::cos(a)), static_cast<float>(std::sin(a))};
+    }
+  }
+  float2* dev = nullptr;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMalloc(&dev, tab.size() * sizeof(float2));
+  if (e == hipSuccess) e = hipMemcpy(dev, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    if (dev) (void)hipFree(dev);
+    return hip_fail(e, "rotary table");
+  }
+  if (p->rope_tab) (void)hipFree(p->rope_tab);
+  p->rope_tab = dev;
+  p->rope_n = n;
+  return SPAN_OK;
+}
+}  // namespace
 
 struct span_plan {
   span_pool* pool = nullptr;
@@ -59,7 +95,7 @@ struct span_plan {
   const WorkTile* tp = nullptr;
   const WorkTile* tc = nullptr;
   const CombineTile* cb = nullptr;
-  const double* inv_freq = nullptr;
+  const float2* rope = nullptr;
   int bm = kGenericBM;
   bool mfma = false;
   bool committed = false;
@@ -202,6 +238,7 @@ int span_pool_destroy(span_pool* p) {
   for (span_plan* pl : live) span_plan_destroy(pl);
   if (p->cfg.device >= 0) (void)hipDeviceSynchronize();
   for (hipEvent_t e : p->event_cache) (void)hipEventDestroy(e);
+  if (p->rope_tab) (void)hipFree(p->rope_tab);
   if (p->owns_dev && p->dev) (void)hipFree(p->dev);
   delete p->index;
   delete p;
@@ -312,14 +349,14 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
   pl->stream = static_cast<hipStream_t>(stream);
   const bool device = pool->cfg.device >= 0;
   pl->mfma = device && pool->use_mfma;
-  pl->bm = pl->mfma ? kMfmaBM : kGenericBM;
+  pl->bm = pl->mfma ? mfma_bm(pool->cfg.num_q_heads / pool->cfg.num_kv_heads) : kGenericBM;
   Tiling t;
   t.bm_prefill = pl->bm;
   t.bm_cross = pl->bm;
   t.kv_heads = pl->mfma ? pool->cfg.num_kv_heads : pool->cfg.num_q_heads;
-  // The MFMA kernel runs one 8-wave work-group per CU: aim the cross launch at one
-  // work-group per CU (256 on MI355X); the generic kernel is latency-bound and wants more.
-  t.target_items = pl->mfma ? 256 : 1024;
+  // The MFMA kernel runs two 4-wave work-groups per CU: aim the cross launch at two
+  // per CU (512 on MI355X); the generic kernel is latency-bound and wants more.
+  t.target_items = pl->mfma ? 512 : 1024;
   std::string msg;
   const auto t_plan0 = std::chrono::steady_clock::now();
   int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
@@ -333,14 +370,21 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
   if (device) {
     Plan& P = pl->plan;
     const int d = pool->cfg.head_dim;
-    std::vector<double> inv(static_cast<size_t>(d / 2));
-    for (int i = 0; i < d / 2; ++i)
-      inv[i] = std::pow(static_cast<double>(pool->cfg.rope_theta), -2.0 * i / d);
+    hipError_t e = hipSetDevice(pool->cfg.device);
+    if (e != hipSuccess) {
+      span_plan_destroy(pl);
+      return hip_fail(e, "span_plan_create: hipSetDevice");
+    }
+    rc = ensure_rope_table(pool, P.max_pos + 1);
+    if (rc) {
+      span_plan_destroy(pl);
+      return rc;
+    }
+    pl->rope = pool->rope_tab;
     auto& hb = pl->host_meta;
     size_t o_kv = put(hb, P.kv), o_k3p = put(hb, P.k3_prefill), o_k3c = put(hb, P.k3_cross);
-    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine), o_inv = put(hb, inv);
-    hipError_t e = hipSetDevice(pool->cfg.device);
-    if (e == hipSuccess) e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
+    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
+    e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
     if (e == hipSuccess) e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
     if (e == hipSuccess && P.n_parts > 0) {
       pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
@@ -358,7 +402,6 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
     pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
     pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
     pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
-    pl->inv_freq = reinterpret_cast<const double*>(pl->dev_meta + o_inv);
   }
   *out = pl;
   return SPAN_OK;
@@ -449,12 +492,12 @@ int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const vo
   PoolGeom g = geom(pl, layer);
   Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 2, s, pl->pool->event_cache);
   tm.mark(0);
-  hipError_t e = launch_rope_write(g, pl->k3p, static_cast<int>(P.k3_prefill.size()), k, v, pl->inv_freq, s);
+  hipError_t e = launch_rope_write(g, pl->k3p, static_cast<int>(P.k3_prefill.size()), k, v, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
   tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s)
-               : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->inv_freq, s);
+  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s)
+               : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
   tm.mark(2);
   if (!tm.ev.empty()) pl->ev_prefill.push_back(tm.ev);
@@ -472,14 +515,14 @@ int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k
   PoolGeom g = geom(pl, layer);
   Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s, pl->pool->event_cache);
   tm.mark(0);
-  hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->inv_freq, s);
+  hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
   tm.mark(1);
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s)
-               : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->inv_freq, s);
+  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s)
+               : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(2);
   e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);

@@ -26,12 +26,14 @@ __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <>
 __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
 
-// sin/cos of pos * inv_freq: the product and its reduction to [-pi, pi] in
-// double precision, the trigonometric evaluation in single precision.
-__device__ __forceinline__ void rope_angle(int pos, double inv_freq, float* sn, float* cs) {
-  const double a = static_cast<double>(pos) * inv_freq;
-  const double r = a - 6.283185307179586476925 * rint(a * 0.15915494309189533577);
-  sincosf(static_cast<float>(r), sn, cs);
+// cos and sin of position `pos` at frequency index i (rotary pair (i, i + d/2)),
+// read from the pool's table of (cos, sin) pairs laid out [position][d/2]; the
+// table is computed on the host in double precision and rounded once.
+__device__ __forceinline__ void rope_cs(const float2* __restrict__ tab, int half, int pos, int i, float* sn,
+                                        float* cs) {
+  const float2 v = tab[static_cast<int64_t>(pos) * half + i];
+  *cs = v.x;
+  *sn = v.y;
 }
 
 }  // namespace spanq

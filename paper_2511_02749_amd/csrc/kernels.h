@@ -17,20 +17,21 @@ struct PoolGeom {
 
 // K3: rotate keys at their positions and write keys/values of new pages.
 hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n_pages, const void* k,
-                             const void* v, const double* inv_freq, hipStream_t s);
+                             const void* v, const float2* rope, hipStream_t s);
 
 // Generic (vector ALU) span attention over work tiles of up to 64 rows.
 constexpr int kGenericBM = 64;
 hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
                                const void* q, void* out, float* part_o, float* part_ml,
-                               const double* inv_freq, hipStream_t s);
+                               const float2* rope, hipStream_t s);
 
-// bf16 MFMA span attention; tiles of kMfmaBM rows, one work-group per (tile, kv head).
-constexpr int kMfmaBM = 64;
+// bf16 MFMA span attention: four waves per work-group, one work-group per (row tile,
+// kv head); a tile has mfma_bm(g) = 128 / g query tokens (g = query heads per kv head).
 bool mfma_supported(int hq, int hkv, int d, int dtype);
+int mfma_bm(int g);
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
                             const void* q, void* out, float* part_o, float* part_ml,
-                            const double* inv_freq, hipStream_t s);
+                            const float2* rope, hipStream_t s);
 
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,

@@ -1,8 +1,7 @@
 // Page writer (K3), generic span attention and KV-split combine for gfx950.
 //
 // Rotary encoding (section 5.5 cites RoFormer): rotate-half pairs (i, i + d/2)
-// at angle pos * theta^(-2i/d).  Angles are formed in double precision, reduced
-// to [-pi, pi] and evaluated in single precision.
+// at angle pos * theta^(-2i/d); cos/sin come from the pool's position table.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -22,7 +21,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restrict__ pages,
                                                          const T* __restrict__ k, const T* __restrict__ v,
                                                          T* __restrict__ pool, int64_t layer_off, int hkv,
-                                                         const double* __restrict__ inv_freq) {
+                                                         const float2* __restrict__ rope) {
   const NewPage pg = pages[blockIdx.x];
   const int64_t page_elems = 2ll * hkv * kPage * D;
   T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems;
@@ -39,7 +38,7 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
       const float x0 = to_f32(k[src + i]);
       const float x1 = to_f32(k[src + i + H]);
       float sn, cs;
-      rope_angle(pg.pos0 + s, inv_freq[i], &sn, &cs);
+      rope_cs(rope, D / 2, pg.pos0 + s, i, &sn, &cs);
       y0 = x0 * cs - x1 * sn;
       y1 = x1 * cs + x0 * sn;
     }
@@ -60,21 +59,21 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
 
 template <typename T, int D>
 static hipError_t rope_write_t(const PoolGeom& g, const NewPage* pages, int n, const void* k, const void* v,
-                               const double* inv_freq, hipStream_t s) {
+                               const float2* rope, hipStream_t s) {
   hipLaunchKernelGGL((rope_write_kernel<T, D>), dim3(n), dim3(256), 0, s, pages, static_cast<const T*>(k),
-                     static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv, inv_freq);
+                     static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv, rope);
   return hipGetLastError();
 }
 
 hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, const void* k, const void* v,
-                             const double* inv_freq, hipStream_t s) {
+                             const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (g.dtype == SPAN_BF16) {
-    if (g.d == 128) return rope_write_t<bf16_t, 128>(g, pages, n, k, v, inv_freq, s);
-    return rope_write_t<bf16_t, 64>(g, pages, n, k, v, inv_freq, s);
+    if (g.d == 128) return rope_write_t<bf16_t, 128>(g, pages, n, k, v, rope, s);
+    return rope_write_t<bf16_t, 64>(g, pages, n, k, v, rope, s);
   }
-  if (g.d == 128) return rope_write_t<float, 128>(g, pages, n, k, v, inv_freq, s);
-  return rope_write_t<float, 64>(g, pages, n, k, v, inv_freq, s);
+  if (g.d == 128) return rope_write_t<float, 128>(g, pages, n, k, v, rope, s);
+  return rope_write_t<float, 64>(g, pages, n, k, v, rope, s);
 }
 
 // ------------------------------------------------------------------ generic attention
@@ -88,7 +87,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
                                                           const T* __restrict__ q, T* __restrict__ out,
                                                           const T* __restrict__ pool, int64_t layer_off, int hq,
                                                           int hkv, float scale_log2,
-                                                          const double* __restrict__ inv_freq,
+                                                          const float2* __restrict__ rope,
                                                           float* __restrict__ part_o, float* __restrict__ part_ml) {
   constexpr int H = D / 2;
   __shared__ float ks[kPage][D + 1];
@@ -110,7 +109,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
 #pragma unroll
     for (int i = 0; i < H; ++i) {
       float sn, cs;
-      rope_angle(qpos, inv_freq[i], &sn, &cs);
+      rope_cs(rope, D / 2, qpos, i, &sn, &cs);
       const float x0 = to_f32(qr[i]);
       const float x1 = to_f32(qr[i + H]);
       qv[i] = x0 * cs - x1 * sn;
@@ -134,7 +133,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
       float x1 = to_f32(kp[s * D + i + H]);
       if (pg.delta != 0) {
         float sn, cs;
-        rope_angle(pg.delta, inv_freq[i], &sn, &cs);
+        rope_cs(rope, D / 2, pg.delta, i, &sn, &cs);
         const float y0 = x0 * cs - x1 * sn;
         x1 = x1 * cs + x0 * sn;
         x0 = y0;
@@ -190,23 +189,23 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
 
 template <typename T, int D>
 static hipError_t attn_generic_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                                 void* out, float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+                                 void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   hipLaunchKernelGGL((attn_generic_kernel<T, D>), dim3(n, g.hq), dim3(64), 0, s, tiles, kv,
                      static_cast<const T*>(q), static_cast<T*>(out), static_cast<const T*>(g.base), g.layer_off,
-                     g.hq, g.hkv, scale_log2, inv_freq, part_o, part_ml);
+                     g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                               void* out, float* part_o, float* part_ml, const double* inv_freq, hipStream_t s) {
+                               void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (g.dtype == SPAN_BF16) {
-    if (g.d == 128) return attn_generic_t<bf16_t, 128>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
-    return attn_generic_t<bf16_t, 64>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+    if (g.d == 128) return attn_generic_t<bf16_t, 128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
+    return attn_generic_t<bf16_t, 64>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
   }
-  if (g.d == 128) return attn_generic_t<float, 128>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
-  return attn_generic_t<float, 64>(g, tiles, n, kv, q, out, part_o, part_ml, inv_freq, s);
+  if (g.d == 128) return attn_generic_t<float, 128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
+  return attn_generic_t<float, 64>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
 }
 
 // ------------------------------------------------------------------ K4 combine

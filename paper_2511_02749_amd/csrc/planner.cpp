@@ -328,6 +328,7 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     }
     cross.canon0 = at;
     cross.final0 = at;
+    p->max_pos = std::max(p->max_pos, at + cross.n_tok);
   }
   // ---- prefill: new pages and row tiles of every span that computes pages
   for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {

@@ -83,6 +83,7 @@ struct Plan {
   std::vector<RowRun> rows_prefill, rows_cross;  // one run per row tile, in work order
   int32_t n_parts = 0;
   int32_t kv_splits = 1;
+  int32_t max_pos = 0;  // every position (and reposition delta) used is below this
   int bm_cross = 64;
 
   int64_t pages_hit = 0, pages_new = 0, tokens_hit = 0, tokens_new = 0, tokens_cross = 0;
