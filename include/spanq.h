@@ -71,7 +71,7 @@ extern "C" {
 #define SPAN_KERNEL_AUTO 0    /* bf16 MFMA kernel where the shape allows, else generic */
 #define SPAN_KERNEL_GENERIC 1 /* vector-ALU kernel, any supported shape / dtype */
 #define SPAN_KERNEL_MFMA 2    /* bf16 MFMA kernel: bf16 pools, head_dim 64 or 128, num_q_heads /
-                                 num_kv_heads in {1, 2, 4} (SPAN_EINVAL otherwise) */
+                                 num_kv_heads in {1, 2, 4, 8} (SPAN_EINVAL otherwise) */
 
 #define SPAN_FLAG_TIMING 1    /* bracket every kernel launch with HIP events (span_plan_kernel_times) */
 
@@ -100,7 +100,8 @@ typedef struct {
 /* Bytes of device memory a pool with this config needs:
  *   num_layers * num_pages * 2 * num_kv_heads * page_size * head_dim * elem_size.
  * Page layout (one layer): K as [kv_head][slot][head_dim], then V as
- * [kv_head][head_dim][slot] (transposed so the P.V contraction reads it directly). */
+ * [kv_head][head_dim][v_pos(slot)] (transposed so the P.V contraction reads it
+ * directly), where v_pos swaps bits 2 and 3 of the slot (device pools, 16 slots). */
 int span_pool_bytes(const span_pool_config* cfg, size_t* bytes);
 
 /* Create a pool.  With device >= 0 the page memory is device memory (allocated
@@ -126,7 +127,8 @@ int span_pool_get_info(const span_pool* pool, span_pool_info* info);
 
 /* Base device address of the page memory and the element offset of (layer, page):
  * K of kv head h, slot s, dim i at base + off + (h*page_size + s)*head_dim + i;
- * V at base + off + num_kv_heads*page_size*head_dim + (h*head_dim + i)*page_size + s. */
+ * V at base + off + num_kv_heads*page_size*head_dim + (h*head_dim + i)*page_size + v_pos(s),
+ * v_pos(s) = (s & 3) | ((s & 4) << 1) | ((s & 8) >> 1). */
 int span_pool_page_address(const span_pool* pool, int32_t layer, int32_t page_id,
                            void** base, int64_t* elem_offset);
 

@@ -357,6 +357,7 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
   // The MFMA kernel runs two 4-wave work-groups per CU: aim the cross launch at two
   // per CU (512 on MI355X); the generic kernel is latency-bound and wants more.
   t.target_items = pl->mfma ? 512 : 1024;
+  t.pad4 = pl->mfma;
   std::string msg;
   const auto t_plan0 = std::chrono::steady_clock::now();
   int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
@@ -496,7 +497,7 @@ int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const vo
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
   tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s)
+  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, false, s)
                : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
   tm.mark(2);
@@ -521,7 +522,7 @@ int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s)
+  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, true, s)
                : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(2);

@@ -26,6 +26,11 @@ __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <>
 __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
 
+// Position of key slot s (0..15) inside a page's transposed V rows: bits 2 and 3
+// swapped, i.e. quads ordered {0-3, 8-11, 4-7, 12-15}.  A P.V operand of the MFMA
+// kernel then covers 8 consecutive positions (one 16-byte LDS read).
+__host__ __device__ __forceinline__ int v_pos(int s) { return (s & 3) | ((s & 4) << 1) | ((s & 8) >> 1); }
+
 // cos and sin of position `pos` at frequency index i (rotary pair (i, i + d/2)),
 // read from the pool's table of (cos, sin) pairs laid out [position][d/2]; the
 // table is computed on the host in double precision and rounded once.

@@ -25,13 +25,15 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_t
                                const void* q, void* out, float* part_o, float* part_ml,
                                const float2* rope, hipStream_t s);
 
-// bf16 MFMA span attention: four waves per work-group, one work-group per (row tile,
-// kv head); a tile has mfma_bm(g) = 128 / g query tokens (g = query heads per kv head).
+// bf16 MFMA span attention: eight waves per work-group, one work-group per (row
+// tile, kv head); a tile has mfma_bm(g) = 256 / g query tokens (g = query heads per
+// kv head).  Key lists must come in whole 4-page tiles with one delta per tile;
+// `reposition` enables the per-tile query rotation by that delta.
 bool mfma_supported(int hq, int hkv, int d, int dtype);
 int mfma_bm(int g);
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
                             const void* q, void* out, float* part_o, float* part_ml,
-                            const float2* rope, hipStream_t s);
+                            const float2* rope, bool reposition, hipStream_t s);
 
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,

@@ -15,8 +15,8 @@ namespace spanq {
 
 // ------------------------------------------------------------------ K3
 // One work-group per new page.  K goes to [kv_head][slot][d] rotated at its
-// position; V goes transposed to [kv_head][d][slot].  Unfilled slots are zeroed
-// so that masked keys never feed a NaN into the P.V product.
+// position; V goes transposed to [kv_head][d][v_pos(slot)].  Unfilled slots are
+// zeroed so that masked keys never feed a NaN into the P.V product.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restrict__ pages,
                                                          const T* __restrict__ k, const T* __restrict__ v,
@@ -53,7 +53,7 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
     const int s = rem - dd * kPage;
     T val = from_f32<T>(0.f);
     if (s < pg.n_valid) val = v[(static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + dd];
-    vp[(static_cast<int64_t>(h) * D + dd) * kPage + s] = val;
+    vp[(static_cast<int64_t>(h) * D + dd) * kPage + v_pos(s)] = val;
   }
 }
 
@@ -141,7 +141,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
       ks[s][i] = x0;
       ks[s][i + H] = x1;
     }
-    for (int e = lane; e < D * kPage; e += 64) vs[e / kPage][e % kPage] = to_f32(vp[e]);
+    for (int e = lane; e < D * kPage; e += 64) vs[e / kPage][e % kPage] = to_f32(vp[(e / kPage) * kPage + v_pos(e % kPage)]);
     __syncthreads();
     if (!active) continue;
     float sc[kPage];

@@ -309,6 +309,32 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   return SPAN_OK;
 }
 
+namespace {
+// Append the pages of one span to a key list.  Page pg holds tokens 16pg.. at
+// positions pos_base + 16pg.. in the reader's frame; `delta` is the rotation the
+// reader still has to apply.  With pad4 the span's run is padded to a multiple of
+// four pages with empty (n_valid = 0, fully masked) copies of its last page, so a
+// 4-page tile never mixes spans (one delta per tile).
+void append_span(std::vector<KvPage>& kv, const std::vector<int32_t>& pages, int32_t n_tok, int32_t ps,
+                 int32_t pos_base, int32_t delta, bool pad4) {
+  const int32_t np = static_cast<int32_t>(pages.size());
+  for (int32_t pg = 0; pg < np; ++pg)
+    kv.push_back(KvPage{pages[pg], std::min(ps, n_tok - pg * ps), pos_base + pg * ps, delta});
+  if (pad4 && np > 0)
+    for (int32_t pg = np; pg % 4 != 0; ++pg) kv.push_back(KvPage{pages[np - 1], 0, pos_base + (np - 1) * ps, delta});
+}
+
+// One past the last page of kv[kv0, kv1) whose first position is <= last_pos
+// (positions are non-decreasing along a list); rounded up to whole 4-page tiles
+// with pad4 (the extra pages are masked by position or are empty).
+int32_t list_end(const std::vector<KvPage>& kv, int32_t kv0, int32_t kv1, int32_t last_pos, bool pad4) {
+  int32_t end = kv0;
+  while (end < kv1 && kv[end].pos0 <= last_pos) ++end;
+  if (pad4) end = std::min(kv1, kv0 + ((end - kv0 + 3) / 4) * 4);
+  return end;
+}
+}  // namespace
+
 void PoolIndex::build_work(Plan* p, const Tiling& t) {
   const int32_t ps = page_size_;
   p->bm_cross = t.bm_cross;
@@ -342,19 +368,13 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
         p->k3_prefill.push_back(NewPage{s.pages[pg], std::min(ps, s.n_tok - pg * ps),
                                         static_cast<int32_t>(s.row + pg * ps), s.canon0 + pg * ps});
       const int32_t kv0 = static_cast<int32_t>(p->kv.size());
-      if (s.kind == 1)
-        for (size_t pg = 0; pg < prefix.pages.size(); ++pg)
-          p->kv.push_back(KvPage{prefix.pages[pg], std::min<int32_t>(ps, prefix.n_tok - static_cast<int32_t>(pg) * ps),
-                                 static_cast<int32_t>(pg) * ps, 0});
-      for (int32_t pg = 0; pg < np; ++pg)
-        p->kv.push_back(KvPage{s.pages[pg], std::min(ps, s.n_tok - pg * ps), s.canon0 + pg * ps, 0});
+      if (s.kind == 1) append_span(p->kv, prefix.pages, prefix.n_tok, ps, 0, 0, t.pad4);
+      append_span(p->kv, s.pages, s.n_tok, ps, s.canon0, 0, t.pad4);
       const int32_t kv1 = static_cast<int32_t>(p->kv.size());
       const int32_t pre = (s.kind == 1) ? prefix.n_tok : 0;
       for (int32_t j0 = s.n_hit * ps; j0 < s.n_tok; j0 += t.bm_prefill) {
         int32_t n = std::min(t.bm_prefill, s.n_tok - j0);
-        int32_t last_pos = s.canon0 + j0 + n - 1;
-        int32_t end = kv0;
-        while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
+        int32_t end = list_end(p->kv, kv0, kv1, s.canon0 + j0 + n - 1, t.pad4);
         p->t_prefill.push_back(WorkTile{static_cast<int32_t>(s.row + j0), n, s.canon0 + j0, kv0, end, -1, 0, 0});
         p->rows_prefill.push_back(Plan::RowRun{s.row + j0, n});
         // rows j0..j0+n-1 see pre + j + 1 keys each
@@ -380,20 +400,14 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     const int32_t kv0 = static_cast<int32_t>(p->kv.size());
     for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
       const SpanPlan& s = p->spans[ids[c]];
-      for (size_t pg = 0; pg < s.pages.size(); ++pg)
-        p->kv.push_back(KvPage{s.pages[pg], std::min<int32_t>(ps, s.n_tok - static_cast<int32_t>(pg) * ps),
-                               s.final0 + static_cast<int32_t>(pg) * ps, s.final0 - s.canon0});
+      append_span(p->kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, t.pad4);
     }
-    for (size_t pg = 0; pg < cross.pages.size(); ++pg)
-      p->kv.push_back(KvPage{cross.pages[pg], std::min<int32_t>(ps, cross.n_tok - static_cast<int32_t>(pg) * ps),
-                             cross.final0 + static_cast<int32_t>(pg) * ps, 0});
+    append_span(p->kv, cross.pages, cross.n_tok, ps, cross.final0, 0, t.pad4);
     const int32_t kv1 = static_cast<int32_t>(p->kv.size());
     p->cross_kv_pages += kv1 - kv0;
     for (int32_t j0 = 0; j0 < cross.n_tok; j0 += t.bm_cross) {
       int32_t n = std::min(t.bm_cross, cross.n_tok - j0);
-      int32_t last_pos = cross.final0 + j0 + n - 1;
-      int32_t end = kv0;
-      while (end < kv1 && p->kv[end].pos0 <= last_pos) ++end;
+      int32_t end = list_end(p->kv, kv0, kv1, cross.final0 + j0 + n - 1, t.pad4);
       ct.push_back(CrossTile{static_cast<int32_t>(cross.row + j0), n, cross.final0 + j0, kv0, end});
       max_pages = std::max(max_pages, end - kv0);
       p->rows_cross.push_back(Plan::RowRun{cross.row + j0, n});
@@ -408,9 +422,11 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     splits = static_cast<int32_t>(std::max<int64_t>(1, std::min(want, cap)));
   }
   p->kv_splits = splits;
+  const int32_t align = t.pad4 ? 4 : 1;
   for (const CrossTile& c : ct) {
     int32_t n_pages = c.kv1 - c.kv0;
     int32_t chunk = (n_pages + splits - 1) / splits;
+    chunk = ((chunk + align - 1) / align) * align;   // splits cut at whole tiles
     int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
     if (parts <= 1) {
       p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});

@@ -59,6 +59,7 @@ struct Tiling {
   int kv_heads = 1;      // work items per tile (one per kv head)
   int target_items = 512;     // work-groups the cross launch aims for (KV splits x tiles x heads)
   int min_split_pages = 16;   // at least 256 keys per KV split
+  bool pad4 = false;          // pad span runs to 4-page tiles (MFMA kernel)
 };
 
 class PoolIndex;

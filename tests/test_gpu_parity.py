@@ -108,7 +108,10 @@ def _page_kv(run, page_id, wl):
         raw = (raw.astype(np.uint32) << 16).view(np.float32)
     hkv, d = wl.n_kv_heads, wl.head_dim
     k = raw[: hkv * 16 * d].reshape(hkv, 16, d)
-    v = raw[hkv * 16 * d:].reshape(hkv, d, 16).transpose(0, 2, 1)
+    vt = raw[hkv * 16 * d:].reshape(hkv, d, 16)
+    # slot s of a page sits at position s with bits 2 and 3 swapped
+    vpos = [(s & 3) | ((s & 4) << 1) | ((s & 8) >> 1) for s in range(16)]
+    v = vt[:, :, vpos].transpose(0, 2, 1)
     return k, v
 
 
