@@ -200,9 +200,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int64_t page_elems = 2ll * hkv * kPage * D;
   const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
 
-  // ---- first two key tiles in flight while the query rows are loaded and rotated
+  // ---- first key tiles in flight while the query rows are loaded and rotated
+  // (three ahead for the software-pipelined loop, two for the repositioning one)
+  constexpr int AHEAD = ROT ? 2 : 3;
   TilePages tp;
-  for (int j = 0; j < 2 && j < n_tiles; ++j) {
+  for (int j = 0; j < AHEAD && j < n_tiles; ++j) {
     read_pages(kv, t.kv_begin + 4 * j, tp);
     issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + j * GE::STAGE, rope, wave, lane);
   }
@@ -269,50 +271,16 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   float m = -INFINITY;
   float l = 0.f;
 
-  for (int j = 0; j < n_tiles; ++j) {
-    if (j + 2 < n_tiles) {
-      read_pages(kv, t.kv_begin + 4 * (j + 2), tp);
-      issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + ((j + 2) & 3) * GE::STAGE, rope, wave, lane);
-    }
-    const int ahead = min(2, n_tiles - 1 - j);  // tiles issued after tile j
-    wait_vm(ahead * NDMA);
-    block_sync();
+  const int xor32_addr = (lane ^ 32) << 2;  // ds_bpermute byte address of the other half-wave
 
-    TilePages cur;
-    read_pages(kv, t.kv_begin + 4 * j, cur);
-    const unsigned char* stage = lds + (j & 3) * GE::STAGE;
+  // ---- building blocks of one 64-key tile
+  // S^T = K Q^T over the tile (two 32-key blocks, interleaved accumulator chains)
+  auto qk = [&](const unsigned char* stage, f32x16_t (&sc)[2]) {
     const bf16_t* kl = reinterpret_cast<const bf16_t*>(stage);
-    const bf16_t* vl = reinterpret_cast<const bf16_t*>(stage + GE::KBYTES);
-
-    if (ROT && cur.delta != q_delta) {
-      // query at (position - delta) = R(-delta) applied to the query at delta 0
-      q_delta = cur.delta;
-      const float2* row_cs = reinterpret_cast<const float2*>(stage + GE::KBYTES + GE::VBYTES);
-#pragma unroll
-      for (int s = 0; s < GE::KS / 2; ++s) {
-        const u32x4_t a4 = __builtin_bit_cast(u32x4_t, qbase[s]);
-        const u32x4_t b4 = __builtin_bit_cast(u32x4_t, qbase[s + GE::KS / 2]);
-        u32x4_t na, nb;
-        const float4* cs4 = reinterpret_cast<const float4*>(row_cs + 16 * s + 8 * h2);
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float4 v = cs4[w];  // (cos, sin) of frequencies 16s + 8h2 + 2w and +1
-          const float a0 = lo_bf16(a4[w]), a1 = hi_bf16(a4[w]);
-          const float b0 = lo_bf16(b4[w]), b1 = hi_bf16(b4[w]);
-          na[w] = pack_bf16x2(a0 * v.x + b0 * v.y, a1 * v.z + b1 * v.w);
-          nb[w] = pack_bf16x2(b0 * v.x - a0 * v.y, b1 * v.z - a1 * v.w);
-        }
-        qf[s] = __builtin_bit_cast(bf16x8_t, na);
-        qf[s + GE::KS / 2] = __builtin_bit_cast(bf16x8_t, nb);
-      }
-    }
-
-    // ---- S^T = K Q^T over 64 keys (two 32-key blocks, interleaved chains)
-    f32x16_t s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
+      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < GE::KS; ++ks)
 #pragma unroll
@@ -320,10 +288,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const int key = 32 * kb + r;
         const int c = (2 * ks + h2) ^ kswz<D>(key);
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kl + key * D + 8 * c);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[kb], 0, 0, 0);
+        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sc[kb], 0, 0, 0);
       }
-
-    // ---- mask: causal positions and partial/empty pages (wave-uniform test)
+  };
+  // causal positions and partial/empty pages; the test is wave-uniform
+  auto mask = [&](f32x16_t (&sc)[2], const TilePages& cur) {
     bool need = false;
 #pragma unroll
     for (int p = 0; p < 4; ++p) need |= (cur.nv[p] < kPage) || (cur.pos0[p] + kPage - 1 > wave_min_pos);
@@ -336,32 +305,36 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const int p = 2 * kb + (i >> 3);
           const int slot = 8 * ((i >> 2) & 1) + 4 * h2 + (i & 3);
           const bool ok = slot < cur.nv[p] && cur.pos0[p] + slot <= qpos;
-          if (!ok) s[kb][i] = -INFINITY;
+          if (!ok) sc[kb][i] = -INFINITY;
         }
     }
-
-    // ---- online softmax (base 2; scores already scaled), one max per tile
+  };
+  // online softmax (base 2; scores already scaled), one running max per tile
+  auto softmax_max = [&](const f32x16_t (&sc)[2]) -> float {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[kb][i]);
+    mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(mx))));
     const float m_new = fmaxf(m, mx);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     const float corr = __builtin_amdgcn_exp2f(m - m_use);
     m = m_new;
-    // the running max moves on few tiles once it has settled: rescale only then
-    if (__any(corr != 1.f)) {
+    // the running max moves on few tiles once it has settled: rescale only then (a
+    // real branch; the empty volatile asm keeps the compiler from if-converting it)
+    if (__builtin_expect(__any(corr != 1.f), 0)) {
+      __asm__ volatile("");
 #pragma unroll
       for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= corr;
     }
     l *= corr;
-
-    // ---- P = 2^(S - m) to bf16, then O^T += V^T P^T (step g covers page g of the tile)
-    bf16x8_t pk[4];
+    return m_use;
+  };
+  // P = 2^(S - m) to bf16; step g of the P.V contraction covers page g of the tile
+  auto softmax_exp = [&](const f32x16_t (&sc)[2], float m_use, bf16x8_t (&pk)[4]) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int kb = g >> 1, half = g & 1;
@@ -369,14 +342,18 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       u32x4_t w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(s[kb][8 * half + 2 * e] - m_use);
-        const float p1 = __builtin_amdgcn_exp2f(s[kb][8 * half + 2 * e + 1] - m_use);
+        const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e] - m_use);
+        const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e + 1] - m_use);
         psum += p0 + p1;
         w[e] = pack_bf16x2(p0, p1);
       }
       l += psum;
       pk[g] = __builtin_bit_cast(bf16x8_t, w);
     }
+  };
+  // O^T += V^T P^T
+  auto pv = [&](const unsigned char* stage, const bf16x8_t (&pk)[4]) {
+    const bf16_t* vl = reinterpret_cast<const bf16_t*>(stage + GE::KBYTES);
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
@@ -386,10 +363,95 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vl + d * kBN + 8 * c);
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[g], o[db], 0, 0, 0);
       }
+  };
+  // query at (position - delta) = R(-delta) applied to the query at delta 0
+  auto rotate_q = [&](const unsigned char* stage) {
+    const float2* row_cs = reinterpret_cast<const float2*>(stage + GE::KBYTES + GE::VBYTES);
+#pragma unroll
+    for (int s = 0; s < GE::KS / 2; ++s) {
+      const u32x4_t a4 = __builtin_bit_cast(u32x4_t, qbase[s]);
+      const u32x4_t b4 = __builtin_bit_cast(u32x4_t, qbase[s + GE::KS / 2]);
+      u32x4_t na, nb;
+      const float4* cs4 = reinterpret_cast<const float4*>(row_cs + 16 * s + 8 * h2);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float4 v = cs4[w];  // (cos, sin) of frequencies 16s + 8h2 + 2w and +1
+        const float a0 = lo_bf16(a4[w]), a1 = hi_bf16(a4[w]);
+        const float b0 = lo_bf16(b4[w]), b1 = hi_bf16(b4[w]);
+        na[w] = pack_bf16x2(a0 * v.x + b0 * v.y, a1 * v.z + b1 * v.w);
+        nb[w] = pack_bf16x2(b0 * v.x - a0 * v.y, b1 * v.z - a1 * v.w);
+      }
+      qf[s] = __builtin_bit_cast(bf16x8_t, na);
+      qf[s + GE::KS / 2] = __builtin_bit_cast(bf16x8_t, nb);
+    }
+  };
+
+  if constexpr (!ROT) {
+    // ---- software pipeline: scores of tile j+1 are formed (MFMA) while the softmax
+    // of tile j runs (VALU / transcendental), then tile j's P.V.  Stages in use during
+    // iteration j: j (V), j+1 (K), j+2 and j+3 (in flight).
+    // One step consumes the scores `cur` of tile j and forms `nxt` for tile j+1; for
+    // the last tile the extra QK reads a stale stage and its result is dropped (that
+    // keeps the step free of branches around the MFMAs it interleaves).
+    auto step = [&](int j, f32x16_t (&cur)[2], f32x16_t (&nxt)[2]) {
+      wait_vm((j + 2 < n_tiles ? 1 : 0) * NDMA);  // tile j+1 landed (only j+2 may be in flight)
+      block_sync();                                // ... for every wave; tile j-1 is done
+      if (j + 3 < n_tiles) {
+        read_pages(kv, t.kv_begin + 4 * (j + 3), tp);
+        issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + ((j + 3) & 3) * GE::STAGE, rope, wave,
+                           lane);
+      }
+      TilePages pg;
+      read_pages(kv, t.kv_begin + 4 * j, pg);
+      mask(cur, pg);
+      const float m_use = softmax_max(cur);
+      bf16x8_t pk[4];
+      softmax_exp(cur, m_use, pk);
+      qk(lds + ((j + 1) & 3) * GE::STAGE, nxt);
+      pv(lds + (j & 3) * GE::STAGE, pk);
+    };
+    f32x16_t sa[2], sb[2];
+    if (n_tiles > 0) {
+      wait_vm(min(2, n_tiles - 1) * NDMA);
+      block_sync();
+      qk(lds, sa);
+    }
+    int j = 0;
+    for (; j + 1 < n_tiles; j += 2) {
+      step(j, sa, sb);
+      step(j + 1, sb, sa);
+    }
+    if (j < n_tiles) step(j, sa, sb);
+  } else {
+    for (int j = 0; j < n_tiles; ++j) {
+      if (j + 2 < n_tiles) {
+        read_pages(kv, t.kv_begin + 4 * (j + 2), tp);
+        issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + ((j + 2) & 3) * GE::STAGE, rope, wave,
+                           lane);
+      }
+      const int ahead = min(2, n_tiles - 1 - j);  // tiles issued after tile j
+      wait_vm(ahead * NDMA);
+      block_sync();
+
+      TilePages cur;
+      read_pages(kv, t.kv_begin + 4 * j, cur);
+      const unsigned char* stage = lds + (j & 3) * GE::STAGE;
+      if (cur.delta != q_delta) {
+        q_delta = cur.delta;
+        rotate_q(stage);
+      }
+      f32x16_t sc[2];
+      qk(stage, sc);
+      mask(sc, cur);
+      const float m_use = softmax_max(sc);
+      bf16x8_t pk[4];
+      softmax_exp(sc, m_use, pk);
+      pv(stage, pk);
+    }
   }
 
   // ---- epilogue
-  const float l_row = l + __shfl_xor(l, 32);
+  const float l_row = l + __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(l)));
   if (!row_ok) return;
   const int64_t orow = static_cast<int64_t>(t.q_row0 + row);
   if (t.part < 0) {
