@@ -37,6 +37,52 @@ METRIC = "span-prefill attention TFLOP/s + cache-hit TTFT (ms), 16×512-tok frag
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
+# Measured HBM traffic of the span-prefill kernel lives in a profile summary, tagged
+# with a digest of the sources that decide it (kernel, tiling, planner); once any of
+# them changes the figure is stale and `traffic` is reported as null.
+TRAFFIC_FILE = {"c2": "profiles/span_prefill_attention_c2_traffic.md",
+                "c3": "profiles/span_prefill_attention_c3_traffic.md"}
+TRAFFIC_SOURCES = ["paper_2511_02749_amd/csrc/attn_mfma.hip", "paper_2511_02749_amd/csrc/planner.cpp",
+                   "paper_2511_02749_amd/csrc/planner.h", "paper_2511_02749_amd/csrc/work.h"]
+
+
+def sources_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config):
+    """HBM bytes per launch of the span-prefill kernel from the committed counter
+    summary, or None if it is missing or was taken on other sources."""
+    path = os.path.join(ROOT, TRAFFIC_FILE[config])
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json:"):
+                rec = json.loads(line.split(":", 1)[1])
+                if rec.get("sources") == sources_digest():
+                    return rec["traffic_bytes"]
+    return None
+
+
+def copy_calibration(mib, reps=5):
+    """A plain streaming copy (y = x * 1, float32) of `mib` MiB, for scaling the HBM
+    byte counters: each launch reads and writes exactly mib MiB."""
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"bytes_read": n * 4, "bytes_written": n * 4, "launches": reps}}),
+          flush=True)
+
 
 def _pct(xs, p):
     import numpy as np
@@ -86,6 +132,8 @@ def main():
     ap.add_argument("--ttft-reps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the span-query path here is a single-GPU build "
@@ -100,6 +148,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
+        return
     t_gen = time.perf_counter()
     wl = W.config_c2() if args.config == "c2" else W.config_c3()
     batch = wl.batches[0]
@@ -148,6 +199,9 @@ def main():
     k1_tflops = k1_flops / (mean["prefill_attention_ms"] * 1e-3) / 1e12
     k2_tflops = k2_flops / (mean["cross_attention_ms"] * 1e-3) / 1e12
     kv_bytes_page = 2 * wl.n_kv_heads * 16 * wl.head_dim * 2
+    # least HBM bytes one span-prefill launch must move: its query rows in, its output
+    # rows out (bf16), every newly written K/V page read once
+    k1_bytes = 2 * st["tokens_new"] * wl.n_q_heads * wl.head_dim * 2 + st["pages_new"] * kv_bytes_page
     print(f"[bench] step {ms_step:.3f} ms; K1 {mean['prefill_attention_ms']:.3f} ms {k1_tflops:.1f} TFLOP/s; "
           f"K2 {mean['cross_attention_ms']:.3f} ms {k2_tflops:.1f} TFLOP/s; combine {mean['combine_ms']:.3f} ms; "
           f"host plan {host_plan_us:.0f} us upload {host_upload_us:.0f} us", file=sys.stderr, flush=True)
@@ -247,7 +301,8 @@ def main():
         },
         "roofline": {"kernel": "span_prefill_attention", "bound": "mfma", "achieved": k1_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": k1_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": None},
+                     "traffic": measured_traffic(args.config) if args.kernel != "generic" else None,
+                     "algorithmic_bytes": k1_bytes, "launch_flops": k1_flops},
         "ttft": ttft,
         "cpu_baseline": cpu,
     }

@@ -76,7 +76,7 @@ extern "C" {
 #define SPAN_FLAG_TIMING 1    /* bracket every kernel launch with HIP events (span_plan_kernel_times) */
 
 typedef struct span_pool span_pool;
-typedef struct span_plan span_plan;
+typedef struct span_plan_t span_plan_t;
 
 typedef struct {
   int32_t num_layers;   /* >= 1; each layer has its own page slab */
@@ -186,8 +186,8 @@ typedef struct {
  * (cross pages).  The device work lists are copied once, on `stream`.
  * SPAN_ENOMEM (pool unchanged) if the batch needs more pages than are free or
  * evictable.  Host-only pools plan but cannot run attention. */
-int span_plan_create(span_pool* pool, const span_query* queries, int32_t n_queries, void* stream,
-                     span_plan** out);
+int span_plan(span_pool* pool, const span_query* queries, int32_t n_queries, void* stream,
+              span_plan_t** out);
 
 typedef struct {
   int64_t pages_hit;        /* prefix/fragment pages served from cache (incl. batch dedup) */
@@ -206,20 +206,20 @@ typedef struct {
   double host_plan_us;      /* host time of hashing, lookup, allocation and work lists */
   double host_upload_us;    /* host time of device metadata allocation + copy enqueue */
 } span_stats;
-int span_plan_stats(const span_plan* plan, span_stats* stats);
+int span_plan_stats(const span_plan_t* plan, span_stats* stats);
 
 /* Block table of one span: span = -1 prefix, 0..n_frags-1 fragment children,
  * n_frags cross.  Writes up to cap page ids; *n = pages of the span, *n_hit =
  * leading pages that were hits. */
-int span_plan_block_table(const span_plan* plan, int32_t query, int32_t span, int32_t* page_ids,
+int span_plan_block_table(const span_plan_t* plan, int32_t query, int32_t span, int32_t* page_ids,
                           int32_t cap, int32_t* n, int32_t* n_hit);
 
 /* Page ids evicted by this plan, in eviction order. */
-int span_plan_evicted(const span_plan* plan, int32_t* page_ids, int32_t cap, int32_t* n);
+int span_plan_evicted(const span_plan_t* plan, int32_t* page_ids, int32_t cap, int32_t* n);
 
 /* Caller rows the plan reads (q, k, v) and writes (out): the new prefix/fragment
  * token rows (prefill) then the cross rows, in work order. */
-int span_plan_rows(const span_plan* plan, int64_t* rows, int64_t cap, int64_t* n_prefill,
+int span_plan_rows(const span_plan_t* plan, int64_t* rows, int64_t cap, int64_t* n_prefill,
                    int64_t* n_cross);
 
 /* ---------------------------------------------------------------- attention */
@@ -229,7 +229,7 @@ int span_plan_rows(const span_plan* plan, int64_t* rows, int64_t cap, int64_t* n
  * token j at P + j), write keys and values into their pages, then write out[row] =
  * softmax over the span mask of q.k / sqrt(d) times V, with the query also at its
  * canonical position.  No-op when every page hit. */
-int span_prefill_fragments(span_plan* plan, int32_t layer, const void* q, const void* k,
+int span_prefill_fragments(span_plan_t* plan, int32_t layer, const void* q, const void* k,
                            const void* v, void* out, void* stream);
 
 /* Cross attention for one layer (sections 5.5, 5.6): write the cross tokens' keys
@@ -238,18 +238,18 @@ int span_prefill_fragments(span_plan* plan, int32_t layer, const void* q, const 
  * all at final positions (index in prefix | F_s1 | ... | F_sn | cross).  Cached
  * fragment keys are rotated by (final - canonical) position as they are read; pages
  * are never rewritten.  Must follow span_prefill_fragments for the same layer. */
-int span_cross_attend(span_plan* plan, int32_t layer, const void* q, const void* k, const void* v,
+int span_cross_attend(span_plan_t* plan, int32_t layer, const void* q, const void* k, const void* v,
                       void* out, void* stream);
 
 /* Publish the plan's new prefix/fragment pages in the cache index, unpin its pages
  * and free its cross pages.  Call after the last layer's kernels are enqueued; pages
  * released here may be reused by the next plan's kernels, so a next plan on another
  * stream must be ordered after this plan's work by the caller. */
-int span_plan_commit(span_plan* plan);
+int span_plan_commit(span_plan_t* plan);
 
 /* Free the plan.  Without a prior commit its new pages are freed unpublished and its
  * hits unpinned.  Device metadata is released on the plan's stream. */
-int span_plan_destroy(span_plan* plan);
+int span_plan_destroy(span_plan_t* plan);
 
 /* ---------------------------------------------------------------- debug */
 
@@ -265,7 +265,7 @@ typedef struct {
   int32_t prefill_calls;
   int32_t cross_calls;
 } span_kernel_times;
-int span_plan_kernel_times(const span_plan* plan, span_kernel_times* times);
+int span_plan_kernel_times(const span_plan_t* plan, span_kernel_times* times);
 
 const char* span_last_error(void);
 

@@ -25,7 +25,7 @@ SPAN_HASH_FRAG_TAG = 0x13198A2E03707344
 EXPORTS = [
     "span_last_error", "span_hash_mix", "span_pool_bytes", "span_pool_create", "span_pool_destroy",
     "span_pool_reset", "span_pool_get_info", "span_pool_page_address", "span_pool_read_page",
-    "span_hash_pages", "kv_lookup", "span_plan_create", "span_plan_stats", "span_plan_block_table",
+    "span_hash_pages", "kv_lookup", "span_plan", "span_plan_stats", "span_plan_block_table",
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times",
 ]
@@ -108,7 +108,7 @@ def load():
         "span_pool_read_page": (I32, [VP, I32, I32, VP, ctypes.c_size_t]),
         "span_hash_pages": (I32, [U64, P(I32), I32, I32, I32, P(U64), P(I32)]),
         "kv_lookup": (I32, [VP, P(U64), I32, P(I32), P(I32)]),
-        "span_plan_create": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
+        "span_plan": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
@@ -259,7 +259,7 @@ class Plan:
         self.n_frags = [len(q.frags) for q in queries]
         self._h = ctypes.c_void_p()
         self._stream = _stream(stream)
-        _check(lib.span_plan_create(pool.handle, arr, len(queries), self._stream, ctypes.byref(self._h)))
+        _check(lib.span_plan(pool.handle, arr, len(queries), self._stream, ctypes.byref(self._h)))
         pool._plans.add(self)
 
     def stats(self) -> dict:

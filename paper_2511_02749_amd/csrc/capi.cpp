@@ -40,7 +40,7 @@ struct span_pool {
   void* dev = nullptr;
   bool owns_dev = false;
   bool use_mfma = false;
-  std::set<span_plan*> plans;
+  std::set<span_plan_t*> plans;
   std::vector<hipEvent_t> event_cache;  // reusable timing events
   float2* rope_tab = nullptr;           // (cos, sin) per [position][head_dim / 2]
   int64_t rope_n = 0;                   // positions in rope_tab
@@ -80,7 +80,7 @@ int ensure_rope_table(span_pool* p, int64_t need) {
 }
 }  // namespace
 
-struct span_plan {
+struct span_plan_t {
   span_pool* pool = nullptr;
   Plan plan;
   hipStream_t stream = nullptr;
@@ -135,9 +135,9 @@ void release_events(std::vector<std::vector<hipEvent_t>>& groups, std::vector<hi
 }  // namespace
 
 static int check_span(const span_tokens& s, const char* what) {
-  if (s.n < 0 || (s.n > 0 && !s.tokens)) return fail(SPAN_EINVAL, std::string("span_plan_create: bad ") + what);
+  if (s.n < 0 || (s.n > 0 && !s.tokens)) return fail(SPAN_EINVAL, std::string("span_plan: bad ") + what);
   if (s.n > 0 && (s.row < 0 || s.row + s.n > std::numeric_limits<int32_t>::max()))
-    return fail(SPAN_EINVAL, std::string("span_plan_create: ") + what + " rows must lie in [0, 2^31)");
+    return fail(SPAN_EINVAL, std::string("span_plan: ") + what + " rows must lie in [0, 2^31)");
   return SPAN_OK;
 }
 
@@ -230,12 +230,12 @@ int span_pool_create(const span_pool_config* c, span_pool** out) {
   return SPAN_OK;
 }
 
-int span_plan_destroy(span_plan* plan);
+int span_plan_destroy(span_plan_t* plan);
 
 int span_pool_destroy(span_pool* p) {
   if (!p) return fail(SPAN_EINVAL, "span_pool_destroy: null pool");
-  std::vector<span_plan*> live(p->plans.begin(), p->plans.end());
-  for (span_plan* pl : live) span_plan_destroy(pl);
+  std::vector<span_plan_t*> live(p->plans.begin(), p->plans.end());
+  for (span_plan_t* pl : live) span_plan_destroy(pl);
   if (p->cfg.device >= 0) (void)hipDeviceSynchronize();
   for (hipEvent_t e : p->event_cache) (void)hipEventDestroy(e);
   if (p->rope_tab) (void)hipFree(p->rope_tab);
@@ -247,7 +247,7 @@ int span_pool_destroy(span_pool* p) {
 
 int span_pool_reset(span_pool* p) {
   if (!p) return fail(SPAN_EINVAL, "span_pool_reset: null pool");
-  for (const span_plan* pl : p->plans)
+  for (const span_plan_t* pl : p->plans)
     if (!pl->committed) return fail(SPAN_ESTATE, "span_pool_reset: an uncommitted plan is alive");
   p->index->reset();
   return SPAN_OK;
@@ -323,8 +323,8 @@ int kv_lookup(const span_pool* p, const uint64_t* hashes, int32_t n, int32_t* pa
   return SPAN_OK;
 }
 
-int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan** out) {
-  if (!pool || !out || nq < 0 || (nq > 0 && !qs)) return fail(SPAN_EINVAL, "span_plan_create: bad argument");
+int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan_t** out) {
+  if (!pool || !out || nq < 0 || (nq > 0 && !qs)) return fail(SPAN_EINVAL, "span_plan: bad argument");
   *out = nullptr;
   std::vector<QueryIn> in(static_cast<size_t>(nq));
   for (int32_t i = 0; i < nq; ++i) {
@@ -332,9 +332,9 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
     int rc = check_span(q.prefix, "prefix");
     if (!rc) rc = check_span(q.cross, "cross");
     if (rc) return rc;
-    if (q.n_frags < 0 || (q.n_frags > 0 && !q.frags)) return fail(SPAN_EINVAL, "span_plan_create: bad fragment list");
+    if (q.n_frags < 0 || (q.n_frags > 0 && !q.frags)) return fail(SPAN_EINVAL, "span_plan: bad fragment list");
     if (pool->cfg.hash_mode == SPAN_HASH_STOCK && (q.n_frags != 0 || q.cross.n != 0))
-      return fail(SPAN_EINVAL, "span_plan_create: stock hashing takes prefix-only queries");
+      return fail(SPAN_EINVAL, "span_plan: stock hashing takes prefix-only queries");
     in[i].prefix = SpanIn{q.prefix.tokens, q.prefix.n, q.prefix.row};
     in[i].cross = SpanIn{q.cross.tokens, q.cross.n, q.cross.row};
     for (int32_t f = 0; f < q.n_frags; ++f) {
@@ -343,21 +343,14 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
       in[i].frags.push_back(SpanIn{q.frags[f].tokens, q.frags[f].n, q.frags[f].row});
     }
   }
-  span_plan* pl = new (std::nothrow) span_plan();
-  if (!pl) return fail(SPAN_ENOMEM, "span_plan_create: host allocation");
+  span_plan_t* pl = new (std::nothrow) span_plan_t();
+  if (!pl) return fail(SPAN_ENOMEM, "span_plan: host allocation");
   pl->pool = pool;
   pl->stream = static_cast<hipStream_t>(stream);
   const bool device = pool->cfg.device >= 0;
   pl->mfma = device && pool->use_mfma;
   pl->bm = pl->mfma ? mfma_bm(pool->cfg.num_q_heads / pool->cfg.num_kv_heads) : kGenericBM;
-  Tiling t;
-  t.bm_prefill = pl->bm;
-  t.bm_cross = pl->bm;
-  t.kv_heads = pl->mfma ? pool->cfg.num_kv_heads : pool->cfg.num_q_heads;
-  // The MFMA kernel runs two 4-wave work-groups per CU: aim the cross launch at two
-  // per CU (512 on MI355X); the generic kernel is latency-bound and wants more.
-  t.target_items = pl->mfma ? 512 : 1024;
-  t.pad4 = pl->mfma;
+  const Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
   std::string msg;
   const auto t_plan0 = std::chrono::steady_clock::now();
   int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
@@ -374,7 +367,7 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
     hipError_t e = hipSetDevice(pool->cfg.device);
     if (e != hipSuccess) {
       span_plan_destroy(pl);
-      return hip_fail(e, "span_plan_create: hipSetDevice");
+      return hip_fail(e, "span_plan: hipSetDevice");
     }
     rc = ensure_rope_table(pool, P.max_pos + 1);
     if (rc) {
@@ -394,7 +387,7 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
     }
     if (e != hipSuccess) {
       span_plan_destroy(pl);
-      return hip_fail(e, "span_plan_create: device metadata");
+      return hip_fail(e, "span_plan: device metadata");
     }
     pl->host_upload_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t_plan1).count();
     pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
@@ -408,7 +401,7 @@ int span_plan_create(span_pool* pool, const span_query* qs, int32_t nq, void* st
   return SPAN_OK;
 }
 
-int span_plan_stats(const span_plan* pl, span_stats* s) {
+int span_plan_stats(const span_plan_t* pl, span_stats* s) {
   if (!pl || !s) return fail(SPAN_EINVAL, "span_plan_stats: null argument");
   const Plan& P = pl->plan;
   s->pages_hit = P.pages_hit;
@@ -429,7 +422,7 @@ int span_plan_stats(const span_plan* pl, span_stats* s) {
   return SPAN_OK;
 }
 
-int span_plan_block_table(const span_plan* pl, int32_t query, int32_t span, int32_t* ids, int32_t cap, int32_t* n,
+int span_plan_block_table(const span_plan_t* pl, int32_t query, int32_t span, int32_t* ids, int32_t cap, int32_t* n,
                           int32_t* n_hit) {
   if (!pl || !n || !n_hit || cap < 0 || (cap > 0 && !ids)) return fail(SPAN_EINVAL, "span_plan_block_table: bad argument");
   const Plan& P = pl->plan;
@@ -445,7 +438,7 @@ int span_plan_block_table(const span_plan* pl, int32_t query, int32_t span, int3
   return SPAN_OK;
 }
 
-int span_plan_evicted(const span_plan* pl, int32_t* ids, int32_t cap, int32_t* n) {
+int span_plan_evicted(const span_plan_t* pl, int32_t* ids, int32_t cap, int32_t* n) {
   if (!pl || !n || cap < 0 || (cap > 0 && !ids)) return fail(SPAN_EINVAL, "span_plan_evicted: bad argument");
   const auto& ev = pl->plan.evicted;
   *n = static_cast<int32_t>(ev.size());
@@ -453,7 +446,7 @@ int span_plan_evicted(const span_plan* pl, int32_t* ids, int32_t cap, int32_t* n
   return SPAN_OK;
 }
 
-int span_plan_rows(const span_plan* pl, int64_t* rows, int64_t cap, int64_t* n_prefill, int64_t* n_cross) {
+int span_plan_rows(const span_plan_t* pl, int64_t* rows, int64_t cap, int64_t* n_prefill, int64_t* n_cross) {
   if (!pl || !n_prefill || !n_cross || cap < 0 || (cap > 0 && !rows)) return fail(SPAN_EINVAL, "span_plan_rows: bad argument");
   const Plan& P = pl->plan;
   *n_prefill = 0;
@@ -467,7 +460,7 @@ int span_plan_rows(const span_plan* pl, int64_t* rows, int64_t cap, int64_t* n_p
   return SPAN_OK;
 }
 
-static int attention_common(span_plan* pl, int32_t layer, const char* who) {
+static int attention_common(span_plan_t* pl, int32_t layer, const char* who) {
   if (!pl) return fail(SPAN_EINVAL, std::string(who) + ": null plan");
   if (pl->pool->cfg.device < 0) return fail(SPAN_ESTATE, std::string(who) + ": host-only pool");
   if (pl->committed) return fail(SPAN_ESTATE, std::string(who) + ": plan already committed");
@@ -475,14 +468,14 @@ static int attention_common(span_plan* pl, int32_t layer, const char* who) {
   return SPAN_OK;
 }
 
-static PoolGeom geom(const span_plan* pl, int32_t layer) {
+static PoolGeom geom(const span_plan_t* pl, int32_t layer) {
   const span_pool_config& c = pl->pool->cfg;
   const int64_t page_elems = 2ll * c.num_kv_heads * c.page_size * c.head_dim;
   return PoolGeom{pl->pool->dev, static_cast<int64_t>(layer) * c.num_pages * page_elems, c.num_q_heads,
                   c.num_kv_heads, c.head_dim, c.dtype};
 }
 
-int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
+int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
                            void* stream) {
   int rc = attention_common(pl, layer, "span_prefill_fragments");
   if (rc) return rc;
@@ -505,7 +498,7 @@ int span_prefill_fragments(span_plan* pl, int32_t layer, const void* q, const vo
   return SPAN_OK;
 }
 
-int span_cross_attend(span_plan* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
+int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
                       void* stream) {
   int rc = attention_common(pl, layer, "span_cross_attend");
   if (rc) return rc;
@@ -539,7 +532,7 @@ static float elapsed(hipEvent_t a, hipEvent_t b) {
   return ms;
 }
 
-int span_plan_kernel_times(const span_plan* pl, span_kernel_times* t) {
+int span_plan_kernel_times(const span_plan_t* pl, span_kernel_times* t) {
   if (!pl || !t) return fail(SPAN_EINVAL, "span_plan_kernel_times: null argument");
   std::memset(t, 0, sizeof(*t));
   for (const auto& ev : pl->ev_prefill) {
@@ -556,7 +549,7 @@ int span_plan_kernel_times(const span_plan* pl, span_kernel_times* t) {
   return SPAN_OK;
 }
 
-int span_plan_commit(span_plan* pl) {
+int span_plan_commit(span_plan_t* pl) {
   if (!pl) return fail(SPAN_EINVAL, "span_plan_commit: null plan");
   if (pl->committed) return fail(SPAN_ESTATE, "span_plan_commit: already committed");
   pl->pool->index->commit(&pl->plan);
@@ -564,7 +557,7 @@ int span_plan_commit(span_plan* pl) {
   return SPAN_OK;
 }
 
-int span_plan_destroy(span_plan* pl) {
+int span_plan_destroy(span_plan_t* pl) {
   if (!pl) return fail(SPAN_EINVAL, "span_plan_destroy: null plan");
   if (!pl->committed) pl->pool->index->release(&pl->plan);
   release_events(pl->ev_prefill, pl->pool->event_cache);

@@ -62,6 +62,21 @@ struct Tiling {
   bool pad4 = false;          // pad span runs to 4-page tiles (MFMA kernel)
 };
 
+// Work-list shape for the attention kernels.  The MFMA kernel (one work-group per
+// row tile and kv head) holds a CU with one 8-wave work-group, its LDS ring taking
+// 132 KiB at head_dim 128: the cross launch aims at two rounds over the 256 CUs.
+// The generic kernel (one wave per row tile and query head) is latency-bound and
+// wants more work-groups.
+inline Tiling tiling_for(bool mfma, int bm, int hq, int hkv) {
+  Tiling t;
+  t.bm_prefill = bm;
+  t.bm_cross = bm;
+  t.kv_heads = mfma ? hkv : hq;
+  t.target_items = mfma ? 512 : 1024;
+  t.pad4 = mfma;
+  return t;
+}
+
 class PoolIndex;
 
 struct Plan {
