@@ -10,10 +10,14 @@
   one-hot segment values the output is the exact fraction of allowed keys in
   each segment.
 * Rotary identities: R(a)^T R(b) = R(b - a).
+* Brute force: on tiny inputs, a pure-Python loop over (row, key, dim) that
+  applies the visibility and position rules pair by pair agrees to 1e-12.
 * Invariants from the paper: permuting commuting children leaves each child's
   cached KV bit-identical; cached-then-repositioned keys equal keys encoded
   at their final positions.
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -212,3 +216,75 @@ def test_repositioned_cache_equals_encoding_at_final_positions():
         delta = lay.pos_final[sel] - lay.pos_canon[sel]
         moved = A.rope(kc, delta, theta)
         np.testing.assert_allclose(moved, A.rope(k[sel], lay.pos_final[sel], theta), atol=1e-12, rtol=0)
+
+
+def _brute_force(q, k, v, P, Ls, Q, theta):
+    """Span attention from the rules alone, one (row, key, dim) at a time in plain
+    Python floats: who may see whom (prefix causal; fragment rows see the prefix and
+    their own fragment causally; cross rows see everything before them), at which
+    positions (canonical for prefix/fragment rows, index in the sequence for cross
+    rows), rotate-half rotary, softmax with math.exp."""
+    seg, idx = [], []
+    for t in range(P):
+        seg.append(("p", 0)); idx.append(t)
+    for i, L in enumerate(Ls):
+        for j in range(L):
+            seg.append(("f", i)); idx.append(j)
+    for t in range(Q):
+        seg.append(("c", 0)); idx.append(t)
+    n = len(seg)
+    hq, hkv, d = q.shape[1], k.shape[1], q.shape[2]
+    half = d // 2
+
+    def sees(r, c):
+        (kr, ir), (kc, ic) = seg[r], seg[c]
+        if kr == "c":
+            return c <= r
+        if kr == "p":
+            return kc == "p" and c <= r
+        return kc == "p" or (kc == "f" and ic == ir and idx[c] <= idx[r])
+
+    def canon(t):
+        return idx[t] if seg[t][0] == "p" else P + idx[t] if seg[t][0] == "f" else P + sum(Ls) + idx[t]
+
+    def rot(x, pos):
+        out = [0.0] * d
+        for i in range(half):
+            a = pos * theta ** (-2.0 * i / d)
+            out[i] = x[i] * math.cos(a) - x[i + half] * math.sin(a)
+            out[i + half] = x[i + half] * math.cos(a) + x[i] * math.sin(a)
+        return out
+
+    out = np.zeros((n, hq, d))
+    for r in range(n):
+        for h in range(hq):
+            g = h * hkv // hq
+            pos = (lambda t: t) if seg[r][0] == "c" else canon
+            qr = rot([float(x) for x in q[r, h]], pos(r))
+            keys = [c for c in range(n) if sees(r, c)]
+            s = []
+            for c in keys:
+                kc = rot([float(x) for x in k[c, g]], pos(c))
+                s.append(sum(qr[i] * kc[i] for i in range(d)) / math.sqrt(d))
+            mx = max(s)
+            w = [math.exp(x - mx) for x in s]
+            z = sum(w)
+            for e in range(d):
+                out[r, h, e] = sum(w[j] * float(v[c, g, e]) for j, c in enumerate(keys)) / z
+    return out
+
+
+@pytest.mark.parametrize("P,Ls,Q,hq,hkv,d", [
+    (3, (4, 1, 2), 3, 2, 1, 4),     # three fragments, one of length 1
+    (0, (5, 3), 2, 2, 2, 2),        # no prefix
+    (2, (6,), 0, 4, 2, 4),          # one fragment, no cross segment
+    (4, (), 5, 2, 1, 6),            # no fragment
+    (1, (2, 2, 2, 2), 4, 2, 1, 4),  # equal lengths (order-sensitive index errors)
+])
+def test_brute_force_agrees_on_tiny_inputs(P, Ls, Q, hq, hkv, d):
+    n = P + sum(Ls) + Q
+    q, k, v = _rand((n, hq, d), 11), _rand((n, hkv, d), 12), _rand((n, hkv, d), 13)
+    lay = A.layout(P, Ls, Q)
+    got = A.span_attention(q, k, v, lay, 10000.0)
+    ref = _brute_force(q, k, v, P, Ls, Q, 10000.0)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
