@@ -1,13 +1,18 @@
 // bf16 MFMA span attention for gfx950 (CDNA4).
 //
-// One work-group of eight waves per (row tile of 256/G query tokens, kv head).  The
-// G query heads that share the kv head are packed into the work-group: wave w
-// handles head (w mod G) and token rows 32*(w div G) .. +31, so every K/V tile
-// staged in LDS feeds all eight waves.
+// Work items are (row tile of 256/G query tokens, kv head).  The G query heads that
+// share a kv head are packed into one item: wave w of the eight handles head
+// (w mod G) and token rows 32*(w div G) .. +31, so every K/V tile staged in LDS
+// feeds all eight waves.
+//
+// The kernel is persistent: one work-group per CU walks the items b, b + grid, ...
+// in order.  Key tiles of consecutive items form one stream through the LDS ring,
+// so the next item's first tiles are already in flight while the current item
+// finishes, and no work-group launch or ring refill sits between items.
 //
 // Scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
 //   A = K tile (32 keys x 16 dims, from LDS), B = Q^T (16 dims x 32 rows, kept in
-//   registers for the whole key loop), C = 32 keys x 32 rows.
+//   registers for the whole item), C = 32 keys x 32 rows.
 // In that C layout each lane owns one query row (lane mod 32) and 16 of the 32
 // keys, so the running max needs a single exchange between the two half-waves
 // and the row sum needs none until the end.  P^T is then already a valid B operand
@@ -18,10 +23,10 @@
 //
 // Keys are read in tiles of 4 pages (64 keys) through the block table.  Tiles go
 // straight from HBM to LDS (global_load_lds_dwordx4, no register staging) into a
-// ring of four stages, two tiles ahead of the one being computed; the LDS tiles
+// ring of four stages, three tiles ahead of the one being computed; the LDS tiles
 // are XOR-swizzled at 16-byte granularity so MFMA operand reads are free of bank
 // conflicts.  One barrier per tile: passing it means every wave has finished the
-// tile two back, whose stage the next prefetch overwrites.
+// previous tile, whose stage the next prefetch overwrites.
 //
 // Repositioning (cross rows over cached fragments): the planner pads each span's
 // run of pages to whole tiles, so all keys of a tile share one delta d between the
@@ -31,6 +36,7 @@
 // Cached pages are never rewritten.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -61,17 +67,25 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-template <int D>
+template <int D, bool ROT>
 struct Geo {
   static constexpr int KS = D / 16;                // 16-dim steps of the QK contraction
   static constexpr int DB = D / 32;                // 32-dim blocks of the output
   static constexpr int KBYTES = kBN * D * 2;       // K tile: [64 keys][D], rows of 2D bytes
   static constexpr int VBYTES = D * kBN * 2;       // V tile: [D][64 positions], rows of 128 bytes
-  static constexpr int RBYTES = 1024;              // cos/sin row of the tile's delta (4D bytes used)
+  static constexpr int RBYTES = ROT ? 1024 : 0;    // cos/sin row of the tile's delta (4D bytes used)
   static constexpr int STAGE = KBYTES + VBYTES + RBYTES;
   static constexpr int KPW = KBYTES / 1024 / kNW;  // K DMA instructions per wave per tile
   static constexpr int VPW = VBYTES / 1024 / kNW;  // V DMA instructions per wave per tile
   static constexpr int RPW = 4 * D / kNW;          // bytes of the cos/sin row per wave
+  static constexpr int NDMA = KPW + VPW + (ROT ? 1 : 0);  // DMA instructions per wave per tile
+  // Beyond the ring (query-side rotation of the non-repositioning kernel): the
+  // rotary rows of positions 0..31 for the whole kernel, and one rotary row per
+  // wave (its 32-row block's first position) for the next item.
+  static constexpr int CH = D / 4;                     // 16-byte chunks per rotary row
+  static constexpr int RTBYTES = ROT ? 0 : 32 * 4 * D;
+  static constexpr int BRBYTES = ROT ? 0 : kNW * 4 * D;
+  static constexpr int LDS = kStages * STAGE + RTBYTES + BRBYTES;
 };
 
 // 16-byte chunk swizzles: chunk c of K row `key` sits at c ^ kswz(key); chunk c of
@@ -83,21 +97,26 @@ __device__ __forceinline__ int kswz(int key) {
 }
 __device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
 
+// A tile's four pages come from one span: consecutive positions, and only the
+// span's last page may be partial (then followed by empty padding pages).  So key k
+// of the tile (0..63) is a real key iff k < nk, at position pos0 + k.
 struct TilePages {
   int id[4];
-  int nv[4];
-  int pos0[4];
-  int delta;
+  int pos0;   // position of key 0
+  int nk;     // real keys in the tile
+  int delta;  // reposition delta of every key of the tile
 };
 
 __device__ __forceinline__ void read_pages(const KvPage* __restrict__ kv, int first, TilePages& tp) {
+  int nk = 0;
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
     const KvPage pg = kv[first + p];
     tp.id[p] = pg.page_id;
-    tp.nv[p] = pg.n_valid;
-    tp.pos0[p] = pg.pos0;
+    nk += pg.n_valid;
   }
+  tp.nk = nk;
+  tp.pos0 = kv[first].pos0;
   tp.delta = kv[first].delta;
 }
 
@@ -122,6 +141,7 @@ __device__ __forceinline__ void wait_vm(int n) {
     case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
     case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
     case 10: __builtin_amdgcn_s_waitcnt(0x0F7A); break;
+    case 12: __builtin_amdgcn_s_waitcnt(0x0F7C); break;
     default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
   }
 }
@@ -137,7 +157,11 @@ template <int D, bool ROT>
 __device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
                                            int hkv, int kvh, const TilePages& tp, unsigned char* stage,
                                            const float2* __restrict__ rope, int wave, int lane) {
-  using G = Geo<D>;
+  using G = Geo<D, ROT>;
+  // The per-lane address parts are recomputed for every tile from an opaque copy of
+  // the lane id: hoisted out of the tile loop they would pin a dozen 64-bit
+  // registers for the whole kernel.
+  __asm__ volatile("" : "+v"(lane));
   // K rows: instruction q covers bytes [1024q, 1024q + 1024), keys of one page
 #pragma unroll
   for (int u = 0; u < G::KPW; ++u) {
@@ -173,105 +197,73 @@ __device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int6
   }
 }
 
+// Work item i: row tile i / hkv of the work list, kv head i % hkv.  The DMA side
+// only needs where the item's key list starts, its tile count and its kv head.
+struct ItemKeys {
+  int kv_begin;
+  int n;  // key tiles
+  int kvh;
+};
+
+__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tiles, int hkv, int i, ItemKeys& it) {
+  const WorkTile* t = tiles + i / hkv;
+  it.kv_begin = t->kv_begin;
+  it.n = (t->kv_end - t->kv_begin) >> 2;
+  it.kvh = i % hkv;
+}
+
 }  // namespace
 
 template <int D, int G, bool ROT>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
-    const WorkTile* __restrict__ tiles, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
+    const WorkTile* __restrict__ tiles, int n_items, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
-  using GE = Geo<D>;
+  using GE = Geo<D, ROT>;
   constexpr int BM = 32 * (kNW / G);
-  constexpr int NDMA = GE::KPW + GE::VPW + (ROT ? 1 : 0);  // DMA instructions per wave per tile
+  constexpr int NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
-  const WorkTile t = tiles[blockIdx.x];
-  const int kvh = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int head = kvh * G + (wave % G);
-  const int rb = wave / G;
+  const int hsub = wave % G;  // head inside the kv head's group
+  const int rb = wave / G;    // 32-row block
   const int h2 = lane >> 5;
   const int r = lane & 31;
   const int row = 32 * rb + r;
-  const bool row_ok = row < t.n_rows;
-  const int qpos = t.q_pos0 + row;
-  const int wave_min_pos = t.q_pos0 + 32 * rb;
   const int64_t page_elems = 2ll * hkv * kPage * D;
-  const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
-
-  // ---- first key tiles in flight while the query rows are loaded and rotated
-  // (three ahead for the software-pipelined loop, two for the repositioning one)
-  constexpr int AHEAD = ROT ? 2 : 3;
-  TilePages tp;
-  for (int j = 0; j < AHEAD && j < n_tiles; ++j) {
-    read_pages(kv, t.kv_begin + 4 * j, tp);
-    issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + j * GE::STAGE, rope, wave, lane);
-  }
-
-  // ---- Q^T operand, rotated at the row's position and pre-scaled by log2(e)/sqrt(d)
-  bf16x8_t qf[GE::KS];
-  {
-    float x[GE::KS][8];
-    if (row_ok) {
-      const bf16_t* src = q + (static_cast<int64_t>(t.q_row0 + row) * hq + head) * D + 8 * h2;
-#pragma unroll
-      for (int s = 0; s < GE::KS; ++s) {
-        const u32x4_t w = *reinterpret_cast<const u32x4_t*>(src + 16 * s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          x[s][2 * e] = lo_bf16(w[e]);
-          x[s][2 * e + 1] = hi_bf16(w[e]);
-        }
-      }
-#pragma unroll
-      for (int s = 0; s < GE::KS / 2; ++s) {
-        // frequencies 16s + 8h2 .. +7: 8 consecutive (cos, sin) pairs, 64 bytes
-        const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(qpos) * (D / 2) + 16 * s + 8 * h2);
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          const float4 v = cs4[e2];
-#pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int e = 2 * e2 + u;
-            const float cs = u ? v.z : v.x;
-            const float sn = u ? v.w : v.y;
-            const float a = x[s][e], b = x[s + GE::KS / 2][e];
-            x[s][e] = (a * cs - b * sn) * scale_log2;
-            x[s + GE::KS / 2][e] = (b * cs + a * sn) * scale_log2;
-          }
-        }
-      }
-    } else {
-#pragma unroll
-      for (int s = 0; s < GE::KS; ++s)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
-    }
-#pragma unroll
-    for (int s = 0; s < GE::KS; ++s) {
-      u32x4_t w;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(x[s][2 * e], x[s][2 * e + 1]);
-      qf[s] = __builtin_bit_cast(bf16x8_t, w);
-    }
-  }
-  bf16x8_t qbase[ROT ? GE::KS : 1];  // query at delta 0 (cross rows only)
-  if (ROT) {
-#pragma unroll
-    for (int s = 0; s < GE::KS; ++s) qbase[s] = qf[s];
-  }
-  int q_delta = 0;
-
-  f32x16_t o[GE::DB];
-#pragma unroll
-  for (int db = 0; db < GE::DB; ++db)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
-  float m = -INFINITY;
-  float l = 0.f;
-
   const int xor32_addr = (lane ^ 32) << 2;  // ds_bpermute byte address of the other half-wave
+  const int stride = gridDim.x;
+
+  // ---- DMA side of the tile stream: item `is_i`, its tile `is_j`
+  ItemKeys is;
+  int is_i = blockIdx.x, is_j = 0;
+  bool is_ok = is_i < n_items;
+  if (is_ok) load_item_keys(tiles, hkv, is_i, is);
+  int n_issued = 0;  // tiles of the stream issued so far
+  auto issue_next = [&]() {
+    while (is_ok && is_j >= is.n) {
+      is_i += stride;
+      is_j = 0;
+      is_ok = is_i < n_items;
+      if (is_ok) load_item_keys(tiles, hkv, is_i, is);
+    }
+    if (!is_ok) return;
+    TilePages tp;
+    read_pages(kv, is.kv_begin + 4 * is_j, tp);
+    issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, is.kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
+                       lane);
+    ++is_j;
+    ++n_issued;
+  };
+  for (int k = 0; k < kStages - 1; ++k) issue_next();
+
+  bf16x8_t qf[GE::KS];                // Q^T operand of the current item
+  bf16x8_t qbase[ROT ? GE::KS : 1];   // query at delta 0 (cross rows only)
+  f32x16_t o[GE::DB];
+  float m, l;
+  int q_delta = 0;
+  int qpos = 0, wave_min_pos = 0;
 
   // ---- building blocks of one 64-key tile
   // S^T = K Q^T over the tile (two 32-key blocks, interleaved accumulator chains)
@@ -293,19 +285,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   // causal positions and partial/empty pages; the test is wave-uniform
   auto mask = [&](f32x16_t (&sc)[2], const TilePages& cur) {
-    bool need = false;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) need |= (cur.nv[p] < kPage) || (cur.pos0[p] + kPage - 1 > wave_min_pos);
-    if (need) {
+    if (cur.nk < kBN || cur.pos0 + kBN - 1 > wave_min_pos) {
+      // key k is kept iff k < nk and pos0 + k <= qpos
+      const int lim = min(cur.nk, qpos - cur.pos0 + 1);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          // key 32kb + 8(i/4) + 4h2 + i%4 lies in page 2kb + i/8, slot 8((i/4)%2) + 4h2 + i%4
-          const int p = 2 * kb + (i >> 3);
-          const int slot = 8 * ((i >> 2) & 1) + 4 * h2 + (i & 3);
-          const bool ok = slot < cur.nv[p] && cur.pos0[p] + slot <= qpos;
-          if (!ok) sc[kb][i] = -INFINITY;
+          const int k = 32 * kb + 8 * (i >> 2) + 4 * h2 + (i & 3);
+          if (k >= lim) sc[kb][i] = -INFINITY;
         }
     }
   };
@@ -386,57 +374,167 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
 
+  // ---- query-side rotation of the non-repositioning kernel without scattered
+  // table reads: the rotary angles of row r (0..31) of a wave's 32-row block come
+  // from R(base + r) = R(base) R(r), with R(0..31) kept in LDS for the whole kernel
+  // and R(base) (base = the block's first position) brought into LDS by DMA
+  // together with the item's raw query.
+  unsigned char* const rt_lds = lds + kStages * GE::STAGE;
+  unsigned char* const br_lds = rt_lds + GE::RTBYTES + wave * 4 * D;
+  auto prefetch = [&](int ni, bf16x8_t (&qn)[GE::KS]) {
+    const WorkTile tn = tiles[ni / hkv];
+    const int headn = (ni % hkv) * G + hsub;
+    if (32 * rb < tn.n_rows && lane < GE::CH) {
+      const unsigned char* src =
+          reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tn.q_pos0 + 32 * rb) * (D / 2)) + 16 * lane;
+      dma16(src, br_lds);
+    }
+    if (row < tn.n_rows) {
+      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + row) * hq + headn) * D + 8 * h2;
+#pragma unroll
+      for (int s = 0; s < GE::KS; ++s) qn[s] = *reinterpret_cast<const bf16x8_t*>(src + 16 * s);
+    } else {
+#pragma unroll
+      for (int s = 0; s < GE::KS; ++s) qn[s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+    }
+  };
+  // qf <- R(position) qn * log2(e)/sqrt(d), rounded to bf16 once
+  auto rotate_next = [&](int n_rows, const bf16x8_t (&qn)[GE::KS]) {
+    wait_vm(0);  // this wave's base row and query have landed
+    __asm__ volatile("" ::: "memory");
+    if (32 * rb >= n_rows) {  // no row of this wave is real
+#pragma unroll
+      for (int s = 0; s < GE::KS; ++s) qf[s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+      return;
+    }
+    const float4* br = reinterpret_cast<const float4*>(br_lds);
+    const float4* rt = reinterpret_cast<const float4*>(rt_lds + r * 4 * D);
+#pragma unroll
+    for (int s = 0; s < GE::KS / 2; ++s) {
+      const u32x4_t a4 = __builtin_bit_cast(u32x4_t, qn[s]);
+      const u32x4_t b4 = __builtin_bit_cast(u32x4_t, qn[s + GE::KS / 2]);
+      u32x4_t na, nb;
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        // frequencies 16s + 8h2 + 2e2 and +1: one 16-byte chunk of each rotary row
+        const int ch = 8 * s + 4 * h2 + e2;
+        const float4 vb = br[ch];
+        const float4 vr = rt[ch ^ (r & (GE::CH - 1))];
+        float ra[2], rb2[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float cb = u ? vb.z : vb.x, sb = u ? vb.w : vb.y;
+          const float cr = u ? vr.z : vr.x, sr = u ? vr.w : vr.y;
+          const float cs = cb * cr - sb * sr;
+          const float sn = sb * cr + cb * sr;
+          const float a = u ? hi_bf16(a4[e2]) : lo_bf16(a4[e2]);
+          const float b = u ? hi_bf16(b4[e2]) : lo_bf16(b4[e2]);
+          ra[u] = (a * cs - b * sn) * scale_log2;
+          rb2[u] = (b * cs + a * sn) * scale_log2;
+        }
+        na[e2] = pack_bf16x2(ra[0], ra[1]);
+        nb[e2] = pack_bf16x2(rb2[0], rb2[1]);
+      }
+      qf[s] = __builtin_bit_cast(bf16x8_t, na);
+      qf[s + GE::KS / 2] = __builtin_bit_cast(bf16x8_t, nb);
+    }
+  };
   if constexpr (!ROT) {
-    // ---- software pipeline: scores of tile j+1 are formed (MFMA) while the softmax
-    // of tile j runs (VALU / transcendental), then tile j's P.V.  Stages in use during
-    // iteration j: j (V), j+1 (K), j+2 and j+3 (in flight).
-    // One step consumes the scores `cur` of tile j and forms `nxt` for tile j+1; for
-    // the last tile the extra QK reads a stale stage and its result is dropped (that
-    // keeps the step free of branches around the MFMAs it interleaves).
-    auto step = [&](int j, f32x16_t (&cur)[2], f32x16_t (&nxt)[2]) {
-      wait_vm((j + 2 < n_tiles ? 1 : 0) * NDMA);  // tile j+1 landed (only j+2 may be in flight)
-      block_sync();                                // ... for every wave; tile j-1 is done
-      if (j + 3 < n_tiles) {
-        read_pages(kv, t.kv_begin + 4 * (j + 3), tp);
-        issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + ((j + 3) & 3) * GE::STAGE, rope, wave,
-                           lane);
+    if (blockIdx.x < n_items) {
+      // rotary rows 0..31, chunk c of row r stored at chunk c ^ (r mod CH)
+      constexpr int RT_PER_WAVE = GE::RTBYTES / 1024 / kNW;
+#pragma unroll
+      for (int u = 0; u < RT_PER_WAVE; ++u) {
+        const int qi = wave * RT_PER_WAVE + u;
+        const int pos = qi * 64 + lane;  // 16-byte chunk index in the LDS table
+        const int rr = pos / GE::CH, cc = pos % GE::CH;
+        const unsigned char* src =
+            reinterpret_cast<const unsigned char*>(rope) + rr * 4 * D + 16 * (cc ^ (rr & (GE::CH - 1)));
+        dma16(src, rt_lds + qi * 1024);
       }
-      TilePages pg;
-      read_pages(kv, t.kv_begin + 4 * j, pg);
-      mask(cur, pg);
-      const float m_use = softmax_max(cur);
-      bf16x8_t pk[4];
-      softmax_exp(cur, m_use, pk);
-      qk(lds + ((j + 1) & 3) * GE::STAGE, nxt);
-      pv(lds + (j & 3) * GE::STAGE, pk);
-    };
-    f32x16_t sa[2], sb[2];
-    if (n_tiles > 0) {
-      wait_vm(min(2, n_tiles - 1) * NDMA);
-      block_sync();
-      qk(lds, sa);
+      bf16x8_t qn[GE::KS];
+      prefetch(blockIdx.x, qn);
+      wait_vm(0);
+      block_sync();  // every wave's share of the table has landed
+      rotate_next(tiles[blockIdx.x / hkv].n_rows, qn);
     }
-    int j = 0;
-    for (; j + 1 < n_tiles; j += 2) {
-      step(j, sa, sb);
-      step(j + 1, sb, sa);
-    }
-    if (j < n_tiles) step(j, sa, sb);
-  } else {
-    for (int j = 0; j < n_tiles; ++j) {
-      if (j + 2 < n_tiles) {
-        read_pages(kv, t.kv_begin + 4 * (j + 2), tp);
-        issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + ((j + 2) & 3) * GE::STAGE, rope, wave,
-                           lane);
-      }
-      const int ahead = min(2, n_tiles - 1 - j);  // tiles issued after tile j
-      wait_vm(ahead * NDMA);
-      block_sync();
+  }
 
+  int c = 0;  // stream index of the tile being computed
+  for (int ci = blockIdx.x; ci < n_items;) {
+    const WorkTile t = tiles[ci / hkv];
+    const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
+    const int head = (ci % hkv) * G + hsub;
+    const bool row_ok = row < t.n_rows;
+    const bool has_next = ci + stride < n_items;
+    qpos = t.q_pos0 + row;
+    wave_min_pos = t.q_pos0 + 32 * rb;
+
+    if constexpr (ROT) {
+      // ---- Q^T operand, rotated at the row's position and pre-scaled by log2(e)/sqrt(d)
+      float x[GE::KS][8];
+      if (row_ok) {
+        const bf16_t* src = q + (static_cast<int64_t>(t.q_row0 + row) * hq + head) * D + 8 * h2;
+#pragma unroll
+        for (int s = 0; s < GE::KS; ++s) {
+          const u32x4_t w = *reinterpret_cast<const u32x4_t*>(src + 16 * s);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            x[s][2 * e] = lo_bf16(w[e]);
+            x[s][2 * e + 1] = hi_bf16(w[e]);
+          }
+        }
+#pragma unroll
+        for (int s = 0; s < GE::KS / 2; ++s) {
+          // frequencies 16s + 8h2 .. +7: 8 consecutive (cos, sin) pairs, 64 bytes
+          const float4* cs4 =
+              reinterpret_cast<const float4*>(rope + static_cast<int64_t>(qpos) * (D / 2) + 16 * s + 8 * h2);
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            const float4 v = cs4[e2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int e = 2 * e2 + u;
+              const float cs = u ? v.z : v.x;
+              const float sn = u ? v.w : v.y;
+              const float a = x[s][e], b = x[s + GE::KS / 2][e];
+              x[s][e] = (a * cs - b * sn) * scale_log2;
+              x[s + GE::KS / 2][e] = (b * cs + a * sn) * scale_log2;
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < GE::KS; ++s)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
+      }
+#pragma unroll
+      for (int s = 0; s < GE::KS; ++s) {
+        u32x4_t w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(x[s][2 * e], x[s][2 * e + 1]);
+        qf[s] = __builtin_bit_cast(bf16x8_t, w);
+        qbase[s] = qf[s];
+      }
+      q_delta = 0;
+    }
+#pragma unroll
+    for (int db = 0; db < GE::DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+    m = -INFINITY;
+    l = 0.f;
+
+    // ---- key tiles of this item
+    auto tile = [&](int j) {
+      wait_vm(min(2, n_issued - 1 - c) * NDMA);  // tile c landed (tiles after it may be in flight)
+      block_sync();                              // ... for every wave; tile c - 1 is done
+      issue_next();                              // into the stage of tile c - 1
+      const unsigned char* stage = lds + (c & 3) * GE::STAGE;
       TilePages cur;
       read_pages(kv, t.kv_begin + 4 * j, cur);
-      const unsigned char* stage = lds + (j & 3) * GE::STAGE;
-      if (cur.delta != q_delta) {
+      if (ROT && cur.delta != q_delta) {
         q_delta = cur.delta;
         rotate_q(stage);
       }
@@ -447,40 +545,57 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       bf16x8_t pk[4];
       softmax_exp(sc, m_use, pk);
       pv(stage, pk);
-    }
-  }
+      ++c;
+    };
+    for (int j = 0; j < n_tiles; ++j) tile(j);
 
-  // ---- epilogue
-  const float l_row = l + __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(l)));
-  if (!row_ok) return;
-  const int64_t orow = static_cast<int64_t>(t.q_row0 + row);
-  if (t.part < 0) {
-    const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
-    bf16_t* dst = out + (orow * hq + head) * D;
+    // ---- epilogue of the item.  The next item's query is rotated first, so the
+    // output stores do not sit in front of that wait; the loop is only re-entered
+    // through that rotation, so no path carries a pending query load around it.
+    const float l_row = l + __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(l)));
+    auto store = [&]() {
+      if (!row_ok) return;
+      const int64_t orow = static_cast<int64_t>(t.q_row0 + row);
+      if (t.part < 0) {
+        const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
+        bf16_t* dst = out + (orow * hq + head) * D;
 #pragma unroll
-    for (int db = 0; db < GE::DB; ++db)
+        for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * db + 8 * g4 + 4 * h2;
-        const u32x2_t w = u32x2_t{pack_bf16x2(o[db][4 * g4] * inv, o[db][4 * g4 + 1] * inv),
-                                  pack_bf16x2(o[db][4 * g4 + 2] * inv, o[db][4 * g4 + 3] * inv)};
-        *reinterpret_cast<u32x2_t*>(dst + d0) = w;
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int d0 = 32 * db + 8 * g4 + 4 * h2;
+            const u32x2_t w = u32x2_t{pack_bf16x2(o[db][4 * g4] * inv, o[db][4 * g4 + 1] * inv),
+                                      pack_bf16x2(o[db][4 * g4 + 2] * inv, o[db][4 * g4 + 3] * inv)};
+            *reinterpret_cast<u32x2_t*>(dst + d0) = w;
+          }
+      } else {
+        const int64_t slot = (static_cast<int64_t>(t.part) * hq + head) * BM + row;
+        float* po = part_o + slot * D;
+#pragma unroll
+        for (int db = 0; db < GE::DB; ++db)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int d0 = 32 * db + 8 * g4 + 4 * h2;
+            *reinterpret_cast<float4*>(po + d0) =
+                float4{o[db][4 * g4], o[db][4 * g4 + 1], o[db][4 * g4 + 2], o[db][4 * g4 + 3]};
+          }
+        if (h2 == 0) {
+          part_ml[slot * 2] = m;
+          part_ml[slot * 2 + 1] = l_row;
+        }
       }
-  } else {
-    const int64_t slot = (static_cast<int64_t>(t.part) * hq + head) * BM + row;
-    float* po = part_o + slot * D;
-#pragma unroll
-    for (int db = 0; db < GE::DB; ++db)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * db + 8 * g4 + 4 * h2;
-        *reinterpret_cast<float4*>(po + d0) =
-            float4{o[db][4 * g4], o[db][4 * g4 + 1], o[db][4 * g4 + 2], o[db][4 * g4 + 3]};
-      }
-    if (h2 == 0) {
-      part_ml[slot * 2] = m;
-      part_ml[slot * 2 + 1] = l_row;
+    };
+    if (!has_next) {
+      store();
+      break;
     }
+    if constexpr (!ROT) {
+      bf16x8_t qn[GE::KS];  // raw query of the next item
+      prefetch(ci + stride, qn);
+      rotate_next(tiles[(ci + stride) / hkv].n_rows, qn);
+    }
+    store();
+    ci += stride;
   }
 }
 
@@ -492,15 +607,37 @@ bool mfma_supported(int hq, int hkv, int d, int dtype) {
   return (d == 64 || d == 128) && (g == 1 || g == 2 || g == 4 || g == 8);
 }
 
+// Compute units of the current device (one persistent work-group each).
+static hipError_t cu_count(int* n) {
+  static int cached[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && cached[dev] > 0) {
+    *n = cached[dev];
+    return hipSuccess;
+  }
+  e = hipDeviceGetAttribute(n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) cached[dev] = *n;
+  return hipSuccess;
+}
+
 template <int D, int G, bool ROT>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
                            float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
-  const size_t lds = static_cast<size_t>(kStages) * Geo<D>::STAGE;
+  const size_t lds = Geo<D, ROT>::LDS;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<D, G, ROT>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((attn_mfma_kernel<D, G, ROT>), dim3(n, g.hkv), dim3(kNT), lds, s, tiles, kv,
+  int cus = 0;
+  hipError_t e = cu_count(&cus);
+  if (e != hipSuccess) return e;
+  const int64_t items = static_cast<int64_t>(n) * g.hkv;
+  if (items > INT32_MAX) return hipErrorInvalidValue;
+  const int grid = static_cast<int>(std::min<int64_t>(items, cus));
+  hipLaunchKernelGGL((attn_mfma_kernel<D, G, ROT>), dim3(grid), dim3(kNT), lds, s, tiles, static_cast<int>(items), kv,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
                      g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
