@@ -120,8 +120,11 @@ __device__ __forceinline__ void read_pages(const KvPage* __restrict__ kv, int fi
   tp.delta = kv[first].delta;
 }
 
+// a[p] for p in 0..3, as two levels of selects (no branches, no indexed access)
 __device__ __forceinline__ int pick4(const int (&a)[4], int p) {
-  return p == 0 ? a[0] : p == 1 ? a[1] : p == 2 ? a[2] : a[3];
+  const int lo = (p & 1) ? a[1] : a[0];
+  const int hi = (p & 1) ? a[3] : a[2];
+  return (p & 2) ? hi : lo;
 }
 
 // One lane's 16 bytes from global memory to LDS at lds_wave + 16 * lane.
@@ -158,10 +161,10 @@ __device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int6
                                            int hkv, int kvh, const TilePages& tp, unsigned char* stage,
                                            const float2* __restrict__ rope, int wave, int lane) {
   using G = Geo<D, ROT>;
-  // The per-lane address parts are recomputed for every tile from an opaque copy of
-  // the lane id: hoisted out of the tile loop they would pin a dozen 64-bit
-  // registers for the whole kernel.
-  __asm__ volatile("" : "+v"(lane));
+  // The repositioning kernel has no registers to spare: there the per-lane address
+  // parts are recomputed for every tile from an opaque copy of the lane id instead
+  // of being hoisted out of the tile loop into a dozen 64-bit registers.
+  if (ROT) __asm__ volatile("" : "+v"(lane));
   // K rows: instruction q covers bytes [1024q, 1024q + 1024), keys of one page
 #pragma unroll
   for (int u = 0; u < G::KPW; ++u) {
@@ -197,26 +200,22 @@ __device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int6
   }
 }
 
-// Work item i: row tile i / hkv of the work list, kv head i % hkv.  The DMA side
-// only needs where the item's key list starts, its tile count and its kv head.
+// The DMA side of an item only needs where its key list starts and its tile count.
 struct ItemKeys {
   int kv_begin;
   int n;  // key tiles
-  int kvh;
 };
 
-__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tiles, int hkv, int i, ItemKeys& it) {
-  const WorkTile* t = tiles + i / hkv;
-  it.kv_begin = t->kv_begin;
-  it.n = (t->kv_end - t->kv_begin) >> 2;
-  it.kvh = i % hkv;
+__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tile, ItemKeys& it) {
+  it.kv_begin = tile->kv_begin;
+  it.n = (tile->kv_end - tile->kv_begin) >> 2;
 }
 
 }  // namespace
 
 template <int D, int G, bool ROT>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
-    const WorkTile* __restrict__ tiles, int n_items, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
+    const WorkTile* __restrict__ tiles, int n_tiles_total, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = Geo<D, ROT>;
@@ -233,25 +232,30 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int row = 32 * rb + r;
   const int64_t page_elems = 2ll * hkv * kPage * D;
   const int xor32_addr = (lane ^ 32) << 2;  // ds_bpermute byte address of the other half-wave
-  const int stride = gridDim.x;
+  // Work items are (row tile, kv head).  The grid is a multiple of hkv, so a
+  // work-group keeps one kv head and walks row tiles t0, t0 + tstride, ...
+  const int kvh = blockIdx.x % hkv;
+  const int t0 = blockIdx.x / hkv;
+  const int tstride = gridDim.x / hkv;
+  const int head = kvh * G + hsub;
 
   // ---- DMA side of the tile stream: item `is_i`, its tile `is_j`
   ItemKeys is;
-  int is_i = blockIdx.x, is_j = 0;
-  bool is_ok = is_i < n_items;
-  if (is_ok) load_item_keys(tiles, hkv, is_i, is);
+  int is_t = t0, is_j = 0;
+  bool is_ok = is_t < n_tiles_total;
+  if (is_ok) load_item_keys(tiles + is_t, is);
   int n_issued = 0;  // tiles of the stream issued so far
   auto issue_next = [&]() {
     while (is_ok && is_j >= is.n) {
-      is_i += stride;
+      is_t += tstride;
       is_j = 0;
-      is_ok = is_i < n_items;
-      if (is_ok) load_item_keys(tiles, hkv, is_i, is);
+      is_ok = is_t < n_tiles_total;
+      if (is_ok) load_item_keys(tiles + is_t, is);
     }
     if (!is_ok) return;
     TilePages tp;
     read_pages(kv, is.kv_begin + 4 * is_j, tp);
-    issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, is.kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
+    issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
                        lane);
     ++is_j;
     ++n_issued;
@@ -267,21 +271,31 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   // ---- building blocks of one 64-key tile
   // S^T = K Q^T over the tile (two 32-key blocks, interleaved accumulator chains)
+  // (the K operands of step ks + 1 are read while the MFMAs of step ks run)
   auto qk = [&](const unsigned char* stage, f32x16_t (&sc)[2]) {
     const bf16_t* kl = reinterpret_cast<const bf16_t*>(stage);
+    auto kop = [&](int ks, int kb) {
+      const int key = 32 * kb + r;
+      const int c = (2 * ks + h2) ^ kswz<D>(key);
+      return *reinterpret_cast<const bf16x8_t*>(kl + key * D + 8 * c);
+    };
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+    bf16x8_t a0 = kop(0, 0), a1 = kop(0, 1);
 #pragma unroll
-    for (int ks = 0; ks < GE::KS; ++ks)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int key = 32 * kb + r;
-        const int c = (2 * ks + h2) ^ kswz<D>(key);
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kl + key * D + 8 * c);
-        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sc[kb], 0, 0, 0);
+    for (int ks = 0; ks < GE::KS; ++ks) {
+      bf16x8_t n0 = a0, n1 = a1;
+      if (ks + 1 < GE::KS) {
+        n0 = kop(ks + 1, 0);
+        n1 = kop(ks + 1, 1);
       }
+      sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], sc[0], 0, 0, 0);
+      sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], sc[1], 0, 0, 0);
+      a0 = n0;
+      a1 = n1;
+    }
   };
   // causal positions and partial/empty pages; the test is wave-uniform
   auto mask = [&](f32x16_t (&sc)[2], const TilePages& cur) {
@@ -381,16 +395,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // together with the item's raw query.
   unsigned char* const rt_lds = lds + kStages * GE::STAGE;
   unsigned char* const br_lds = rt_lds + GE::RTBYTES + wave * 4 * D;
-  auto prefetch = [&](int ni, bf16x8_t (&qn)[GE::KS]) {
-    const WorkTile tn = tiles[ni / hkv];
-    const int headn = (ni % hkv) * G + hsub;
+  auto prefetch = [&](int ti, bf16x8_t (&qn)[GE::KS]) {
+    const WorkTile tn = tiles[ti];
     if (32 * rb < tn.n_rows && lane < GE::CH) {
       const unsigned char* src =
           reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tn.q_pos0 + 32 * rb) * (D / 2)) + 16 * lane;
       dma16(src, br_lds);
     }
     if (row < tn.n_rows) {
-      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + row) * hq + headn) * D + 8 * h2;
+      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + row) * hq + head) * D + 8 * h2;
 #pragma unroll
       for (int s = 0; s < GE::KS; ++s) qn[s] = *reinterpret_cast<const bf16x8_t*>(src + 16 * s);
     } else {
@@ -440,7 +453,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
   if constexpr (!ROT) {
-    if (blockIdx.x < n_items) {
+    if (t0 < n_tiles_total) {
       // rotary rows 0..31, chunk c of row r stored at chunk c ^ (r mod CH)
       constexpr int RT_PER_WAVE = GE::RTBYTES / 1024 / kNW;
 #pragma unroll
@@ -453,20 +466,19 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         dma16(src, rt_lds + qi * 1024);
       }
       bf16x8_t qn[GE::KS];
-      prefetch(blockIdx.x, qn);
+      prefetch(t0, qn);
       wait_vm(0);
       block_sync();  // every wave's share of the table has landed
-      rotate_next(tiles[blockIdx.x / hkv].n_rows, qn);
+      rotate_next(tiles[t0].n_rows, qn);
     }
   }
 
   int c = 0;  // stream index of the tile being computed
-  for (int ci = blockIdx.x; ci < n_items;) {
-    const WorkTile t = tiles[ci / hkv];
+  for (int ct = t0; ct < n_tiles_total;) {
+    const WorkTile t = tiles[ct];
     const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
-    const int head = (ci % hkv) * G + hsub;
     const bool row_ok = row < t.n_rows;
-    const bool has_next = ci + stride < n_items;
+    const bool has_next = ct + tstride < n_tiles_total;
     qpos = t.q_pos0 + row;
     wave_min_pos = t.q_pos0 + 32 * rb;
 
@@ -591,11 +603,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
     if constexpr (!ROT) {
       bf16x8_t qn[GE::KS];  // raw query of the next item
-      prefetch(ci + stride, qn);
-      rotate_next(tiles[(ci + stride) / hkv].n_rows, qn);
+      prefetch(ct + tstride, qn);
+      rotate_next(tiles[ct + tstride].n_rows, qn);
     }
     store();
-    ci += stride;
+    ct += tstride;
   }
 }
 
@@ -634,10 +646,10 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   int cus = 0;
   hipError_t e = cu_count(&cus);
   if (e != hipSuccess) return e;
+  // one work-group per CU, a multiple of hkv (each keeps one kv head)
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
-  if (items > INT32_MAX) return hipErrorInvalidValue;
-  const int grid = static_cast<int>(std::min<int64_t>(items, cus));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, G, ROT>), dim3(grid), dim3(kNT), lds, s, tiles, static_cast<int>(items), kv,
+  const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
+  hipLaunchKernelGGL((attn_mfma_kernel<D, G, ROT>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
                      g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
