@@ -79,12 +79,12 @@ struct Geo {
   static constexpr int VPW = VBYTES / 1024 / kNW;  // V DMA instructions per wave per tile
   static constexpr int RPW = 4 * D / kNW;          // bytes of the cos/sin row per wave
   static constexpr int NDMA = KPW + VPW + (ROT ? 1 : 0);  // DMA instructions per wave per tile
-  // Beyond the ring (query-side rotation of the non-repositioning kernel): the
-  // rotary rows of positions 0..31 for the whole kernel, and one rotary row per
-  // wave (its 32-row block's first position) for the next item.
+  // Beyond the ring (query rotation at item start): the rotary rows of positions
+  // 0..31 for the whole kernel, and one rotary row per wave (its 32-row block's
+  // first position) for the next item.
   static constexpr int CH = D / 4;                     // 16-byte chunks per rotary row
-  static constexpr int RTBYTES = ROT ? 0 : 32 * 4 * D;
-  static constexpr int BRBYTES = ROT ? 0 : kNW * 4 * D;
+  static constexpr int RTBYTES = 32 * 4 * D;
+  static constexpr int BRBYTES = kNW * 4 * D;
   static constexpr int LDS = kStages * STAGE + RTBYTES + BRBYTES;
 };
 
@@ -133,20 +133,23 @@ __device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
                                    (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
 }
 
-// Wait until at most n of this wave's vector-memory operations are outstanding.
-__device__ __forceinline__ void wait_vm(int n) {
-  // s_waitcnt: vmcnt in bits 3:0, expcnt 6:4 and lgkmcnt 11:8 left at their maximum
-  switch (n) {
-    case 2: __builtin_amdgcn_s_waitcnt(0x0F72); break;
-    case 3: __builtin_amdgcn_s_waitcnt(0x0F73); break;
-    case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
-    case 5: __builtin_amdgcn_s_waitcnt(0x0F75); break;
-    case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
-    case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
-    case 10: __builtin_amdgcn_s_waitcnt(0x0F7A); break;
-    case 12: __builtin_amdgcn_s_waitcnt(0x0F7C); break;
-    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-  }
+// s_waitcnt with vmcnt = N (bits 3:0 and 15:14); expcnt and lgkmcnt left at their
+// maximum, so only vector-memory operations are waited for.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+__device__ __forceinline__ void wait_vm_all() { wait_vmcnt<0>(); }
+// Wait until at most k tiles (NDMA operations each) of this wave's DMA are in flight.
+template <int NDMA>
+__device__ __forceinline__ void wait_tiles(int k) {
+  if (k >= 2)
+    wait_vmcnt<2 * NDMA>();
+  else if (k == 1)
+    wait_vmcnt<NDMA>();
+  else
+    wait_vmcnt<0>();
 }
 
 __device__ __forceinline__ void block_sync() {
@@ -206,7 +209,8 @@ struct ItemKeys {
   int n;  // key tiles
 };
 
-__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tile, ItemKeys& it) {
+__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tiles, int ti, ItemKeys& it) {
+  const WorkTile* tile = tiles + __builtin_amdgcn_readfirstlane(ti);  // a scalar load
   it.kv_begin = tile->kv_begin;
   it.n = (tile->kv_end - tile->kv_begin) >> 2;
 }
@@ -243,14 +247,14 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   ItemKeys is;
   int is_t = t0, is_j = 0;
   bool is_ok = is_t < n_tiles_total;
-  if (is_ok) load_item_keys(tiles + is_t, is);
+  if (is_ok) load_item_keys(tiles, is_t, is);
   int n_issued = 0;  // tiles of the stream issued so far
   auto issue_next = [&]() {
     while (is_ok && is_j >= is.n) {
       is_t += tstride;
       is_j = 0;
       is_ok = is_t < n_tiles_total;
-      if (is_ok) load_item_keys(tiles + is_t, is);
+      if (is_ok) load_item_keys(tiles, is_t, is);
     }
     if (!is_ok) return;
     TilePages tp;
@@ -283,18 +287,19 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
-    bf16x8_t a0 = kop(0, 0), a1 = kop(0, 1);
 #pragma unroll
     for (int ks = 0; ks < GE::KS; ++ks) {
-      bf16x8_t n0 = a0, n1 = a1;
-      if (ks + 1 < GE::KS) {
-        n0 = kop(ks + 1, 0);
-        n1 = kop(ks + 1, 1);
-      }
+      const bf16x8_t a0 = kop(ks, 0), a1 = kop(ks, 1);
       sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], sc[0], 0, 0, 0);
       sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], sc[1], 0, 0, 0);
-      a0 = n0;
-      a1 = n1;
+    }
+    // instruction order: reads of two steps ahead, then per step its two MFMAs and
+    // the reads of the step after next
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int ks = 0; ks < GE::KS; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      if (ks + 2 < GE::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
   };
   // causal positions and partial/empty pages; the test is wave-uniform
@@ -367,14 +372,28 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
   };
   // query at (position - delta) = R(-delta) applied to the query at delta 0
+  // The cos/sin row came with the tile's DMA, which the tile's wait and barrier
+  // already cover; it is read with plain ds_read instructions the compiler does not
+  // see, since it would otherwise drain every DMA in flight before reading it.
   auto rotate_q = [&](const unsigned char* stage) {
-    const float2* row_cs = reinterpret_cast<const float2*>(stage + GE::KBYTES + GE::VBYTES);
+    const unsigned row_addr = static_cast<unsigned>(reinterpret_cast<uintptr_t>(stage + GE::KBYTES + GE::VBYTES)) +
+                              64u * h2;
 #pragma unroll
     for (int s = 0; s < GE::KS / 2; ++s) {
       const u32x4_t a4 = __builtin_bit_cast(u32x4_t, qbase[s]);
       const u32x4_t b4 = __builtin_bit_cast(u32x4_t, qbase[s + GE::KS / 2]);
       u32x4_t na, nb;
-      const float4* cs4 = reinterpret_cast<const float4*>(row_cs + 16 * s + 8 * h2);
+      float4 cs4[4];
+      // frequencies 16s + 8h2 .. +7: bytes 128s + 64h2 .. +63 of the row
+      __asm__ volatile(
+          "ds_read_b128 %0, %4 offset:%5\n"
+          "ds_read_b128 %1, %4 offset:%6\n"
+          "ds_read_b128 %2, %4 offset:%7\n"
+          "ds_read_b128 %3, %4 offset:%8\n"
+          "s_waitcnt lgkmcnt(0)"
+          : "=v"(cs4[0]), "=v"(cs4[1]), "=v"(cs4[2]), "=v"(cs4[3])
+          : "v"(row_addr), "i"(128 * s), "i"(128 * s + 16), "i"(128 * s + 32), "i"(128 * s + 48)
+          : "memory");
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const float4 v = cs4[w];  // (cos, sin) of frequencies 16s + 8h2 + 2w and +1
@@ -388,8 +407,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
 
-  // ---- query-side rotation of the non-repositioning kernel without scattered
-  // table reads: the rotary angles of row r (0..31) of a wave's 32-row block come
+  // ---- query rotation at item start without scattered table reads: the rotary
+  // angles of row r (0..31) of a wave's 32-row block come
   // from R(base + r) = R(base) R(r), with R(0..31) kept in LDS for the whole kernel
   // and R(base) (base = the block's first position) brought into LDS by DMA
   // together with the item's raw query.
@@ -413,7 +432,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   // qf <- R(position) qn * log2(e)/sqrt(d), rounded to bf16 once
   auto rotate_next = [&](int n_rows, const bf16x8_t (&qn)[GE::KS]) {
-    wait_vm(0);  // this wave's base row and query have landed
+    wait_vm_all();  // this wave's base row and query have landed
     __asm__ volatile("" ::: "memory");
     if (32 * rb >= n_rows) {  // no row of this wave is real
 #pragma unroll
@@ -452,7 +471,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       qf[s + GE::KS / 2] = __builtin_bit_cast(bf16x8_t, nb);
     }
   };
-  if constexpr (!ROT) {
+  {
     if (t0 < n_tiles_total) {
       // rotary rows 0..31, chunk c of row r stored at chunk c ^ (r mod CH)
       constexpr int RT_PER_WAVE = GE::RTBYTES / 1024 / kNW;
@@ -467,7 +486,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
       bf16x8_t qn[GE::KS];
       prefetch(t0, qn);
-      wait_vm(0);
+      wait_vm_all();
       block_sync();  // every wave's share of the table has landed
       rotate_next(tiles[t0].n_rows, qn);
     }
@@ -483,52 +502,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     wave_min_pos = t.q_pos0 + 32 * rb;
 
     if constexpr (ROT) {
-      // ---- Q^T operand, rotated at the row's position and pre-scaled by log2(e)/sqrt(d)
-      float x[GE::KS][8];
-      if (row_ok) {
-        const bf16_t* src = q + (static_cast<int64_t>(t.q_row0 + row) * hq + head) * D + 8 * h2;
 #pragma unroll
-        for (int s = 0; s < GE::KS; ++s) {
-          const u32x4_t w = *reinterpret_cast<const u32x4_t*>(src + 16 * s);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            x[s][2 * e] = lo_bf16(w[e]);
-            x[s][2 * e + 1] = hi_bf16(w[e]);
-          }
-        }
-#pragma unroll
-        for (int s = 0; s < GE::KS / 2; ++s) {
-          // frequencies 16s + 8h2 .. +7: 8 consecutive (cos, sin) pairs, 64 bytes
-          const float4* cs4 =
-              reinterpret_cast<const float4*>(rope + static_cast<int64_t>(qpos) * (D / 2) + 16 * s + 8 * h2);
-#pragma unroll
-          for (int e2 = 0; e2 < 4; ++e2) {
-            const float4 v = cs4[e2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int e = 2 * e2 + u;
-              const float cs = u ? v.z : v.x;
-              const float sn = u ? v.w : v.y;
-              const float a = x[s][e], b = x[s + GE::KS / 2][e];
-              x[s][e] = (a * cs - b * sn) * scale_log2;
-              x[s + GE::KS / 2][e] = (b * cs + a * sn) * scale_log2;
-            }
-          }
-        }
-      } else {
-#pragma unroll
-        for (int s = 0; s < GE::KS; ++s)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[s][e] = 0.f;
-      }
-#pragma unroll
-      for (int s = 0; s < GE::KS; ++s) {
-        u32x4_t w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(x[s][2 * e], x[s][2 * e + 1]);
-        qf[s] = __builtin_bit_cast(bf16x8_t, w);
-        qbase[s] = qf[s];
-      }
+      for (int s = 0; s < GE::KS; ++s) qbase[s] = qf[s];
       q_delta = 0;
     }
 #pragma unroll
@@ -540,12 +515,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
     // ---- key tiles of this item
     auto tile = [&](int j) {
-      wait_vm(min(2, n_issued - 1 - c) * NDMA);  // tile c landed (tiles after it may be in flight)
+      // page entries of this tile, consumed here: a scalar-load wait later on would
+      // also drain the LDS reads of the QK step (both share one counter)
+      TilePages cur;
+      read_pages(kv, t.kv_begin + 4 * j, cur);
+      __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
+      wait_tiles<NDMA>(n_issued - 1 - c);  // tile c landed (later tiles may be in flight)
       block_sync();                              // ... for every wave; tile c - 1 is done
       issue_next();                              // into the stage of tile c - 1
       const unsigned char* stage = lds + (c & 3) * GE::STAGE;
-      TilePages cur;
-      read_pages(kv, t.kv_begin + 4 * j, cur);
       if (ROT && cur.delta != q_delta) {
         q_delta = cur.delta;
         rotate_q(stage);
@@ -601,7 +579,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       store();
       break;
     }
-    if constexpr (!ROT) {
+    {
       bf16x8_t qn[GE::KS];  // raw query of the next item
       prefetch(ct + tstride, qn);
       rotate_next(tiles[ct + tstride].n_rows, qn);
