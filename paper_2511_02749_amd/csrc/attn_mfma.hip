@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     ++is_j;
     ++n_issued;
   };
-  for (int k = 0; k < kStages - 1; ++k) issue_next();
+  for (int k = 0; k < kStages - 2; ++k) issue_next();
 
   bf16x8_t qf[GE::KS];                // Q^T operand of the current item
   bf16x8_t qbase[ROT ? GE::KS : 1];   // query at delta 0 (cross rows only)
@@ -305,15 +305,14 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // causal positions and partial/empty pages; the test is wave-uniform
   auto mask = [&](f32x16_t (&sc)[2], const TilePages& cur) {
     if (cur.nk < kBN || cur.pos0 + kBN - 1 > wave_min_pos) {
-      // key k is kept iff k < nk and pos0 + k <= qpos
-      const int lim = min(cur.nk, qpos - cur.pos0 + 1);
+      // key k is kept iff k < nk and pos0 + k <= qpos; element i of block kb is key
+      // 32kb + 8(i/4) + 4h2 + i%4, compared as a constant against lim - 4h2
+      const int lim = min(cur.nk, qpos - cur.pos0 + 1) - 4 * h2;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int k = 32 * kb + 8 * (i >> 2) + 4 * h2 + (i & 3);
-          if (k >= lim) sc[kb][i] = -INFINITY;
-        }
+        for (int i = 0; i < 16; ++i)
+          if (32 * kb + 8 * (i >> 2) + (i & 3) >= lim) sc[kb][i] = -INFINITY;
     }
   };
   // online softmax (base 2; scores already scaled), one running max per tile
@@ -514,15 +513,25 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     l = 0.f;
 
     // ---- key tiles of this item
-    auto tile = [&](int j) {
+    // raw query of the next item: loaded during the last tile (the repositioning
+    // kernel, short of registers, loads it after the tile loop)
+    bf16x8_t qn[GE::KS];
+    auto tile = [&](int j, bool last) {
       // page entries of this tile, consumed here: a scalar-load wait later on would
       // also drain the LDS reads of the QK step (both share one counter)
       TilePages cur;
       read_pages(kv, t.kv_begin + 4 * j, cur);
       __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
-      wait_tiles<NDMA>(n_issued - 1 - c);  // tile c landed (later tiles may be in flight)
-      block_sync();                              // ... for every wave; tile c - 1 is done
-      issue_next();                              // into the stage of tile c - 1
+      if ((c & 1) == 0) {
+        // one barrier per pair of stream tiles: tiles c and c + 1 have landed for
+        // every wave, and every wave is done with c - 2 and c - 1, whose stages take
+        // tiles c + 2 and c + 3
+        wait_tiles<NDMA>(n_issued - 2 - c);
+        block_sync();
+        if (n_issued < c + 4) issue_next();
+        if (n_issued < c + 4) issue_next();
+      }
+      if (!ROT && last && has_next) prefetch(ct + tstride, qn);
       const unsigned char* stage = lds + (c & 3) * GE::STAGE;
       if (ROT && cur.delta != q_delta) {
         q_delta = cur.delta;
@@ -537,7 +546,12 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       pv(stage, pk);
       ++c;
     };
-    for (int j = 0; j < n_tiles; ++j) tile(j);
+    if constexpr (ROT) {
+      for (int j = 0; j < n_tiles; ++j) tile(j, false);
+    } else {
+      for (int j = 0; j + 1 < n_tiles; ++j) tile(j, false);
+      if (n_tiles > 0) tile(n_tiles - 1, true);
+    }
 
     // ---- epilogue of the item.  The next item's query is rotated first, so the
     // output stores do not sit in front of that wait; the loop is only re-entered
@@ -579,11 +593,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       store();
       break;
     }
-    {
-      bf16x8_t qn[GE::KS];  // raw query of the next item
-      prefetch(ct + tstride, qn);
-      rotate_next(tiles[ct + tstride].n_rows, qn);
-    }
+    if (ROT || n_tiles == 0) prefetch(ct + tstride, qn);
+    rotate_next(tiles[ct + tstride].n_rows, qn);
     store();
     ct += tstride;
   }
