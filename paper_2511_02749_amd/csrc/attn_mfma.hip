@@ -224,6 +224,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = Geo<D, ROT>;
   constexpr int BM = 32 * (kNW / G);
+  // Prefill (compute-bound) synchronises once per pair of tiles; cross attention,
+  // which also serves few-row queries over long contexts where the ring's bytes in
+  // flight bound the page-gather rate, keeps three tiles in flight behind one
+  // barrier per tile.
+  constexpr bool kPairs = !ROT;
   constexpr int NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
@@ -264,7 +269,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     ++is_j;
     ++n_issued;
   };
-  for (int k = 0; k < kStages - 2; ++k) issue_next();
+  for (int k = 0; k < (kPairs ? kStages - 2 : kStages - 1); ++k) issue_next();
 
   bf16x8_t qf[GE::KS];                // Q^T operand of the current item
   bf16x8_t qbase[ROT ? GE::KS : 1];   // query at delta 0 (cross rows only)
@@ -496,6 +501,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const WorkTile t = tiles[ct];
     const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
     const bool row_ok = row < t.n_rows;
+    // a wave whose 32-row block is past the item's rows only moves tiles (few-row
+    // items, e.g. short cross segments, then cost half the compute)
+    const bool active = 32 * rb < t.n_rows;
     const bool has_next = ct + tstride < n_tiles_total;
     qpos = t.q_pos0 + row;
     wave_min_pos = t.q_pos0 + 32 * rb;
@@ -522,28 +530,38 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       TilePages cur;
       read_pages(kv, t.kv_begin + 4 * j, cur);
       __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
-      if ((c & 1) == 0) {
-        // one barrier per pair of stream tiles: tiles c and c + 1 have landed for
-        // every wave, and every wave is done with c - 2 and c - 1, whose stages take
-        // tiles c + 2 and c + 3
-        wait_tiles<NDMA>(n_issued - 2 - c);
+      if constexpr (kPairs) {
+        if ((c & 1) == 0) {
+          // one barrier per pair of stream tiles: tiles c and c + 1 have landed for
+          // every wave, and every wave is done with c - 2 and c - 1, whose stages take
+          // tiles c + 2 and c + 3
+          wait_tiles<NDMA>(n_issued - 2 - c);
+          block_sync();
+          if (n_issued < c + 4) issue_next();
+          if (n_issued < c + 4) issue_next();
+        }
+      } else {
+        // one barrier per tile: tile c has landed for every wave, and every wave is
+        // done with c - 1, whose stage takes tile c + 3 (three tiles in flight)
+        wait_tiles<NDMA>(n_issued - 1 - c);
         block_sync();
-        if (n_issued < c + 4) issue_next();
-        if (n_issued < c + 4) issue_next();
+        issue_next();
       }
       if (!ROT && last && has_next) prefetch(ct + tstride, qn);
       const unsigned char* stage = lds + (c & 3) * GE::STAGE;
-      if (ROT && cur.delta != q_delta) {
-        q_delta = cur.delta;
-        rotate_q(stage);
+      if (active) {
+        if (ROT && cur.delta != q_delta) {
+          q_delta = cur.delta;
+          rotate_q(stage);
+        }
+        f32x16_t sc[2];
+        qk(stage, sc);
+        mask(sc, cur);
+        const float m_use = softmax_max(sc);
+        bf16x8_t pk[4];
+        softmax_exp(sc, m_use, pk);
+        pv(stage, pk);
       }
-      f32x16_t sc[2];
-      qk(stage, sc);
-      mask(sc, cur);
-      const float m_use = softmax_max(sc);
-      bf16x8_t pk[4];
-      softmax_exp(sc, m_use, pk);
-      pv(stage, pk);
       ++c;
     };
     if constexpr (ROT) {

@@ -200,3 +200,20 @@ def test_c3_full_size_sampled():
     _check_rows(run, batch, pre, TOL["bf16"], limit=64)
     _check_rows(run, batch, cross, TOL["bf16"], limit=64)
     run.close()
+
+
+@pytest.mark.parametrize("cross_len", [1, 4, 16])
+def test_few_cross_rows_over_many_pages(cross_len):
+    """The KV page-gather regime: a handful of cross rows per query over a long
+    cached context (split along the keys, merged by the combine kernel)."""
+    wl = W.rag_workload("gather", seed=3, prefix_len=256, pool_size=8, frag_lens=256, frags_per_query=8,
+                        n_queries=2, cross_len=cross_len, mode="direct",
+                        orders=[list(range(8)), list(range(8))[::-1]], batch_split=[1, 1])
+    run = GpuRun(wl)
+    run.run_batch(wl.batches[0])
+    plan = run.run_batch(wl.batches[1])
+    st = plan.stats()
+    assert st["tokens_new"] == 0 and st["kv_splits"] > 1
+    _, cross = plan.rows()
+    _check_rows(run, wl.batches[1], cross, TOL["bf16"])
+    run.close()

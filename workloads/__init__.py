@@ -246,3 +246,22 @@ def small_workload(name: str = "small", *, seed: int = 0, dtype: str = "bf16", n
                         head_dim=head_dim, hidden=64, prefix_len=prefix_len, pool_size=len(frag_lens),
                         frag_lens=list(frag_lens), frags_per_query=frags_per_query, n_queries=n_queries,
                         cross_len=cross_len, mode=mode, orders=orders, batch_split=batch_split)
+
+
+def gather_queries(seed: int = 0, n_queries: int = 8, prefix_len: int = 2048, n_frags: int = 32,
+                   frag_len: int = 256, cross_len: int = 16):
+    """Independent judge-shaped queries (C3 layout: prompt 2048 + 32 candidates x 256)
+    whose KV pages are all distinct (each query has its own prompt), followed by a
+    short cross segment: the KV page-gather regime, where cross attention reads
+    many pages for few query rows.  Returns (queries, n_rows); the activations
+    are left to the caller (seeded device draws), since the timing does not
+    depend on their values and projecting 80K rows on the host would be slow.
+    """
+    book = _RowBook()
+    queries = []
+    for qi in range(n_queries):
+        prefix = book.add(_tokens(seed, KIND_PREFIX, 1000 + qi, prefix_len))
+        frags = [book.add(_tokens(seed, KIND_FRAG, 1000 * (qi + 1) + f, frag_len)) for f in range(n_frags)]
+        cross = book.add(_tokens(seed, KIND_CROSS, 1000 + qi, cross_len))
+        queries.append(Query(prefix=prefix, frags=frags, cross=cross))
+    return queries, book.next
