@@ -224,11 +224,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = Geo<D, ROT>;
   constexpr int BM = 32 * (kNW / G);
-  // Prefill (compute-bound) synchronises once per pair of tiles; cross attention,
-  // which also serves few-row queries over long contexts where the ring's bytes in
-  // flight bound the page-gather rate, keeps three tiles in flight behind one
-  // barrier per tile.
-  constexpr bool kPairs = !ROT;
+  // Two key groups (cross attention, four query heads per kv head): a few-row item
+  // lets its two 32-row wave groups take alternate key tiles of each pair.
+  constexpr bool kTwoCapable = ROT && kNW / G == 2;
   constexpr int NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
@@ -269,7 +267,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     ++is_j;
     ++n_issued;
   };
-  for (int k = 0; k < (kPairs ? kStages - 2 : kStages - 1); ++k) issue_next();
+  for (int k = 0; k < kStages - 2; ++k) issue_next();
 
   bf16x8_t qf[GE::KS];                // Q^T operand of the current item
   bf16x8_t qbase[ROT ? GE::KS : 1];   // query at delta 0 (cross rows only)
@@ -418,15 +416,19 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // together with the item's raw query.
   unsigned char* const rt_lds = lds + kStages * GE::STAGE;
   unsigned char* const br_lds = rt_lds + GE::RTBYTES + wave * 4 * D;
+  // An item in two-key-group mode gives both wave groups rows 0..31 (the group
+  // picks key tiles instead); otherwise wave group rb holds rows 32rb .. 32rb + 31.
+  auto two_groups = [&](const WorkTile& w) { return kTwoCapable && (w.flags & kTwoKeyGroups) != 0; };
   auto prefetch = [&](int ti, bf16x8_t (&qn)[GE::KS]) {
     const WorkTile tn = tiles[ti];
-    if (32 * rb < tn.n_rows && lane < GE::CH) {
+    const int rbn = two_groups(tn) ? 0 : rb;
+    if (32 * rbn < tn.n_rows && lane < GE::CH) {
       const unsigned char* src =
-          reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tn.q_pos0 + 32 * rb) * (D / 2)) + 16 * lane;
+          reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tn.q_pos0 + 32 * rbn) * (D / 2)) + 16 * lane;
       dma16(src, br_lds);
     }
-    if (row < tn.n_rows) {
-      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + row) * hq + head) * D + 8 * h2;
+    if (32 * rbn + r < tn.n_rows) {
+      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + 32 * rbn + r) * hq + head) * D + 8 * h2;
 #pragma unroll
       for (int s = 0; s < GE::KS; ++s) qn[s] = *reinterpret_cast<const bf16x8_t*>(src + 16 * s);
     } else {
@@ -435,10 +437,10 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
   // qf <- R(position) qn * log2(e)/sqrt(d), rounded to bf16 once
-  auto rotate_next = [&](int n_rows, const bf16x8_t (&qn)[GE::KS]) {
+  auto rotate_next = [&](const WorkTile& tn, const bf16x8_t (&qn)[GE::KS]) {
     wait_vm_all();  // this wave's base row and query have landed
     __asm__ volatile("" ::: "memory");
-    if (32 * rb >= n_rows) {  // no row of this wave is real
+    if (32 * (two_groups(tn) ? 0 : rb) >= tn.n_rows) {  // no row of this wave is real
 #pragma unroll
       for (int s = 0; s < GE::KS; ++s) qf[s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
       return;
@@ -492,7 +494,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       prefetch(t0, qn);
       wait_vm_all();
       block_sync();  // every wave's share of the table has landed
-      rotate_next(tiles[t0].n_rows, qn);
+      rotate_next(tiles[t0], qn);
     }
   }
 
@@ -500,13 +502,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   for (int ct = t0; ct < n_tiles_total;) {
     const WorkTile t = tiles[ct];
     const int n_tiles = (t.kv_end - t.kv_begin) >> 2;
-    const bool row_ok = row < t.n_rows;
-    // a wave whose 32-row block is past the item's rows only moves tiles (few-row
+    const bool two = two_groups(t);
+    const int grp = two ? rb : 0;          // key group of this wave
+    const int irow = two ? r : row;        // this lane's row inside the item
+    const int rb0 = two ? 0 : 32 * rb;     // first row of this wave
+    const bool row_ok = irow < t.n_rows;
+    // a wave whose rows are all past the item's rows only moves tiles (few-row
     // items, e.g. short cross segments, then cost half the compute)
-    const bool active = 32 * rb < t.n_rows;
+    const bool active = rb0 < t.n_rows;
     const bool has_next = ct + tstride < n_tiles_total;
-    qpos = t.q_pos0 + row;
-    wave_min_pos = t.q_pos0 + 32 * rb;
+    qpos = t.q_pos0 + irow;
+    wave_min_pos = t.q_pos0 + rb0;
 
     if constexpr (ROT) {
 #pragma unroll
@@ -520,55 +526,46 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     m = -INFINITY;
     l = 0.f;
 
-    // ---- key tiles of this item
-    // raw query of the next item: loaded during the last tile (the repositioning
-    // kernel, short of registers, loads it after the tile loop)
+    // ---- key tiles of this item, in groups of two (one for an odd last tile)
+    // raw query of the next item, loaded during the last group (the repositioning
+    // kernel, short of registers, loads it after the loop)
     bf16x8_t qn[GE::KS];
-    auto tile = [&](int j, bool last) {
-      // page entries of this tile, consumed here: a scalar-load wait later on would
+    auto compute = [&](int j, int cs) {  // tile j of the item, stream slot cs
+      // page entries of the tile, consumed here: a scalar-load wait later on would
       // also drain the LDS reads of the QK step (both share one counter)
       TilePages cur;
       read_pages(kv, t.kv_begin + 4 * j, cur);
       __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
-      if constexpr (kPairs) {
-        if ((c & 1) == 0) {
-          // one barrier per pair of stream tiles: tiles c and c + 1 have landed for
-          // every wave, and every wave is done with c - 2 and c - 1, whose stages take
-          // tiles c + 2 and c + 3
-          wait_tiles<NDMA>(n_issued - 2 - c);
-          block_sync();
-          if (n_issued < c + 4) issue_next();
-          if (n_issued < c + 4) issue_next();
-        }
-      } else {
-        // one barrier per tile: tile c has landed for every wave, and every wave is
-        // done with c - 1, whose stage takes tile c + 3 (three tiles in flight)
-        wait_tiles<NDMA>(n_issued - 1 - c);
-        block_sync();
-        issue_next();
+      const unsigned char* stage = lds + (cs & 3) * GE::STAGE;
+      if (ROT && cur.delta != q_delta) {
+        q_delta = cur.delta;
+        rotate_q(stage);
       }
-      if (!ROT && last && has_next) prefetch(ct + tstride, qn);
-      const unsigned char* stage = lds + (c & 3) * GE::STAGE;
-      if (active) {
-        if (ROT && cur.delta != q_delta) {
-          q_delta = cur.delta;
-          rotate_q(stage);
-        }
-        f32x16_t sc[2];
-        qk(stage, sc);
-        mask(sc, cur);
-        const float m_use = softmax_max(sc);
-        bf16x8_t pk[4];
-        softmax_exp(sc, m_use, pk);
-        pv(stage, pk);
-      }
-      ++c;
+      f32x16_t sc[2];
+      qk(stage, sc);
+      mask(sc, cur);
+      const float m_use = softmax_max(sc);
+      bf16x8_t pk[4];
+      softmax_exp(sc, m_use, pk);
+      pv(stage, pk);
     };
-    if constexpr (ROT) {
-      for (int j = 0; j < n_tiles; ++j) tile(j, false);
-    } else {
-      for (int j = 0; j + 1 < n_tiles; ++j) tile(j, false);
-      if (n_tiles > 0) tile(n_tiles - 1, true);
+    for (int j = 0; j < n_tiles;) {
+      const int sz = min(2, n_tiles - j);
+      // tiles c .. c + sz - 1 have landed for every wave, and every wave is done with
+      // the tiles before c, whose stages take the next ones (up to c + 3)
+      wait_tiles<NDMA>(n_issued - c - sz);
+      block_sync();
+#pragma unroll
+      for (int u = 0; u < kStages - 1; ++u)
+        if (n_issued < c + kStages) issue_next();
+      if (!ROT && j + sz == n_tiles && has_next) prefetch(ct + tstride, qn);
+      if (active) {
+        // two key groups: this wave takes tile grp of the pair; otherwise both
+        const int u1 = two ? min(grp + 1, sz) : sz;
+        for (int u = grp; u < u1; ++u) compute(j + u, c + u);
+      }
+      c += sz;
+      j += sz;
     }
 
     // ---- epilogue of the item.  The next item's query is rotated first, so the
@@ -577,7 +574,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const float l_row = l + __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(l)));
     auto store = [&]() {
       if (!row_ok) return;
-      const int64_t orow = static_cast<int64_t>(t.q_row0 + row);
+      const int64_t orow = static_cast<int64_t>(t.q_row0 + irow);
       if (t.part < 0) {
         const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
         bf16_t* dst = out + (orow * hq + head) * D;
@@ -591,7 +588,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             *reinterpret_cast<u32x2_t*>(dst + d0) = w;
           }
       } else {
-        const int64_t slot = (static_cast<int64_t>(t.part) * hq + head) * BM + row;
+        const int64_t slot = (static_cast<int64_t>(t.part + grp) * hq + head) * BM + irow;
         float* po = part_o + slot * D;
 #pragma unroll
         for (int db = 0; db < GE::DB; ++db)
@@ -612,7 +609,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       break;
     }
     if (ROT || n_tiles == 0) prefetch(ct + tstride, qn);
-    rotate_next(tiles[ct + tstride].n_rows, qn);
+    rotate_next(tiles[ct + tstride], qn);
     store();
     ct += tstride;
   }

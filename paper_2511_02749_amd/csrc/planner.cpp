@@ -428,7 +428,8 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     int32_t chunk = (n_pages + splits - 1) / splits;
     chunk = ((chunk + align - 1) / align) * align;   // splits cut at whole tiles
     int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
-    if (parts <= 1) {
+    const bool two = c.n <= t.two_group_rows;     // each split writes two partials
+    if (parts <= 1 && !two) {
       p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});
       continue;
     }
@@ -436,9 +437,10 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     for (int32_t s = 0; s < parts; ++s) {
       int32_t b = c.kv0 + s * chunk;
       int32_t e = std::min(c.kv1, b + chunk);
-      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, b, e, p->n_parts++, 0, 0});
+      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, b, e, p->n_parts, two ? kTwoKeyGroups : 0, 0});
+      p->n_parts += two ? 2 : 1;
     }
-    p->combine.push_back(CombineTile{c.row0, c.n, part0, parts});
+    p->combine.push_back(CombineTile{c.row0, c.n, part0, p->n_parts - part0});
   }
 }
 

@@ -60,6 +60,7 @@ struct Tiling {
   int target_items = 512;     // work-groups the cross launch aims for (KV splits x tiles x heads)
   int min_split_pages = 16;   // at least 256 keys per KV split
   bool pad4 = false;          // pad span runs to 4-page tiles (MFMA kernel)
+  int two_group_rows = 0;     // cross tiles of at most this many rows use kTwoKeyGroups
 };
 
 // Work-list shape for the attention kernels.  The MFMA kernel (one work-group per
@@ -67,6 +68,9 @@ struct Tiling {
 // 132 KiB at head_dim 128: the cross launch aims at two rounds over the 256 CUs.
 // The generic kernel (one wave per row tile and query head) is latency-bound and
 // wants more work-groups.
+// Few-row cross tiles (a short question over a long context) let the MFMA
+// kernel's two wave groups work on alternate key tiles; that needs four query
+// heads per kv head (two 32-row groups of four waves).
 inline Tiling tiling_for(bool mfma, int bm, int hq, int hkv) {
   Tiling t;
   t.bm_prefill = bm;
@@ -74,6 +78,7 @@ inline Tiling tiling_for(bool mfma, int bm, int hq, int hkv) {
   t.kv_heads = mfma ? hkv : hq;
   t.target_items = mfma ? 512 : 1024;
   t.pad4 = mfma;
+  t.two_group_rows = (mfma && hq == 4 * hkv) ? 32 : 0;
   return t;
 }
 

@@ -28,7 +28,11 @@ struct NewPage {
 
 // A tile of up to BM consecutive query rows of one span, against the key pages
 // kv[kv_begin, kv_end).  part < 0: write the normalised output; else write the
-// unnormalised partial (one KV split) into partial slot `part`.
+// unnormalised partial (one KV split) into partial slot `part`.  With
+// kTwoKeyGroups (MFMA kernel, rows <= 32, four query heads per kv head) the two
+// 32-row wave groups of the work-group take alternate key tiles instead of two
+// row blocks, and write partial slots part and part + 1.
+constexpr int32_t kTwoKeyGroups = 1;
 struct WorkTile {
   int32_t q_row0;
   int32_t n_rows;
@@ -36,7 +40,7 @@ struct WorkTile {
   int32_t kv_begin;
   int32_t kv_end;
   int32_t part;
-  int32_t pad0;
+  int32_t flags;
   int32_t pad1;
 };
 
