@@ -73,6 +73,9 @@ SMALL = [
     dict(name="ragged", head_dim=128, n_q_heads=8, n_kv_heads=2),
     dict(name="d64", head_dim=64, n_q_heads=8, n_kv_heads=2),
     dict(name="mha", head_dim=128, n_q_heads=4, n_kv_heads=4),
+    dict(name="g2", head_dim=128, n_q_heads=8, n_kv_heads=4),
+    dict(name="g8", head_dim=128, n_q_heads=16, n_kv_heads=2),
+    dict(name="g8d64", head_dim=64, n_q_heads=16, n_kv_heads=2, cross_len=70),
     dict(name="noprefix", prefix_len=0, frag_lens=(16, 1, 77, 130), cross_len=40),
     dict(name="nocross", cross_len=0),
     dict(name="bigtiles", prefix_len=100, frag_lens=(300, 129, 64), frags_per_query=3, cross_len=150),
