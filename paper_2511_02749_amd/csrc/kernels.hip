@@ -16,44 +16,102 @@ namespace spanq {
 // ------------------------------------------------------------------ K3
 // One work-group per new page.  K goes to [kv_head][slot][d] rotated at its
 // position; V goes transposed to [kv_head][d][v_pos(slot)].  Unfilled slots are
-// zeroed so that masked keys never feed a NaN into the P.V product.
+// zeroed so that masked keys never feed a NaN into the P.V product.  Every global
+// access is a 16-byte chunk; the V transpose goes through LDS, a group of kv heads
+// at a time.
+template <typename T>
+struct Chunk16 {
+  static constexpr int E = 16 / static_cast<int>(sizeof(T));  // elements per chunk
+  T x[E];
+};
+
+template <typename T>
+__device__ __forceinline__ Chunk16<T> load16(const T* p) {
+  return __builtin_bit_cast(Chunk16<T>, *reinterpret_cast<const uint4*>(p));
+}
+template <typename T>
+__device__ __forceinline__ void store16(T* p, const Chunk16<T>& c) {
+  *reinterpret_cast<uint4*>(p) = __builtin_bit_cast(uint4, c);
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restrict__ pages,
                                                          const T* __restrict__ k, const T* __restrict__ v,
                                                          T* __restrict__ pool, int64_t layer_off, int hkv,
                                                          const float2* __restrict__ rope) {
+  constexpr int E = Chunk16<T>::E;
+  constexpr int H = D / 2;
+  constexpr int HG = 32768 / (kPage * D * static_cast<int>(sizeof(T)));  // kv heads per LDS pass
+  __shared__ uint4 lds_raw[32768 / 16];
+  T* tile = reinterpret_cast<T*>(lds_raw);  // [slot][head of the group][d]
+
   const NewPage pg = pages[blockIdx.x];
   const int64_t page_elems = 2ll * hkv * kPage * D;
   T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems;
   T* vp = kp + static_cast<int64_t>(hkv) * kPage * D;
-  constexpr int H = D / 2;
-  for (int e = threadIdx.x; e < hkv * kPage * H; e += blockDim.x) {
-    const int h = e / (kPage * H);
-    const int rem = e - h * (kPage * H);
-    const int s = rem / H;
-    const int i = rem - s * H;
-    float y0 = 0.f, y1 = 0.f;
+
+  // K: item (head, slot, chunk of E rotary pairs (i, i + H))
+  for (int e = threadIdx.x; e < hkv * kPage * (H / E); e += blockDim.x) {
+    const int q = e % (H / E);
+    const int hs = e / (H / E);
+    const int s = hs % kPage;
+    const int h = hs / kPage;
+    Chunk16<T> y0, y1;
     if (s < pg.n_valid) {
-      const int64_t src = (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D;
-      const float x0 = to_f32(k[src + i]);
-      const float x1 = to_f32(k[src + i + H]);
-      float sn, cs;
-      rope_cs(rope, D / 2, pg.pos0 + s, i, &sn, &cs);
-      y0 = x0 * cs - x1 * sn;
-      y1 = x1 * cs + x0 * sn;
+      const T* src = k + (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + q * E;
+      const Chunk16<T> x0 = load16(src), x1 = load16(src + H);
+      const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(pg.pos0 + s) * H + q * E);
+#pragma unroll
+      for (int u2 = 0; u2 < E / 2; ++u2) {
+        const float4 w = cs4[u2];  // (cos, sin) of pairs q*E + 2u2 and + 1
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int u = 2 * u2 + b;
+          const float cs = b ? w.z : w.x, sn = b ? w.w : w.y;
+          const float a0 = to_f32(x0.x[u]), a1 = to_f32(x1.x[u]);
+          y0.x[u] = from_f32<T>(a0 * cs - a1 * sn);
+          y1.x[u] = from_f32<T>(a1 * cs + a0 * sn);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < E; ++u) y0.x[u] = y1.x[u] = from_f32<T>(0.f);
     }
-    T* dst = kp + (static_cast<int64_t>(h) * kPage + s) * D;
-    dst[i] = from_f32<T>(y0);
-    dst[i + H] = from_f32<T>(y1);
+    T* dst = kp + (static_cast<int64_t>(h) * kPage + s) * D + q * E;
+    store16(dst, y0);
+    store16(dst + H, y1);
   }
-  for (int e = threadIdx.x; e < hkv * D * kPage; e += blockDim.x) {
-    const int h = e / (D * kPage);
-    const int rem = e - h * (D * kPage);
-    const int dd = rem / kPage;
-    const int s = rem - dd * kPage;
-    T val = from_f32<T>(0.f);
-    if (s < pg.n_valid) val = v[(static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + dd];
-    vp[(static_cast<int64_t>(h) * D + dd) * kPage + v_pos(s)] = val;
+
+  // V: rows [slot][d] of a group of heads into LDS, then transposed rows out
+  for (int h0 = 0; h0 < hkv; h0 += HG) {
+    const int hn = min(HG, hkv - h0);
+    for (int e = threadIdx.x; e < kPage * hn * (D / E); e += blockDim.x) {
+      const int qd = e % (D / E);
+      const int sh = e / (D / E);
+      const int hh = sh % hn;
+      const int s = sh / hn;
+      Chunk16<T> val;
+      if (s < pg.n_valid) {
+        val = load16(v + (static_cast<int64_t>(pg.src_row + s) * hkv + h0 + hh) * D + qd * E);
+      } else {
+#pragma unroll
+        for (int u = 0; u < E; ++u) val.x[u] = from_f32<T>(0.f);
+      }
+      store16(tile + (s * HG + hh) * D + qd * E, val);
+    }
+    __syncthreads();
+    // row (head, d) holds 16 positions; position p carries slot v_pos(p) (an involution)
+    for (int e = threadIdx.x; e < hn * D * (kPage / E); e += blockDim.x) {
+      const int pc = e % (kPage / E);
+      const int hd = e / (kPage / E);
+      const int d = hd % D;
+      const int hh = hd / D;
+      Chunk16<T> out;
+#pragma unroll
+      for (int u = 0; u < E; ++u) out.x[u] = tile[(v_pos(pc * E + u) * HG + hh) * D + d];
+      store16(vp + (static_cast<int64_t>(h0 + hh) * D + d) * kPage + pc * E, out);
+    }
+    __syncthreads();
   }
 }
 
@@ -211,6 +269,12 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, 
 // ------------------------------------------------------------------ K4 combine
 // out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.  One
 // work-group per (tile, query head); a thread merges 8 consecutive dims of a row.
+// K4: one thread per (row, 8 output dims) of one head; a work-group covers
+// kCombineRows rows of one (tile, head).  The partials' maxima are read first
+// (independent loads), then the weighted sum over parts, four parts per step so
+// their loads are in flight together.
+constexpr int kCombineRows = 16;
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restrict__ tiles,
                                                       const float* __restrict__ part_o,
@@ -219,40 +283,52 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restr
   const CombineTile t = tiles[blockIdx.x];
   const int h = blockIdx.y;
   constexpr int C8 = D / 8;
-  for (int e = threadIdx.x; e < t.n_rows * C8; e += blockDim.x) {
-    const int r = e / C8;
-    const int c = e - r * C8;
-    float M = -INFINITY;
-    for (int p = 0; p < t.n_parts; ++p)
-      M = fmaxf(M, part_ml[((static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r) * 2]);
-    float L = 0.f;
-    float acc[8];
+  const int r = blockIdx.z * kCombineRows + threadIdx.x / C8;
+  const int c = threadIdx.x % C8;
+  if (threadIdx.x >= kCombineRows * C8 || r >= t.n_rows) return;
+  auto slot_of = [&](int p) { return (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r; };
+  float M = -INFINITY;
+  for (int p = 0; p < t.n_parts; ++p) M = fmaxf(M, part_ml[slot_of(p) * 2]);
+  float L = 0.f;
+  float acc[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-    if (M != -INFINITY) {
-      for (int p = 0; p < t.n_parts; ++p) {
-        const int64_t slot = (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r;
-        const float mp = part_ml[slot * 2];
-        if (mp == -INFINITY) continue;
-        const float w = exp2f(mp - M);
-        L += part_ml[slot * 2 + 1] * w;
-        const float4 a = *reinterpret_cast<const float4*>(part_o + slot * D + 8 * c);
-        const float4 b = *reinterpret_cast<const float4*>(part_o + slot * D + 8 * c + 4);
-        acc[0] += a.x * w; acc[1] += a.y * w; acc[2] += a.z * w; acc[3] += a.w * w;
-        acc[4] += b.x * w; acc[5] += b.y * w; acc[6] += b.z * w; acc[7] += b.w * w;
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  if (M != -INFINITY) {
+    for (int p0 = 0; p0 < t.n_parts; p0 += 4) {
+      float2 ml[4];
+      float4 a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (p0 + u < t.n_parts) {
+          const int64_t sl = slot_of(p0 + u);
+          ml[u] = *reinterpret_cast<const float2*>(part_ml + sl * 2);
+          a[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c);
+          b[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c + 4);
+        } else {
+          ml[u] = float2{-INFINITY, 0.f};
+          a[u] = b[u] = float4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (ml[u].x == -INFINITY) continue;  // a split that saw no key of this row
+        const float w = exp2f(ml[u].x - M);
+        L += ml[u].y * w;
+        acc[0] += a[u].x * w; acc[1] += a[u].y * w; acc[2] += a[u].z * w; acc[3] += a[u].w * w;
+        acc[4] += b[u].x * w; acc[5] += b[u].y * w; acc[6] += b[u].z * w; acc[7] += b[u].w * w;
       }
     }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    T* dst = out + (static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + 8 * c;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) dst[i] = from_f32<T>(acc[i] * inv);
   }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  T* dst = out + (static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + 8 * c;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) dst[i] = from_f32<T>(acc[i] * inv);
 }
 
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n, const float* part_o,
                           const float* part_ml, int bm, void* out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  dim3 grid(n, g.hq);
+  dim3 grid(n, g.hq, (bm + kCombineRows - 1) / kCombineRows);
   if (g.dtype == SPAN_BF16) {
     if (g.d == 128)
       hipLaunchKernelGGL((combine_kernel<bf16_t, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,

@@ -63,9 +63,9 @@ struct Tiling {
   int two_group_rows = 0;     // cross tiles of at most this many rows use kTwoKeyGroups
 };
 
-// Work-list shape for the attention kernels.  The MFMA kernel (one work-group per
-// row tile and kv head) holds a CU with one 8-wave work-group, its LDS ring taking
-// 132 KiB at head_dim 128: the cross launch aims at two rounds over the 256 CUs.
+// Work-list shape for the attention kernels.  The MFMA kernel is persistent, one
+// 8-wave work-group per CU walking (row tile, kv head) items: the cross launch aims
+// at one item per CU (splitting the keys further only adds partials to merge).
 // The generic kernel (one wave per row tile and query head) is latency-bound and
 // wants more work-groups.
 // Few-row cross tiles (a short question over a long context) let the MFMA
@@ -76,7 +76,7 @@ inline Tiling tiling_for(bool mfma, int bm, int hq, int hkv) {
   t.bm_prefill = bm;
   t.bm_cross = bm;
   t.kv_heads = mfma ? hkv : hq;
-  t.target_items = mfma ? 512 : 1024;
+  t.target_items = mfma ? 256 : 1024;
   t.pad4 = mfma;
   t.two_group_rows = (mfma && hq == 4 * hkv) ? 32 : 0;
   return t;
