@@ -32,9 +32,45 @@ uint64_t page_hash(uint64_t prev, const int32_t* tok, int32_t n, int32_t page_id
 
 uint64_t fragment_seed(uint64_t prefix_last_or_root) { return mix64(prefix_last_or_root ^ SPAN_HASH_FRAG_TAG); }
 
+namespace {
+// The page-hash chains of up to four spans, advanced in lockstep: the chains are
+// independent, so their multiply latencies overlap.  out[c] is exactly the chain
+// page_hash gives for span c from seeds[c].
+void chains4(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps, std::vector<uint64_t>* out) {
+  uint64_t h[4];
+  int32_t n[4];
+  const int32_t* t[4];
+  int32_t nmax = 0;
+  for (int c = 0; c < 4; ++c) {
+    h[c] = c < k ? seeds[c] : 0;
+    n[c] = c < k ? spans[c]->n : 0;
+    t[c] = c < k ? spans[c]->tok : nullptr;
+    nmax = std::max(nmax, n[c]);
+    if (c < k) {
+      out[c].clear();
+      out[c].reserve(static_cast<size_t>((n[c] + ps - 1) / ps));
+    }
+  }
+  for (int32_t p = 0; p * ps < nmax; ++p) {
+    const int32_t base = p * ps;
+    for (int32_t i = 0; i < ps; ++i)
+      for (int c = 0; c < 4; ++c)
+        if (base + i < n[c]) h[c] = mix64(h[c] ^ static_cast<uint64_t>(static_cast<uint32_t>(t[c][base + i])));
+    for (int c = 0; c < 4; ++c)
+      if (base < n[c]) {
+        const int32_t m = std::min(ps, n[c] - base);
+        h[c] = mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(m)) << 32) ^
+                     static_cast<uint64_t>(static_cast<uint32_t>(p)));
+        out[c].push_back(h[c]);
+      }
+  }
+}
+}  // namespace
+
 PoolIndex::PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode)
     : num_pages_(num_pages), page_size_(page_size), hash_mode_(hash_mode) {
   pages_.resize(static_cast<size_t>(num_pages));
+  gen_.assign(static_cast<size_t>(num_pages), 0u);
   page_tokens_.resize(static_cast<size_t>(num_pages) * page_size);
   index_.reserve(static_cast<size_t>(std::min<int64_t>(num_pages, 1 << 20)));
   reset();
@@ -44,7 +80,8 @@ void PoolIndex::reset() {
   // Records of ids >= watermark_ are rewritten when they are allocated again.
   for (int64_t i = 0; i < watermark_; ++i) pages_[i] = PageRec{};
   index_.clear();
-  evictable_.clear();
+  lru_.clear();
+  n_evictable_ = 0;
   freed_.clear();
   watermark_ = 0;
 }
@@ -95,10 +132,47 @@ void PoolIndex::push_free(int32_t pid) {
   }
 }
 
+namespace {
+// min-heap order of LRU entries: (last_use, -idx, id) ascending
+template <typename E>
+bool lru_after(const E& a, const E& b) {
+  if (a.last_use != b.last_use) return a.last_use > b.last_use;
+  if (a.neg_idx != b.neg_idx) return a.neg_idx > b.neg_idx;
+  return a.pid > b.pid;
+}
+}  // namespace
+
+bool PoolIndex::lru_current(const LruEntry& e) const {
+  const PageRec& r = pages_[e.pid];
+  return r.published && r.pins == 0 && gen_[e.pid] == e.gen;
+}
+
+void PoolIndex::make_evictable(int32_t pid) {
+  const PageRec& r = pages_[pid];
+  const uint32_t g = ++gen_[pid];
+  lru_.push_back(LruEntry{r.last_use, -r.idx, pid, g});
+  std::push_heap(lru_.begin(), lru_.end(), lru_after<LruEntry>);
+  ++n_evictable_;
+  // drop stale entries once they outnumber the live ones
+  if (lru_.size() > 2 * static_cast<size_t>(n_evictable_) + 1024) {
+    std::vector<LruEntry> keep;
+    keep.reserve(static_cast<size_t>(n_evictable_));
+    for (const LruEntry& e : lru_)
+      if (lru_current(e)) keep.push_back(e);
+    std::make_heap(keep.begin(), keep.end(), lru_after<LruEntry>);
+    lru_.swap(keep);
+  }
+}
+
 void PoolIndex::evict_one(Plan* p) {
-  auto it = evictable_.begin();
-  int32_t pid = std::get<2>(*it);
-  evictable_.erase(it);
+  while (!lru_current(lru_.front())) {
+    std::pop_heap(lru_.begin(), lru_.end(), lru_after<LruEntry>);
+    lru_.pop_back();
+  }
+  const int32_t pid = lru_.front().pid;
+  std::pop_heap(lru_.begin(), lru_.end(), lru_after<LruEntry>);
+  lru_.pop_back();
+  --n_evictable_;
   index_.erase(pages_[pid].hash);
   p->evicted.push_back(pid);
   ++total_evictions_;
@@ -170,6 +244,21 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     } else {
       const std::vector<uint64_t>& ph = chain_of(SPAN_HASH_ROOT, q.prefix);
       uint64_t fs = fragment_seed(ph.empty() ? SPAN_HASH_ROOT : ph.back());
+      // the fragments' chains (all from seed fs), four at a time
+      std::vector<const SpanIn*> todo;
+      for (const SpanIn& f : q.frags)
+        if (memo.find(MemoKey{f.tok, f.n, fs}) == memo.end()) {
+          bool dup = false;
+          for (const SpanIn* o : todo) dup |= (o->tok == f.tok && o->n == f.n);
+          if (!dup) todo.push_back(&f);
+        }
+      for (size_t i = 0; i < todo.size(); i += 4) {
+        const int k = static_cast<int>(std::min<size_t>(4, todo.size() - i));
+        const uint64_t seeds[4] = {fs, fs, fs, fs};
+        std::vector<uint64_t> hs[4];
+        chains4(seeds, &todo[i], k, ps, hs);
+        for (int c = 0; c < k; ++c) memo.emplace(MemoKey{todo[i + c]->tok, todo[i + c]->n, fs}, std::move(hs[c]));
+      }
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, true});
       for (size_t c = 0; c < q.frags.size(); ++c) srcs.push_back({fs, q.frags[c], 1, static_cast<int>(c), true});
     }
@@ -225,7 +314,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
         hit_pids.push_back(e.x);
       }
   int64_t need = static_cast<int64_t>(specs.size());
-  int64_t evictable = static_cast<int64_t>(evictable_.size());
+  int64_t evictable = n_evictable_;
   for (int32_t pid : hit_pids)
     if (pages_[pid].published && pages_[pid].pins == 0) --evictable;
   if (need > free_count() + evictable) {
@@ -240,7 +329,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   P.tick = ++tick_;
   for (int32_t pid : hit_pids) {
     PageRec& r = pages_[pid];
-    if (r.published && r.pins == 0) evictable_.erase(std::make_tuple(r.last_use, -r.idx, pid));
+    if (r.published && r.pins == 0) --n_evictable_;  // its heap entry goes stale
     r.pins += 1;
     r.last_use = P.tick;
   }
@@ -457,13 +546,13 @@ void PoolIndex::commit(Plan* p) {
     if (!r.published) {
       push_free(pid);
     } else if (r.pins == 0) {
-      evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+      make_evictable(pid);
     }
   }
   for (int32_t pid : p->hits) {
     PageRec& r = pages_[pid];
     r.pins -= 1;
-    if (r.published && r.pins == 0) evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+    if (r.published && r.pins == 0) make_evictable(pid);
   }
   p->committed = true;
   --live_plans;
@@ -475,7 +564,7 @@ void PoolIndex::release(Plan* p) {
   for (int32_t pid : p->hits) {
     PageRec& r = pages_[pid];
     r.pins -= 1;
-    if (r.published && r.pins == 0) evictable_.insert(std::make_tuple(r.last_use, -r.idx, pid));
+    if (r.published && r.pins == 0) make_evictable(pid);
   }
   p->committed = true;
   --live_plans;

@@ -126,6 +126,7 @@ class PoolIndex {
   int64_t num_pages() const { return num_pages_; }
   int64_t free_count() const { return static_cast<int64_t>(freed_.size()) + (num_pages_ - watermark_); }
   int64_t cached_count() const { return static_cast<int64_t>(index_.size()); }
+  int64_t evictable_count() const { return n_evictable_; }
   int64_t pinned_count() const;
   int64_t tick() const { return tick_; }
   int64_t total_evictions() const { return total_evictions_; }
@@ -155,7 +156,22 @@ class PoolIndex {
   // Free page ids: every id >= watermark_, plus the ids in freed_ (all < watermark_).
   std::set<int32_t> freed_;
   int64_t watermark_ = 0;
-  std::set<std::tuple<int64_t, int32_t, int32_t>> evictable_;  // (last_use, -idx, id)
+  // Evictable pages (published, unpinned) in LRU order: a binary min-heap of
+  // (last_use, -idx, id) entries with lazy deletion.  An entry is current iff its
+  // page is still published and unpinned and the page's generation (bumped each
+  // time the page becomes evictable) matches; pinning a page just leaves its entry
+  // stale.  Victims come out in the same order as from an ordered set.
+  struct LruEntry {
+    int64_t last_use;
+    int32_t neg_idx;
+    int32_t pid;
+    uint32_t gen;
+  };
+  std::vector<LruEntry> lru_;
+  std::vector<uint32_t> gen_;   // per page; survives the page being freed
+  int64_t n_evictable_ = 0;
+  void make_evictable(int32_t pid);
+  bool lru_current(const LruEntry& e) const;
   int64_t tick_ = 0;
   int64_t stamp_ = 0;  // counts plan() calls, successful or not
   int64_t total_evictions_ = 0;

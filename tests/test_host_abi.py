@@ -92,6 +92,17 @@ def test_paper_chat_example(lib):
 
 @pytest.mark.parametrize("seed", range(8))
 def test_planner_matches_oracle_replay(lib, seed):
+    _replay(seed, steps=60)
+
+
+@pytest.mark.parametrize("seed", [20, 21])
+def test_planner_matches_oracle_replay_long_stream(lib, seed):
+    """Hundreds of plans over a small pool: the LRU structure goes through many
+    evictions, re-pins and rebuilds of its lazy heap."""
+    _replay(seed, steps=700)
+
+
+def _replay(seed, steps):
     rnd = random.Random(100 + seed)
     ps = 16
     vocab = 40 if seed % 2 else 128256   # small vocab: many equal pages, exercises verification/dedup
@@ -101,7 +112,7 @@ def test_planner_matches_oracle_replay(lib, seed):
     pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=num_pages, device=-1, dtype="f32")
     ref = PoolReplay(num_pages=num_pages, page_size=ps)
     live = []
-    for step in range(60):
+    for step in range(steps):
         qs = []
         for _ in range(rnd.randrange(1, 4)):
             chosen = rnd.sample(range(10), rnd.randrange(0, 5))
