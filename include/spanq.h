@@ -228,7 +228,9 @@ int span_plan_rows(const span_plan_t* plan, int64_t* rows, int64_t cap, int64_t*
  * rotate each new key at its canonical position (prefix token t at t, fragment
  * token j at P + j), write keys and values into their pages, then write out[row] =
  * softmax over the span mask of q.k / sqrt(d) times V, with the query also at its
- * canonical position.  No-op when every page hit. */
+ * canonical position.  No-op when every page hit.  Calls on one plan may run
+ * concurrently on different streams, up to 64 of them in flight at once (the
+ * bf16 kernel schedules its work items through per-launch counters the plan owns). */
 int span_prefill_fragments(span_plan_t* plan, int32_t layer, const void* q, const void* k,
                            const void* v, void* out, void* stream);
 

@@ -1,4 +1,8 @@
-// bf16 MFMA span attention for gfx950 (CDNA4).
+// bf16 MFMA cross attention for gfx950 (CDNA4): rows that attend over cached
+// fragment pages at positions other than the ones the pages were written at
+// (repositioning, section 5.5 of the paper), optionally with the key list of an
+// item split into parts whose partial results a combine pass merges.  Span prefill
+// has a software-pipelined kernel of its own (prefill_mfma.hip).
 //
 // Work items are (row tile of 256/G query tokens, kv head).  The G query heads that
 // share a kv head are packed into one item: wave w of the eight handles head
@@ -43,42 +47,28 @@
 #include "../../include/spanq.h"
 #include "dev_common.h"
 #include "kernels.h"
+#include "mfma_common.h"
 
 namespace spanq {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-
 namespace {
 
-constexpr int kBN = 64;     // keys per tile (4 pages)
-constexpr int kNW = 8;      // waves per work-group
-constexpr int kNT = 64 * kNW;
+using namespace mfma;
+
 constexpr int kStages = 4;  // LDS ring depth; tiles are fetched two ahead
 
-// Two floats to packed bfloat16, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
-}
-__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-template <int D, bool ROT>
+template <int D>
 struct Geo {
   static constexpr int KS = D / 16;                // 16-dim steps of the QK contraction
   static constexpr int DB = D / 32;                // 32-dim blocks of the output
   static constexpr int KBYTES = kBN * D * 2;       // K tile: [64 keys][D], rows of 2D bytes
   static constexpr int VBYTES = D * kBN * 2;       // V tile: [D][64 positions], rows of 128 bytes
-  static constexpr int RBYTES = ROT ? 1024 : 0;    // cos/sin row of the tile's delta (4D bytes used)
+  static constexpr int RBYTES = 1024;              // cos/sin row of the tile's delta (4D bytes used)
   static constexpr int STAGE = KBYTES + VBYTES + RBYTES;
   static constexpr int KPW = KBYTES / 1024 / kNW;  // K DMA instructions per wave per tile
   static constexpr int VPW = VBYTES / 1024 / kNW;  // V DMA instructions per wave per tile
   static constexpr int RPW = 4 * D / kNW;          // bytes of the cos/sin row per wave
-  static constexpr int NDMA = KPW + VPW + (ROT ? 1 : 0);  // DMA instructions per wave per tile
+  static constexpr int NDMA = KPW + VPW + 1;       // DMA instructions per wave per tile
   // Beyond the ring (query rotation at item start): the rotary rows of positions
   // 0..31 for the whole kernel, and one rotary row per wave (its 32-row block's
   // first position) for the next item.
@@ -88,59 +78,6 @@ struct Geo {
   static constexpr int LDS = kStages * STAGE + RTBYTES + BRBYTES;
 };
 
-// 16-byte chunk swizzles: chunk c of K row `key` sits at c ^ kswz(key); chunk c of
-// V row d at c ^ vswz(d).  16 consecutive lanes reading one chunk column then hit
-// 16 distinct 16-byte bank groups.
-template <int D>
-__device__ __forceinline__ int kswz(int key) {
-  return D == 128 ? (key & 15) : ((key >> 1) & 7);
-}
-__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
-
-// A tile's four pages come from one span: consecutive positions, and only the
-// span's last page may be partial (then followed by empty padding pages).  So key k
-// of the tile (0..63) is a real key iff k < nk, at position pos0 + k.
-struct TilePages {
-  int id[4];
-  int pos0;   // position of key 0
-  int nk;     // real keys in the tile
-  int delta;  // reposition delta of every key of the tile
-};
-
-__device__ __forceinline__ void read_pages(const KvPage* __restrict__ kv, int first, TilePages& tp) {
-  int nk = 0;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const KvPage pg = kv[first + p];
-    tp.id[p] = pg.page_id;
-    nk += pg.n_valid;
-  }
-  tp.nk = nk;
-  tp.pos0 = kv[first].pos0;
-  tp.delta = kv[first].delta;
-}
-
-// a[p] for p in 0..3, as two levels of selects (no branches, no indexed access)
-__device__ __forceinline__ int pick4(const int (&a)[4], int p) {
-  const int lo = (p & 1) ? a[1] : a[0];
-  const int hi = (p & 1) ? a[3] : a[2];
-  return (p & 2) ? hi : lo;
-}
-
-// One lane's 16 bytes from global memory to LDS at lds_wave + 16 * lane.
-__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
-                                   (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
-}
-
-// s_waitcnt with vmcnt = N (bits 3:0 and 15:14); expcnt and lgkmcnt left at their
-// maximum, so only vector-memory operations are waited for.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
-}
-__device__ __forceinline__ void wait_vm_all() { wait_vmcnt<0>(); }
 // Wait until at most k tiles (NDMA operations each) of this wave's DMA are in flight.
 template <int NDMA>
 __device__ __forceinline__ void wait_tiles(int k) {
@@ -152,81 +89,39 @@ __device__ __forceinline__ void wait_tiles(int k) {
     wait_vmcnt<0>();
 }
 
-__device__ __forceinline__ void block_sync() {
-  __asm__ volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  __asm__ volatile("" ::: "memory");
-}
-
-// Issue the DMA of one key tile (4 pages) into an LDS stage.
-template <int D, bool ROT>
+// Issue the DMA of one key tile (4 pages) and of the cos/sin row of its delta into
+// an LDS stage.
+template <int D>
 __device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
                                            int hkv, int kvh, const TilePages& tp, unsigned char* stage,
                                            const float2* __restrict__ rope, int wave, int lane) {
-  using G = Geo<D, ROT>;
-  // The repositioning kernel has no registers to spare: there the per-lane address
-  // parts are recomputed for every tile from an opaque copy of the lane id instead
-  // of being hoisted out of the tile loop into a dozen 64-bit registers.
-  if (ROT) __asm__ volatile("" : "+v"(lane));
-  // K rows: instruction q covers bytes [1024q, 1024q + 1024), keys of one page
-#pragma unroll
-  for (int u = 0; u < G::KPW; ++u) {
-    const int q = wave * G::KPW + u;
-    const int byte = q * 1024 + 16 * lane;
-    const int key = byte / (2 * D);
-    const int c = ((byte % (2 * D)) >> 4) ^ kswz<D>(key);
-    const int pid = pick4(tp.id, __builtin_amdgcn_readfirstlane(key >> 4));
-    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(kvh) * kPage * D) +
-                        ((key & 15) * D + 8 * c);
-    dma16(src, stage + q * 1024);
+  using G = Geo<D>;
+  // No registers to spare: the per-lane address parts are recomputed for every tile
+  // from an opaque copy of the lane id instead of being hoisted out of the tile loop
+  // into a dozen 64-bit registers.
+  __asm__ volatile("" : "+v"(lane));
+  issue_k<D>(pool, layer_off, page_elems, kvh, tp, stage, wave, lane);
+  issue_v<D>(pool, layer_off, page_elems, hkv, kvh, tp, stage + G::KBYTES, wave, lane);
+  // cos/sin of the tile's delta: each wave brings RPW bytes with its first lanes
+  if (lane < G::RPW / 16) {
+    const unsigned char* src = reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tp.delta) * (D / 2)) +
+                               wave * G::RPW + 16 * lane;
+    dma16(src, stage + G::KBYTES + G::VBYTES + wave * G::RPW);
   }
-  // V rows: row d holds the 64 key positions of the tile (16 per page)
-#pragma unroll
-  for (int u = 0; u < G::VPW; ++u) {
-    const int q = wave * G::VPW + u;
-    const int byte = q * 1024 + 16 * lane;
-    const int d = byte >> 7;
-    const int c = ((byte & 127) >> 4) ^ vswz(d);
-    const int pid = pick4(tp.id, c >> 1);
-    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(hkv) * kPage * D +
-                                static_cast<int64_t>(kvh) * D * kPage) +
-                        (d * kPage + 8 * (c & 1));
-    dma16(src, stage + G::KBYTES + q * 1024);
-  }
-  if (ROT) {
-    // cos/sin of the tile's delta: each wave brings RPW bytes with its first lanes
-    if (lane < G::RPW / 16) {
-      const unsigned char* src = reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tp.delta) * (D / 2)) +
-                                 wave * G::RPW + 16 * lane;
-      dma16(src, stage + G::KBYTES + G::VBYTES + wave * G::RPW);
-    }
-  }
-}
-
-// The DMA side of an item only needs where its key list starts and its tile count.
-struct ItemKeys {
-  int kv_begin;
-  int n;  // key tiles
-};
-
-__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tiles, int ti, ItemKeys& it) {
-  const WorkTile* tile = tiles + __builtin_amdgcn_readfirstlane(ti);  // a scalar load
-  it.kv_begin = tile->kv_begin;
-  it.n = (tile->kv_end - tile->kv_begin) >> 2;
 }
 
 }  // namespace
 
-template <int D, int G, bool ROT>
+template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
     const WorkTile* __restrict__ tiles, int n_tiles_total, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
-  using GE = Geo<D, ROT>;
+  using GE = Geo<D>;
   constexpr int BM = 32 * (kNW / G);
   // Two key groups (cross attention, four query heads per kv head): a few-row item
   // lets its two 32-row wave groups take alternate key tiles of each pair.
-  constexpr bool kTwoCapable = ROT && kNW / G == 2;
+  constexpr bool kTwoCapable = kNW / G == 2;
   constexpr int NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
@@ -262,7 +157,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (!is_ok) return;
     TilePages tp;
     read_pages(kv, is.kv_begin + 4 * is_j, tp);
-    issue_tile<D, ROT>(pool, layer_off, page_elems, hkv, kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
+    issue_tile<D>(pool, layer_off, page_elems, hkv, kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
                        lane);
     ++is_j;
     ++n_issued;
@@ -270,7 +165,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   for (int k = 0; k < kStages - 2; ++k) issue_next();
 
   bf16x8_t qf[GE::KS];                // Q^T operand of the current item
-  bf16x8_t qbase[ROT ? GE::KS : 1];   // query at delta 0 (cross rows only)
+  bf16x8_t qbase[GE::KS];             // query at delta 0
   f32x16_t o[GE::DB];
   float m, l;
   int q_delta = 0;
@@ -514,11 +409,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     qpos = t.q_pos0 + irow;
     wave_min_pos = t.q_pos0 + rb0;
 
-    if constexpr (ROT) {
 #pragma unroll
-      for (int s = 0; s < GE::KS; ++s) qbase[s] = qf[s];
-      q_delta = 0;
-    }
+    for (int s = 0; s < GE::KS; ++s) qbase[s] = qf[s];
+    q_delta = 0;
 #pragma unroll
     for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
@@ -527,9 +420,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     l = 0.f;
 
     // ---- key tiles of this item, in groups of two (one for an odd last tile)
-    // raw query of the next item, loaded during the last group (the repositioning
-    // kernel, short of registers, loads it after the loop)
-    bf16x8_t qn[GE::KS];
+    bf16x8_t qn[GE::KS];  // raw query of the next item, loaded after the loop
     auto compute = [&](int j, int cs) {  // tile j of the item, stream slot cs
       // page entries of the tile, consumed here: a scalar-load wait later on would
       // also drain the LDS reads of the QK step (both share one counter)
@@ -537,7 +428,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       read_pages(kv, t.kv_begin + 4 * j, cur);
       __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
       const unsigned char* stage = lds + (cs & 3) * GE::STAGE;
-      if (ROT && cur.delta != q_delta) {
+      if (cur.delta != q_delta) {
         q_delta = cur.delta;
         rotate_q(stage);
       }
@@ -558,7 +449,6 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int u = 0; u < kStages - 1; ++u)
         if (n_issued < c + kStages) issue_next();
-      if (!ROT && j + sz == n_tiles && has_next) prefetch(ct + tstride, qn);
       if (active) {
         // two key groups: this wave takes tile grp of the pair; otherwise both
         const int u1 = two ? min(grp + 1, sz) : sz;
@@ -608,7 +498,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       store();
       break;
     }
-    if (ROT || n_tiles == 0) prefetch(ct + tstride, qn);
+    prefetch(ct + tstride, qn);
     rotate_next(tiles[ct + tstride], qn);
     store();
     ct += tstride;
@@ -623,8 +513,7 @@ bool mfma_supported(int hq, int hkv, int d, int dtype) {
   return (d == 64 || d == 128) && (g == 1 || g == 2 || g == 4 || g == 8);
 }
 
-// Compute units of the current device (one persistent work-group each).
-static hipError_t cu_count(int* n) {
+hipError_t cu_count(int* n) {
   static int cached[64] = {0};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -639,12 +528,12 @@ static hipError_t cu_count(int* n) {
   return hipSuccess;
 }
 
-template <int D, int G, bool ROT>
+template <int D, int G>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
                            float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
-  const size_t lds = Geo<D, ROT>::LDS;
-  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<D, G, ROT>),
+  const size_t lds = Geo<D>::LDS;
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<D, G>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (attr != hipSuccess) return attr;
   int cus = 0;
@@ -653,34 +542,30 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   // one work-group per CU, a multiple of hkv (each keeps one kv head)
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, G, ROT>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
+  hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
                      g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
 }
 
-template <int D, bool ROT>
+template <int D>
 static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
                            float* po, float* pml, const float2* rope, hipStream_t s) {
   switch (g.hq / g.hkv) {
-    case 1: return launch_t<D, 1, ROT>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 2: return launch_t<D, 2, ROT>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 4: return launch_t<D, 4, ROT>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 8: return launch_t<D, 8, ROT>(g, tiles, n, kv, q, out, po, pml, rope, s);
+    case 1: return launch_t<D, 1>(g, tiles, n, kv, q, out, po, pml, rope, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kv, q, out, po, pml, rope, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kv, q, out, po, pml, rope, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kv, q, out, po, pml, rope, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                            void* out, float* part_o, float* part_ml, const float2* rope, bool reposition,
-                            hipStream_t s) {
+                            void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype)) return hipErrorInvalidValue;
-  if (g.d == 128)
-    return reposition ? launch_d<128, true>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s)
-                      : launch_d<128, false>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
-  return reposition ? launch_d<64, true>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s)
-                    : launch_d<64, false>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s)
+                    : launch_d<64>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
 }
 
 }  // namespace spanq

@@ -96,6 +96,12 @@ struct span_plan_t {
   const WorkTile* tc = nullptr;
   const CombineTile* cb = nullptr;
   const float2* rope = nullptr;
+  // item counters of the span-prefill kernel: kSchedSlots pairs of words, zeroed at
+  // upload and left zeroed by each launch; launches take them in turn, so up to
+  // kSchedSlots launches of one plan may overlap (on different streams)
+  static constexpr int kSchedSlots = 64;
+  unsigned* sched = nullptr;
+  unsigned sched_next = 0;
   int bm = kGenericBM;
   bool mfma = false;
   bool committed = false;
@@ -378,6 +384,7 @@ int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, s
     auto& hb = pl->host_meta;
     size_t o_kv = put(hb, P.kv), o_k3p = put(hb, P.k3_prefill), o_k3c = put(hb, P.k3_cross);
     size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
+    size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
     e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
     if (e == hipSuccess) e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
     if (e == hipSuccess && P.n_parts > 0) {
@@ -396,6 +403,7 @@ int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, s
     pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
     pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
     pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
+    pl->sched = reinterpret_cast<unsigned*>(pl->dev_meta + o_sc);
   }
   *out = pl;
   return SPAN_OK;
@@ -490,7 +498,8 @@ int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const 
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
   tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, false, s)
+  unsigned* sched = pl->sched + 2 * (pl->sched_next++ % span_plan_t::kSchedSlots);
+  e = pl->mfma ? launch_prefill_mfma(g, pl->tp, nt, pl->kv, q, out, pl->rope, sched, s)
                : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
   tm.mark(2);
@@ -515,7 +524,7 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, true, s)
+  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s)
                : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(2);

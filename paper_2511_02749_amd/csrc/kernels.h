@@ -1,4 +1,4 @@
-// Launchers of the HIP kernels (kernels.hip, attn_mfma.hip).
+// Launchers of the HIP kernels (kernels.hip, attn_mfma.hip, prefill_mfma.hip).
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -25,15 +25,27 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_t
                                const void* q, void* out, float* part_o, float* part_ml,
                                const float2* rope, hipStream_t s);
 
-// bf16 MFMA span attention: eight waves per work-group, one work-group per (row
-// tile, kv head); a tile has mfma_bm(g) = 256 / g query tokens (g = query heads per
-// kv head).  Key lists must come in whole 4-page tiles with one delta per tile;
-// `reposition` enables the per-tile query rotation by that delta.
+// bf16 MFMA attention kernels: eight waves per work-group, work items (row tile,
+// kv head); a row tile has mfma_bm(g) = 256 / g query tokens (g = query heads per
+// kv head).  Key lists come in whole 4-page tiles with one delta per tile.
 bool mfma_supported(int hq, int hkv, int d, int dtype);
 int mfma_bm(int g);
+// Compute units of the current device (the persistent kernels run one work-group
+// on each).
+hipError_t cu_count(int* n);
+
+// Cross attention: the query is rotated by each tile's delta; tiles with
+// part >= 0 write fp32 partials for the combine pass.
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
                             const void* q, void* out, float* part_o, float* part_ml,
-                            const float2* rope, bool reposition, hipStream_t s);
+                            const float2* rope, hipStream_t s);
+
+// Span prefill (no repositioning, no key splits), the software-pipelined kernel.
+// Every tile must have at least one key tile.  `sched` is two zeroed device words,
+// the launch's item counter; the kernel leaves them at zero when it ends, so
+// launches that run one after another may share them and overlapping ones may not.
+hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
+                               const void* q, void* out, const float2* rope, unsigned* sched, hipStream_t s);
 
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,

@@ -1,0 +1,151 @@
+// Device pieces shared by the two bf16 MFMA attention kernels (attn_mfma.hip,
+// prefill_mfma.hip): operand types, LDS swizzles, the key-tile page record, the
+// global-to-LDS DMA of one key tile and the wait/barrier primitives.
+//
+// A key tile is 4 pages (64 keys) of one kv head.  In LDS its K rows are
+// [64 keys][D] and its V rows [D][64 positions], both XOR-swizzled at 16-byte
+// granularity so that the MFMA operand reads of 16 consecutive lanes hit 16
+// distinct bank groups.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "dev_common.h"
+#include "work.h"
+
+namespace spanq {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+namespace mfma {
+
+constexpr int kBN = 64;  // keys per tile (4 pages)
+constexpr int kNW = 8;   // waves per work-group
+constexpr int kNT = 64 * kNW;
+
+// Two floats to packed bfloat16, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// 16-byte chunk swizzles: chunk c of K row `key` sits at c ^ kswz(key); chunk c of
+// V row d at c ^ vswz(d).
+template <int D>
+__device__ __forceinline__ int kswz(int key) {
+  return D == 128 ? (key & 15) : ((key >> 1) & 7);
+}
+__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
+
+// A tile's four pages come from one span: consecutive positions, and only the
+// span's last page may be partial (then followed by empty padding pages).  So key k
+// of the tile (0..63) is a real key iff k < nk, at position pos0 + k.
+struct TilePages {
+  int id[4];
+  int pos0;   // position of key 0
+  int nk;     // real keys in the tile
+  int delta;  // reposition delta of every key of the tile
+};
+
+__device__ __forceinline__ void read_pages(const KvPage* __restrict__ kv, int first, TilePages& tp) {
+  int nk = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const KvPage pg = kv[first + p];
+    tp.id[p] = pg.page_id;
+    nk += pg.n_valid;
+  }
+  tp.nk = nk;
+  tp.pos0 = kv[first].pos0;
+  tp.delta = kv[first].delta;
+}
+
+// a[p] for p in 0..3, as two levels of selects (no branches, no indexed access)
+__device__ __forceinline__ int pick4(const int (&a)[4], int p) {
+  const int lo = (p & 1) ? a[1] : a[0];
+  const int hi = (p & 1) ? a[3] : a[2];
+  return (p & 2) ? hi : lo;
+}
+
+// One lane's 16 bytes from global memory to LDS at lds_wave + 16 * lane.
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                   (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
+}
+
+// s_waitcnt with vmcnt = N (bits 3:0 and 15:14); expcnt and lgkmcnt left at their
+// maximum, so only vector-memory operations are waited for.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+__device__ __forceinline__ void wait_vm_all() { wait_vmcnt<0>(); }
+
+__device__ __forceinline__ void block_sync() {
+  __asm__ volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  __asm__ volatile("" ::: "memory");
+}
+
+// K rows of a tile: [64 keys][D] at `dst`.  The tile is 64 * 2D bytes, moved by
+// KBYTES / 1024 / kNW instructions per wave; instruction q covers bytes
+// [1024q, 1024q + 1024).
+template <int D>
+__device__ __forceinline__ void issue_k(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
+                                        int kvh, const TilePages& tp, unsigned char* dst, int wave, int lane) {
+  constexpr int KPW = kBN * D * 2 / 1024 / kNW;
+#pragma unroll
+  for (int u = 0; u < KPW; ++u) {
+    const int q = wave * KPW + u;
+    const int byte = q * 1024 + 16 * lane;
+    const int key = byte / (2 * D);
+    const int c = ((byte % (2 * D)) >> 4) ^ kswz<D>(key);
+    const int pid = pick4(tp.id, __builtin_amdgcn_readfirstlane(key >> 4));
+    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(kvh) * kPage * D) +
+                        ((key & 15) * D + 8 * c);
+    dma16(src, dst + q * 1024);
+  }
+}
+
+// V rows of a tile: [D][64 positions] at `dst`; row d holds 16 positions per page.
+template <int D>
+__device__ __forceinline__ void issue_v(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
+                                        int hkv, int kvh, const TilePages& tp, unsigned char* dst, int wave,
+                                        int lane) {
+  constexpr int VPW = D * kBN * 2 / 1024 / kNW;
+#pragma unroll
+  for (int u = 0; u < VPW; ++u) {
+    const int q = wave * VPW + u;
+    const int byte = q * 1024 + 16 * lane;
+    const int d = byte >> 7;
+    const int c = ((byte & 127) >> 4) ^ vswz(d);
+    const int pid = pick4(tp.id, c >> 1);
+    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(hkv) * kPage * D +
+                                static_cast<int64_t>(kvh) * D * kPage) +
+                        (d * kPage + 8 * (c & 1));
+    dma16(src, dst + q * 1024);
+  }
+}
+
+// The DMA side of an item only needs where its key list starts and its tile count.
+struct ItemKeys {
+  int kv_begin;
+  int n;  // key tiles
+};
+
+__device__ __forceinline__ void load_item_keys(const WorkTile* __restrict__ tiles, int ti, ItemKeys& it) {
+  const WorkTile* tile = tiles + __builtin_amdgcn_readfirstlane(ti);  // a scalar load
+  it.kv_begin = tile->kv_begin;
+  it.n = (tile->kv_end - tile->kv_begin) >> 2;
+}
+
+}  // namespace mfma
+}  // namespace spanq

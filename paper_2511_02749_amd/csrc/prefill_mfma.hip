@@ -1,0 +1,701 @@
+// Span-prefill attention (rows of new prefix and fragment pages) as a
+// software-pipelined bf16 MFMA kernel for gfx950 (CDNA4).
+//
+// What it computes (span-query prefill, sections 5.1 and 5.6 of the paper): every
+// row of a fragment attends causally to the shared prefix and to its own fragment,
+// at the fragment's query-independent (canonical) positions; prefix rows attend
+// causally to the prefix.  The planner has already laid out, per row tile, the list
+// of key pages the tile may see, padded to whole 4-page tiles; keys past a row's own
+// position and empty page slots are masked here.
+//
+// Work items, operand layouts and the query rotation are those of the cross kernel
+// (attn_mfma.hip): an item is (row tile of 256/G tokens, kv head), wave w handles
+// query head w mod G and rows 32(w div G) .. +31, scores are formed transposed
+// (S^T = K Q^T, v_mfma_f32_32x32x16_bf16) so each lane owns one query row, and P^T
+// feeds O^T = V^T P^T straight from registers.
+//
+// The difference is the tile loop.  Tile x of an item is processed as
+//     QK(x + 1)  ||  softmax(x)  ||  PV(x - 1)
+// in one basic block: the QK and PV MFMAs of neighbouring tiles run while this
+// wave's vector ALU does the softmax of the tile between them, instead of every
+// wave alternating between MFMA-only and VALU-only phases.
+//
+// Softmax uses a lazily raised running max: P = 2^(S - m) is taken against the
+// current m, and m is raised (with the rescale of O and of the row sum) only when a
+// tile's row max exceeds m by more than 2^8.  P then stays below 256, which bf16
+// and the fp32 accumulators hold exactly as well as values below 1; the result
+// O / l does not depend on which m was used.  The rare raise is a separate branch
+// after the pipelined block, so the block itself has no data-dependent control.
+// The row max is reduced with a max3 tree and one v_permlane32_swap (no LDS round
+// trip); the row sum comes from v_dot2 over the packed bf16 P, i.e. exactly the
+// weights the PV MFMAs use.
+//
+// K/V stream: the key tiles of a work-group's items form one stream.  Before the
+// QK of stream tile x every wave waits for its own DMA of tiles <= x, passes one
+// barrier, and issues the DMA of tile x + 2 (HBM to LDS, global_load_lds, no
+// register staging).  K(x) is read only by QK(x), before the barrier of tile x + 1,
+// and V(x) only by PV(x), before the barrier of tile x + 2; so the fetch at the
+// barrier of tile x may overwrite the K of tile x - 1 and the V of tile x - 2: a
+// 3-slot K ring and a 4-slot V ring (132 KiB of LDS at head dim 128 with the rotary
+// rows).  Both tiles' LDS layouts are read conflict-free by 16 consecutive lanes.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <type_traits>
+
+#include "../../include/spanq.h"
+#include "dev_common.h"
+#include "kernels.h"
+#include "mfma_common.h"
+
+namespace spanq {
+
+namespace {
+
+using namespace mfma;
+
+template <int D>
+struct PGeo {
+  static constexpr int KS = D / 16;                         // 16-dim steps of the QK contraction
+  static constexpr int DB = D / 32;                         // 32-dim blocks of the output
+  static constexpr int KBYTES = kBN * D * 2;                // K tile [64 keys][D]
+  static constexpr int VBYTES = D * kBN * 2;                // V tile [D][64 positions]
+  static constexpr int KPW = KBYTES / 1024 / kNW;         // K DMA instructions per wave per tile
+  static constexpr int VPW = VBYTES / 1024 / kNW;         // V DMA instructions per wave per tile
+  static constexpr int NDMA = KPW + VPW;
+  static constexpr int NK = 3;                              // K ring slots
+  static constexpr int NV = 4;                              // V ring slots
+  static constexpr int CH = D / 4;                          // 16-byte chunks per rotary row
+  static constexpr int RTBYTES = 32 * 4 * D;                // rotary rows of positions 0..31
+  static constexpr int BRBYTES = kNW * 4 * D;               // one rotary row per wave (its rows' base)
+  static constexpr int VOFF = NK * KBYTES;
+  static constexpr int RTOFF = VOFF + NV * VBYTES;
+  static constexpr int BROFF = RTOFF + RTBYTES;
+  // Output staging, per wave 32 rows of SROW bytes: at head dim 128 the V slot freed
+  // by the previous item (16 KiB, one 32-dim block per pass), at 64 a region of its
+  // own (whole 128-byte rows in one pass).
+  static constexpr bool STAGE_IN_V = D == 128;
+  static constexpr int SROW = STAGE_IN_V ? VBYTES / kNW / 32 : 2 * D;
+  static constexpr int STOFF = BROFF + BRBYTES;
+  static constexpr int SCHOFF = STOFF + (STAGE_IN_V ? 0 : kNW * 32 * SROW);  // two item indices
+  static constexpr int LDS = SCHOFF + 16;
+  static_assert(SROW % 64 == 0 && (2 * D) % SROW == 0, "a pass covers whole 32-dim blocks");
+};
+
+constexpr float kLazy = 8.f;     // raise the running max only past m + 8 (log2 units)
+constexpr float kNoMax = -1e30f;  // running max before any key; finite, so 2^(-inf - m) = 0
+
+__device__ __forceinline__ float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
+
+// Combine a value with the one of the other half-wave (lane ^ 32).
+__device__ __forceinline__ float swap_max(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float swap_sum(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// One lane's 16 bytes from global memory to LDS byte address lds_byte + 16 * lane.
+// Issued as inline assembly so that the compiler's wait-count model does not see
+// the LDS write in flight: with it visible, every LDS operand read would wait for
+// all LDS operations (lgkmcnt(0)).  The kernel orders every read of DMA'd data
+// itself (vmcnt waits and barriers).
+__device__ __forceinline__ void dma16_m0(const void* g, uint32_t lds_byte) {
+  __asm__ volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_byte) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_byte(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+
+// s_waitcnt vmcnt(n) for n in {0, N}
+template <int N>
+__device__ __forceinline__ void wait_group(int n) {
+  if (n)
+    wait_vmcnt<N>();
+  else
+    wait_vmcnt<0>();
+}
+
+}  // namespace
+
+template <int D, int G>
+__global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefill_mfma_kernel(
+    const WorkTile* __restrict__ tiles, int n_items, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
+    bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
+    const float2* __restrict__ rope, unsigned* __restrict__ sched) {
+  using GE = PGeo<D>;
+  constexpr int KS = GE::KS, DB = GE::DB, NDMA = GE::NDMA;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
+
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int hsub = wave % G;  // head inside the kv head's group
+  const int rb = wave / G;    // 32-row block
+  const int h2 = lane >> 5;
+  const int r = lane & 31;
+  const int row = 32 * rb + r;  // this lane's row inside an item
+  const int64_t page_elems = 2ll * hkv * kPage * D;
+  unsigned char* const kring = lds;
+  unsigned char* const vring = lds + GE::VOFF;
+  unsigned char* const rt_lds = lds + GE::RTOFF;
+  unsigned char* const br_lds = lds + GE::BROFF + wave * 4 * D;
+
+  // ---------------- item schedule.  Item e is (row tile e / hkv, kv head e mod hkv);
+  // row tiles come sorted by key count, longest first.  Work-group b takes items b
+  // and b + grid, then one item at a time from the launch's counter sched[0], so
+  // compute units that run faster take more items (the XCDs of one chip do not run
+  // this kernel equally fast).  The grab for item k + 3 is issued during the last
+  // block of item k and published at the first barrier of item k + 1: while it
+  // computes item k a work-group knows items k .. k + 2, which is as far as the key
+  // tile stream runs ahead.  Item indices at or past n_total stand for "none"; the
+  // counter only grows, so once one grab comes back empty all later ones would too.
+  // The grab for item k + 3 is issued right after the first barrier of item k and
+  // its result is first read at the first barrier of item k + 1, after that
+  // barrier's full wait: the atomic's latency hides behind a whole item.  (The
+  // build turns off the compiler's atomic optimizer, whose broadcast of the result
+  // would read it, and so wait for it, right after the atomic.)
+  const int n_total = n_items * hkv;
+  const int grid = gridDim.x;
+  int ec0 = blockIdx.x;                                        // compute item k
+  int ec1 = min(n_total, static_cast<int>(blockIdx.x) + grid);  // item k + 1
+  int ec2 = n_total;                                           // item k + 2, read at item k's first barrier
+  unsigned grab_raw = 0;   // thread 0: counter value the last grab returned
+  bool grabbed = false;    // the last grab was issued (not skipped as known empty)
+  int* const sched_lds = reinterpret_cast<int*>(lds + GE::SCHOFF);  // two slots, by item parity
+  auto grab = [&](int last_known) __attribute__((always_inline)) {
+    grabbed = last_known < n_total;
+    if (grabbed && threadIdx.x == 0) grab_raw = atomicAdd(sched, 1u);
+  };
+  auto grabbed_item = [&]() __attribute__((always_inline)) {
+    return grabbed ? min(n_total, 2 * grid + static_cast<int>(grab_raw)) : n_total;
+  };
+
+  // ---------------- DMA side: the stream's next tile is tile dk_j of item dk_e, which
+  // is item k + dk_k of the schedule
+  ItemKeys dk;
+  int dk_k = 0, dk_e = ec0, dk_j = 0;
+  bool dk_ok = true;
+  load_item_keys(tiles, dk_e / hkv, dk);
+  int dk_kvh = dk_e % hkv;
+  int fk = 0, fv = 0;  // ring slots of the next fetch
+  // Per-lane source offsets (bytes, inside a page) of this wave's DMA instructions.
+  // K instruction u fills LDS bytes [1024q, 1024q + 1024) of the K tile, q = wave
+  // KPW + u: keys 4q.. (head dim 128) of one page, chunk c of key k stored at chunk
+  // c ^ kswz(k).  V instruction u fills 1024 bytes of the V tile, which is laid out
+  // [page][d][two 16-byte halves], half h of row d stored at h ^ (d >> 3 & 1): rows
+  // 32b .. 32b + 31 of one page.  So every instruction reads a single page, and a
+  // tile's fetch is a scalar page base plus these offsets.
+  constexpr int CPK = D / 8;  // 16-byte chunks per key row
+  uint32_t dk_ofs[GE::KPW], dv_ofs[GE::VPW];
+  int dk_page[GE::KPW], dv_page[GE::VPW];
+#pragma unroll
+  for (int u = 0; u < GE::KPW; ++u) {
+    const int qi = wave * GE::KPW + u;
+    const int key = qi * (64 / CPK) + lane / CPK;
+    const int c = (lane % CPK) ^ kswz<D>(key);
+    dk_page[u] = (qi * (64 / CPK)) >> 4;  // the instruction's keys share one page
+    dk_ofs[u] = 2u * static_cast<uint32_t>((key & 15) * D + 8 * c);
+  }
+#pragma unroll
+  for (int u = 0; u < GE::VPW; ++u) {
+    const int qi = wave * GE::VPW + u;
+    const int d = 32 * (qi % (D / 32)) + (lane >> 1);
+    const int h = (lane & 1) ^ ((d >> 3) & 1);
+    dv_page[u] = qi / (D / 32);
+    dv_ofs[u] = 2u * static_cast<uint32_t>(hkv * kPage * D + d * kPage + 8 * h);
+  }
+  // (position of key 0, real keys) of stream tiles x, x + 1, x + 2 after the fetch
+  // at the barrier of tile x
+  int mp0 = 0, mn0 = 0, mp1 = 0, mn1 = 0, mp2 = 0, mn2 = 0;
+  auto fetch_next = [&]() __attribute__((always_inline)) -> int {  // DMA instructions this wave issued
+    if (dk_ok && dk_j >= dk.n) {  // every item has at least one key tile
+      ++dk_k;
+      dk_e = dk_k == 1 ? ec1 : ec2;
+      dk_j = 0;
+      dk_ok = dk_e < n_total;
+      if (dk_ok) {
+        load_item_keys(tiles, dk_e / hkv, dk);
+        dk_kvh = dk_e % hkv;
+      }
+    }
+    mp0 = mp1;
+    mn0 = mn1;
+    mp1 = mp2;
+    mn1 = mn2;
+    if (!dk_ok) return 0;
+    TilePages tp;
+    read_pages(kv, dk.kv_begin + 4 * dk_j, tp);
+    mp2 = tp.pos0;
+    mn2 = tp.nk;
+    // the kv head's K rows of a page start kvh * 16 * D elements in, its V rows as many
+    // elements past the page's V half
+    const unsigned char* pg = reinterpret_cast<const unsigned char*>(pool + layer_off + dk_kvh * kPage * D);
+#pragma unroll
+    for (int u = 0; u < GE::KPW; ++u)
+      dma16_m0(pg + static_cast<int64_t>(pick4(tp.id, dk_page[u])) * (page_elems * 2) + dk_ofs[u],
+               lds_byte(kring + fk * GE::KBYTES + (wave * GE::KPW + u) * 1024));
+#pragma unroll
+    for (int u = 0; u < GE::VPW; ++u)
+      dma16_m0(pg + static_cast<int64_t>(pick4(tp.id, dv_page[u])) * (page_elems * 2) + dv_ofs[u],
+               lds_byte(vring + fv * GE::VBYTES + (wave * GE::VPW + u) * 1024));
+    ++dk_j;
+    fk = (fk == GE::NK - 1) ? 0 : fk + 1;
+    fv = (fv == GE::NV - 1) ? 0 : fv + 1;
+    return NDMA;
+  };
+
+  // ---------------- compute-side state
+  bf16x8_t qf[KS];  // Q^T operand of the current item (rotated, scaled by log2(e)/sqrt(d))
+  f32x16_t o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m = kNoMax, l = 0.f;
+  int qpos = 0, wave_min_pos = 0;
+
+  // Per-lane LDS byte offsets of the MFMA operand reads inside a ring slot: K step
+  // ks of key block 0 (block 1 is 32 rows further, a constant), and the V operand of
+  // page 0, dims 0..31 (other pages and dim blocks are constant offsets).
+  uint32_t kofs[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) kofs[ks] = 2u * (r * D + 8 * ((2 * ks + h2) ^ kswz<D>(r)));
+  const uint32_t vofs = 32u * r + 16u * (h2 ^ ((r >> 3) & 1));
+  auto lds_at = [&](uint32_t base, uint32_t ofs) __attribute__((always_inline)) {
+    return reinterpret_cast<const bf16x8_t*>(lds + base + ofs);
+  };
+
+  // ---- building blocks of one 32-key block (block kb of a 64-key tile)
+  // S^T = K Q^T over the block
+  auto qk = [&](uint32_t kbase, int kb, f32x16_t& sc) __attribute__((always_inline)) {
+    kbase += kb * 32 * D * 2;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*lds_at(kbase, kofs[ks]), qf[ks], sc, 0, 0, 0);
+  };
+  // causal positions and partial/empty pages, for block kb of a tile whose key 0 is
+  // at pos0 with nk real keys; the test is wave-uniform.  Element i is key
+  // 32kb + 8(i/4) + 4h2 + i%4 of the tile, kept iff it is a real key (< nk) at a
+  // position <= the row's.
+  auto mask = [&](f32x16_t& sc, int kb, int pos0, int nk) __attribute__((always_inline)) {
+    if (nk < 32 * kb + 32 || pos0 + 32 * kb + 31 > wave_min_pos) {
+      const int lim = min(nk, qpos - pos0 + 1) - 32 * kb - 4 * h2;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (8 * (i >> 2) + (i & 3) >= lim) sc[i] = -INFINITY;
+    }
+  };
+  // the block's row max (both half-waves)
+  auto row_max = [&](const f32x16_t& sc) __attribute__((always_inline)) -> float {
+    const float a0 = max3f(sc[0], sc[1], sc[2]), a1 = max3f(sc[3], sc[4], sc[5]);
+    const float a2 = max3f(sc[6], sc[7], sc[8]), a3 = max3f(sc[9], sc[10], sc[11]);
+    const float a4 = max3f(sc[12], sc[13], sc[14]);
+    return swap_max(max3f(max3f(a0, a1, a2), max3f(a3, a4, sc[15]), -INFINITY));
+  };
+  // O^T += V^T P^T over block kb of a tile (its pages 2kb, 2kb + 1); the V operand of
+  // page g, dims 32db.. is 16 bytes at [g][32db + r][half h2]
+  auto pv = [&](uint32_t vbase, int kb, const bf16x8_t (&pk)[2]) __attribute__((always_inline)) {
+    vbase += kb * 2 * D * 32;
+    const bf16x8_t* a = lds_at(vbase, vofs);
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)  // DB independent accumulator chains
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(half * D * 32 + db * 1024) / 16], pk[half], o[db], 0, 0, 0);
+  };
+  // Lazily raised running max, decided before the block's exponentials without a
+  // branch: m moves (to the block max) only when some row's block max exceeds it by
+  // more than kLazy.  corr rescales what was accumulated against the old m.
+  auto raise_max = [&](const f32x16_t& sc, float& corr) __attribute__((always_inline)) -> bool {
+    const float mx = row_max(sc);
+    const bool up = __any(mx > m + kLazy);
+    const float m_new = up ? fmaxf(m, mx) : m;
+    corr = up ? __builtin_amdgcn_exp2f(m - m_new) : 1.f;
+    m = m_new;
+    return up;
+  };
+  // after the block (whose PV MFMAs still added terms taken against the old m): the
+  // rare rescale of O, then the row sum
+  auto rescale = [&](bool up, float corr, float tsum) __attribute__((always_inline)) {
+    if (__builtin_expect(up, 0)) {
+      __asm__ volatile("");
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+    }
+    l = l * corr + tsum;
+  };
+
+  // One pipelined block, in a fixed instruction order: the softmax of scores s_in
+  // (lazily raised max, P = 2^(S - m) packed into pk_out, its row sum) runs in KS
+  // chunks; chunk t also issues the QK MFMA of step t of the next key block (WQK, K
+  // tile at byte kaddr) and the PV MFMA t of the previous block (WPV, V of pages
+  // vaddr.., operand pk_prev), and the LDS reads of the operands two chunks ahead.
+  // The chunks are fenced, so the compiler keeps this order and at most four
+  // operand reads (16 registers) are in flight.
+  auto block = [&](auto wqk, auto wpv, const f32x16_t& s_in, bf16x8_t (&pk_out)[2], uint32_t kaddr,
+                   f32x16_t& s_out, uint32_t vaddr, const bf16x8_t (&pk_prev)[2], float& corr,
+                   float& tsum) __attribute__((always_inline)) -> bool {
+    constexpr bool WQK = decltype(wqk)::value, WPV = decltype(wpv)::value;
+    constexpr int WPC = 8 / KS;  // packed words of P per chunk (8 words per block)
+    auto rdk = [&](int t) __attribute__((always_inline)) { return *lds_at(kaddr, kofs[t]); };
+    auto rdv = [&](int t) __attribute__((always_inline)) {
+      return lds_at(vaddr, vofs)[((t / DB) * D * 32 + (t % DB) * 1024) / 16];
+    };
+    bf16x8_t ak[KS], av[KS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if constexpr (WQK) ak[t] = rdk(t);
+      if constexpr (WPV) av[t] = rdv(t);
+    }
+    const bool up = raise_max(s_in, corr);
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+    float ts0 = 0.f, ts1 = 0.f;
+    u32x4_t w[2];
+#pragma unroll
+    for (int t = 0; t < KS; ++t) {
+      if constexpr (WQK) {
+        s_out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[t], qf[t], t == 0 ? f32x16_t{} : s_out, 0, 0, 0);
+        if (t + 2 < KS) ak[t + 2] = rdk(t + 2);
+      }
+      if constexpr (WPV) {
+        o[t % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[t], pk_prev[t / DB], o[t % DB], 0, 0, 0);
+        if (t + 2 < KS) av[t + 2] = rdv(t + 2);
+      }
+#pragma unroll
+      for (int x = 0; x < WPC; ++x) {
+        const int wd = t * WPC + x, half = wd >> 2, e = wd & 3;
+        const float p0 = __builtin_amdgcn_exp2f(s_in[8 * half + 2 * e] - m);
+        const float p1 = __builtin_amdgcn_exp2f(s_in[8 * half + 2 * e + 1] - m);
+        // the dot product takes the packed word itself, not w[.][e] read back: with
+        // the read-back form, hipcc 7.2 at -O3 feeds every fdot2 the vector's element 0
+        const uint32_t pw = pack_bf16x2(p0, p1);
+        w[half][e] = pw;
+        if (e & 1)
+          ts1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts1, false);
+        else
+          ts0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts0, false);
+      }
+      // the chunk's exponentials end here: without this, the optimizer moves every
+      // one of them behind the block's last MFMA
+      __asm__ volatile("" : "+v"(ts0), "+v"(ts1));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    pk_out[0] = __builtin_bit_cast(bf16x8_t, w[0]);
+    pk_out[1] = __builtin_bit_cast(bf16x8_t, w[1]);
+    tsum = ts0 + ts1;
+    return up;
+  };
+
+  // ---------------- query rotation at item start: the rotary angles of row r (0..31)
+  // of a wave's 32-row block come from R(base + r) = R(base) R(r), with R(0..31)
+  // kept in LDS for the whole kernel and R(base) (base = the block's first
+  // position) brought into LDS by DMA together with the item's raw query.
+  // (these helpers run once per item; their per-lane address parts are derived
+  // from an opaque copy of the lane id so that none of them is hoisted out of the
+  // item loop into registers held across the tile loop)
+  auto prefetch = [&](int e, bf16x8_t (&qn)[KS]) __attribute__((always_inline)) {
+    const WorkTile tn = tiles[e / hkv];
+    const int head = (e % hkv) * G + hsub;
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+    const int lrow = 32 * rb + (ln & 31), lh2 = ln >> 5;
+    if (32 * rb < tn.n_rows && ln < GE::CH) {
+      const unsigned char* src =
+          reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tn.q_pos0 + 32 * rb) * (D / 2)) +
+          16 * ln;
+      dma16(src, br_lds);
+    }
+    if (lrow < tn.n_rows) {
+      const bf16_t* src = q + (static_cast<int64_t>(tn.q_row0 + lrow) * hq + head) * D + 8 * lh2;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qn[s] = *reinterpret_cast<const bf16x8_t*>(src + 16 * s);
+    } else {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qn[s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+    }
+  };
+  // qf <- R(position) qn * log2(e)/sqrt(d), rounded to bf16 once (the loads of qn
+  // and of the base row must have landed)
+  auto rotate = [&](const WorkTile& tn, const bf16x8_t (&qn)[KS]) __attribute__((always_inline)) {
+    __asm__ volatile("" ::: "memory");
+    if (32 * rb >= tn.n_rows) {  // no row of this wave is real
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+      return;
+    }
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+    const int lr = ln & 31, lh2 = ln >> 5;
+    const float4* br = reinterpret_cast<const float4*>(br_lds);
+    const float4* rt = reinterpret_cast<const float4*>(rt_lds + lr * 4 * D);
+#pragma unroll
+    for (int s = 0; s < KS / 2; ++s) {
+      const u32x4_t a4 = __builtin_bit_cast(u32x4_t, qn[s]);
+      const u32x4_t b4 = __builtin_bit_cast(u32x4_t, qn[s + KS / 2]);
+      u32x4_t na, nb;
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        // frequencies 16s + 8h2 + 2e2 and +1: one 16-byte chunk of each rotary row
+        const int ch = 8 * s + 4 * lh2 + e2;
+        const float4 vb = br[ch];
+        const float4 vr = rt[ch ^ (lr & (GE::CH - 1))];
+        float ra[2], rb2[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float cb = u ? vb.z : vb.x, sb = u ? vb.w : vb.y;
+          const float cr = u ? vr.z : vr.x, sr = u ? vr.w : vr.y;
+          const float cs = cb * cr - sb * sr;
+          const float sn = sb * cr + cb * sr;
+          const float a = u ? hi_bf16(a4[e2]) : lo_bf16(a4[e2]);
+          const float b = u ? hi_bf16(b4[e2]) : lo_bf16(b4[e2]);
+          ra[u] = (a * cs - b * sn) * scale_log2;
+          rb2[u] = (b * cs + a * sn) * scale_log2;
+        }
+        na[e2] = pack_bf16x2(ra[0], ra[1]);
+        nb[e2] = pack_bf16x2(rb2[0], rb2[1]);
+      }
+      qf[s] = __builtin_bit_cast(bf16x8_t, na);
+      qf[s + KS / 2] = __builtin_bit_cast(bf16x8_t, nb);
+      // one frequency block at a time: its rotary rows are 8 LDS reads, all of them
+      // at once would need 128 registers next to O and both queries
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // ---------------- output of the previous item, stored at the next item's first
+  // barrier so the stores sit behind no DMA wait (st_rows = 0: nothing pending;
+  // the call then only clears O).  A lane holds one row and 4 of every 8
+  // consecutive dims, so stored straight from registers each instruction would
+  // touch 32 rows 16 bytes at a time; instead the rows pass through this wave's
+  // LDS staging area and leave as 16-byte pieces of whole 64- or 128-byte row
+  // segments.  `stage` must not be read or written by any other wave meanwhile.
+  int st_row0 = 0, st_rows = 0, st_head = 0;
+  float st_inv = 0.f;
+  auto store_out = [&](uint32_t stage) __attribute__((always_inline)) {
+    constexpr int SROW = GE::SROW;
+    constexpr int CPR = SROW / 16;     // 16-byte chunks per staged row
+    constexpr int RPG = 256 / SROW;    // staged rows per 256 bytes (one pass of the banks)
+    constexpr int DBP = SROW / 64;     // 32-dim blocks per pass
+    constexpr int RPI = 64 / CPR;      // rows per store instruction
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+    const int lr = ln & 31, lh2 = ln >> 5;
+    if (st_rows > 0) {
+#pragma unroll
+      for (int ps = 0; ps < DB / DBP; ++ps) {
+        // chunk c of staged row x sits at chunk c ^ ((x / RPG) mod CPR): the 32
+        // rows of one 8-byte write then spread over every bank pair twice
+#pragma unroll
+        for (int dd = 0; dd < DBP; ++dd)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int db = ps * DBP + dd;
+            const int c = (4 * dd + g4) ^ ((lr / RPG) & (CPR - 1));
+            const u32x2_t w = u32x2_t{pack_bf16x2(o[db][4 * g4] * st_inv, o[db][4 * g4 + 1] * st_inv),
+                                      pack_bf16x2(o[db][4 * g4 + 2] * st_inv, o[db][4 * g4 + 3] * st_inv)};
+            *reinterpret_cast<u32x2_t*>(lds + stage + lr * SROW + 16 * c + 8 * lh2) = w;
+          }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int k = 0; k < 32 / RPI; ++k) {
+          const int x = k * RPI + ln / CPR, c = ln % CPR;
+          const u32x4_t v = *reinterpret_cast<const u32x4_t*>(lds + stage + x * SROW + 16 * (c ^ ((x / RPG) & (CPR - 1))));
+          const int lrow = 32 * rb + x;
+          if (lrow < st_rows)
+            *reinterpret_cast<u32x4_t*>(out + (static_cast<int64_t>(st_row0 + lrow) * hq + st_head) * D +
+                                        32 * DBP * ps + 8 * c) = v;
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+    st_rows = 0;
+  };
+
+  // ---------------- kernel prologue: rotary rows 0..31, stream tiles 0 and 1, first query
+  int last_ops = 0;  // DMA instructions of the most recent fetch group
+  // raw query rows of the next item: loaded during an item's last block and rotated
+  // at the next item's first barrier, after the previous item's rows are stored
+  bf16x8_t qn[KS];
+  {
+    constexpr int RT_PER_WAVE = GE::RTBYTES / 1024 / kNW;
+#pragma unroll
+    for (int u = 0; u < RT_PER_WAVE; ++u) {  // chunk c of row r stored at chunk c ^ (r mod CH)
+      const int qi = wave * RT_PER_WAVE + u;
+      const int pos = qi * 64 + lane;
+      const int rr = pos / GE::CH, cc = pos % GE::CH;
+      const unsigned char* src =
+          reinterpret_cast<const unsigned char*>(rope) + rr * 4 * D + 16 * (cc ^ (rr & (GE::CH - 1)));
+      dma16(src, rt_lds + qi * 1024);
+    }
+    fetch_next();
+    fetch_next();
+    prefetch(ec0, qn);
+    grab(ec1);  // item 2
+    wait_vm_all();
+    block_sync();
+  }
+
+  int ck = 0, cv = 0;  // ring slots of the compute tile
+  auto kslot = [&](int k) __attribute__((always_inline)) { return static_cast<uint32_t>(k * GE::KBYTES); };
+  auto vslot = [&](int v) __attribute__((always_inline)) { return static_cast<uint32_t>(GE::VOFF + v * GE::VBYTES); };
+  auto next3 = [](int k) __attribute__((always_inline)) { return k == 2 ? 0 : k + 1; };
+  auto next4 = [](int v) __attribute__((always_inline)) { return (v + 1) & 3; };
+  // this wave's output staging: at head dim 128 in V slot cv - 1, which holds the
+  // tile consumed last; it is refilled only by the fetch after the next barrier
+  auto stage_at = [&](int v) __attribute__((always_inline)) {
+    return static_cast<uint32_t>((GE::STAGE_IN_V ? GE::VOFF + ((v + 3) & 3) * GE::VBYTES : GE::STOFF) +
+                                 wave * 32 * GE::SROW);
+  };
+
+  int kpar = 0;  // parity of the compute item: its schedule slot
+  while (ec0 < n_total) {
+    const WorkTile t = tiles[ec0 / hkv];
+    const int head = (ec0 % hkv) * G + hsub;
+    const int n = (t.kv_end - t.kv_begin) >> 2;  // at least 1: a row tile sees its own first page
+    const bool has_next = ec1 < n_total;
+    qpos = t.q_pos0 + row;
+    wave_min_pos = t.q_pos0 + 32 * rb;
+    m = kNoMax;
+    l = 0.f;
+
+    // the barrier before the QK of a stream tile, then the fetch of the tile two ahead
+    auto sync_fetch = [&]() __attribute__((always_inline)) {
+      wait_group<NDMA>(last_ops);
+      block_sync();
+      last_ops = fetch_next();
+    };
+
+    // Key blocks u = 0 .. 2n-1 of the item (block u&1 of tile u/2), processed as
+    //   QK(u + 1) || softmax(u) || PV(u - 1);
+    // the barrier and fetch come before the QK that opens a tile (u + 1 even).
+    f32x16_t S[2];
+    bf16x8_t P[2][2];
+    // u = 2j: QK(2j + 1) (same tile) || softmax(2j) || PV(2j - 1) (previous tile)
+    auto step_even = [&](auto with_pv, uint32_t kslot0, uint32_t vprev) __attribute__((always_inline)) {
+      float corr, tsum;
+      const bool up = block(std::true_type{}, with_pv, S[0], P[0], kslot0 + 32 * D * 2, S[1], vprev + 2 * D * 32,
+                            P[1], corr, tsum);
+      rescale(up, corr, tsum);
+      mask(S[1], 1, mp0, mn0);
+    };
+    // u = 2j + 1 (not the last): barrier; QK(2j + 2) (next tile) || softmax(2j + 1) || PV(2j)
+    auto step_odd = [&](uint32_t knext, uint32_t vcur) __attribute__((always_inline)) {
+      sync_fetch();
+      __builtin_amdgcn_sched_barrier(0);
+      float corr, tsum;
+      const bool up = block(std::true_type{}, std::true_type{}, S[1], P[1], knext, S[0], vcur, P[0], corr, tsum);
+      rescale(up, corr, tsum);
+      mask(S[0], 0, mp0, mn0);
+    };
+    // u = 2n - 1: softmax(2n - 1) || PV(2n - 2), then PV(2n - 1)
+    auto last_odd = [&](uint32_t vcur) __attribute__((always_inline)) {
+      if (has_next) prefetch(ec1, qn);  // the next item's query rows
+      float corr, tsum;
+      const bool up = block(std::false_type{}, std::true_type{}, S[1], P[1], 0u, S[0], vcur, P[0], corr, tsum);
+      rescale(up, corr, tsum);
+      pv(vcur, 1, P[1]);
+    };
+
+    // ---- the barrier of tile 0 (its wait also covers the query rows loaded during
+    // the previous item's last block and the previous grab): publish item k + 2, grab
+    // item k + 3, store the previous item's rows, rotate this item's query, fetch
+    wait_vm_all();
+    if (threadIdx.x == 0) sched_lds[kpar] = grabbed_item();
+    block_sync();
+    ec2 = __builtin_amdgcn_readfirstlane(sched_lds[kpar]);
+    kpar ^= 1;
+    grab(ec2);
+    store_out(stage_at(cv));
+    rotate(t, qn);
+    last_ops = fetch_next();
+    qk(kslot(ck), 0, S[0]);
+    mask(S[0], 0, mp0, mn0);
+    step_even(std::false_type{}, kslot(ck), 0u);
+    for (int j = 0; j + 1 < n; ++j) {
+      const int ck1 = next3(ck), cv1 = next4(cv);
+      step_odd(kslot(ck1), vslot(cv));
+      step_even(std::true_type{}, kslot(ck1), vslot(cv));
+      ck = ck1;
+      cv = cv1;
+    }
+    last_odd(vslot(cv));
+    ck = next3(ck);
+    cv = next4(cv);
+
+    // ---- this item's rows are stored at the next barrier
+    const float l_row = swap_sum(l);
+    st_row0 = t.q_row0;
+    st_rows = t.n_rows;
+    st_head = head;
+    st_inv = l_row > 0.f ? 1.f / l_row : 0.f;
+    ec0 = ec1;  // next item
+    ec1 = ec2;
+    --dk_k;
+  }
+  block_sync();  // every wave is done with the last V tile
+  store_out(stage_at(cv));
+  // The work-group that finishes last leaves the counters at zero for the next
+  // launch; the fence orders this work-group's grabs before its count.
+  if (threadIdx.x == 0) {
+    __threadfence();
+    if (atomicAdd(sched + 1, 1u) == gridDim.x - 1) {
+      atomicExch(sched, 0u);
+      atomicExch(sched + 1, 0u);
+    }
+  }
+}
+
+template <int D, int G>
+static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+                           const float2* rope, unsigned* sched, int cus, hipStream_t s) {
+  const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  const size_t lds = PGeo<D>::LDS;
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_mfma_kernel<D, G>),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (attr != hipSuccess) return attr;
+  // one work-group per CU; items are scheduled dynamically
+  const int64_t items = static_cast<int64_t>(n) * g.hkv;
+  if (items >= (1ll << 30)) return hipErrorInvalidValue;
+  const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus)));
+  hipLaunchKernelGGL((prefill_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
+                     static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
+                     g.layer_off, g.hq, g.hkv, scale_log2, rope, sched);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+                           const float2* rope, unsigned* sched, int cus, hipStream_t s) {
+  switch (g.hq / g.hkv) {
+    case 1: return launch_t<D, 1>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
+                               void* out, const float2* rope, unsigned* sched, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype) || sched == nullptr) return hipErrorInvalidValue;
+  int cus = 0;
+  const hipError_t e = cu_count(&cus);
+  if (e != hipSuccess) return e;
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kv, q, out, rope, sched, cus, s)
+                    : launch_d<64>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+}
+
+}  // namespace spanq
