@@ -332,42 +332,63 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     l = l * corr + tsum;
   };
 
+  // Operands of a block's chunks 0 and 1, read during the block before it.
+  struct Pre {
+    bf16x8_t k[2], v[2];
+  };
   // One pipelined block, in a fixed instruction order: the softmax of scores s_in
   // (lazily raised max, P = 2^(S - m) packed into pk_out, its row sum) runs in KS
   // chunks; chunk t also issues the QK MFMA of step t of the next key block (WQK, K
   // tile at byte kaddr) and the PV MFMA t of the previous block (WPV, V of pages
   // vaddr.., operand pk_prev), and the LDS reads of the operands two chunks ahead.
-  // The chunks are fenced, so the compiler keeps this order and at most four
-  // operand reads (16 registers) are in flight.
-  auto block = [&](auto wqk, auto wpv, const f32x16_t& s_in, bf16x8_t (&pk_out)[2], uint32_t kaddr,
-                   f32x16_t& s_out, uint32_t vaddr, const bf16x8_t (&pk_prev)[2], float& corr,
+  // The operands of chunks 0 and 1 come from the previous block (pre.v always;
+  // pre.k if PREK, else K is read here, right after the barrier that made it
+  // valid), and the last two chunks read those of the next block (K at nkaddr if
+  // NXK, V at nvaddr if NXV), so the MFMAs of chunk 0 need not wait for LDS.  Chunk
+  // 0 issues its MFMAs before the row max, which they do not depend on.  The chunks
+  // are fenced, so the compiler keeps this order and at most four operand reads (16
+  // registers) are in flight.
+  auto block = [&](auto wqk, auto wpv, auto prek, auto nxk, auto nxv, const f32x16_t& s_in,
+                   bf16x8_t (&pk_out)[2], uint32_t kaddr, f32x16_t& s_out, uint32_t vaddr,
+                   const bf16x8_t (&pk_prev)[2], Pre& pre, uint32_t nkaddr, uint32_t nvaddr, float& corr,
                    float& tsum) __attribute__((always_inline)) -> bool {
-    constexpr bool WQK = decltype(wqk)::value, WPV = decltype(wpv)::value;
+    constexpr bool WQK = decltype(wqk)::value, WPV = decltype(wpv)::value, PREK = decltype(prek)::value;
+    constexpr bool NXK = decltype(nxk)::value, NXV = decltype(nxv)::value;
     constexpr int WPC = 8 / KS;  // packed words of P per chunk (8 words per block)
-    auto rdk = [&](int t) __attribute__((always_inline)) { return *lds_at(kaddr, kofs[t]); };
-    auto rdv = [&](int t) __attribute__((always_inline)) {
-      return lds_at(vaddr, vofs)[((t / DB) * D * 32 + (t % DB) * 1024) / 16];
+    auto rdk = [&](uint32_t base, int t) __attribute__((always_inline)) { return *lds_at(base, kofs[t]); };
+    auto rdv = [&](uint32_t base, int t) __attribute__((always_inline)) {
+      return lds_at(base, vofs)[((t / DB) * D * 32 + (t % DB) * 1024) / 16];
     };
     bf16x8_t ak[KS], av[KS];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      if constexpr (WQK) ak[t] = rdk(t);
-      if constexpr (WPV) av[t] = rdv(t);
+      if constexpr (WQK) ak[t] = PREK ? pre.k[t] : rdk(kaddr, t);
+      if constexpr (WPV) av[t] = pre.v[t];
     }
-    const bool up = raise_max(s_in, corr);
-    __builtin_amdgcn_sched_barrier(0);
+    auto qk_mfma = [&](int t) __attribute__((always_inline)) {
+      s_out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[t], qf[t], t == 0 ? f32x16_t{} : s_out, 0, 0, 0);
+    };
     const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
     float ts0 = 0.f, ts1 = 0.f;
     u32x4_t w[2];
+    bool up = false;
 #pragma unroll
     for (int t = 0; t < KS; ++t) {
       if constexpr (WQK) {
-        s_out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[t], qf[t], t == 0 ? f32x16_t{} : s_out, 0, 0, 0);
-        if (t + 2 < KS) ak[t + 2] = rdk(t + 2);
+        if (PREK || t > 0) qk_mfma(t);
       }
-      if constexpr (WPV) {
-        o[t % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[t], pk_prev[t / DB], o[t % DB], 0, 0, 0);
-        if (t + 2 < KS) av[t + 2] = rdv(t + 2);
+      if constexpr (WPV) o[t % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[t], pk_prev[t / DB], o[t % DB], 0, 0, 0);
+      if (t + 2 < KS) {
+        if constexpr (WQK) ak[t + 2] = rdk(kaddr, t + 2);
+        if constexpr (WPV) av[t + 2] = rdv(vaddr, t + 2);
+      } else {
+        if constexpr (NXK) pre.k[t + 2 - KS] = rdk(nkaddr, t + 2 - KS);
+        if constexpr (NXV) pre.v[t + 2 - KS] = rdv(nvaddr, t + 2 - KS);
+      }
+      if (t == 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        up = raise_max(s_in, corr);
+        if constexpr (WQK && !PREK) qk_mfma(0);
       }
 #pragma unroll
       for (int x = 0; x < WPC; ++x) {
@@ -582,20 +603,27 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // the barrier and fetch come before the QK that opens a tile (u + 1 even).
     f32x16_t S[2];
     bf16x8_t P[2][2];
-    // u = 2j: QK(2j + 1) (same tile) || softmax(2j) || PV(2j - 1) (previous tile)
-    auto step_even = [&](auto with_pv, uint32_t kslot0, uint32_t vprev) __attribute__((always_inline)) {
+    Pre pre;
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    // u = 2j: QK(2j + 1) (same tile) || softmax(2j) || PV(2j - 1) (previous tile); reads
+    // the V operands of the next block (block 0 of the V tile at vnext)
+    auto step_even = [&](auto with_pv, auto prek, uint32_t kslot0, uint32_t vprev,
+                         uint32_t vnext) __attribute__((always_inline)) {
       float corr, tsum;
-      const bool up = block(std::true_type{}, with_pv, S[0], P[0], kslot0 + 32 * D * 2, S[1], vprev + 2 * D * 32,
-                            P[1], corr, tsum);
+      const bool up = block(T_{}, with_pv, prek, F_{}, T_{}, S[0], P[0], kslot0 + 32 * D * 2, S[1],
+                            vprev + 2 * D * 32, P[1], pre, 0u, vnext, corr, tsum);
       rescale(up, corr, tsum);
       mask(S[1], 1, mp0, mn0);
     };
-    // u = 2j + 1 (not the last): barrier; QK(2j + 2) (next tile) || softmax(2j + 1) || PV(2j)
+    // u = 2j + 1 (not the last): barrier; QK(2j + 2) (next tile) || softmax(2j + 1) || PV(2j);
+    // reads the operands of the block after it (block 1 of the same K and V tiles)
     auto step_odd = [&](uint32_t knext, uint32_t vcur) __attribute__((always_inline)) {
       sync_fetch();
       __builtin_amdgcn_sched_barrier(0);
       float corr, tsum;
-      const bool up = block(std::true_type{}, std::true_type{}, S[1], P[1], knext, S[0], vcur, P[0], corr, tsum);
+      const bool up = block(T_{}, T_{}, F_{}, T_{}, T_{}, S[1], P[1], knext, S[0], vcur, P[0], pre,
+                            knext + 32 * D * 2, vcur + 2 * D * 32, corr, tsum);
       rescale(up, corr, tsum);
       mask(S[0], 0, mp0, mn0);
     };
@@ -603,7 +631,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     auto last_odd = [&](uint32_t vcur) __attribute__((always_inline)) {
       if (has_next) prefetch(ec1, qn);  // the next item's query rows
       float corr, tsum;
-      const bool up = block(std::false_type{}, std::true_type{}, S[1], P[1], 0u, S[0], vcur, P[0], corr, tsum);
+      const bool up = block(F_{}, T_{}, F_{}, F_{}, F_{}, S[1], P[1], 0u, S[0], vcur, P[0], pre, 0u, 0u, corr, tsum);
       rescale(up, corr, tsum);
       pv(vcur, 1, P[1]);
     };
@@ -622,11 +650,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     last_ops = fetch_next();
     qk(kslot(ck), 0, S[0]);
     mask(S[0], 0, mp0, mn0);
-    step_even(std::false_type{}, kslot(ck), 0u);
+    step_even(F_{}, F_{}, kslot(ck), 0u, vslot(cv));
     for (int j = 0; j + 1 < n; ++j) {
       const int ck1 = next3(ck), cv1 = next4(cv);
       step_odd(kslot(ck1), vslot(cv));
-      step_even(std::true_type{}, kslot(ck1), vslot(cv));
+      step_even(T_{}, T_{}, kslot(ck1), vslot(cv), vslot(cv1));
       ck = ck1;
       cv = cv1;
     }
