@@ -45,8 +45,9 @@ PEAK_HBM_GBS = 8000.0
 # them changes the figure is stale and `traffic` is reported as null.
 TRAFFIC_FILE = {"c2": "profiles/span_prefill_attention_c2_traffic.md",
                 "c3": "profiles/span_prefill_attention_c3_traffic.md"}
-TRAFFIC_SOURCES = ["paper_2511_02749_amd/csrc/attn_mfma.hip", "paper_2511_02749_amd/csrc/planner.cpp",
-                   "paper_2511_02749_amd/csrc/planner.h", "paper_2511_02749_amd/csrc/work.h"]
+TRAFFIC_SOURCES = ["paper_2511_02749_amd/csrc/prefill_mfma.hip", "paper_2511_02749_amd/csrc/mfma_common.h",
+                   "paper_2511_02749_amd/csrc/planner.cpp", "paper_2511_02749_amd/csrc/planner.h",
+                   "paper_2511_02749_amd/csrc/work.h"]
 
 
 def sources_digest():
