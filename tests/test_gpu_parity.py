@@ -220,3 +220,42 @@ def test_few_cross_rows_over_many_pages(cross_len):
     _, cross = plan.rows()
     _check_rows(run, wl.batches[1], cross, TOL["bf16"])
     run.close()
+
+
+def test_prefill_relaunches_and_concurrent_streams():
+    """The bf16 prefill kernel hands out work items from a per-launch counter that
+    each launch leaves at zero.  Launch it repeatedly on one plan (both layers of a
+    two-layer pool), then twice at once on two streams, and check every launch."""
+    wl = W.config_c2()
+    run = GpuRun(wl, num_layers=2)
+    batch = wl.batches[0]
+    plan = run.pool.plan(batch)
+    pre, _ = plan.rows()
+    rows = pre[np.linspace(0, pre.size - 1, 48).astype(np.int64)]
+    ref = {}
+    for q in batch:
+        mine = [r for r in query_rows(q) if int(r) in set(int(x) for x in rows) and int(r) not in ref]
+        ref.update(oracle_rows(wl, q, mine))
+    assert len(ref) == rows.size
+
+    def check(out):
+        o = out[torch.as_tensor(rows, device="cuda")].cpu().numpy()
+        got = (o.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+        worst = max(max_err(got[i], ref[int(r)]) for i, r in enumerate(rows))
+        assert worst <= TOL["bf16"], f"max abs err {worst}"
+
+    for layer in (0, 1, 0, 1, 0):
+        run.out.zero_()
+        plan.prefill(layer, run.q, run.k, run.v, run.out)
+        torch.cuda.synchronize()
+        check(run.out)
+    outs = [torch.zeros_like(run.out) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for layer, (s, o) in enumerate(zip(streams, outs)):
+        plan.prefill(layer, run.q, run.k, run.v, o, stream=s)
+    torch.cuda.synchronize()
+    for o in outs:
+        check(o)
+    plan.commit()
+    run.close()
