@@ -27,10 +27,10 @@
 //
 // Keys are read in tiles of 4 pages (64 keys) through the block table.  Tiles go
 // straight from HBM to LDS (global_load_lds_dwordx4, no register staging) into a
-// ring of four stages, three tiles ahead of the one being computed; the LDS tiles
-// are XOR-swizzled at 16-byte granularity so MFMA operand reads are free of bank
-// conflicts.  One barrier per tile: passing it means every wave has finished the
-// previous tile, whose stage the next prefetch overwrites.
+// ring of four stages; the LDS tiles are XOR-swizzled at 16-byte granularity so MFMA
+// operand reads are free of bank conflicts.  Tiles are taken in pairs, with one wait
+// and one barrier per pair: passing it means every wave has finished the previous
+// pair, whose stages the next fetches overwrite.
 //
 // Repositioning (cross rows over cached fragments): the planner pads each span's
 // run of pages to whole tiles, so all keys of a tile share one delta d between the
@@ -62,12 +62,13 @@ struct Geo {
   static constexpr int KS = D / 16;                // 16-dim steps of the QK contraction
   static constexpr int DB = D / 32;                // 32-dim blocks of the output
   static constexpr int KBYTES = kBN * D * 2;       // K tile: [64 keys][D], rows of 2D bytes
-  static constexpr int VBYTES = D * kBN * 2;       // V tile: [D][64 positions], rows of 128 bytes
+  static constexpr int VBYTES = D * kBN * 2;       // V tile: [4 pages][D][16 positions]
   static constexpr int RBYTES = 1024;              // cos/sin row of the tile's delta (4D bytes used)
   static constexpr int STAGE = KBYTES + VBYTES + RBYTES;
   static constexpr int KPW = KBYTES / 1024 / kNW;  // K DMA instructions per wave per tile
   static constexpr int VPW = VBYTES / 1024 / kNW;  // V DMA instructions per wave per tile
   static constexpr int RPW = 4 * D / kNW;          // bytes of the cos/sin row per wave
+
   static constexpr int NDMA = KPW + VPW + 1;       // DMA instructions per wave per tile
   // Beyond the ring (query rotation at item start): the rotary rows of positions
   // 0..31 for the whole kernel, and one rotary row per wave (its 32-row block's
@@ -87,27 +88,6 @@ __device__ __forceinline__ void wait_tiles(int k) {
     wait_vmcnt<NDMA>();
   else
     wait_vmcnt<0>();
-}
-
-// Issue the DMA of one key tile (4 pages) and of the cos/sin row of its delta into
-// an LDS stage.
-template <int D>
-__device__ __forceinline__ void issue_tile(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
-                                           int hkv, int kvh, const TilePages& tp, unsigned char* stage,
-                                           const float2* __restrict__ rope, int wave, int lane) {
-  using G = Geo<D>;
-  // No registers to spare: the per-lane address parts are recomputed for every tile
-  // from an opaque copy of the lane id instead of being hoisted out of the tile loop
-  // into a dozen 64-bit registers.
-  __asm__ volatile("" : "+v"(lane));
-  issue_k<D>(pool, layer_off, page_elems, kvh, tp, stage, wave, lane);
-  issue_v<D>(pool, layer_off, page_elems, hkv, kvh, tp, stage + G::KBYTES, wave, lane);
-  // cos/sin of the tile's delta: each wave brings RPW bytes with its first lanes
-  if (lane < G::RPW / 16) {
-    const unsigned char* src = reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(tp.delta) * (D / 2)) +
-                               wave * G::RPW + 16 * lane;
-    dma16(src, stage + G::KBYTES + G::VBYTES + wave * G::RPW);
-  }
 }
 
 }  // namespace
@@ -147,6 +127,31 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   bool is_ok = is_t < n_tiles_total;
   if (is_ok) load_item_keys(tiles, is_t, is);
   int n_issued = 0;  // tiles of the stream issued so far
+  // Per-lane source offsets (bytes, inside a page) of this wave's DMA instructions.
+  // K instruction u fills LDS bytes [1024q, 1024q + 1024) of the K tile, q = wave KPW
+  // + u: 1024 / 2D keys of one page, chunk c of key k stored at chunk c ^ kswz(k).  V
+  // instruction u fills 1024 bytes of the V tile, laid out [page][d][two 16-byte
+  // halves] with half h of row d stored at h ^ (d >> 3 & 1): 32 rows of one page.
+  // All of a wave's instructions read the same page of the tile (page wave / 2), so
+  // a tile's fetch is one page id per wave plus these offsets: the uniform work of
+  // the fetch, which all eight waves repeat on the CU's one scalar unit, stays small.
+  // (No registers to spare here: the offsets are recomputed for every tile from an
+  // opaque copy of the lane id, not hoisted out of the tile loop.)
+  constexpr int CPK = D / 8;  // 16-byte chunks per key row
+  auto dk_ofs = [&](int ln, int u) __attribute__((always_inline)) {
+    const int qi = wave * GE::KPW + u;
+    const int key = qi * (64 / CPK) + ln / CPK;
+    const int c = (ln % CPK) ^ kswz<D>(key);
+    return 2u * static_cast<uint32_t>(kvh * kPage * D + (key & 15) * D + 8 * c);
+  };
+  auto dv_ofs = [&](int ln, int u) __attribute__((always_inline)) {
+    const int qi = wave * GE::VPW + u;
+    const int d = 32 * (qi % (D / 32)) + (ln >> 1);
+    const int h = (ln & 1) ^ ((d >> 3) & 1);
+    return 2u * static_cast<uint32_t>(hkv * kPage * D + kvh * D * kPage + d * kPage + 8 * h);
+  };
+  const int wpage = wave / 2;  // the page of the tile this wave's instructions read
+  static_assert(GE::KPW * (64 / CPK) * 2 == 16 && GE::VPW * 2 == D / 32, "one page per wave");
   auto issue_next = [&]() {
     while (is_ok && is_j >= is.n) {
       is_t += tstride;
@@ -155,10 +160,24 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if (is_ok) load_item_keys(tiles, is_t, is);
     }
     if (!is_ok) return;
-    TilePages tp;
-    read_pages(kv, is.kv_begin + 4 * is_j, tp);
-    issue_tile<D>(pool, layer_off, page_elems, hkv, kvh, tp, lds + (n_issued & 3) * GE::STAGE, rope, wave,
-                       lane);
+    const KvPage* rec = kv + is.kv_begin + 4 * is_j;
+    const int pid = rec[wpage].page_id;
+    const int delta = rec[0].delta;
+    unsigned char* const stage = lds + (n_issued & 3) * GE::STAGE;
+    const unsigned char* pg =
+        reinterpret_cast<const unsigned char*>(pool + layer_off) + static_cast<int64_t>(pid) * (page_elems * 2);
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+#pragma unroll
+    for (int u = 0; u < GE::KPW; ++u) dma16_m0(pg + dk_ofs(ln, u), lds_byte(stage + (wave * GE::KPW + u) * 1024));
+#pragma unroll
+    for (int u = 0; u < GE::VPW; ++u)
+      dma16_m0(pg + dv_ofs(ln, u), lds_byte(stage + GE::KBYTES + (wave * GE::VPW + u) * 1024));
+    // cos/sin of the tile's delta: each wave brings RPW bytes with its first lanes
+    if (lane < GE::RPW / 16)
+      dma16_m0(reinterpret_cast<const unsigned char*>(rope + static_cast<int64_t>(delta) * (D / 2)) + wave * GE::RPW +
+                   16 * lane,
+               lds_byte(stage + GE::KBYTES + GE::VBYTES + wave * GE::RPW));
     ++is_j;
     ++n_issued;
   };
@@ -256,17 +275,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
   // O^T += V^T P^T
+  // (the V operand of page g, dims 32db + r: 16 bytes at [g][32db + r][half h2])
   auto pv = [&](const unsigned char* stage, const bf16x8_t (&pk)[4]) {
-    const bf16_t* vl = reinterpret_cast<const bf16_t*>(stage + GE::KBYTES);
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+    const uint32_t vofs = 32u * (ln & 31) + 16u * ((ln >> 5) ^ ((ln >> 3) & 1));
+    const bf16x8_t* a = reinterpret_cast<const bf16x8_t*>(stage + GE::KBYTES + vofs);
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
-      for (int db = 0; db < GE::DB; ++db) {  // DB independent accumulator chains, interleaved
-        const int d = 32 * db + r;
-        const int c = (2 * g + h2) ^ vswz(d);
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vl + d * kBN + 8 * c);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[g], o[db], 0, 0, 0);
-      }
+      for (int db = 0; db < GE::DB; ++db)  // DB independent accumulator chains, interleaved
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(g * D * 32 + db * 1024) / 16], pk[g], o[db], 0, 0, 0);
   };
   // query at (position - delta) = R(-delta) applied to the query at delta 0
   // The cos/sin row came with the tile's DMA, which the tile's wait and barrier

@@ -3,8 +3,8 @@
 // global-to-LDS DMA of one key tile and the wait/barrier primitives.
 //
 // A key tile is 4 pages (64 keys) of one kv head.  In LDS its K rows are
-// [64 keys][D] and its V rows [D][64 positions], both XOR-swizzled at 16-byte
-// granularity so that the MFMA operand reads of 16 consecutive lanes hit 16
+// [64 keys][D] and its V rows [4 pages][D][16 positions], both XOR-swizzled at
+// 16-byte granularity so that the MFMA operand reads of 16 consecutive lanes hit 16
 // distinct bank groups.
 #pragma once
 #include <hip/hip_runtime.h>
@@ -36,13 +36,11 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// 16-byte chunk swizzles: chunk c of K row `key` sits at c ^ kswz(key); chunk c of
-// V row d at c ^ vswz(d).
+// 16-byte chunk swizzle of the K rows: chunk c of row `key` sits at c ^ kswz(key).
 template <int D>
 __device__ __forceinline__ int kswz(int key) {
   return D == 128 ? (key & 15) : ((key >> 1) & 7);
 }
-__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
 
 // A tile's four pages come from one span: consecutive positions, and only the
 // span's last page may be partial (then followed by empty padding pages).  So key k
@@ -74,11 +72,18 @@ __device__ __forceinline__ int pick4(const int (&a)[4], int p) {
   return (p & 2) ? hi : lo;
 }
 
-// One lane's 16 bytes from global memory to LDS at lds_wave + 16 * lane.
-__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
-                                   (__attribute__((address_space(3))) void*)lds_wave, 16, 0, 0);
+// One lane's 16 bytes from global memory to LDS at lds_wave + 16 * lane.  Issued as
+// inline assembly with the LDS address in M0, so that the compiler's wait-count
+// model does not see the LDS write in flight: with it visible, every later LDS
+// operand read would wait for all LDS traffic (lgkmcnt(0)), DMA included.  The
+// kernels order every read of DMA'd data themselves (vmcnt waits and barriers).
+__device__ __forceinline__ uint32_t lds_byte(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
 }
+__device__ __forceinline__ void dma16_m0(const void* g, uint32_t lds_wave) {
+  __asm__ volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_wave) : "memory");
+}
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave) { dma16_m0(g, lds_byte(lds_wave)); }
 
 // s_waitcnt with vmcnt = N (bits 3:0 and 15:14); expcnt and lgkmcnt left at their
 // maximum, so only vector-memory operations are waited for.
@@ -93,46 +98,6 @@ __device__ __forceinline__ void block_sync() {
   __asm__ volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   __asm__ volatile("" ::: "memory");
-}
-
-// K rows of a tile: [64 keys][D] at `dst`.  The tile is 64 * 2D bytes, moved by
-// KBYTES / 1024 / kNW instructions per wave; instruction q covers bytes
-// [1024q, 1024q + 1024).
-template <int D>
-__device__ __forceinline__ void issue_k(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
-                                        int kvh, const TilePages& tp, unsigned char* dst, int wave, int lane) {
-  constexpr int KPW = kBN * D * 2 / 1024 / kNW;
-#pragma unroll
-  for (int u = 0; u < KPW; ++u) {
-    const int q = wave * KPW + u;
-    const int byte = q * 1024 + 16 * lane;
-    const int key = byte / (2 * D);
-    const int c = ((byte % (2 * D)) >> 4) ^ kswz<D>(key);
-    const int pid = pick4(tp.id, __builtin_amdgcn_readfirstlane(key >> 4));
-    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(kvh) * kPage * D) +
-                        ((key & 15) * D + 8 * c);
-    dma16(src, dst + q * 1024);
-  }
-}
-
-// V rows of a tile: [D][64 positions] at `dst`; row d holds 16 positions per page.
-template <int D>
-__device__ __forceinline__ void issue_v(const bf16_t* __restrict__ pool, int64_t layer_off, int64_t page_elems,
-                                        int hkv, int kvh, const TilePages& tp, unsigned char* dst, int wave,
-                                        int lane) {
-  constexpr int VPW = D * kBN * 2 / 1024 / kNW;
-#pragma unroll
-  for (int u = 0; u < VPW; ++u) {
-    const int q = wave * VPW + u;
-    const int byte = q * 1024 + 16 * lane;
-    const int d = byte >> 7;
-    const int c = ((byte & 127) >> 4) ^ vswz(d);
-    const int pid = pick4(tp.id, c >> 1);
-    const bf16_t* src = pool + (layer_off + pid * page_elems + static_cast<int64_t>(hkv) * kPage * D +
-                                static_cast<int64_t>(kvh) * D * kPage) +
-                        (d * kPage + 8 * (c & 1));
-    dma16(src, dst + q * 1024);
-  }
 }
 
 // The DMA side of an item only needs where its key list starts and its tile count.

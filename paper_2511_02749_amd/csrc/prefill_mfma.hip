@@ -99,17 +99,6 @@ __device__ __forceinline__ float swap_sum(float x) {
   return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
-// One lane's 16 bytes from global memory to LDS byte address lds_byte + 16 * lane.
-// Issued as inline assembly so that the compiler's wait-count model does not see
-// the LDS write in flight: with it visible, every LDS operand read would wait for
-// all LDS operations (lgkmcnt(0)).  The kernel orders every read of DMA'd data
-// itself (vmcnt waits and barriers).
-__device__ __forceinline__ void dma16_m0(const void* g, uint32_t lds_byte) {
-  __asm__ volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_byte) : "memory");
-}
-__device__ __forceinline__ uint32_t lds_byte(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
-}
 
 // s_waitcnt vmcnt(n) for n in {0, N}
 template <int N>
