@@ -94,7 +94,7 @@ __device__ __forceinline__ void wait_tiles(int k) {
 
 template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
-    const WorkTile* __restrict__ tiles, int n_tiles_total, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
+    const WorkTile* __restrict__ tiles, int n_tiles_total, const TileRec* __restrict__ kt, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
     const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = Geo<D>;
@@ -160,9 +160,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if (is_ok) load_item_keys(tiles, is_t, is);
     }
     if (!is_ok) return;
-    const KvPage* rec = kv + is.kv_begin + 4 * is_j;
-    const int pid = rec[wpage].page_id;
-    const int delta = rec[0].delta;
+    const TileRec& rec = kt[(is.kv_begin >> 2) + is_j];
+    const int pid = rec.page_id[wpage];
+    const int delta = rec.delta;
     unsigned char* const stage = lds + (n_issued & 3) * GE::STAGE;
     const unsigned char* pg =
         reinterpret_cast<const unsigned char*>(pool + layer_off) + static_cast<int64_t>(pid) * (page_elems * 2);
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       // page entries of the tile, consumed here: a scalar-load wait later on would
       // also drain the LDS reads of the QK step (both share one counter)
       TilePages cur;
-      read_pages(kv, t.kv_begin + 4 * j, cur);
+      read_tile(kt, (t.kv_begin >> 2) + j, cur);
       __asm__ volatile("" ::"s"(cur.pos0), "s"(cur.nk), "s"(cur.delta));
       const unsigned char* stage = lds + (cs & 3) * GE::STAGE;
       if (cur.delta != q_delta) {
@@ -548,7 +548,7 @@ hipError_t cu_count(int* n) {
 }
 
 template <int D, int G>
-static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
                            float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = Geo<D>::LDS;
@@ -561,30 +561,30 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   // one work-group per CU, a multiple of hkv (each keeps one kv head)
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
-  hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
+  hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
                      g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
                            float* po, float* pml, const float2* rope, hipStream_t s) {
   switch (g.hq / g.hkv) {
-    case 1: return launch_t<D, 1>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 2: return launch_t<D, 2>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 4: return launch_t<D, 4>(g, tiles, n, kv, q, out, po, pml, rope, s);
-    case 8: return launch_t<D, 8>(g, tiles, n, kv, q, out, po, pml, rope, s);
+    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, po, pml, rope, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, po, pml, rope, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, po, pml, rope, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, po, pml, rope, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
+hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
                             void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype)) return hipErrorInvalidValue;
-  return g.d == 128 ? launch_d<128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s)
-                    : launch_d<64>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, part_o, part_ml, rope, s)
+                    : launch_d<64>(g, tiles, n, kt, q, out, part_o, part_ml, rope, s);
 }
 
 }  // namespace spanq

@@ -90,6 +90,7 @@ struct span_plan_t {
   size_t part_o_elems = 0;
   // device views
   const KvPage* kv = nullptr;
+  const TileRec* kt = nullptr;
   const NewPage* k3p = nullptr;
   const NewPage* k3c = nullptr;
   const WorkTile* tp = nullptr;
@@ -382,7 +383,8 @@ int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, s
     }
     pl->rope = pool->rope_tab;
     auto& hb = pl->host_meta;
-    size_t o_kv = put(hb, P.kv), o_k3p = put(hb, P.k3_prefill), o_k3c = put(hb, P.k3_cross);
+    size_t o_kv = put(hb, P.kv), o_kt = put(hb, P.kv_tiles), o_k3p = put(hb, P.k3_prefill),
+           o_k3c = put(hb, P.k3_cross);
     size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
     size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
     e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
@@ -398,6 +400,7 @@ int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, s
     }
     pl->host_upload_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t_plan1).count();
     pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
+    pl->kt = reinterpret_cast<const TileRec*>(pl->dev_meta + o_kt);
     pl->k3p = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3p);
     pl->k3c = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3c);
     pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
@@ -499,7 +502,7 @@ int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const 
   tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
   unsigned* sched = pl->sched + 2 * (pl->sched_next++ % span_plan_t::kSchedSlots);
-  e = pl->mfma ? launch_prefill_mfma(g, pl->tp, nt, pl->kv, q, out, pl->rope, sched, s)
+  e = pl->mfma ? launch_prefill_mfma(g, pl->tp, nt, pl->kt, q, out, pl->rope, sched, s)
                : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
   tm.mark(2);
@@ -524,7 +527,7 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s)
+  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kt, q, out, po, pml, pl->rope, s)
                : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(2);

@@ -27,7 +27,8 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_t
 
 // bf16 MFMA attention kernels: eight waves per work-group, work items (row tile,
 // kv head); a row tile has mfma_bm(g) = 256 / g query tokens (g = query heads per
-// kv head).  Key lists come in whole 4-page tiles with one delta per tile.
+// kv head).  Key lists come in whole 4-page tiles with one delta per tile, given as
+// tile records: a work tile's keys are kt[kv_begin / 4 .. kv_end / 4).
 bool mfma_supported(int hq, int hkv, int d, int dtype);
 int mfma_bm(int g);
 // Compute units of the current device (the persistent kernels run one work-group
@@ -36,7 +37,7 @@ hipError_t cu_count(int* n);
 
 // Cross attention: the query is rotated by each tile's delta; tiles with
 // part >= 0 write fp32 partials for the combine pass.
-hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
+hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt,
                             const void* q, void* out, float* part_o, float* part_ml,
                             const float2* rope, hipStream_t s);
 
@@ -44,7 +45,7 @@ hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tile
 // Every tile must have at least one key tile.  `sched` is two zeroed device words,
 // the launch's item counter; the kernel leaves them at zero when it ends, so
 // launches that run one after another may share them and overlapping ones may not.
-hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
+hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt,
                                const void* q, void* out, const float2* rope, unsigned* sched, hipStream_t s);
 
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).

@@ -52,17 +52,14 @@ struct TilePages {
   int delta;  // reposition delta of every key of the tile
 };
 
-__device__ __forceinline__ void read_pages(const KvPage* __restrict__ kv, int first, TilePages& tp) {
-  int nk = 0;
+// Tile `ti` of the tiled key lists (scalar loads: `kt` is read-only for the kernel).
+__device__ __forceinline__ void read_tile(const TileRec* __restrict__ kt, int ti, TilePages& tp) {
+  const TileRec& r = kt[ti];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const KvPage pg = kv[first + p];
-    tp.id[p] = pg.page_id;
-    nk += pg.n_valid;
-  }
-  tp.nk = nk;
-  tp.pos0 = kv[first].pos0;
-  tp.delta = kv[first].delta;
+  for (int p = 0; p < 4; ++p) tp.id[p] = r.page_id[p];
+  tp.nk = r.nk;
+  tp.pos0 = r.pos0;
+  tp.delta = r.delta;
 }
 
 // a[p] for p in 0..3, as two levels of selects (no branches, no indexed access)

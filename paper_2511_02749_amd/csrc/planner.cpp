@@ -531,6 +531,17 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     }
     p->combine.push_back(CombineTile{c.row0, c.n, part0, p->n_parts - part0});
   }
+  // Tiled key lists: every list (and every split of one) starts at a multiple of
+  // four pages, so kv[4i .. 4i + 3] is a tile.
+  p->kv_tiles.clear();
+  if (t.pad4) {
+    p->kv_tiles.reserve(p->kv.size() / 4);
+    for (size_t i = 0; i + 3 < p->kv.size(); i += 4) {
+      const KvPage* k = &p->kv[i];
+      p->kv_tiles.push_back(TileRec{{k[0].page_id, k[1].page_id, k[2].page_id, k[3].page_id}, k[0].pos0,
+                                    k[0].n_valid + k[1].n_valid + k[2].n_valid + k[3].n_valid, k[0].delta, 0});
+    }
+  }
 }
 
 void PoolIndex::commit(Plan* p) {

@@ -94,6 +94,7 @@ struct Plan {
 
   // work lists
   std::vector<KvPage> kv;
+  std::vector<TileRec> kv_tiles;  // pad4 plans: kv in tiles of four pages
   std::vector<NewPage> k3_prefill, k3_cross;
   std::vector<WorkTile> t_prefill, t_cross;
   std::vector<CombineTile> combine;

@@ -113,7 +113,7 @@ __device__ __forceinline__ void wait_group(int n) {
 
 template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefill_mfma_kernel(
-    const WorkTile* __restrict__ tiles, int n_items, const KvPage* __restrict__ kv, const bf16_t* __restrict__ q,
+    const WorkTile* __restrict__ tiles, int n_items, const TileRec* __restrict__ kt, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
     const float2* __restrict__ rope, unsigned* __restrict__ sched) {
   using GE = PGeo<D>;
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     mn1 = mn2;
     if (!dk_ok) return 0;
     TilePages tp;
-    read_pages(kv, dk.kv_begin + 4 * dk_j, tp);
+    read_tile(kt, (dk.kv_begin >> 2) + dk_j, tp);
     mp2 = tp.pos0;
     mn2 = tp.nk;
     // the kv head's K rows of a page start kvh * 16 * D elements in, its V rows as many
@@ -675,7 +675,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 template <int D, int G>
-static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
                            const float2* rope, unsigned* sched, int cus, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = PGeo<D>::LDS;
@@ -686,33 +686,33 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
   if (items >= (1ll << 30)) return hipErrorInvalidValue;
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus)));
-  hipLaunchKernelGGL((prefill_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kv,
+  hipLaunchKernelGGL((prefill_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
                      g.layer_off, g.hq, g.hkv, scale_log2, rope, sched);
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q, void* out,
+static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
                            const float2* rope, unsigned* sched, int cus, hipStream_t s) {
   switch (g.hq / g.hkv) {
-    case 1: return launch_t<D, 1>(g, tiles, n, kv, q, out, rope, sched, cus, s);
-    case 2: return launch_t<D, 2>(g, tiles, n, kv, q, out, rope, sched, cus, s);
-    case 4: return launch_t<D, 4>(g, tiles, n, kv, q, out, rope, sched, cus, s);
-    case 8: return launch_t<D, 8>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, rope, sched, cus, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, rope, sched, cus, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, rope, sched, cus, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, rope, sched, cus, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
+hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
                                void* out, const float2* rope, unsigned* sched, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype) || sched == nullptr) return hipErrorInvalidValue;
   int cus = 0;
   const hipError_t e = cu_count(&cus);
   if (e != hipSuccess) return e;
-  return g.d == 128 ? launch_d<128>(g, tiles, n, kv, q, out, rope, sched, cus, s)
-                    : launch_d<64>(g, tiles, n, kv, q, out, rope, sched, cus, s);
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, rope, sched, cus, s)
+                    : launch_d<64>(g, tiles, n, kt, q, out, rope, sched, cus, s);
 }
 
 }  // namespace spanq

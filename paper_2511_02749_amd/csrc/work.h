@@ -17,6 +17,18 @@ struct KvPage {
   int32_t delta;
 };
 
+// A key tile of the MFMA kernels: the four pages kv[4i .. 4i + 3] of a key list
+// padded to whole tiles, reduced to what the kernels read.  One 32-byte record per
+// tile, so one 64-byte scalar cache line serves two tiles (four 16-byte page
+// records would take a line per tile).
+struct TileRec {
+  int32_t page_id[4];
+  int32_t pos0;   // position of key 0 (all four pages come from one span)
+  int32_t nk;     // real keys: the n_valid of the four pages summed
+  int32_t delta;  // reposition delta, one per tile
+  int32_t pad;
+};
+
 // One page to fill from caller rows: slots 0..n_valid-1 come from rows
 // src_row.., keys rotated at positions pos0...
 struct NewPage {
