@@ -527,8 +527,14 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
-  e = pl->mfma ? launch_attn_mfma(g, pl->tc, nt, pl->kt, q, out, po, pml, pl->rope, s)
-               : launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
+  if (pl->mfma) {
+    // the last n_cross_few tiles (few rows, two key groups) on the 16-row kernel
+    const int nf = P.n_cross_few;
+    e = launch_attn_mfma(g, pl->tc, nt - nf, pl->kt, q, out, po, pml, pl->rope, s);
+    if (e == hipSuccess && nf > 0) e = launch_few_mfma(g, pl->tc + (nt - nf), nf, pl->kt, q, po, pml, pl->rope, s);
+  } else {
+    e = launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
+  }
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(2);
   e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);

@@ -41,6 +41,13 @@ hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tile
                             const void* q, void* out, float* part_o, float* part_ml,
                             const float2* rope, hipStream_t s);
 
+// Cross attention for two-key-group tiles of at most 16 rows (four query heads per
+// kv head, bf16, d 64 or 128) on 16x16x32 MFMAs; writes partial slots part and
+// part + 1 of each tile, like the two-key-group mode of launch_attn_mfma.
+bool few_supported(int hq, int hkv, int d, int dtype);
+hipError_t launch_few_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt, const void* q,
+                           float* part_o, float* part_ml, const float2* rope, hipStream_t s);
+
 // Span prefill (no repositioning, no key splits), the software-pipelined kernel.
 // Every tile must have at least one key tile.  `sched` is two zeroed device words,
 // the launch's item counter; the kernel leaves them at zero when it ends, so

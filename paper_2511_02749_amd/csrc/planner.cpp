@@ -531,6 +531,13 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     }
     p->combine.push_back(CombineTile{c.row0, c.n, part0, p->n_parts - part0});
   }
+  // Few-row two-key-group tiles last, for the kernel that takes them.
+  p->n_cross_few = 0;
+  if (t.few_rows > 0) {
+    auto few = [&](const WorkTile& w) { return (w.flags & kTwoKeyGroups) != 0 && w.n_rows <= t.few_rows; };
+    std::stable_partition(p->t_cross.begin(), p->t_cross.end(), [&](const WorkTile& w) { return !few(w); });
+    p->n_cross_few = static_cast<int32_t>(std::count_if(p->t_cross.begin(), p->t_cross.end(), few));
+  }
   // Tiled key lists: every list (and every split of one) starts at a multiple of
   // four pages, so kv[4i .. 4i + 3] is a tile.
   p->kv_tiles.clear();

@@ -61,6 +61,8 @@ struct Tiling {
   int min_split_pages = 16;   // at least 256 keys per KV split
   bool pad4 = false;          // pad span runs to 4-page tiles (MFMA kernel)
   int two_group_rows = 0;     // cross tiles of at most this many rows use kTwoKeyGroups
+  int few_rows = 0;           // two-key-group tiles of at most this many rows go last
+                              // in the cross list (the 16-row kernel takes them)
 };
 
 // Work-list shape for the attention kernels.  The MFMA kernel is persistent, one
@@ -79,6 +81,7 @@ inline Tiling tiling_for(bool mfma, int bm, int hq, int hkv) {
   t.target_items = mfma ? 256 : 1024;
   t.pad4 = mfma;
   t.two_group_rows = (mfma && hq == 4 * hkv) ? 32 : 0;
+  t.few_rows = t.two_group_rows > 0 ? 16 : 0;
   return t;
 }
 
@@ -104,6 +107,7 @@ struct Plan {
   };
   std::vector<RowRun> rows_prefill, rows_cross;  // one run per row tile, in work order
   int32_t n_parts = 0;
+  int32_t n_cross_few = 0;  // the last n_cross_few cross tiles: two key groups, <= few_rows rows
   int32_t kv_splits = 1;
   int32_t max_pos = 0;  // every position (and reposition delta) used is below this
   int bm_cross = 64;
