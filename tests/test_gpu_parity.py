@@ -95,6 +95,20 @@ def test_small_ragged(case, dtype, kernel):
     run.close()
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("cross_len", [1, 9, 16])
+def test_few_row_cross_tiles(head_dim, cross_len):
+    """Cross segments of at most 16 rows take the 16-row kernel (four query heads per
+    kv head); ragged fragments make partial pages, and every fragment is read at a
+    position other than the one it was written at."""
+    wl = W.small_workload(head_dim=head_dim, cross_len=cross_len, n_queries=3)
+    run = GpuRun(wl)
+    plan = run.run_batch(wl.batches[0])
+    assert plan.stats()["kv_splits"] >= 1
+    _check_rows(run, wl.batches[0], _computed_rows(plan), TOL["bf16"])
+    run.close()
+
+
 def test_duplicate_fragment_in_one_query():
     wl = W.small_workload(orders=[[0, 1, 0], [2, 1, 3], [1, 1, 2]], n_queries=3)
     run = GpuRun(wl)
