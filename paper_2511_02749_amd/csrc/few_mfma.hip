@@ -139,6 +139,13 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int wpage = wave / 2;
   static_assert(GE::KPW * (64 / CPK) * 2 == 16 && GE::VPW * 2 == D / 32, "one page per wave");
   static_assert(GE::RTBYTES % (1024 * kNW) == 0 && GE::LDS <= 160 * 1024, "LDS plan");
+  // This wave's page id and the delta of the next two tiles of the item, loaded by
+  // lanes 0..3 at the end of an issue phase (lane 2u + f: tile rc_tile + u, field f)
+  // so that the next phase need not wait for a scalar load per tile; the wait of the
+  // pair's barrier (all DMA of this wave) also drains this load.
+  int rc_val = 0;
+  int rc_tile = -2;  // record index held in lanes 0, 1; rc_tile + 1 in lanes 2, 3
+  int rc_s[4] = {0, 0, 0, 0};  // the four values, read into scalars right after the barrier
   auto issue_next = [&]() {
     while (is_ok && is_j >= is.n) {
       is_t += tstride;
@@ -147,9 +154,19 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if (is_ok) load_item_keys(tiles, is_t, is);
     }
     if (!is_ok) return;
-    const TileRec& rec = kt[(is.kv_begin >> 2) + is_j];
-    const int pid = rec.page_id[wpage];
-    const int delta = rec.delta;
+    const int ti = (is.kv_begin >> 2) + is_j;
+    int pid, delta;
+    if (ti == rc_tile) {
+      pid = rc_s[0];
+      delta = rc_s[1];
+    } else if (ti == rc_tile + 1) {
+      pid = rc_s[2];
+      delta = rc_s[3];
+    } else {
+      const TileRec& rec = kt[ti];
+      pid = rec.page_id[wpage];
+      delta = rec.delta;
+    }
     unsigned char* const stage = lds + (n_issued & 3) * GE::STAGE;
     const unsigned char* pg =
         reinterpret_cast<const unsigned char*>(pool + layer_off) + static_cast<int64_t>(pid) * (page_elems * 2);
@@ -383,9 +400,21 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       // the tiles before c, whose stages take the next ones (up to c + 3)
       wait_tiles_f<NDMA>(n_issued - c - sz);
       block_sync();
+      // (before this phase issues any DMA: a wait for the load here is no extra wait)
+#pragma unroll
+      for (int x = 0; x < 4; ++x) rc_s[x] = __builtin_amdgcn_readlane(rc_val, x);
+      __asm__ volatile("" ::"s"(rc_s[0]), "s"(rc_s[1]), "s"(rc_s[2]), "s"(rc_s[3]));
 #pragma unroll
       for (int u = 0; u < kFStages - 1; ++u)
         if (n_issued < c + kFStages) issue_next();
+      // the records of the item's next two tiles, for the next phase
+      if (is_ok && is_j < is.n) {
+        const int ti = (is.kv_begin >> 2) + is_j;
+        const int u = min(lane >> 1, is.n - 1 - is_j);  // past the item's end: repeat its last tile
+        const int* rp = reinterpret_cast<const int*>(kt + ti + u);
+        rc_val = (lane & 1) ? rp[6] : rp[wpage];  // TileRec: page_id[0..3], pos0, nk, delta, pad
+        rc_tile = ti;
+      }
       if (kg < sz) compute(j + kg, c + kg);
       c += sz;
       j += sz;
