@@ -2,15 +2,16 @@
 // fragment pages at positions other than the ones the pages were written at
 // (repositioning, section 5.5 of the paper), optionally with the key list of an
 // item split into parts whose partial results a combine pass merges.  Span prefill
-// has a software-pipelined kernel of its own (prefill_mfma.hip).
+// has a software-pipelined kernel of its own (prefill_mfma.hip), and cross tiles of
+// at most 16 rows one on 16-row MFMAs (few_mfma.hip).
 //
 // Work items are (row tile of 256/G query tokens, kv head).  The G query heads that
 // share a kv head are packed into one item: wave w of the eight handles head
 // (w mod G) and token rows 32*(w div G) .. +31, so every K/V tile staged in LDS
 // feeds all eight waves.
 //
-// The kernel is persistent: one work-group per CU walks the items b, b + grid, ...
-// in order.  Key tiles of consecutive items form one stream through the LDS ring,
+// The kernel is persistent: one work-group per CU keeps one kv head and walks the
+// row tiles t0, t0 + stride, ... in order.  Key tiles of consecutive items form one stream through the LDS ring,
 // so the next item's first tiles are already in flight while the current item
 // finishes, and no work-group launch or ring refill sits between items.
 //

@@ -14,16 +14,17 @@
 // (S^T = K Q^T, v_mfma_f32_32x32x16_bf16) so each lane owns one query row, and P^T
 // feeds O^T = V^T P^T straight from registers.
 //
-// The difference is the tile loop.  Tile x of an item is processed as
-//     QK(x + 1)  ||  softmax(x)  ||  PV(x - 1)
-// in one basic block: the QK and PV MFMAs of neighbouring tiles run while this
-// wave's vector ALU does the softmax of the tile between them, instead of every
-// wave alternating between MFMA-only and VALU-only phases.
+// The difference is the key loop.  The 64-key tiles of an item are split into
+// 32-key blocks, and block u is processed as
+//     QK(u + 1)  ||  softmax(u)  ||  PV(u - 1)
+// in one fenced instruction sequence: the QK and PV MFMAs of the neighbouring blocks
+// run while this wave's vector ALU does the softmax of the block between them,
+// instead of every wave alternating between MFMA-only and VALU-only phases.
 //
 // Softmax uses a lazily raised running max: P = 2^(S - m) is taken against the
 // current m, and m is raised (with the rescale of O and of the row sum) only when a
-// tile's row max exceeds m by more than 2^8.  P then stays below 256, which bf16
-// and the fp32 accumulators hold exactly as well as values below 1; the result
+// block's row max exceeds m by more than 8 (log2 units).  P then stays below 2^8,
+// which bf16 and the fp32 accumulators hold as exactly as values below 1; the result
 // O / l does not depend on which m was used.  The rare raise is a separate branch
 // after the pipelined block, so the block itself has no data-dependent control.
 // The row max is reduced with a max3 tree and one v_permlane32_swap (no LDS round
@@ -38,6 +39,10 @@
 // barrier of tile x may overwrite the K of tile x - 1 and the V of tile x - 2: a
 // 3-slot K ring and a 4-slot V ring (132 KiB of LDS at head dim 128 with the rotary
 // rows).  Both tiles' LDS layouts are read conflict-free by 16 consecutive lanes.
+//
+// Work-groups take items from a per-launch counter (three items ahead), so compute
+// units that run slower take fewer; an item's output rows leave through an LDS
+// staging area as whole row segments at the next item's first barrier.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
