@@ -22,11 +22,13 @@
 // instead of every wave alternating between MFMA-only and VALU-only phases.
 //
 // Softmax uses a lazily raised running max: P = 2^(S - m) is taken against the
-// current m, and m is raised (with the rescale of O and of the row sum) only when a
-// block's row max exceeds m by more than 8 (log2 units).  P then stays below 2^8,
-// which bf16 and the fp32 accumulators hold as exactly as values below 1; the result
-// O / l does not depend on which m was used.  The rare raise is a separate branch
-// after the pipelined block, so the block itself has no data-dependent control.
+// current m, which an item's first block sets to its row max and which is raised
+// afterwards only when a block's exponentials, summed per lane, pass 2^16 (or are
+// not finite).  The check costs one compare per block and no row max; the rare
+// raise (row max, P taken again, rescale of O and of the row sum) is a branch after
+// the pipelined block, so the block itself has no data-dependent control.  P stays
+// below 2^16, which bf16 and the fp32 accumulators hold with the same relative
+// precision as values below 1; the result O / l does not depend on which m was used.
 // The row max is reduced with a max3 tree and one v_permlane32_swap (no LDS round
 // trip); the row sum comes from v_dot2 over the packed bf16 P, i.e. exactly the
 // weights the PV MFMAs use.
@@ -89,7 +91,7 @@ struct PGeo {
   static_assert(SROW % 64 == 0 && (2 * D) % SROW == 0, "a pass covers whole 32-dim blocks");
 };
 
-constexpr float kLazy = 8.f;     // raise the running max only past m + 8 (log2 units)
+constexpr float kSumCap = 65536.f;  // raise the running max once a block's P sums past 2^16 in a lane
 constexpr float kNoMax = -1e30f;  // running max before any key; finite, so 2^(-inf - m) = 0
 
 __device__ __forceinline__ float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
@@ -302,19 +304,37 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int db = 0; db < DB; ++db)  // DB independent accumulator chains
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(half * D * 32 + db * 1024) / 16], pk[half], o[db], 0, 0, 0);
   };
-  // Lazily raised running max, decided before the block's exponentials without a
-  // branch: m moves (to the block max) only when some row's block max exceeds it by
-  // more than kLazy.  corr rescales what was accumulated against the old m.
-  auto raise_max = [&](const f32x16_t& sc, float& corr) __attribute__((always_inline)) -> bool {
-    const float mx = row_max(sc);
-    const bool up = __any(mx > m + kLazy);
-    const float m_new = up ? fmaxf(m, mx) : m;
-    corr = up ? __builtin_amdgcn_exp2f(m - m_new) : 1.f;
+  // P = 2^(S - m) of a block's 16 scores in this lane, packed to bf16 in w; the row
+  // sums of the packed values in ts0, ts1
+  auto exp_block = [&](const f32x16_t& sc, u32x4_t (&w)[2], float& ts0, float& ts1) __attribute__((always_inline)) {
+    const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+    ts0 = 0.f;
+    ts1 = 0.f;
+#pragma unroll
+    for (int wd = 0; wd < 8; ++wd) {
+      const int half = wd >> 2, e = wd & 3;
+      const uint32_t pw = pack_bf16x2(__builtin_amdgcn_exp2f(sc[8 * half + 2 * e] - m),
+                                      __builtin_amdgcn_exp2f(sc[8 * half + 2 * e + 1] - m));
+      w[half][e] = pw;
+      if (e & 1)
+        ts1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts1, false);
+      else
+        ts0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts0, false);
+    }
+  };
+  // The rare raise of the running max, after a block whose exponentials (taken
+  // against the current m) summed past kSumCap in some lane or were not finite (a
+  // row's first keys, m still kNoMax): m moves to the block's row max, the block's P
+  // is taken again, and corr = 2^(m_old - m_new) rescales what was accumulated.
+  auto raise_max = [&](const f32x16_t& sc, u32x4_t (&w)[2], float& ts0, float& ts1) __attribute__((always_inline)) -> float {
+    const float m_new = fmaxf(m, row_max(sc));
+    const float corr = __builtin_amdgcn_exp2f(m - m_new);
     m = m_new;
-    return up;
+    exp_block(sc, w, ts0, ts1);
+    return corr;
   };
   // after the block (whose PV MFMAs still added terms taken against the old m): the
-  // rare rescale of O, then the row sum
+  // rare rescale of O and l, then the block's row sum
   auto rescale = [&](bool up, float corr, float tsum) __attribute__((always_inline)) {
     if (__builtin_expect(up, 0)) {
       __asm__ volatile("");
@@ -322,8 +342,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+      l *= corr;
     }
-    l = l * corr + tsum;
+    l += tsum;
   };
 
   // Operands of a block's chunks 0 and 1, read during the block before it.
@@ -381,7 +402,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
       if (t == 0) {
         __builtin_amdgcn_sched_barrier(0);
-        up = raise_max(s_in, corr);
+        // an item's first block (the only one without PV work) sets m to its row max
+        if constexpr (!WPV) m = fmaxf(m, row_max(s_in));
         if constexpr (WQK && !PREK) qk_mfma(0);
       }
 #pragma unroll
@@ -403,9 +425,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       __asm__ volatile("" : "+v"(ts0), "+v"(ts1));
       __builtin_amdgcn_sched_barrier(0);
     }
+    tsum = ts0 + ts1;
+    corr = 1.f;
+    if (WPV && __builtin_expect(__any(!(tsum <= kSumCap)), 0)) {
+      up = true;
+      corr = raise_max(s_in, w, ts0, ts1);
+      tsum = ts0 + ts1;
+    }
     pk_out[0] = __builtin_bit_cast(bf16x8_t, w[0]);
     pk_out[1] = __builtin_bit_cast(bf16x8_t, w[1]);
-    tsum = ts0 + ts1;
     return up;
   };
 

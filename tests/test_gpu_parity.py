@@ -109,6 +109,31 @@ def test_few_row_cross_tiles(head_dim, cross_len):
     run.close()
 
 
+def test_running_max_raised_mid_row():
+    """Scores that jump by more than 2^16 between key blocks: every query row gets a
+    bias along the lowest-frequency rotary pair (dims 63, 127 rotate by at most about
+    0.1 rad over these distances), and the first three 32-key blocks of the prefix
+    are pushed down by about 49, 24 and 0 in log2 units.  Each row past the prefix's
+    first block therefore raises its running max twice after its first block (the
+    block max climbs from about -40 to -18 to +4), once in an odd and once in an even
+    block of the key loop, and the result must not depend on it."""
+    wl = W.small_workload(head_dim=128, prefix_len=96, frag_lens=(300, 129, 64, 200), frags_per_query=3,
+                          cross_len=40)
+    q, k = wl.q.copy(), wl.k.copy()
+    q[:, :, 63] += 8.0
+    for batch in wl.batches:
+        for query in batch:
+            r0 = query.prefix.row
+            k[r0:r0 + 32, :, 63] = -48.0
+            k[r0 + 32:r0 + 64, :, 63] = -24.0
+    wl.q_bits, wl.k_bits = W.round_to_bf16_bits(q), W.round_to_bf16_bits(k)
+    wl.q, wl.k = W.bf16_bits_to_f32(wl.q_bits), W.bf16_bits_to_f32(wl.k_bits)
+    run = GpuRun(wl)
+    plan = run.run_batch(wl.batches[0])
+    _check_rows(run, wl.batches[0], _computed_rows(plan), TOL["bf16"])
+    run.close()
+
+
 def test_duplicate_fragment_in_one_query():
     wl = W.small_workload(orders=[[0, 1, 0], [2, 1, 3], [1, 1, 2]], n_queries=3)
     run = GpuRun(wl)
