@@ -23,6 +23,8 @@ Printed JSON (last stdout line):
   kv_gather  cross attention with 1/4/16 rows per query over eight distinct
              judge-shaped contexts (335 MB of K/V): GB/s of distinct pages read
              against the 8 TB/s HBM peak
+  measured_peaks  what this GPU attains with an MFMA-only loop and a streaming HBM read
+             (library probes), with the prefill kernel's and the gathers' rates against them
   cpu_baseline  the float64 oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -185,6 +187,8 @@ def main():
     ap.add_argument("--ttft-reps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peak-probes", action="store_true",
+                    help="skip the MFMA-only and streaming-read probes of the attainable peaks")
     ap.add_argument("--gather-reps", type=int, default=10,
                     help="timed passes of the KV page-gather measurement (0 skips it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -318,6 +322,21 @@ def main():
         gather = kv_gather(spanq, W, torch, np, args.gather_reps)
         print(f"[bench] kv gather {json.dumps(gather)}", file=sys.stderr, flush=True)
 
+    peaks = None
+    if not args.no_peak_probes:
+        mfma_peak = spanq.probe_mfma_peak(iters=20000, reps=5)
+        buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+        read_peak = spanq.probe_read_peak(buf, reps=10)
+        del buf
+        peaks = {"mfma_bf16_tflops": mfma_peak, "hbm_read_gbs": read_peak,
+                 "span_prefill_attention_frac": k1_tflops / mfma_peak,
+                 "kv_gather_frac": ({k: v["gbs"] / read_peak for k, v in gather["by_rows"].items()}
+                                    if gather else None),
+                 "method": "MFMA-only loop: two waves per SIMD on every CU, four independent "
+                           "v_mfma_f32_32x32x16_bf16 chains; streaming read: 2 GiB device buffer, "
+                           "16-byte non-temporal loads, 10 launches"}
+        print(f"[bench] measured peaks {json.dumps(peaks)}", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, batch[0], args.cpu_seconds)
@@ -365,6 +384,7 @@ def main():
                      "algorithmic_bytes": k1_bytes, "launch_flops": k1_flops},
         "ttft": ttft,
         "kv_gather": gather,
+        "measured_peaks": peaks,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)

@@ -275,6 +275,25 @@ const char* span_last_error(void);
 int span_pool_read_page(const span_pool* pool, int32_t layer, int32_t page_id, void* host_dst,
                         size_t bytes);
 
+/* ---------------------------------------------------------------- machine peaks */
+
+/* Not part of the method: these measure what this GPU attains for the two resources
+ * the attention kernels are bound by, to read the kernels' rates against beside the
+ * published peaks.  Each launches its kernel once untimed, then `reps` times between
+ * two HIP events on `stream` (0 = the null stream), and waits for them.
+ * SPAN_EINVAL on a bad argument, SPAN_EHIP on a HIP error. */
+
+/* bf16 MFMA rate: two waves on every SIMD of every compute unit each run `iters`
+ * rounds of four independent v_mfma_f32_32x32x16_bf16 chains with register operands
+ * and nothing else.  Stores dense TFLOP/s (2 * 32 * 32 * 16 flop per MFMA) in *tflops. */
+int span_probe_mfma_peak(int32_t iters, int32_t reps, void* stream, double* tflops);
+
+/* HBM read rate: a grid-stride kernel reads `bytes` (a positive multiple of 16) of
+ * device memory at `buf` (caller-owned, 16-byte aligned) with 16-byte non-temporal
+ * loads, four in flight per lane.  A buffer well past the 256 MiB last-level cache
+ * (1 GiB or more) measures HBM.  Stores GB/s (10^9 bytes per second) in *gbs. */
+int span_probe_read_peak(const void* buf, size_t bytes, int32_t reps, void* stream, double* gbs);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,4 +18,6 @@ from ._lib import (  # noqa: F401
     hash_pages,
     library_path,
     load,
+    probe_mfma_peak,
+    probe_read_peak,
 )

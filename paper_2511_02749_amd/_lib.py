@@ -27,7 +27,8 @@ EXPORTS = [
     "span_pool_reset", "span_pool_get_info", "span_pool_page_address", "span_pool_read_page",
     "span_hash_pages", "kv_lookup", "span_plan", "span_plan_stats", "span_plan_block_table",
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
-    "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times",
+    "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
+    "span_probe_read_peak",
 ]
 SPAN_FLAG_TIMING = 1
 
@@ -118,6 +119,8 @@ def load():
         "span_plan_commit": (I32, [VP]),
         "span_plan_destroy": (I32, [VP]),
         "span_plan_kernel_times": (I32, [VP, P(KernelTimes)]),
+        "span_probe_mfma_peak": (I32, [I32, I32, VP, P(ctypes.c_double)]),
+        "span_probe_read_peak": (I32, [VP, ctypes.c_size_t, I32, VP, P(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -152,6 +155,21 @@ def _stream(s) -> Optional[int]:
     if isinstance(s, int):
         return s
     return s.cuda_stream
+
+
+def probe_mfma_peak(iters: int = 20000, reps: int = 5, stream=None) -> float:
+    """bf16 MFMA TFLOP/s this GPU attains with an MFMA-only loop (span_probe_mfma_peak)."""
+    out = ctypes.c_double()
+    _check(load().span_probe_mfma_peak(iters, reps, _stream(stream), ctypes.byref(out)))
+    return float(out.value)
+
+
+def probe_read_peak(buf, reps: int = 5, stream=None) -> float:
+    """HBM read GB/s this GPU attains streaming a device tensor (span_probe_read_peak)."""
+    out = ctypes.c_double()
+    nbytes = buf.numel() * buf.element_size()
+    _check(load().span_probe_read_peak(_ptr(buf), nbytes - nbytes % 16, reps, _stream(stream), ctypes.byref(out)))
+    return float(out.value)
 
 
 def hash_mix(x: int) -> int:

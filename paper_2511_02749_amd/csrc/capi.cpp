@@ -588,3 +588,59 @@ int span_plan_destroy(span_plan_t* pl) {
 }
 
 }  // extern "C"
+
+namespace {
+// One untimed launch, then reps launches between two events on stream s; the
+// elapsed time in seconds.
+template <class Launch>
+int time_launches(Launch launch, int reps, hipStream_t s, const char* what, double* sec) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t e = launch();
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = hipEventRecord(e0, s);
+  for (int i = 0; e == hipSuccess && i < reps; ++i) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return hip_fail(e, what);
+  *sec = 1e-3 * ms;
+  return SPAN_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int span_probe_mfma_peak(int32_t iters, int32_t reps, void* stream, double* tflops) {
+  if (iters < 1 || reps < 1 || !tflops) return fail(SPAN_EINVAL, "span_probe_mfma_peak: bad argument");
+  int n_cu = 0;
+  hipError_t e = cu_count(&n_cu);
+  if (e != hipSuccess) return hip_fail(e, "span_probe_mfma_peak: device attributes");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  double sec = 0.0;
+  const int rc = time_launches([&] { return launch_probe_mfma(iters, n_cu, s); }, reps, s,
+                               "span_probe_mfma_peak", &sec);
+  if (rc != SPAN_OK) return rc;
+  *tflops = probe_mfma_flops(iters, n_cu) * reps / sec * 1e-12;
+  return SPAN_OK;
+}
+
+int span_probe_read_peak(const void* buf, size_t bytes, int32_t reps, void* stream, double* gbs) {
+  if (!buf || bytes == 0 || bytes % 16 != 0 || reps < 1 || !gbs)
+    return fail(SPAN_EINVAL, "span_probe_read_peak: bad argument");
+  int n_cu = 0;
+  hipError_t e = cu_count(&n_cu);
+  if (e != hipSuccess) return hip_fail(e, "span_probe_read_peak: device attributes");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  double sec = 0.0;
+  const int rc = time_launches([&] { return launch_probe_read(buf, static_cast<int64_t>(bytes), n_cu, s); }, reps,
+                               s, "span_probe_read_peak", &sec);
+  if (rc != SPAN_OK) return rc;
+  *gbs = static_cast<double>(bytes) * reps / sec * 1e-9;
+  return SPAN_OK;
+}
+
+}  // extern "C"

@@ -1,4 +1,5 @@
-// Launchers of the HIP kernels (kernels.hip, attn_mfma.hip, prefill_mfma.hip).
+// Launchers of the HIP kernels (kernels.hip, attn_mfma.hip, few_mfma.hip, prefill_mfma.hip,
+// probes.hip).
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -58,5 +59,12 @@ hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_t
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,
                           const float* part_ml, int bm, void* out, hipStream_t s);
+
+// Machine-peak probes (probes.hip): an MFMA-only loop on every compute unit (two
+// waves per SIMD, probe_mfma_flops(iters, n_cu) flops per launch) and a streaming
+// read of `bytes` (a multiple of 16) at buf.
+hipError_t launch_probe_mfma(int iters, int n_cu, hipStream_t s);
+double probe_mfma_flops(int iters, int n_cu);
+hipError_t launch_probe_read(const void* buf, int64_t bytes, int n_cu, hipStream_t s);
 
 }  // namespace spanq
