@@ -233,47 +233,60 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           if (32 * kb + 8 * (i >> 2) + (i & 3) >= lim) sc[kb][i] = -INFINITY;
     }
   };
-  // online softmax (base 2; scores already scaled), one running max per tile
-  auto softmax_max = [&](const f32x16_t (&sc)[2]) -> float {
+  // online softmax (base 2; scores already scaled) with the lazily raised running
+  // max of mfma_common.h: the row max over a tile (both half-waves) is formed only on
+  // an item's first tile and on the rare raise
+  auto tile_max = [&](const f32x16_t (&sc)[2]) -> float {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[kb][i]);
-    mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(mx))));
-    const float m_new = fmaxf(m, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = __builtin_amdgcn_exp2f(m - m_use);
-    m = m_new;
-    // the running max moves on few tiles once it has settled: rescale only then (a
-    // real branch; the empty volatile asm keeps the compiler from if-converting it)
-    if (__builtin_expect(__any(corr != 1.f), 0)) {
+    return fmaxf(mx, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(mx))));
+  };
+  // P = 2^(S - m) to bf16 (step g of the P.V contraction covers page g of the tile);
+  // returns this lane's sum of P
+  auto softmax_exp = [&](const f32x16_t (&sc)[2], bf16x8_t (&pk)[4]) -> float {
+    float psum = 0.f;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int kb = g >> 1, half = g & 1;
+      u32x4_t w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e] - m);
+        const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e + 1] - m);
+        psum += p0 + p1;
+        w[e] = pack_bf16x2(p0, p1);
+      }
+      pk[g] = __builtin_bit_cast(bf16x8_t, w);
+    }
+    return psum;
+  };
+  // P of a tile whose scores `scores(sc)` forms (QK and mask); the rare raise sets m
+  // to the tile's row max, rescales O and l and takes P again, with the scores formed
+  // anew from the tile still in LDS, so that they need not stay in registers past the
+  // exponentials (a real branch; the empty volatile asm keeps the compiler from
+  // if-converting it)
+  auto softmax = [&](auto scores, bf16x8_t (&pk)[4], bool first) {
+    f32x16_t sc[2];
+    scores(sc);
+    if (first) m = fmaxf(m, tile_max(sc));
+    float psum = softmax_exp(sc, pk);
+    if (__builtin_expect(__any(!(psum <= kSumCap)), 0)) {
       __asm__ volatile("");
+      scores(sc);
+      const float m_new = fmaxf(m, tile_max(sc));
+      const float corr = __builtin_amdgcn_exp2f(m - m_new);
+      m = m_new;
 #pragma unroll
       for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= corr;
+      l *= corr;
+      psum = softmax_exp(sc, pk);
     }
-    l *= corr;
-    return m_use;
-  };
-  // P = 2^(S - m) to bf16; step g of the P.V contraction covers page g of the tile
-  auto softmax_exp = [&](const f32x16_t (&sc)[2], float m_use, bf16x8_t (&pk)[4]) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int kb = g >> 1, half = g & 1;
-      float psum = 0.f;
-      u32x4_t w;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e] - m_use);
-        const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e + 1] - m_use);
-        psum += p0 + p1;
-        w[e] = pack_bf16x2(p0, p1);
-      }
-      l += psum;
-      pk[g] = __builtin_bit_cast(bf16x8_t, w);
-    }
+    l += psum;
   };
   // O^T += V^T P^T
   // (the V operand of page g, dims 32db + r: 16 bytes at [g][32db + r][half h2])
@@ -436,8 +449,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
       for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
-    m = -INFINITY;
+    m = kNoMax;
     l = 0.f;
+    bool first = true;  // this wave's first tile of the item
 
     // ---- key tiles of this item, in groups of two (one for an odd last tile)
     bf16x8_t qn[GE::KS];  // raw query of the next item, loaded after the loop
@@ -452,12 +466,14 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         q_delta = cur.delta;
         rotate_q(stage);
       }
-      f32x16_t sc[2];
-      qk(stage, sc);
-      mask(sc, cur);
-      const float m_use = softmax_max(sc);
       bf16x8_t pk[4];
-      softmax_exp(sc, m_use, pk);
+      softmax(
+          [&](f32x16_t (&sc)[2]) {
+            qk(stage, sc);
+            mask(sc, cur);
+          },
+          pk, first);
+      first = false;
       pv(stage, pk);
     };
     for (int j = 0; j < n_tiles;) {
@@ -508,8 +524,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             *reinterpret_cast<float4*>(po + d0) =
                 float4{o[db][4 * g4], o[db][4 * g4 + 1], o[db][4 * g4 + 2], o[db][4 * g4 + 3]};
           }
-        if (h2 == 0) {
-          part_ml[slot * 2] = m;
+        if (h2 == 0) {  // a row that saw no key: max -inf, as the merge expects
+          part_ml[slot * 2] = l_row > 0.f ? m : -INFINITY;
           part_ml[slot * 2 + 1] = l_row;
         }
       }

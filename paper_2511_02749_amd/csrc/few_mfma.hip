@@ -188,7 +188,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // tile rotated further by -delta), accumulators
   bf16x8_t qbase[KS], qf[KS];
   f32x4_t o[DB];
-  float m = -INFINITY, l = 0.f;
+  float m = kNoMax, l = 0.f;
   int q_delta = 0;
   int qpos = 0, wave_min_pos = 0;
 
@@ -344,8 +344,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     q_delta = 0;
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    m = -INFINITY;
+    m = kNoMax;
     l = 0.f;
+    bool first = true;  // this wave's first tile of the item
 
     auto compute = [&](int j, int cs) {  // tile j of the item, stream slot cs
       TilePages cur;
@@ -356,42 +357,56 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         q_delta = cur.delta;
         rotate_q(stage);
       }
+      // online softmax (base 2; scores already scaled) with the lazily raised running
+      // max of mfma_common.h: the row max is formed on the wave's first tile of the
+      // item and on the rare raise, which forms the scores anew from the tile still in
+      // LDS rather than keeping them in registers past the exponentials
       f32x4_t sc[4];
       qk(stage, sc);
       mask(sc, cur);
-      // online softmax (base 2; scores already scaled), one running max per tile
-      float mx = -INFINITY;
+      auto tile_max = [&]() {
+        float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int j2 = 0; j2 < 4; ++j2) mx = fmaxf(mx, sc[kb][j2]);
-      mx = row_max4(mx);
-      const float m_new = fmaxf(m, mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float corr = __builtin_amdgcn_exp2f(m - m_use);
-      m = m_new;
-      if (__builtin_expect(__any(corr != 1.f), 0)) {  // the running max moved
+          for (int j2 = 0; j2 < 4; ++j2) mx = fmaxf(mx, sc[kb][j2]);
+        return row_max4(mx);
+      };
+      bf16x8_t pk[2];
+      auto exps = [&]() {
+        float psum = 0.f;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+          u32x4_t w;
+#pragma unroll
+          for (int h = 0; h < 2; ++h)  // block 2t2 + h: elements 4h .. 4h + 3 of the operand
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              const float p0 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e] - m);
+              const float p1 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e + 1] - m);
+              psum += p0 + p1;
+              w[2 * h + e] = pack_bf16x2(p0, p1);
+            }
+          pk[t2] = __builtin_bit_cast(bf16x8_t, w);
+        }
+        return psum;
+      };
+      if (first) m = fmaxf(m, tile_max());
+      first = false;
+      float psum = exps();
+      if (__builtin_expect(__any(!(psum <= kSumCap)), 0)) {
         __asm__ volatile("");
+        qk(stage, sc);
+        mask(sc, cur);
+        const float m_new = fmaxf(m, tile_max());
+        const float corr = __builtin_amdgcn_exp2f(m - m_new);
+        m = m_new;
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db] *= corr;
+        l *= corr;
+        psum = exps();
       }
-      float psum = 0.f;
-      bf16x8_t pk[2];
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        u32x4_t w;
-#pragma unroll
-        for (int h = 0; h < 2; ++h)  // block 2t2 + h: elements 4h .. 4h + 3 of the operand
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const float p0 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e] - m_use);
-            const float p1 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e + 1] - m_use);
-            psum += p0 + p1;
-            w[2 * h + e] = pack_bf16x2(p0, p1);
-          }
-        pk[t2] = __builtin_bit_cast(bf16x8_t, w);
-      }
-      l = l * corr + psum;
+      l += psum;
       pv(stage, pk);
     };
     for (int j = 0; j < n_tiles;) {
@@ -435,8 +450,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int db = 0; db < DB; ++db)
         *reinterpret_cast<float4*>(po + 16 * db + 4 * g) = float4{o[db][0], o[db][1], o[db][2], o[db][3]};
-      if (g == 0) {
-        part_ml[slot * 2] = m;
+      if (g == 0) {  // a row that saw no key: max -inf, as the merge expects
+        part_ml[slot * 2] = l_row > 0.f ? m : -INFINITY;
         part_ml[slot * 2 + 1] = l_row;
       }
     }

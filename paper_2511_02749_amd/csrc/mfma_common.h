@@ -29,6 +29,14 @@ constexpr int kBN = 64;  // keys per tile (4 pages)
 constexpr int kNW = 8;   // waves per work-group
 constexpr int kNT = 64 * kNW;
 
+// Lazily raised running max of the online softmax, in all MFMA kernels: P = 2^(S - m)
+// is taken against the current m, and m is raised (P taken again, the accumulated O
+// and row sum rescaled) only when a lane's P over a block of keys sums past kSumCap or
+// is not finite.  kNoMax, the max before any key, is finite: a masked score gives
+// 2^(-inf - m) = 0 and a real one 2^(S - kNoMax) = inf, which forces the first raise.
+constexpr float kSumCap = 65536.f;
+constexpr float kNoMax = -1e30f;
+
 // Two floats to packed bfloat16, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));

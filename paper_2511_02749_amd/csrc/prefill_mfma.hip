@@ -91,9 +91,6 @@ struct PGeo {
   static_assert(SROW % 64 == 0 && (2 * D) % SROW == 0, "a pass covers whole 32-dim blocks");
 };
 
-constexpr float kSumCap = 65536.f;  // raise the running max once a block's P sums past 2^16 in a lane
-constexpr float kNoMax = -1e30f;  // running max before any key; finite, so 2^(-inf - m) = 0
-
 __device__ __forceinline__ float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
 
 // Combine a value with the one of the other half-wave (lane ^ 32).
