@@ -19,8 +19,9 @@
 //   A = K tile (32 keys x 16 dims, from LDS), B = Q^T (16 dims x 32 rows, kept in
 //   registers for the whole item), C = 32 keys x 32 rows.
 // In that C layout each lane owns one query row (lane mod 32) and 16 of the 32
-// keys, so the running max needs a single exchange between the two half-waves
-// and the row sum needs none until the end.  P^T is then already a valid B operand
+// keys, so a row max needs a single exchange between the two half-waves (and is
+// formed only on an item's first tile and on the rare raise of the lazily raised
+// running max, mfma_common.h), and the row sum needs none until the end.  P^T is then already a valid B operand
 // of O^T = V^T P^T once the key order inside each 16-key step is permuted the same
 // way on the A side: the lane of half h holds keys {4h..4h+3, 8+4h..8+4h+3}.  Pages
 // store V transposed with the slots of each page in exactly that order (bits 2 and
