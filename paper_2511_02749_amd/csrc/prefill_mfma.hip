@@ -463,7 +463,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
   // qf <- R(position) qn * log2(e)/sqrt(d), rounded to bf16 once (the loads of qn
-  // and of the base row must have landed)
+  // and of the base row must have landed; the scale rides on the rotary rows 0..31)
   auto rotate = [&](const WorkTile& tn, const bf16x8_t (&qn)[KS]) __attribute__((always_inline)) {
     __asm__ volatile("" ::: "memory");
     if (32 * rb >= tn.n_rows) {  // no row of this wave is real
@@ -496,8 +496,8 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           const float sn = sb * cr + cb * sr;
           const float a = u ? hi_bf16(a4[e2]) : lo_bf16(a4[e2]);
           const float b = u ? hi_bf16(b4[e2]) : lo_bf16(b4[e2]);
-          ra[u] = (a * cs - b * sn) * scale_log2;
-          rb2[u] = (b * cs + a * sn) * scale_log2;
+          ra[u] = a * cs - b * sn;  // cs, sn carry the scale (rotary rows 0..31 do)
+          rb2[u] = b * cs + a * sn;
         }
         na[e2] = pack_bf16x2(ra[0], ra[1]);
         nb[e2] = pack_bf16x2(rb2[0], rb2[1]);
@@ -584,6 +584,18 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     prefetch(ec0, qn);
     grab(ec1);  // item 2
     wait_vm_all();
+    block_sync();
+    // fold log2(e)/sqrt(d) into the rotary rows of positions 0..31, so that the query
+    // rotation, whose angles compose them with a base row, need not multiply by it
+    float4* rt4 = reinterpret_cast<float4*>(rt_lds);
+    for (int i = threadIdx.x; i < GE::RTBYTES / 16; i += kNT) {
+      float4 v = rt4[i];
+      v.x *= scale_log2;
+      v.y *= scale_log2;
+      v.z *= scale_log2;
+      v.w *= scale_log2;
+      rt4[i] = v;
+    }
     block_sync();
   }
 

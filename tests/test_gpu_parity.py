@@ -109,26 +109,29 @@ def test_few_row_cross_tiles(head_dim, cross_len):
     run.close()
 
 
+@pytest.mark.parametrize("head_dim", [128, 64])
 @pytest.mark.parametrize("cross_len", [40, 9])
-def test_running_max_raised_mid_row(cross_len):
+def test_running_max_raised_mid_row(cross_len, head_dim):
     """Scores that jump by more than 2^16 between key blocks: every query row gets a
-    bias along the lowest-frequency rotary pair (dims 63, 127 rotate by at most about
-    0.1 rad over these distances), and the first three 32-key blocks of the prefix
-    are pushed down by about 49, 24 and 0 in log2 units.  In the prefill kernel each
+    bias along the lowest-frequency rotary pair (dims d/2 - 1 and d - 1, which rotate
+    by at most about 0.1 rad over these distances), and the first three 32-key blocks
+    of the prefix are pushed down by about 49, 24 and 0 in log2 units at d = 128
+    (69, 35, 0 at d = 64).  In the prefill kernel each
     row past the prefix's first block raises its running max twice after its first
     block (the block max climbs from about -40 to -18 to +4), once in an odd and once
     in an even block of the key loop; the cross kernels (40 rows: 32-row tiles, 9 rows:
     the 16-row kernel) take their max on a whole first tile (about -18) and raise it
     on the next.  The result must not depend on any of it."""
-    wl = W.small_workload(head_dim=128, prefix_len=96, frag_lens=(300, 129, 64, 200), frags_per_query=3,
+    wl = W.small_workload(head_dim=head_dim, prefix_len=96, frag_lens=(300, 129, 64, 200), frags_per_query=3,
                           cross_len=cross_len)
     q, k = wl.q.copy(), wl.k.copy()
-    q[:, :, 63] += 8.0
+    low = head_dim // 2 - 1
+    q[:, :, low] += 8.0
     for batch in wl.batches:
         for query in batch:
             r0 = query.prefix.row
-            k[r0:r0 + 32, :, 63] = -48.0
-            k[r0 + 32:r0 + 64, :, 63] = -24.0
+            k[r0:r0 + 32, :, low] = -48.0
+            k[r0 + 32:r0 + 64, :, low] = -24.0
     wl.q_bits, wl.k_bits = W.round_to_bf16_bits(q), W.round_to_bf16_bits(k)
     wl.q, wl.k = W.bf16_bits_to_f32(wl.q_bits), W.bf16_bits_to_f32(wl.k_bits)
     run = GpuRun(wl)
