@@ -291,7 +291,8 @@ int span_probe_mfma_peak(int32_t iters, int32_t reps, void* stream, double* tflo
 /* HBM read rate: a grid-stride kernel reads `bytes` (a positive multiple of 16) of
  * device memory at `buf` (caller-owned, 16-byte aligned) with 16-byte non-temporal
  * loads, four in flight per lane.  A buffer well past the 256 MiB last-level cache
- * (1 GiB or more) measures HBM.  Stores GB/s (10^9 bytes per second) in *gbs. */
+ * (1 GiB or more) measures HBM.  Stores GB/s (10^9 bytes per second) in *gbs.
+ * SPAN_EINVAL also for a buffer that is not 16-byte aligned. */
 int span_probe_read_peak(const void* buf, size_t bytes, int32_t reps, void* stream, double* gbs);
 
 #ifdef __cplusplus

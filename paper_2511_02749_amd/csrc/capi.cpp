@@ -5,6 +5,7 @@
 #include <chrono>
 #include <cmath>
 #include <cstdio>
+#include <cstdint>
 #include <cstring>
 #include <limits>
 #include <new>
@@ -629,7 +630,7 @@ int span_probe_mfma_peak(int32_t iters, int32_t reps, void* stream, double* tflo
 }
 
 int span_probe_read_peak(const void* buf, size_t bytes, int32_t reps, void* stream, double* gbs) {
-  if (!buf || bytes == 0 || bytes % 16 != 0 || reps < 1 || !gbs)
+  if (!buf || reinterpret_cast<uintptr_t>(buf) % 16 != 0 || bytes == 0 || bytes % 16 != 0 || reps < 1 || !gbs)
     return fail(SPAN_EINVAL, "span_probe_read_peak: bad argument");
   int n_cu = 0;
   hipError_t e = cu_count(&n_cu);
