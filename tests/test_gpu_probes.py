@@ -35,3 +35,6 @@ def test_probes_reject_bad_arguments():
     buf = torch.empty(8, dtype=torch.uint8, device="cuda")
     with pytest.raises(spanq.SpanError):
         spanq.probe_read_peak(buf, reps=1)  # 8 bytes: rounded down to 0, rejected
+    big = torch.empty(4096 + 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(spanq.SpanError):
+        spanq.probe_read_peak(big[1:], reps=1)  # not 16-byte aligned
