@@ -24,7 +24,9 @@
 // Softmax uses a lazily raised running max: P = 2^(S - m) is taken against the
 // current m, which an item's first block sets to its row max and which is raised
 // afterwards only when a block's exponentials, summed per lane, pass 2^16 (or are
-// not finite).  The check costs one compare per block and no row max; the rare
+// not finite).  After the first block, a block's QK accumulator starts at -m, so the
+// MFMAs themselves form S - m; a raise by d shifts the next block's scores (already
+// formed) by -d.  The check costs one compare per block and no row max; the rare
 // raise (row max, P taken again, rescale of O and of the row sum) is a branch after
 // the pipelined block, so the block itself has no data-dependent control.  P stays
 // below 2^16, which bf16 and the fp32 accumulators hold with the same relative
@@ -249,6 +251,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
   float m = kNoMax, l = 0.f;
+  // -m in all 16 places: the initial value of a block's QK accumulator, so that the
+  // MFMAs form S - m (every block but an item's first, whose scores are raw)
+  f32x16_t mneg;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mneg[i] = 0.f;
+  auto set_mneg = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mneg[i] = -m;
+  };
   int qpos = 0, wave_min_pos = 0;
 
   // Per-lane LDS byte offsets of the MFMA operand reads inside a ring slot: K step
@@ -301,17 +312,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int db = 0; db < DB; ++db)  // DB independent accumulator chains
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(half * D * 32 + db * 1024) / 16], pk[half], o[db], 0, 0, 0);
   };
-  // P = 2^(S - m) of a block's 16 scores in this lane, packed to bf16 in w; the row
-  // sums of the packed values in ts0, ts1
-  auto exp_block = [&](const f32x16_t& sc, u32x4_t (&w)[2], float& ts0, float& ts1) __attribute__((always_inline)) {
+  // P = 2^(sc - d) of a block's 16 (offset) scores in this lane, packed to bf16 in w;
+  // the row sums of the packed values in ts0, ts1
+  auto exp_block = [&](const f32x16_t& sc, float d, u32x4_t (&w)[2], float& ts0, float& ts1) __attribute__((always_inline)) {
     const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
     ts0 = 0.f;
     ts1 = 0.f;
 #pragma unroll
     for (int wd = 0; wd < 8; ++wd) {
       const int half = wd >> 2, e = wd & 3;
-      const uint32_t pw = pack_bf16x2(__builtin_amdgcn_exp2f(sc[8 * half + 2 * e] - m),
-                                      __builtin_amdgcn_exp2f(sc[8 * half + 2 * e + 1] - m));
+      const uint32_t pw = pack_bf16x2(__builtin_amdgcn_exp2f(sc[8 * half + 2 * e] - d),
+                                      __builtin_amdgcn_exp2f(sc[8 * half + 2 * e + 1] - d));
       w[half][e] = pw;
       if (e & 1)
         ts1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts1, false);
@@ -320,15 +331,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
   };
   // The rare raise of the running max, after a block whose exponentials (taken
-  // against the current m) summed past kSumCap in some lane or were not finite (a
-  // row's first keys, m still kNoMax): m moves to the block's row max, the block's P
-  // is taken again, and corr = 2^(m_old - m_new) rescales what was accumulated.
-  auto raise_max = [&](const f32x16_t& sc, u32x4_t (&w)[2], float& ts0, float& ts1) __attribute__((always_inline)) -> float {
-    const float m_new = fmaxf(m, row_max(sc));
-    const float corr = __builtin_amdgcn_exp2f(m - m_new);
-    m = m_new;
-    exp_block(sc, w, ts0, ts1);
-    return corr;
+  // against the current m; its scores sc are S - m) summed past kSumCap in some lane
+  // or were not finite: m moves up by d to the block's row max, the block's P is
+  // taken again, and corr = 2^-d rescales what was accumulated.  Returns d.
+  auto raise_max = [&](const f32x16_t& sc, u32x4_t (&w)[2], float& ts0, float& ts1, float& corr)
+                       __attribute__((always_inline)) -> float {
+    const float d = fmaxf(0.f, row_max(sc));
+    corr = __builtin_amdgcn_exp2f(-d);
+    m += d;
+    exp_block(sc, d, w, ts0, ts1);
+    set_mneg();
+    return d;
   };
   // after the block (whose PV MFMAs still added terms taken against the old m): the
   // rare rescale of O and l, then the block's row sum
@@ -378,7 +391,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if constexpr (WPV) av[t] = pre.v[t];
     }
     auto qk_mfma = [&](int t) __attribute__((always_inline)) {
-      s_out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[t], qf[t], t == 0 ? f32x16_t{} : s_out, 0, 0, 0);
+      s_out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ak[t], qf[t], t == 0 ? mneg : s_out, 0, 0, 0);
     };
     const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
     float ts0 = 0.f, ts1 = 0.f;
@@ -399,15 +412,22 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
       if (t == 0) {
         __builtin_amdgcn_sched_barrier(0);
-        // an item's first block (the only one without PV work) sets m to its row max
-        if constexpr (!WPV) m = fmaxf(m, row_max(s_in));
+        // an item's first block (the only one without PV work; its scores are raw) sets
+        // m to its row max (every row of an item sees its list's first key; a row that
+        // saw none would start from m = 0, with nothing accumulated yet)
+        if constexpr (!WPV) {
+          m = fmaxf(m, row_max(s_in));
+          m = m == kNoMax ? 0.f : m;
+          set_mneg();
+        }
         if constexpr (WQK && !PREK) qk_mfma(0);
       }
 #pragma unroll
       for (int x = 0; x < WPC; ++x) {
         const int wd = t * WPC + x, half = wd >> 2, e = wd & 3;
-        const float p0 = __builtin_amdgcn_exp2f(s_in[8 * half + 2 * e] - m);
-        const float p1 = __builtin_amdgcn_exp2f(s_in[8 * half + 2 * e + 1] - m);
+        // scores are S - m already, except an item's first block's
+        const float p0 = __builtin_amdgcn_exp2f(WPV ? s_in[8 * half + 2 * e] : s_in[8 * half + 2 * e] - m);
+        const float p1 = __builtin_amdgcn_exp2f(WPV ? s_in[8 * half + 2 * e + 1] : s_in[8 * half + 2 * e + 1] - m);
         // the dot product takes the packed word itself, not w[.][e] read back: with
         // the read-back form, hipcc 7.2 at -O3 feeds every fdot2 the vector's element 0
         const uint32_t pw = pack_bf16x2(p0, p1);
@@ -426,8 +446,12 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     corr = 1.f;
     if (WPV && __builtin_expect(__any(!(tsum <= kSumCap)), 0)) {
       up = true;
-      corr = raise_max(s_in, w, ts0, ts1);
+      const float d = raise_max(s_in, w, ts0, ts1, corr);
       tsum = ts0 + ts1;
+      if constexpr (WQK) {  // the next block's scores were formed against the old m
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s_out[i] -= d;
+      }
     }
     pk_out[0] = __builtin_bit_cast(bf16x8_t, w[0]);
     pk_out[1] = __builtin_bit_cast(bf16x8_t, w[1]);
