@@ -41,8 +41,12 @@
  * - Rotary encoding: rotate-half pairs (i, i + d/2), inverse frequency
  *   rope_theta^(-2i/d).
  * - Device work is enqueued asynchronously on the caller's HIP stream (void* =
- *   hipStream_t; NULL = the null stream).  Caller buffers and the plan must stay
- *   alive until that work completes.
+ *   hipStream_t; NULL = the null stream).  Caller buffers must stay alive until that
+ *   work completes.  A plan's device metadata (and a grown rotary table) are copied
+ *   on the stream given to span_plan; an attention call on any other stream first
+ *   makes that stream wait (hipStreamWaitEvent) for those copies, and
+ *   span_plan_destroy releases the plan's device memory on the plan's stream only
+ *   after the work already enqueued on every stream the plan was launched on.
  * - A pool is not thread-safe; use one thread per pool.
  */
 #ifndef SPANQ_H
@@ -230,7 +234,8 @@ int span_plan_rows(const span_plan_t* plan, int64_t* rows, int64_t cap, int64_t*
  * softmax over the span mask of q.k / sqrt(d) times V, with the query also at its
  * canonical position.  No-op when every page hit.  Calls on one plan may run
  * concurrently on different streams, up to 64 of them in flight at once (the
- * bf16 kernel schedules its work items through per-launch counters the plan owns). */
+ * bf16 kernel schedules its work items through per-launch counters the plan owns);
+ * the ordering after the plan's uploads is enforced as described above. */
 int span_prefill_fragments(span_plan_t* plan, int32_t layer, const void* q, const void* k,
                            const void* v, void* out, void* stream);
 
@@ -250,7 +255,9 @@ int span_cross_attend(span_plan_t* plan, int32_t layer, const void* q, const voi
 int span_plan_commit(span_plan_t* plan);
 
 /* Free the plan.  Without a prior commit its new pages are freed unpublished and its
- * hits unpinned.  Device metadata is released on the plan's stream. */
+ * hits unpinned.  Device metadata is released on the plan's stream, ordered after
+ * the work enqueued so far on every stream the plan's attention calls used; the
+ * call itself does not wait for the device. */
 int span_plan_destroy(span_plan_t* plan);
 
 /* ---------------------------------------------------------------- debug */

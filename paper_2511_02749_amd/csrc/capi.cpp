@@ -43,15 +43,24 @@ struct span_pool {
   bool use_mfma = false;
   std::set<span_plan_t*> plans;
   std::vector<hipEvent_t> event_cache;  // reusable timing events
+  std::vector<hipEvent_t> order_cache;  // reusable ordering events (no timing)
   float2* rope_tab = nullptr;           // (cos, sin) per [position][head_dim / 2]
   int64_t rope_n = 0;                   // positions in rope_tab
+  // Tables replaced by a larger one.  A live plan may still launch kernels that read
+  // the table it was planned with, so replaced tables (and the host copies their
+  // uploads read from) stay allocated until the pool is destroyed; the table doubles
+  // each time, so they add at most its current size.
+  std::vector<float2*> rope_retired;
+  std::vector<std::vector<float2>> rope_host;
 };
 
 namespace {
 // Make the rotary table cover positions [0, need).  Computed on the host in double
-// precision (angle reduced to [-pi, pi] before cos/sin), rounded once to float.
-// Growth synchronises the device, since kernels of other plans may read the old table.
-int ensure_rope_table(span_pool* p, int64_t need) {
+// precision (angle reduced to [-pi, pi] before cos/sin), rounded once to float, and
+// copied on `stream`: kernels of this plan on that stream follow the copy, and
+// launches on other streams wait for the plan's ready event.  The table it replaces
+// is retired, not freed, since plans made before may still read it.
+int ensure_rope_table(span_pool* p, int64_t need, hipStream_t stream) {
   if (need <= p->rope_n) return SPAN_OK;
   int64_t n = 4096;
   while (n < need) n *= 2;
@@ -67,17 +76,28 @@ int ensure_rope_table(span_pool* p, int64_t need) {
     }
   }
   float2* dev = nullptr;
-  hipError_t e = hipDeviceSynchronize();
-  if (e == hipSuccess) e = hipMalloc(&dev, tab.size() * sizeof(float2));
-  if (e == hipSuccess) e = hipMemcpy(dev, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+  hipError_t e = hipMalloc(&dev, tab.size() * sizeof(float2));
+  if (e == hipSuccess) e = hipMemcpyAsync(dev, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) {
     if (dev) (void)hipFree(dev);
     return hip_fail(e, "rotary table");
   }
-  if (p->rope_tab) (void)hipFree(p->rope_tab);
+  if (p->rope_tab) p->rope_retired.push_back(p->rope_tab);
+  p->rope_host.push_back(std::move(tab));
   p->rope_tab = dev;
   p->rope_n = n;
   return SPAN_OK;
+}
+
+hipEvent_t take_order_event(span_pool* p) {
+  if (!p->order_cache.empty()) {
+    hipEvent_t e = p->order_cache.back();
+    p->order_cache.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+  return e;
 }
 }  // namespace
 
@@ -111,6 +131,12 @@ struct span_plan_t {
   double host_upload_us = 0.0;  // device metadata allocation and copy enqueue
   // timing: groups of events recorded around each launch (SPAN_FLAG_TIMING)
   std::vector<std::vector<hipEvent_t>> ev_prefill, ev_cross;
+  // Stream ordering.  The metadata (and a grown rotary table) are copied on the
+  // plan's stream.  The first launch on another stream records `ready` on the plan's
+  // stream and makes that stream wait for it; destroy makes the plan's stream wait
+  // for every such stream before the metadata is freed there.
+  hipEvent_t ready = nullptr;
+  std::vector<hipStream_t> foreign;
 };
 
 namespace {
@@ -246,7 +272,9 @@ int span_pool_destroy(span_pool* p) {
   for (span_plan_t* pl : live) span_plan_destroy(pl);
   if (p->cfg.device >= 0) (void)hipDeviceSynchronize();
   for (hipEvent_t e : p->event_cache) (void)hipEventDestroy(e);
+  for (hipEvent_t e : p->order_cache) (void)hipEventDestroy(e);
   if (p->rope_tab) (void)hipFree(p->rope_tab);
+  for (float2* t : p->rope_retired) (void)hipFree(t);
   if (p->owns_dev && p->dev) (void)hipFree(p->dev);
   delete p->index;
   delete p;
@@ -377,7 +405,7 @@ int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, s
       span_plan_destroy(pl);
       return hip_fail(e, "span_plan: hipSetDevice");
     }
-    rc = ensure_rope_table(pool, P.max_pos + 1);
+    rc = ensure_rope_table(pool, P.max_pos + 1, pl->stream);
     if (rc) {
       span_plan_destroy(pl);
       return rc;
@@ -472,6 +500,23 @@ int span_plan_rows(const span_plan_t* pl, int64_t* rows, int64_t cap, int64_t* n
   return SPAN_OK;
 }
 
+// Launches on a stream other than the plan's wait for the plan's uploads.
+static int order_after_upload(span_plan_t* pl, hipStream_t s, const char* who) {
+  if (s == pl->stream) return SPAN_OK;
+  if (std::find(pl->foreign.begin(), pl->foreign.end(), s) == pl->foreign.end()) {
+    if (!pl->ready) {
+      pl->ready = take_order_event(pl->pool);
+      if (!pl->ready) return fail(SPAN_EHIP, std::string(who) + ": event creation");
+      hipError_t e = hipEventRecord(pl->ready, pl->stream);
+      if (e != hipSuccess) return hip_fail(e, who);
+    }
+    pl->foreign.push_back(s);
+  }
+  hipError_t e = hipStreamWaitEvent(s, pl->ready, 0);
+  if (e != hipSuccess) return hip_fail(e, who);
+  return SPAN_OK;
+}
+
 static int attention_common(span_plan_t* pl, int32_t layer, const char* who) {
   if (!pl) return fail(SPAN_EINVAL, std::string(who) + ": null plan");
   if (pl->pool->cfg.device < 0) return fail(SPAN_ESTATE, std::string(who) + ": host-only pool");
@@ -495,6 +540,8 @@ int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const 
   if (P.k3_prefill.empty() && P.t_prefill.empty()) return SPAN_OK;
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_prefill_fragments: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
+  rc = order_after_upload(pl, s, "span_prefill_fragments");
+  if (rc) return rc;
   PoolGeom g = geom(pl, layer);
   Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 2, s, pl->pool->event_cache);
   tm.mark(0);
@@ -519,6 +566,8 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   if (P.t_cross.empty()) return SPAN_OK;
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_cross_attend: null activation pointer");
   hipStream_t s = static_cast<hipStream_t>(stream);
+  rc = order_after_upload(pl, s, "span_cross_attend");
+  if (rc) return rc;
   PoolGeom g = geom(pl, layer);
   Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s, pl->pool->event_cache);
   tm.mark(0);
@@ -581,6 +630,13 @@ int span_plan_destroy(span_plan_t* pl) {
   if (!pl->committed) pl->pool->index->release(&pl->plan);
   release_events(pl->ev_prefill, pl->pool->event_cache);
   release_events(pl->ev_cross, pl->pool->event_cache);
+  // work enqueued on other streams must end before the plan's memory is released
+  for (hipStream_t s : pl->foreign) {
+    hipEvent_t ev = take_order_event(pl->pool);
+    if (ev && hipEventRecord(ev, s) == hipSuccess) (void)hipStreamWaitEvent(pl->stream, ev, 0);
+    if (ev) pl->pool->order_cache.push_back(ev);
+  }
+  if (pl->ready) pl->pool->order_cache.push_back(pl->ready);
   if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
   if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
   pl->pool->plans.erase(pl);

@@ -79,3 +79,81 @@ class GpuRun:
 
 def max_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(gpu.astype(np.float64) - ref))) if gpu.size else 0.0
+
+
+def computed_rows(plan) -> np.ndarray:
+    """Caller rows a plan computes: new prefix/fragment rows, then cross rows."""
+    pre, cross = plan.rows()
+    return np.concatenate([pre, cross])
+
+
+# Whole-batch checks of bf16 pools (every computed row of the full-size batches):
+# max abs error 2e-2 + 2^-8 |oracle| per element, and at most this fraction of
+# elements past the plain 2e-2.  The relative term is one unit of bf16's relative
+# precision; at |O| of 2 to 5 the bf16 rounding of the cached rotated keys and of the
+# rotated query alone moves a few of 1.2e8 outputs past 2e-2 (DESIGN, Z12).
+BF16_RTOL = 2.0 ** -8
+BF16_OVER_FRAC = 1e-6
+
+
+def check_rows(run, batch, rows, tol, limit=None, progress=None, rtol=0.0, over_frac=None):
+    """Compare GPU output rows with the oracle; each row is evaluated in the first
+    query of the batch that contains it.  ``limit`` samples evenly spaced rows.
+    Every element must satisfy |gpu - oracle| <= tol + rtol |oracle|; with
+    ``over_frac``, at most that fraction of elements may exceed plain ``tol``."""
+    rows = np.asarray(rows, np.int64)
+    if limit is not None and rows.size > limit:
+        rows = rows[np.linspace(0, rows.size - 1, limit).astype(np.int64)]
+    remaining = set(int(r) for r in rows)
+    worst, where = 0.0, ""
+    n_el, n_over, worst_mixed = 0, 0, 0.0
+    for qi, q in enumerate(batch):
+        mine = [r for r in query_rows(q) if int(r) in remaining]
+        if not mine:
+            continue
+        ref = oracle_rows(run.wl, q, mine)
+        got = run.out_rows(mine)
+        cross0 = q.cross.row
+        for i, r in enumerate(mine):
+            e = np.abs(got[i].astype(np.float64) - ref[int(r)])
+            n_el += e.size
+            n_over += int(np.count_nonzero(e > tol))
+            if e.size:
+                worst_mixed = max(worst_mixed, float(np.max(e - rtol * np.abs(ref[int(r)]))))
+            if e.size and e.max() > worst:
+                h, d = np.unravel_index(int(np.argmax(e)), e.shape)
+                worst = float(e.max())
+                kind = "cross" if cross0 <= int(r) < cross0 + q.cross.n else "prefill"
+                where = (f"query {qi} row {int(r)} ({kind}) head {h} dim {d}: gpu {float(got[i][h, d]):.5f} "
+                         f"oracle {float(ref[int(r)][h, d]):.5f}")
+            remaining.discard(int(r))
+        if progress:
+            print(f"{progress}: query {qi}: {len(mine)} rows, max abs err so far {worst:.3g}", flush=True)
+    assert not remaining
+    if over_frac is None and rtol == 0.0:
+        assert worst <= tol, f"max abs err {worst} > {tol} at {where}"
+    else:
+        if progress:
+            print(f"{progress}: {n_el} elements, max abs err {worst:.4g} at {where}; {n_over} past {tol}", flush=True)
+        assert worst_mixed <= tol, f"|err| - {rtol}|oracle| reaches {worst_mixed} > {tol}; max abs err {worst} at {where}"
+        if over_frac is not None:
+            assert n_over <= over_frac * n_el, f"{n_over} of {n_el} elements past {tol}"
+    return worst
+
+
+def replay_queries(batch):
+    """A batch in the oracle pool replay's form: (prefix, [fragments], cross) token lists."""
+    return [(list(map(int, q.prefix.tokens)), [list(map(int, f.tokens)) for f in q.frags],
+             list(map(int, q.cross.tokens))) for q in batch]
+
+
+def assert_tables_match(plan, res, batch):
+    """Block tables, hit counts and evictions of a library plan equal the oracle replay's."""
+    for qi, q in enumerate(batch):
+        qr = res.queries[qi]
+        assert plan.block_table(qi, -1) == (qr.prefix.page_ids, qr.prefix.n_hit)
+        for c in range(len(q.frags)):
+            assert plan.block_table(qi, c) == (qr.frags[c].page_ids, qr.frags[c].n_hit)
+        ids, nh = plan.block_table(qi, len(q.frags))
+        assert ids == qr.cross.page_ids and nh == 0
+    assert plan.evicted() == res.evicted

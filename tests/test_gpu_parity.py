@@ -12,7 +12,8 @@ import pytest
 
 import workloads as W
 from oracle import attention as OA
-from tests.helpers import TOL, GpuRun, max_err, oracle_rows, query_layout, query_rows
+from tests.helpers import (TOL, GpuRun, check_rows, computed_rows, max_err, oracle_rows, query_layout,
+                           query_rows)
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -25,31 +26,8 @@ def _need_gpu():
     print(flush=True)
 
 
-def _computed_rows(plan):
-    pre, cross = plan.rows()
-    return np.concatenate([pre, cross])
-
-
-def _check_rows(run, batch, rows, tol, limit=None):
-    """Compare GPU output rows with the oracle; each row is evaluated in the first
-    query of the batch that contains it."""
-    rows = np.asarray(rows, np.int64)
-    if limit is not None and rows.size > limit:
-        rows = rows[np.linspace(0, rows.size - 1, limit).astype(np.int64)]
-    remaining = set(int(r) for r in rows)
-    worst = 0.0
-    for q in batch:
-        mine = [r for r in query_rows(q) if int(r) in remaining]
-        if not mine:
-            continue
-        ref = oracle_rows(run.wl, q, mine)
-        got = run.out_rows(mine)
-        for i, r in enumerate(mine):
-            worst = max(worst, max_err(got[i], ref[int(r)]))
-            remaining.discard(int(r))
-    assert not remaining
-    assert worst <= tol, f"max abs err {worst} > {tol}"
-    return worst
+_computed_rows = computed_rows
+_check_rows = check_rows
 
 
 @pytest.mark.parametrize("mode", ["proj", "direct"])

@@ -167,17 +167,25 @@ def rag_workload(name: str = "rag", *, seed: int = 0, dtype: str = "bf16", n_q_h
                  frags_per_query: int = 16, n_queries: int = 8, cross_len: int = 128,
                  x_std: float = 1.0, w_std: float = 0.02, mode: str = "proj",
                  rope_theta: float = 1e4, batch_split: Optional[Sequence[int]] = None,
-                 orders: Optional[Sequence[Sequence[int]]] = None) -> Workload:
+                 orders: Optional[Sequence[Sequence[int]]] = None,
+                 frag_tokens: Optional[Sequence[Optional[np.ndarray]]] = None) -> Workload:
     """A shared prefix, a pool of fragments, queries drawing fragments in random order.
 
     ``orders`` overrides the random draw with explicit fragment orders per query.
     ``batch_split`` groups queries into successive span_plan calls (default: one batch).
+    ``frag_tokens[f]``, where given, replaces fragment f's drawn tokens (its length
+    then overrides ``frag_lens[f]``).
     """
     book = _RowBook()
     prefix = book.add(_tokens(seed, KIND_PREFIX, 0, prefix_len))
     if isinstance(frag_lens, int):
         frag_lens = [frag_lens] * pool_size
-    frags = [book.add(_tokens(seed, KIND_FRAG, f, int(frag_lens[f]))) for f in range(pool_size)]
+    frags = []
+    for f in range(pool_size):
+        given = frag_tokens[f] if frag_tokens is not None and f < len(frag_tokens) else None
+        toks = (np.ascontiguousarray(given, dtype=np.int32) if given is not None
+                else _tokens(seed, KIND_FRAG, f, int(frag_lens[f])))
+        frags.append(book.add(toks))
     queries = []
     for qi in range(n_queries):
         if orders is not None:
@@ -240,12 +248,25 @@ def small_workload(name: str = "small", *, seed: int = 0, dtype: str = "bf16", n
                    n_kv_heads: int = 2, head_dim: int = 128, prefix_len: int = 40,
                    frag_lens: Sequence[int] = (37, 64, 5, 100), n_queries: int = 3,
                    frags_per_query: int = 3, cross_len: int = 23, mode: str = "direct",
-                   orders=None, batch_split=None) -> Workload:
+                   orders=None, batch_split=None, frag_tokens=None) -> Workload:
     """Small ragged case for parity: lengths off page boundaries, several tiles."""
     return rag_workload(name, seed=seed, dtype=dtype, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                         head_dim=head_dim, hidden=64, prefix_len=prefix_len, pool_size=len(frag_lens),
                         frag_lens=list(frag_lens), frags_per_query=frags_per_query, n_queries=n_queries,
-                        cross_len=cross_len, mode=mode, orders=orders, batch_split=batch_split)
+                        cross_len=cross_len, mode=mode, orders=orders, batch_split=batch_split,
+                        frag_tokens=frag_tokens)
+
+
+def shared_head_tokens(seed: int, base_len: int, shares: Sequence[int], lens: Sequence[int]) -> List[np.ndarray]:
+    """Fragment token arrays for cache-reuse cases: fragment 0 is ``base_len`` drawn
+    tokens; fragment i >= 1 repeats the first ``shares[i-1]`` tokens of fragment 0 and
+    continues with ``lens[i-1] - shares[i-1]`` tokens of its own draw."""
+    base = _tokens(seed, KIND_FRAG, 0, base_len)
+    out = [base]
+    for i, (share, n) in enumerate(zip(shares, lens)):
+        tail = _tokens(seed, KIND_FRAG, 10_000 + i, int(n) - int(share))
+        out.append(np.concatenate([base[:share], tail]).astype(np.int32))
+    return out
 
 
 def gather_queries(seed: int = 0, n_queries: int = 8, prefix_len: int = 2048, n_frags: int = 32,
