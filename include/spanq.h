@@ -226,6 +226,32 @@ int span_plan_evicted(const span_plan_t* plan, int32_t* page_ids, int32_t cap, i
 int span_plan_rows(const span_plan_t* plan, int64_t* rows, int64_t cap, int64_t* n_prefill,
                    int64_t* n_cross);
 
+/* Device scratch reserved per GPU for span_plan_static (64 MiB). */
+#define SPAN_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* span_plan for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same planning,
+ * same arguments, same kernels; the plan's device data (work lists, scheduling
+ * counters, split-KV partials) go to a device array of SPAN_STATIC_SCRATCH_BYTES
+ * that the library holds on each GPU until the process ends, instead of the
+ * stream-ordered allocations span_plan makes.  No hipMalloc, hipFree or other
+ * device allocation is made by this call or by the attention calls and destroy of
+ * its plan.
+ * - SPAN_EINVAL if the plan's device data exceed SPAN_STATIC_SCRATCH_BYTES, or if
+ *   the pool's rotary table does not cover the plan's positions (a pool covers 4096
+ *   positions from creation; one span_plan of a longer query grows it).  The plan
+ *   is then released as by span_plan_destroy without commit: pages it evicted stay
+ *   evicted.
+ * - SPAN_ESTATE while another span_plan_static plan on the same GPU is alive
+ *   (created and not yet destroyed): every such plan on a GPU shares its array.
+ * - The array keeps the last plan's contents; what must start at zero (the
+ *   scheduling counters) is part of the copy each call makes on `stream`.  A plan
+ *   made after an earlier one was destroyed overwrites the array on its own
+ *   stream: the caller must order it after the earlier plan's kernels (one stream,
+ *   or a synchronisation); calls that overlap on one GPU race. */
+int span_plan_static(span_pool* pool, const span_query* queries, int32_t n_queries, void* stream,
+                     span_plan_t** out);
+
 /* ---------------------------------------------------------------- attention */
 
 /* Prefill of the new prefix and fragment tokens for one layer (sections 5.1, 5.6):

@@ -28,8 +28,9 @@ EXPORTS = [
     "span_hash_pages", "kv_lookup", "span_plan", "span_plan_stats", "span_plan_block_table",
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
-    "span_probe_read_peak",
+    "span_probe_read_peak", "span_plan_static",
 ]
+SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
 
 
@@ -110,6 +111,7 @@ def load():
         "span_hash_pages": (I32, [U64, P(I32), I32, I32, I32, P(U64), P(I32)]),
         "kv_lookup": (I32, [VP, P(U64), I32, P(I32), P(I32)]),
         "span_plan": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
+        "span_plan_static": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
@@ -249,9 +251,10 @@ class Pool:
         _check(load().span_pool_read_page(self._h, layer, page_id, buf.ctypes.data, buf.nbytes))
         return buf
 
-    def plan(self, queries: Iterable, stream=None) -> "Plan":
-        """queries: objects with .prefix, .frags, .cross; each span has .tokens (int32) and .row."""
-        return Plan(self, list(queries), stream)
+    def plan(self, queries: Iterable, stream=None, static: bool = False) -> "Plan":
+        """queries: objects with .prefix, .frags, .cross; each span has .tokens (int32) and .row.
+        static=True plans through span_plan_static (no device allocation)."""
+        return Plan(self, list(queries), stream, static)
 
 
 def _span(s, keep: list) -> SpanTokens:
@@ -263,7 +266,7 @@ def _span(s, keep: list) -> SpanTokens:
 
 
 class Plan:
-    def __init__(self, pool: Pool, queries: list, stream=None):
+    def __init__(self, pool: Pool, queries: list, stream=None, static: bool = False):
         lib = load()
         self.pool = pool
         keep: list = []
@@ -277,7 +280,8 @@ class Plan:
         self.n_frags = [len(q.frags) for q in queries]
         self._h = ctypes.c_void_p()
         self._stream = _stream(stream)
-        _check(lib.span_plan(pool.handle, arr, len(queries), self._stream, ctypes.byref(self._h)))
+        entry = lib.span_plan_static if static else lib.span_plan
+        _check(entry(pool.handle, arr, len(queries), self._stream, ctypes.byref(self._h)))
         pool._plans.add(self)
 
     def stats(self) -> dict:

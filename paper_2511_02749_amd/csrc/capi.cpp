@@ -8,12 +8,14 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <set>
 #include <string>
 #include <vector>
 
 #include "../../include/spanq.h"
+#include "capi_internal.h"
 #include "kernels.h"
 #include "planner.h"
 
@@ -137,7 +139,22 @@ struct span_plan_t {
   // for every such stream before the metadata is freed there.
   hipEvent_t ready = nullptr;
   std::vector<hipStream_t> foreign;
+  // Device data in a caller-side region (span_plan_static) instead of stream-ordered
+  // allocations: nothing to free at destroy, and the region is released for the
+  // next such plan on the device.
+  bool in_scratch = false;
 };
+
+namespace {
+// The plan whose device data occupy each device's scratch region (span_plan_static).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+span_plan_t* g_scratch_owner[kMaxDevices] = {};
+}  // namespace
+
+int spanq::pool_device(const span_pool* pool) { return pool ? pool->cfg.device : -1; }
+
+int spanq::report(int code, const char* msg) { return fail(code, msg); }
 
 namespace {
 // Records n+1 events around n launches; returns an empty vector if timing is off.
@@ -181,6 +198,125 @@ static size_t put(std::vector<unsigned char>& buf, const std::vector<T>& v) {
   buf.resize(at + v.size() * sizeof(T));
   if (!v.empty()) std::memcpy(buf.data() + at, v.data(), v.size() * sizeof(T));
   return at;
+}
+
+int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan_t** out,
+                     unsigned char* region, size_t region_bytes, const char* who) {
+  if (!pool || !out || nq < 0 || (nq > 0 && !qs)) return fail(SPAN_EINVAL, std::string(who) + ": bad argument");
+  *out = nullptr;
+  std::vector<QueryIn> in(static_cast<size_t>(nq));
+  for (int32_t i = 0; i < nq; ++i) {
+    const span_query& q = qs[i];
+    int rc = check_span(q.prefix, "prefix");
+    if (!rc) rc = check_span(q.cross, "cross");
+    if (rc) return rc;
+    if (q.n_frags < 0 || (q.n_frags > 0 && !q.frags)) return fail(SPAN_EINVAL, "span_plan: bad fragment list");
+    if (pool->cfg.hash_mode == SPAN_HASH_STOCK && (q.n_frags != 0 || q.cross.n != 0))
+      return fail(SPAN_EINVAL, "span_plan: stock hashing takes prefix-only queries");
+    in[i].prefix = SpanIn{q.prefix.tokens, q.prefix.n, q.prefix.row};
+    in[i].cross = SpanIn{q.cross.tokens, q.cross.n, q.cross.row};
+    for (int32_t f = 0; f < q.n_frags; ++f) {
+      rc = check_span(q.frags[f], "fragment");
+      if (rc) return rc;
+      in[i].frags.push_back(SpanIn{q.frags[f].tokens, q.frags[f].n, q.frags[f].row});
+    }
+  }
+  span_plan_t* pl = new (std::nothrow) span_plan_t();
+  if (!pl) return fail(SPAN_ENOMEM, "span_plan: host allocation");
+  pl->pool = pool;
+  pl->stream = static_cast<hipStream_t>(stream);
+  const bool device = pool->cfg.device >= 0;
+  pl->mfma = device && pool->use_mfma;
+  pl->bm = pl->mfma ? mfma_bm(pool->cfg.num_q_heads / pool->cfg.num_kv_heads) : kGenericBM;
+  const Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
+  std::string msg;
+  const auto t_plan0 = std::chrono::steady_clock::now();
+  int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
+  const auto t_plan1 = std::chrono::steady_clock::now();
+  pl->host_plan_us = std::chrono::duration<double, std::micro>(t_plan1 - t_plan0).count();
+  if (rc) {
+    delete pl;
+    return fail(rc, msg);
+  }
+  pool->plans.insert(pl);
+  if (device) {
+    Plan& P = pl->plan;
+    const int d = pool->cfg.head_dim;
+    hipError_t e = hipSetDevice(pool->cfg.device);
+    if (e != hipSuccess) {
+      span_plan_destroy(pl);
+      return hip_fail(e, (std::string(who) + ": hipSetDevice").c_str());
+    }
+    if (region) {
+      // no allocation: the rotary table must already cover the plan's positions
+      if (P.max_pos + 1 > pool->rope_n) {
+        span_plan_destroy(pl);
+        return fail(SPAN_EINVAL, std::string(who) + ": the pool's rotary table covers " + std::to_string(pool->rope_n) +
+                                     " positions, the plan needs " + std::to_string(P.max_pos + 1) +
+                                     " (one span_plan of that length grows it)");
+      }
+    } else {
+      rc = ensure_rope_table(pool, P.max_pos + 1, pl->stream);
+      if (rc) {
+        span_plan_destroy(pl);
+        return rc;
+      }
+    }
+    pl->rope = pool->rope_tab;
+    auto& hb = pl->host_meta;
+    size_t o_kv = put(hb, P.kv), o_kt = put(hb, P.kv_tiles), o_k3p = put(hb, P.k3_prefill),
+           o_k3c = put(hb, P.k3_cross);
+    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
+    size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
+    pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
+    const size_t part_bytes =
+        (pl->part_o_elems + static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2) * sizeof(float);
+    if (region) {
+      const size_t meta_bytes = (hb.size() + 255) & ~static_cast<size_t>(255);
+      if (meta_bytes + part_bytes > region_bytes) {
+        span_plan_destroy(pl);
+        return fail(SPAN_EINVAL, std::string(who) + ": the plan needs " + std::to_string(meta_bytes + part_bytes) +
+                                     " bytes of device scratch, the limit is " + std::to_string(region_bytes));
+      }
+      {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        const int dv = pool->cfg.device;
+        if (dv >= kMaxDevices) {
+          span_plan_destroy(pl);
+          return fail(SPAN_EINVAL, std::string(who) + ": device ordinal too large");
+        }
+        if (g_scratch_owner[dv]) {
+          span_plan_destroy(pl);
+          return fail(SPAN_ESTATE, std::string(who) + ": another plan of this kind is alive on the device");
+        }
+        g_scratch_owner[dv] = pl;
+      }
+      pl->in_scratch = true;
+      pl->dev_meta = region;
+      if (P.n_parts > 0) pl->part = reinterpret_cast<float*>(region + meta_bytes);
+      e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
+    } else {
+      e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
+      if (e == hipSuccess) e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
+      if (e == hipSuccess && P.n_parts > 0)
+        e = hipMallocAsync(reinterpret_cast<void**>(&pl->part), part_bytes, pl->stream);
+    }
+    if (e != hipSuccess) {
+      span_plan_destroy(pl);
+      return hip_fail(e, (std::string(who) + ": device metadata").c_str());
+    }
+    pl->host_upload_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t_plan1).count();
+    pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
+    pl->kt = reinterpret_cast<const TileRec*>(pl->dev_meta + o_kt);
+    pl->k3p = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3p);
+    pl->k3c = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3c);
+    pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
+    pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
+    pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
+    pl->sched = reinterpret_cast<unsigned*>(pl->dev_meta + o_sc);
+  }
+  *out = pl;
+  return SPAN_OK;
 }
 
 extern "C" {
@@ -253,6 +389,15 @@ int span_pool_create(const span_pool_config* c, span_pool** out) {
     }
     p->use_mfma = c->kernel == SPAN_KERNEL_MFMA ||
                   (c->kernel == SPAN_KERNEL_AUTO && mfma_supported(c->num_q_heads, c->num_kv_heads, c->head_dim, c->dtype));
+    // the first 4096 positions of the rotary table, ready before any plan
+    int rc = ensure_rope_table(p, 1, nullptr);
+    if (rc == SPAN_OK && hipDeviceSynchronize() != hipSuccess) rc = fail(SPAN_EHIP, "span_pool_create: rotary table copy");
+    if (rc != SPAN_OK) {
+      if (p->rope_tab) (void)hipFree(p->rope_tab);
+      if (p->owns_dev) (void)hipFree(p->dev);
+      delete p;
+      return rc;
+    }
   }
   p->index = new (std::nothrow) PoolIndex(c->num_pages, c->page_size, c->hash_mode);
   if (!p->index) {
@@ -360,85 +505,7 @@ int kv_lookup(const span_pool* p, const uint64_t* hashes, int32_t n, int32_t* pa
 }
 
 int span_plan(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan_t** out) {
-  if (!pool || !out || nq < 0 || (nq > 0 && !qs)) return fail(SPAN_EINVAL, "span_plan: bad argument");
-  *out = nullptr;
-  std::vector<QueryIn> in(static_cast<size_t>(nq));
-  for (int32_t i = 0; i < nq; ++i) {
-    const span_query& q = qs[i];
-    int rc = check_span(q.prefix, "prefix");
-    if (!rc) rc = check_span(q.cross, "cross");
-    if (rc) return rc;
-    if (q.n_frags < 0 || (q.n_frags > 0 && !q.frags)) return fail(SPAN_EINVAL, "span_plan: bad fragment list");
-    if (pool->cfg.hash_mode == SPAN_HASH_STOCK && (q.n_frags != 0 || q.cross.n != 0))
-      return fail(SPAN_EINVAL, "span_plan: stock hashing takes prefix-only queries");
-    in[i].prefix = SpanIn{q.prefix.tokens, q.prefix.n, q.prefix.row};
-    in[i].cross = SpanIn{q.cross.tokens, q.cross.n, q.cross.row};
-    for (int32_t f = 0; f < q.n_frags; ++f) {
-      rc = check_span(q.frags[f], "fragment");
-      if (rc) return rc;
-      in[i].frags.push_back(SpanIn{q.frags[f].tokens, q.frags[f].n, q.frags[f].row});
-    }
-  }
-  span_plan_t* pl = new (std::nothrow) span_plan_t();
-  if (!pl) return fail(SPAN_ENOMEM, "span_plan: host allocation");
-  pl->pool = pool;
-  pl->stream = static_cast<hipStream_t>(stream);
-  const bool device = pool->cfg.device >= 0;
-  pl->mfma = device && pool->use_mfma;
-  pl->bm = pl->mfma ? mfma_bm(pool->cfg.num_q_heads / pool->cfg.num_kv_heads) : kGenericBM;
-  const Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
-  std::string msg;
-  const auto t_plan0 = std::chrono::steady_clock::now();
-  int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
-  const auto t_plan1 = std::chrono::steady_clock::now();
-  pl->host_plan_us = std::chrono::duration<double, std::micro>(t_plan1 - t_plan0).count();
-  if (rc) {
-    delete pl;
-    return fail(rc, msg);
-  }
-  pool->plans.insert(pl);
-  if (device) {
-    Plan& P = pl->plan;
-    const int d = pool->cfg.head_dim;
-    hipError_t e = hipSetDevice(pool->cfg.device);
-    if (e != hipSuccess) {
-      span_plan_destroy(pl);
-      return hip_fail(e, "span_plan: hipSetDevice");
-    }
-    rc = ensure_rope_table(pool, P.max_pos + 1, pl->stream);
-    if (rc) {
-      span_plan_destroy(pl);
-      return rc;
-    }
-    pl->rope = pool->rope_tab;
-    auto& hb = pl->host_meta;
-    size_t o_kv = put(hb, P.kv), o_kt = put(hb, P.kv_tiles), o_k3p = put(hb, P.k3_prefill),
-           o_k3c = put(hb, P.k3_cross);
-    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
-    size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
-    e = hipMallocAsync(reinterpret_cast<void**>(&pl->dev_meta), hb.size(), pl->stream);
-    if (e == hipSuccess) e = hipMemcpyAsync(pl->dev_meta, hb.data(), hb.size(), hipMemcpyHostToDevice, pl->stream);
-    if (e == hipSuccess && P.n_parts > 0) {
-      pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
-      size_t ml = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2;
-      e = hipMallocAsync(reinterpret_cast<void**>(&pl->part), (pl->part_o_elems + ml) * sizeof(float), pl->stream);
-    }
-    if (e != hipSuccess) {
-      span_plan_destroy(pl);
-      return hip_fail(e, "span_plan: device metadata");
-    }
-    pl->host_upload_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t_plan1).count();
-    pl->kv = reinterpret_cast<const KvPage*>(pl->dev_meta + o_kv);
-    pl->kt = reinterpret_cast<const TileRec*>(pl->dev_meta + o_kt);
-    pl->k3p = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3p);
-    pl->k3c = reinterpret_cast<const NewPage*>(pl->dev_meta + o_k3c);
-    pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
-    pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
-    pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
-    pl->sched = reinterpret_cast<unsigned*>(pl->dev_meta + o_sc);
-  }
-  *out = pl;
-  return SPAN_OK;
+  return spanq::plan_impl(pool, qs, nq, stream, out, nullptr, 0, "span_plan");
 }
 
 int span_plan_stats(const span_plan_t* pl, span_stats* s) {
@@ -637,8 +704,13 @@ int span_plan_destroy(span_plan_t* pl) {
     if (ev) pl->pool->order_cache.push_back(ev);
   }
   if (pl->ready) pl->pool->order_cache.push_back(pl->ready);
-  if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
-  if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
+  if (pl->in_scratch) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    g_scratch_owner[pl->pool->cfg.device] = nullptr;
+  } else {
+    if (pl->dev_meta) (void)hipFreeAsync(pl->dev_meta, pl->stream);
+    if (pl->part) (void)hipFreeAsync(pl->part, pl->stream);
+  }
   pl->pool->plans.erase(pl);
   delete pl;
   return SPAN_OK;

@@ -1,0 +1,28 @@
+// Internal entries shared by the C-ABI sources (not part of the public ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/spanq.h"
+
+namespace spanq {
+
+// span_plan's work.  With region == nullptr the plan's device data (work lists,
+// scheduling counters, split-KV partials) come from the device's stream-ordered
+// allocator and the rotary table grows as needed.  With a region, they are placed
+// in region[0, region_bytes) (256-byte aligned device memory of the pool's device)
+// and nothing is allocated: SPAN_EINVAL if they do not fit or the table is too
+// short, SPAN_ESTATE while another plan holds the device's region.  `who` names
+// the entry point in error messages.
+int plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* stream, span_plan_t** out,
+              unsigned char* region, size_t region_bytes, const char* who);
+
+// Device ordinal of a pool; -1 for a null or host-only pool.
+int pool_device(const span_pool* pool);
+
+// Record a failure for span_last_error and return its status.
+int report(int code, const char* msg);
+
+}  // namespace spanq
