@@ -11,6 +11,9 @@ to Optimize for Cache and Attention Locality"):
   commuting child (sections 2 and 5.4).
 * ``pool``: a replay of the page cache's lookup, deduplication, allocation
   and LRU eviction rules.
+* ``stack``: a Llama-shaped decoder around span attention (RMSNorm, q/k/v and
+  output projections, SwiGLU, residuals, final norm, LM head, first-token
+  argmax), with the bf16 storage rounding of a bf16 model as an option.
 
 Only the test suite, the smoke check and the benchmark's CPU baseline may
 import this package.  It shares no code with the HIP library and never imports

@@ -286,3 +286,155 @@ def gather_queries(seed: int = 0, n_queries: int = 8, prefix_len: int = 2048, n_
         cross = book.add(_tokens(seed, KIND_CROSS, 1000 + qi, cross_len))
         queries.append(Query(prefix=prefix, frags=frags, cross=cross))
     return queries, book.next
+
+
+# ---------------------------------------------------------------- decoder stacks
+
+KIND_STACK_W = 9
+KIND_STACK_TOK = 10
+
+
+@dataclass
+class StackWeights:
+    """Random-init weights of a Llama-shaped decoder, as bf16 bit patterns (uint16).
+
+    x @ W convention (W is [in, out]).  w_qkv[l] holds the q, k and v projections side
+    by side ([hidden, (Hq + 2 Hkv) d]); w_gate_up[l] the gate then the up projection
+    ([hidden, 2 ffn]).  Projection and embedding entries are N(0, std^2); norm gains
+    are 1 + N(0, norm_std^2), so that a missing gain shows in parity.
+    """
+    n_layers: int
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn: int
+    vocab: int
+    embed: np.ndarray
+    attn_norm: List[np.ndarray]
+    w_qkv: List[np.ndarray]
+    w_o: List[np.ndarray]
+    ffn_norm: List[np.ndarray]
+    w_gate_up: List[np.ndarray]
+    w_down: List[np.ndarray]
+    final_norm: np.ndarray
+    lm_head: np.ndarray
+
+    def f32(self, a: np.ndarray) -> np.ndarray:
+        return bf16_bits_to_f32(a)
+
+    def nbytes(self) -> int:
+        arrs = [self.embed, self.final_norm, self.lm_head, *self.attn_norm, *self.w_qkv, *self.w_o,
+                *self.ffn_norm, *self.w_gate_up, *self.w_down]
+        return int(sum(a.nbytes for a in arrs))
+
+
+def stack_weights(seed: int, n_layers: int, hidden: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                  ffn: int, vocab: int, std: float = 0.02, norm_std: float = 0.1,
+                  threads: int = 8) -> StackWeights:
+    """Seeded weights, one PCG64 stream per matrix (drawn in parallel threads)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    qkv = (n_q_heads + 2 * n_kv_heads) * head_dim
+    specs = [("embed", 0, (vocab, hidden), std, 0.0), ("final_norm", 0, (hidden,), norm_std, 1.0),
+             ("lm_head", 0, (hidden, vocab), std, 0.0)]
+    for l in range(n_layers):
+        specs += [("attn_norm", l, (hidden,), norm_std, 1.0), ("w_qkv", l, (hidden, qkv), std, 0.0),
+                  ("w_o", l, (n_q_heads * head_dim, hidden), std, 0.0), ("ffn_norm", l, (hidden,), norm_std, 1.0),
+                  ("w_gate_up", l, (hidden, 2 * ffn), std, 0.0), ("w_down", l, (ffn, hidden), std, 0.0)]
+    names = ["embed", "final_norm", "lm_head", "attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
+
+    # a matrix is drawn in chunks of at most 2^22 entries of whole rows, chunk c from
+    # its own stream (matrix, layer, c), so large matrices draw in parallel too
+    chunk_elems = 1 << 22
+    jobs = []
+    outs = []
+    for name, l, shape, s, mean in specs:
+        out = np.empty(shape, np.uint16)
+        outs.append(out)
+        rows = shape[0]
+        per = max(1, chunk_elems // max(1, int(np.prod(shape[1:], dtype=np.int64))))
+        for c, r0 in enumerate(range(0, rows, per)):
+            jobs.append((name, l, c, out, r0, min(rows, r0 + per), s, mean))
+
+    def draw(job):
+        name, l, c, out, r0, r1, s, mean = job
+        g = rng(seed, KIND_STACK_W, (1000 * names.index(name) + l) * 4096 + c)
+        a = g.standard_normal((r1 - r0,) + out.shape[1:], dtype=np.float32)
+        a *= np.float32(s)
+        if mean:
+            a += np.float32(mean)
+        out[r0:r1] = round_to_bf16_bits(a)
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(draw, jobs))
+    arrs = outs
+    got = {n: [None] * n_layers for n in names[3:]}
+    top = {}
+    for (name, l, _, _, _), a in zip(specs, arrs):
+        if name in got:
+            got[name][l] = a
+        else:
+            top[name] = a
+    return StackWeights(n_layers=n_layers, hidden=hidden, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
+                        head_dim=head_dim, ffn=ffn, vocab=vocab, embed=top["embed"], final_norm=top["final_norm"],
+                        lm_head=top["lm_head"], **got)
+
+
+@dataclass
+class StackWorkload:
+    """Span queries over token ids for a decoder stack.  Every distinct span owns a
+    run of caller rows; ``row_tokens[r]`` is the token id at caller row r."""
+    name: str
+    weights: StackWeights
+    batches: List[List[Query]]
+    row_tokens: np.ndarray
+    rope_theta: float = 1e4
+    rms_eps: float = 1e-5
+    meta: dict = field(default_factory=dict)
+
+
+def stack_queries(seed: int, vocab: int, prefix_len: int, frag_lens: Sequence[int], cross_len: int,
+                  orders: Sequence[Sequence[int]], batch_split: Optional[Sequence[int]] = None):
+    """A shared prefix, a pool of fragments (token ids uniform over [0, vocab)) and one
+    query per entry of ``orders`` (fragment indices in this query's order), each with a
+    cross segment of its own.  Returns (batches, row_tokens)."""
+    book = _RowBook()
+    tok = lambda kind, i, n: rng(seed, KIND_STACK_TOK, 100_000 * kind + i).integers(  # noqa: E731
+        0, vocab, size=n, dtype=np.int64).astype(np.int32)
+    prefix = book.add(tok(KIND_PREFIX, 0, prefix_len))
+    frags = [book.add(tok(KIND_FRAG, f, int(n))) for f, n in enumerate(frag_lens)]
+    queries = []
+    for qi, order in enumerate(orders):
+        cross = book.add(tok(KIND_CROSS, qi, cross_len))
+        queries.append(Query(prefix=prefix, frags=[frags[int(f)] for f in order], cross=cross))
+    if batch_split is None:
+        batches = [queries]
+    else:
+        batches, at = [], 0
+        for n in batch_split:
+            batches.append(queries[at: at + n])
+            at += n
+    return batches, book.all_tokens()
+
+
+def stack_small(seed: int = 0, head_dim: int = 64, n_layers: int = 3, orders=((0, 1, 2), (2, 0, 3)),
+                batch_split=None) -> StackWorkload:
+    """A small stack for whole-output parity: hidden 4 heads x head_dim, one kv head
+    (four query heads per kv head), SwiGLU 2 x hidden, vocab 1000; prefix 40, ragged
+    fragments (37, 64, 100, 5), cross 23."""
+    hq, hkv = 4, 1
+    hidden = hq * head_dim
+    w = stack_weights(seed, n_layers, hidden, hq, hkv, head_dim, 2 * hidden, 1000)
+    batches, rt = stack_queries(seed, 1000, 40, (37, 64, 100, 5), 23, orders, batch_split)
+    return StackWorkload(name=f"stack_small_d{head_dim}", weights=w, batches=batches, row_tokens=rt)
+
+
+def config_c4(seed: int = 0, n_layers: int = 32) -> StackWorkload:
+    """2B-class decoder: 32 layers, hidden 2048, 32 query / 8 kv heads x 64, SwiGLU 8192,
+    vocab 128256, RMSNorm eps 1e-5, rotary theta 1e4, bf16.  One RAG query: prefix 512 +
+    32 fragments x 1024 + question 256."""
+    w = stack_weights(seed, n_layers, 2048, 32, 8, 64, 8192, VOCAB)
+    batches, rt = stack_queries(seed, VOCAB, 512, [1024] * 32, 256, [list(range(32))])
+    return StackWorkload(name="c4", weights=w, batches=batches, row_tokens=rt,
+                         meta=dict(prefix_len=512, n_frags=32, frag_len=1024, cross_len=256))
