@@ -286,6 +286,68 @@ int span_plan_commit(span_plan_t* plan);
  * call itself does not wait for the device. */
 int span_plan_destroy(span_plan_t* plan);
 
+/* ---------------------------------------------------------------- decoder stack */
+
+/* A decoder stack that a span query's prefill runs through (the paper's latency
+ * results are whole-model time to first token, sections 5.6 and 5.7; it names no
+ * architecture for them).  The layer is the pre-norm Llama block:
+ *     n = RMSNorm(x) g_attn;  q | k | v = n W_qkv;  o = span attention (the calls above)
+ *     h = x + o W_o;  n2 = RMSNorm(h) g_ffn;  x' = h + (silu(n2 W_gate) * (n2 W_up)) W_down
+ * with RMSNorm(x) = x / sqrt(mean(x^2) + eps) and silu(z) = z / (1 + e^-z); then a
+ * final RMSNorm and the LM head on each query's last cross token, and the argmax of
+ * its logits (lowest id on ties) as the first generated token.
+ * Weights are caller-owned device memory, bf16, row-major, x @ W convention
+ * (W is [in][out]); the per-layer tables are host arrays of num_layers pointers.
+ * The model copies the tables; the weights must outlive it. */
+typedef struct span_model span_model;
+
+
+typedef struct {
+  int32_t num_layers;    /* == the pool's */
+  int32_t hidden;        /* multiple of 8, at most 8192 */
+  int32_t num_q_heads;   /* == the pool's */
+  int32_t num_kv_heads;  /* == the pool's */
+  int32_t head_dim;      /* == the pool's */
+  int32_t ffn;           /* SwiGLU width, multiple of 8 */
+  int32_t vocab;         /* multiple of 8 */
+  float rms_eps;         /* > 0 */
+  int32_t reserved;      /* 0 */
+  const void* embed;                /* [vocab][hidden] */
+  const void* const* attn_norm;     /* per layer [hidden] */
+  const void* const* w_qkv;         /* per layer [hidden][(num_q_heads + 2 num_kv_heads) head_dim]: q | k | v */
+  const void* const* w_o;           /* per layer [num_q_heads head_dim][hidden] */
+  const void* const* ffn_norm;      /* per layer [hidden] */
+  const void* const* w_gate_up;     /* per layer [hidden][2 ffn]: gate | up */
+  const void* const* w_down;        /* per layer [ffn][hidden] */
+  const void* final_norm;           /* [hidden] */
+  const void* lm_head;              /* [hidden][vocab] */
+} span_model_config;
+
+/* Bind a model to a bf16 device pool of the same layers and heads.  Allocates a
+ * GEMM workspace; activation buffers are allocated by the first forward call and
+ * grown when a later one needs more.  SPAN_EINVAL on a shape mismatch. */
+int span_model_create(span_pool* pool, const span_model_config* cfg, span_model** out);
+int span_model_destroy(span_model* model);
+
+/* Run the rows a plan computes (span_plan_rows: new prefix/fragment tokens, then
+ * cross tokens) through the first n_layers layers, calling span_prefill_fragments
+ * and span_cross_attend of `plan` per layer; cached rows are not computed, their
+ * keys and values are read from the pool's pages.
+ * - row_tokens: host int32 [n_rows], the token id at each caller row (the rows of
+ *   the plan's spans must lie below n_rows).
+ * - hidden_out: optional device bf16 [n_rows][hidden]; receives the residual stream
+ *   after n_layers layers at the computed rows (other rows untouched).
+ * - logits_out: optional device float [m][vocab], m = number of the plan's queries
+ *   with a cross segment, in query order: the LM head logits of each one's last
+ *   cross token.  Needs n_layers == num_layers.
+ * - first_tokens: optional host int32 [n_queries]: the argmax of those logits, -1
+ *   for a query without a cross segment.  Needs n_layers == num_layers; the call
+ *   then waits for the stream.
+ * Work is enqueued on `stream`.  The model's buffers are reused by the next call:
+ * calls on one model are ordered by the caller (one stream). */
+int span_model_forward(span_model* model, span_plan_t* plan, const int32_t* row_tokens, int64_t n_rows,
+                       int32_t n_layers, void* hidden_out, float* logits_out, int32_t* first_tokens, void* stream);
+
 /* ---------------------------------------------------------------- debug */
 
 /* Kernel durations of a plan's launches on a pool created with SPAN_FLAG_TIMING,

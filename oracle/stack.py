@@ -102,7 +102,7 @@ def stack_forward(tokens: Sequence[int], lay: A.Layout, W: Weights, n_layers: in
     """Hidden states of every token of S after ``n_layers`` layers (float64 [N, hidden]).
     With ``keep``, returns {layer count: hidden states} for each count in keep (0 = the
     embeddings)."""
-    x = np.asarray(W.embed, np.float64)[np.asarray(tokens, np.int64)]
+    x = np.asarray(np.asarray(W.embed)[np.asarray(tokens, np.int64)], np.float64)
     kept = {}
     if keep is not None and 0 in keep:
         kept[0] = x.copy()

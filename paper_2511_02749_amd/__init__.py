@@ -11,6 +11,7 @@ from ._lib import (  # noqa: F401
     SPAN_F32,
     SPAN_HASH_FRAG_TAG,
     SPAN_HASH_ROOT,
+    Model,
     Plan,
     Pool,
     SpanError,

@@ -28,7 +28,7 @@ EXPORTS = [
     "span_hash_pages", "kv_lookup", "span_plan", "span_plan_stats", "span_plan_block_table",
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
-    "span_probe_read_peak", "span_plan_static",
+    "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -81,6 +81,17 @@ class KernelTimes(ctypes.Structure):
                                                             ("cross_calls", ctypes.c_int32)]
 
 
+class ModelConfig(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("embed", ctypes.c_void_p),
+                ("attn_norm", ctypes.POINTER(ctypes.c_void_p)), ("w_qkv", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_o", ctypes.POINTER(ctypes.c_void_p)), ("ffn_norm", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_gate_up", ctypes.POINTER(ctypes.c_void_p)), ("w_down", ctypes.POINTER(ctypes.c_void_p)),
+                ("final_norm", ctypes.c_void_p), ("lm_head", ctypes.c_void_p)]
+
+
 _LIB = None
 
 
@@ -112,6 +123,9 @@ def load():
         "kv_lookup": (I32, [VP, P(U64), I32, P(I32), P(I32)]),
         "span_plan": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
         "span_plan_static": (I32, [VP, P(SpanQuery), I32, VP, P(VP)]),
+        "span_model_create": (I32, [VP, P(ModelConfig), P(VP)]),
+        "span_model_destroy": (I32, [VP]),
+        "span_model_forward": (I32, [VP, VP, P(I32), I64, I32, VP, VP, P(I32), VP]),
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
@@ -342,5 +356,57 @@ class Plan:
     def __del__(self):
         try:
             self.destroy()
+        except Exception:
+            pass
+
+
+class Model:
+    """A decoder stack bound to a pool (span_model_*).  Weights are device tensors or
+    device addresses (bf16, x @ W layout); per-layer weights are sequences."""
+
+    def __init__(self, pool: Pool, *, hidden: int, ffn: int, vocab: int, rms_eps: float, embed, attn_norm, w_qkv,
+                 w_o, ffn_norm, w_gate_up, w_down, final_norm, lm_head):
+        lib = load()
+        L = pool.cfg.num_layers
+        self._keep = [embed, attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down, final_norm, lm_head]
+        tables = []
+        for seq in (attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down):
+            assert len(seq) == L
+            tables.append((ctypes.c_void_p * L)(*[_ptr(x) for x in seq]))
+        self._tables = tables
+        self.cfg = ModelConfig(num_layers=L, hidden=hidden, num_q_heads=pool.cfg.num_q_heads,
+                               num_kv_heads=pool.cfg.num_kv_heads, head_dim=pool.cfg.head_dim, ffn=ffn, vocab=vocab,
+                               rms_eps=rms_eps, reserved=0, embed=_ptr(embed),
+                               attn_norm=ctypes.cast(tables[0], ctypes.POINTER(ctypes.c_void_p)),
+                               w_qkv=ctypes.cast(tables[1], ctypes.POINTER(ctypes.c_void_p)),
+                               w_o=ctypes.cast(tables[2], ctypes.POINTER(ctypes.c_void_p)),
+                               ffn_norm=ctypes.cast(tables[3], ctypes.POINTER(ctypes.c_void_p)),
+                               w_gate_up=ctypes.cast(tables[4], ctypes.POINTER(ctypes.c_void_p)),
+                               w_down=ctypes.cast(tables[5], ctypes.POINTER(ctypes.c_void_p)),
+                               final_norm=_ptr(final_norm), lm_head=_ptr(lm_head))
+        self.pool = pool
+        self._h = ctypes.c_void_p()
+        _check(lib.span_model_create(pool.handle, ctypes.byref(self.cfg), ctypes.byref(self._h)))
+
+    def forward(self, plan: "Plan", row_tokens, n_layers: Optional[int] = None, hidden_out=None, logits_out=None,
+                first_tokens: bool = True, stream=None):
+        """Run the plan's computed rows through the stack; returns the first token of
+        each query (or None with first_tokens=False)."""
+        rt = np.ascontiguousarray(row_tokens, dtype=np.int32)
+        L = self.cfg.num_layers if n_layers is None else n_layers
+        toks = np.zeros(max(1, plan.n_queries), np.int32) if first_tokens else None
+        _check(load().span_model_forward(self._h, plan._h, _i32p(rt), rt.size, L, _ptr(hidden_out), _ptr(logits_out),
+                                         _i32p(toks) if toks is not None else None,
+                                         _stream(stream) if stream is not None else plan._stream))
+        return [int(t) for t in toks[: plan.n_queries]] if toks is not None else None
+
+    def close(self):
+        if self._h:
+            _check(load().span_model_destroy(self._h))
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
         except Exception:
             pass

@@ -156,6 +156,25 @@ int spanq::pool_device(const span_pool* pool) { return pool ? pool->cfg.device :
 
 int spanq::report(int code, const char* msg) { return fail(code, msg); }
 
+span_pool* spanq::plan_pool(const span_plan_t* plan) { return plan ? plan->pool : nullptr; }
+
+void spanq::pool_shape(const span_pool* pool, int32_t out[5]) {
+  const span_pool_config& c = pool->cfg;
+  out[0] = c.num_layers;
+  out[1] = c.num_q_heads;
+  out[2] = c.num_kv_heads;
+  out[3] = c.head_dim;
+  out[4] = c.dtype;
+}
+
+void spanq::plan_last_cross_rows(const span_plan_t* plan, std::vector<int64_t>* rows) {
+  rows->clear();
+  for (const auto& ids : plan->plan.query_spans) {
+    const SpanPlan& c = plan->plan.spans[ids.back()];
+    rows->push_back(c.n_tok > 0 ? c.row + c.n_tok - 1 : -1);
+  }
+}
+
 namespace {
 // Records n+1 events around n launches; returns an empty vector if timing is off.
 struct Timer {

@@ -4,6 +4,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include "../../include/spanq.h"
 
@@ -24,5 +25,14 @@ int pool_device(const span_pool* pool);
 
 // Record a failure for span_last_error and return its status.
 int report(int code, const char* msg);
+
+// The pool a plan was made on.
+span_pool* plan_pool(const span_plan_t* plan);
+
+// Pool shape: {num_layers, num_q_heads, num_kv_heads, head_dim, dtype}.
+void pool_shape(const span_pool* pool, int32_t out[5]);
+
+// Caller row of each query's last cross token, -1 for a query without one.
+void plan_last_cross_rows(const span_plan_t* plan, std::vector<int64_t>* rows);
 
 }  // namespace spanq

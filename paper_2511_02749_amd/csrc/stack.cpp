@@ -1,0 +1,400 @@
+// Decoder stack around span attention: the model the span query's prefill runs
+// through (the harness of the attention path).  Per layer, over the rows a plan
+// computes (new prefix/fragment tokens, then cross tokens):
+//
+//   n = RMSNorm(x) g_attn; qkv = n W_qkv            hipBLASLt GEMM, bf16 out
+//   q, k, v -> caller rows; span_prefill_fragments and span_cross_attend
+//   x = x + o W_o                                    GEMM with the residual as C (beta 1)
+//   n = RMSNorm(x) g_ffn; gu = n W_gate_up           GEMM
+//   x = x + (silu(gate) * up) W_down                 SwiGLU kernel, GEMM with residual
+//
+// then the final RMSNorm of each query's last cross row, the LM head and the
+// argmax (the first generated token).  Rows that hit the cache are never
+// computed: their keys and values are already in the pool's pages, which is the
+// point of the method (section 5.6).
+#include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <map>
+#include <string>
+#include <tuple>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/spanq.h"
+#include "capi_internal.h"
+#include "stack_kernels.h"
+
+using namespace spanq;
+
+namespace {
+
+int hip_err(hipError_t e, const std::string& what) {
+  return report(SPAN_EHIP, (what + ": " + hipGetErrorString(e)).c_str());
+}
+
+int lt_err(hipblasStatus_t st, const std::string& what) {
+  return report(SPAN_EHIP, (what + ": hipBLASLt status " + std::to_string(static_cast<int>(st))).c_str());
+}
+
+// A device buffer that only grows (callers synchronise before it is replaced).
+struct Buf {
+  void* p = nullptr;
+  size_t cap = 0;
+  hipError_t ensure(size_t bytes) {
+    if (bytes <= cap) return hipSuccess;
+    if (p) {
+      hipError_t e = hipFree(p);
+      if (e != hipSuccess) return e;
+      p = nullptr;
+      cap = 0;
+    }
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e == hipSuccess) cap = bytes;
+    return e;
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+  }
+  template <class T>
+  T* as() const { return static_cast<T*>(p); }
+};
+
+// Row-major Y[M][N] = X[M][K] W[K][N] (+ Y when residual), bf16 in and out, fp32
+// accumulation.  In hipBLASLt's column-major terms this is Y^T = W^T X^T: its A is W
+// seen as an N x K matrix, its B is X seen as K x M, and its D is Y seen as N x M.
+// Each (M, N, K) takes the heuristic's first choice.  That choice, and even one
+// algorithm's split of the K loop, depend on M, so a row's result may change in its
+// last bits with the number of rows computed together.
+struct Gemm {
+  hipblasLtHandle_t h = nullptr;
+  hipblasLtMatmulDesc_t desc = nullptr;
+  hipblasLtMatmulPreference_t pref = nullptr;
+  Buf ws;
+  size_t ws_bytes = size_t{64} << 20;
+  struct Plan {
+    hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
+    hipblasLtMatmulAlgo_t algo{};
+    size_t ws = 0;
+  };
+  std::map<std::tuple<int64_t, int64_t, int64_t, bool>, Plan> plans;
+
+  int init() {
+    hipblasStatus_t st = hipblasLtCreate(&h);
+    if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtCreate");
+    st = hipblasLtMatmulDescCreate(&desc, HIPBLAS_COMPUTE_32F, HIP_R_32F);
+    if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtMatmulDescCreate");
+    st = hipblasLtMatmulPreferenceCreate(&pref);
+    if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtMatmulPreferenceCreate");
+    uint64_t wsb = ws_bytes;
+    st = hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &wsb, sizeof(wsb));
+    if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtMatmulPreferenceSetAttribute");
+    hipError_t e = ws.ensure(ws_bytes);
+    if (e != hipSuccess) return hip_err(e, "GEMM workspace");
+    return SPAN_OK;
+  }
+
+  void destroy() {
+    for (auto& kv : plans) {
+      hipblasLtMatrixLayoutDestroy(kv.second.a);
+      hipblasLtMatrixLayoutDestroy(kv.second.b);
+      hipblasLtMatrixLayoutDestroy(kv.second.c);
+    }
+    plans.clear();
+    if (pref) hipblasLtMatmulPreferenceDestroy(pref);
+    if (desc) hipblasLtMatmulDescDestroy(desc);
+    if (h) hipblasLtDestroy(h);
+    ws.release();
+  }
+
+  int run(const void* x, const void* w, void* y, int64_t M, int64_t N, int64_t K, bool residual, hipStream_t s) {
+    if (M == 0) return SPAN_OK;
+    auto key = std::make_tuple(M, N, K, residual);
+    auto it = plans.find(key);
+    if (it == plans.end()) {
+      Plan p;
+      hipblasStatus_t st = hipblasLtMatrixLayoutCreate(&p.a, HIP_R_16BF, N, K, N);
+      if (st == HIPBLAS_STATUS_SUCCESS) st = hipblasLtMatrixLayoutCreate(&p.b, HIP_R_16BF, K, M, K);
+      if (st == HIPBLAS_STATUS_SUCCESS) st = hipblasLtMatrixLayoutCreate(&p.c, HIP_R_16BF, N, M, N);
+      if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtMatrixLayoutCreate");
+      hipblasLtMatmulHeuristicResult_t res[1];
+      int n = 0;
+      st = hipblasLtMatmulAlgoGetHeuristic(h, desc, p.a, p.b, p.c, p.c, pref, 1, res, &n);
+      if (st != HIPBLAS_STATUS_SUCCESS || n < 1 || res[0].workspaceSize > ws_bytes) {
+        hipblasLtMatrixLayoutDestroy(p.a);
+        hipblasLtMatrixLayoutDestroy(p.b);
+        hipblasLtMatrixLayoutDestroy(p.c);
+        return report(SPAN_EHIP, ("hipBLASLt: no algorithm for M=" + std::to_string(M) + " N=" + std::to_string(N) +
+                                  " K=" + std::to_string(K)).c_str());
+      }
+      p.algo = res[0].algo;
+      p.ws = res[0].workspaceSize;
+      it = plans.emplace(key, p).first;
+    }
+    const float alpha = 1.f, beta = residual ? 1.f : 0.f;
+    const Plan& p = it->second;
+    hipblasStatus_t st = hipblasLtMatmul(h, desc, &alpha, w, p.a, x, p.b, &beta, y, p.c, y, p.c, &p.algo, ws.p,
+                                         p.ws ? ws_bytes : 0, s);
+    if (st != HIPBLAS_STATUS_SUCCESS) return lt_err(st, "hipblasLtMatmul");
+    return SPAN_OK;
+  }
+};
+
+}  // namespace
+
+struct span_model {
+  span_pool* pool = nullptr;
+  int device = 0;
+  span_model_config cfg{};
+  std::vector<const void*> attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
+  Gemm gemm;
+  // compact activations over the computed rows
+  Buf x, n, qkv, oc, gu, act;
+  // caller-row activations the attention entry points read and write
+  Buf q, k, v, o;
+  // row lists, LM head
+  Buf rows, toks, last, nf, part, logits, tok_out;
+  int32_t* host_stage = nullptr;  // pinned staging of the row lists
+  size_t host_stage_cap = 0;
+  hipEvent_t staged = nullptr;     // the last upload from host_stage
+};
+
+namespace {
+
+int check_config(span_pool* pool, const span_model_config* c) {
+  if (!pool || !c) return report(SPAN_EINVAL, "span_model_create: null argument");
+  int32_t sh[5];
+  pool_shape(pool, sh);
+  if (pool_device(pool) < 0) return report(SPAN_EINVAL, "span_model_create: the pool must be a device pool");
+  if (sh[4] != SPAN_BF16) return report(SPAN_EINVAL, "span_model_create: the pool must hold bf16 pages");
+  if (c->num_layers != sh[0] || c->num_q_heads != sh[1] || c->num_kv_heads != sh[2] || c->head_dim != sh[3])
+    return report(SPAN_EINVAL, "span_model_create: layers, heads and head_dim must equal the pool's");
+  if (c->hidden < 8 || c->hidden % 8 != 0 || c->hidden > 8192)
+    return report(SPAN_EINVAL, "span_model_create: hidden must be a multiple of 8 in [8, 8192]");
+  if (c->ffn < 8 || c->ffn % 8 != 0) return report(SPAN_EINVAL, "span_model_create: ffn must be a positive multiple of 8");
+  if (c->vocab < 8 || c->vocab % 8 != 0) return report(SPAN_EINVAL, "span_model_create: vocab must be a positive multiple of 8");
+  if (!(c->rms_eps > 0.f)) return report(SPAN_EINVAL, "span_model_create: rms_eps must be positive");
+  if (!c->embed || !c->final_norm || !c->lm_head || !c->attn_norm || !c->w_qkv || !c->w_o || !c->ffn_norm ||
+      !c->w_gate_up || !c->w_down)
+    return report(SPAN_EINVAL, "span_model_create: null weight pointer");
+  for (int l = 0; l < c->num_layers; ++l)
+    if (!c->attn_norm[l] || !c->w_qkv[l] || !c->w_o[l] || !c->ffn_norm[l] || !c->w_gate_up[l] || !c->w_down[l])
+      return report(SPAN_EINVAL, "span_model_create: null weight pointer in a layer table");
+  return SPAN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int span_model_create(span_pool* pool, const span_model_config* cfg, span_model** out) {
+  if (!out) return report(SPAN_EINVAL, "span_model_create: null argument");
+  *out = nullptr;
+  int rc = check_config(pool, cfg);
+  if (rc) return rc;
+  span_model* m = new (std::nothrow) span_model();
+  if (!m) return report(SPAN_ENOMEM, "span_model_create: host allocation");
+  m->pool = pool;
+  m->device = pool_device(pool);
+  m->cfg = *cfg;
+  const int L = cfg->num_layers;
+  m->attn_norm.assign(cfg->attn_norm, cfg->attn_norm + L);
+  m->w_qkv.assign(cfg->w_qkv, cfg->w_qkv + L);
+  m->w_o.assign(cfg->w_o, cfg->w_o + L);
+  m->ffn_norm.assign(cfg->ffn_norm, cfg->ffn_norm + L);
+  m->w_gate_up.assign(cfg->w_gate_up, cfg->w_gate_up + L);
+  m->w_down.assign(cfg->w_down, cfg->w_down + L);
+  m->cfg.attn_norm = m->cfg.w_qkv = m->cfg.w_o = m->cfg.ffn_norm = m->cfg.w_gate_up = m->cfg.w_down = nullptr;
+  hipError_t e = hipSetDevice(m->device);
+  if (e != hipSuccess) {
+    delete m;
+    return hip_err(e, "span_model_create: hipSetDevice");
+  }
+  rc = m->gemm.init();
+  if (rc == SPAN_OK) {
+    e = hipEventCreateWithFlags(&m->staged, hipEventDisableTiming);
+    if (e != hipSuccess) rc = hip_err(e, "span_model_create: event");
+  }
+  if (rc) {
+    m->gemm.destroy();
+    delete m;
+    return rc;
+  }
+  *out = m;
+  return SPAN_OK;
+}
+
+int span_model_destroy(span_model* m) {
+  if (!m) return report(SPAN_EINVAL, "span_model_destroy: null model");
+  (void)hipSetDevice(m->device);
+  (void)hipDeviceSynchronize();
+  m->gemm.destroy();
+  for (Buf* b : {&m->x, &m->n, &m->qkv, &m->oc, &m->gu, &m->act, &m->q, &m->k, &m->v, &m->o, &m->rows, &m->toks,
+                 &m->last, &m->nf, &m->part, &m->logits, &m->tok_out})
+    b->release();
+  if (m->host_stage) (void)hipHostFree(m->host_stage);
+  if (m->staged) (void)hipEventDestroy(m->staged);
+  delete m;
+  return SPAN_OK;
+}
+
+int span_model_forward(span_model* m, span_plan_t* plan, const int32_t* row_tokens, int64_t n_rows, int32_t n_layers,
+                       void* hidden_out, float* logits_out, int32_t* first_tokens, void* stream) {
+  if (!m || !plan || (!row_tokens && n_rows > 0) || n_rows < 0)
+    return report(SPAN_EINVAL, "span_model_forward: bad argument");
+  if (plan_pool(plan) != m->pool) return report(SPAN_EINVAL, "span_model_forward: the plan belongs to another pool");
+  const span_model_config& c = m->cfg;
+  if (n_layers < 0 || n_layers > c.num_layers)
+    return report(SPAN_EINVAL, "span_model_forward: n_layers must lie in [0, num_layers]");
+  if ((first_tokens || logits_out) && n_layers != c.num_layers)
+    return report(SPAN_EINVAL, "span_model_forward: the LM head needs every layer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSetDevice(m->device);
+  if (e != hipSuccess) return hip_err(e, "span_model_forward: hipSetDevice");
+
+  // ---- the rows the plan computes, their tokens, each query's last cross row
+  int64_t n_pre = 0, n_cross = 0;
+  int rc = span_plan_rows(plan, nullptr, 0, &n_pre, &n_cross);
+  if (rc) return rc;
+  const int64_t T = n_pre + n_cross;
+  std::vector<int64_t> rows64(static_cast<size_t>(T));
+  rc = span_plan_rows(plan, rows64.data(), T, &n_pre, &n_cross);
+  if (rc) return rc;
+  std::vector<int64_t> last_rows;
+  plan_last_cross_rows(plan, &last_rows);
+  const int nq = static_cast<int>(last_rows.size());
+  std::unordered_map<int64_t, int32_t> last_at;
+  for (int64_t r : last_rows)
+    if (r >= 0) last_at.emplace(r, -1);
+  const size_t stage_n = 2 * static_cast<size_t>(T) + static_cast<size_t>(nq) + 8;
+  if (stage_n > m->host_stage_cap) {
+    e = hipEventSynchronize(m->staged);
+    if (e == hipSuccess && m->host_stage) e = hipHostFree(m->host_stage);
+    m->host_stage = nullptr;
+    m->host_stage_cap = 0;
+    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->host_stage), stage_n * sizeof(int32_t), 0);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: pinned staging");
+    m->host_stage_cap = stage_n;
+  } else {
+    e = hipEventSynchronize(m->staged);  // the previous upload has left the staging area
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: staging");
+  }
+  int32_t* h_rows = m->host_stage;
+  int32_t* h_toks = h_rows + T;
+  int32_t* h_last = h_toks + T;
+  for (int64_t i = 0; i < T; ++i) {
+    const int64_t r = rows64[static_cast<size_t>(i)];
+    if (r < 0 || r >= n_rows) return report(SPAN_EINVAL, "span_model_forward: a planned row lies outside row_tokens");
+    const int32_t t = row_tokens[r];
+    if (t < 0 || t >= c.vocab) return report(SPAN_EINVAL, "span_model_forward: token id outside the vocabulary");
+    h_rows[i] = static_cast<int32_t>(r);
+    h_toks[i] = t;
+    auto it = last_at.find(r);
+    if (it != last_at.end()) it->second = static_cast<int32_t>(i);
+  }
+  std::vector<int> q_of;  // queries with a cross row, in order
+  for (int qi = 0; qi < nq; ++qi)
+    if (last_rows[qi] >= 0) {
+      const int32_t at = last_at[last_rows[qi]];
+      if (at < 0) return report(SPAN_EINVAL, "span_model_forward: a query's last cross row is not computed by the plan");
+      h_last[q_of.size()] = at;
+      q_of.push_back(qi);
+    }
+  const int nh = static_cast<int>(q_of.size());
+
+  // ---- buffers (grown with the stream drained, so no launch still reads the old ones)
+  const int H = c.hidden, hq = c.num_q_heads, hkv = c.num_kv_heads, d = c.head_dim, F = c.ffn, V = c.vocab;
+  const int64_t qkv_w = static_cast<int64_t>(hq + 2 * hkv) * d;
+  const size_t bf = 2;
+  const size_t Tz = static_cast<size_t>(T), Rz = static_cast<size_t>(n_rows);
+  struct Need {
+    Buf* b;
+    size_t bytes;
+  } needs[] = {
+      {&m->x, Tz * H * bf}, {&m->n, Tz * H * bf}, {&m->qkv, Tz * qkv_w * bf}, {&m->oc, Tz * hq * d * bf},
+      {&m->gu, Tz * 2 * F * bf}, {&m->act, Tz * F * bf}, {&m->q, Rz * hq * d * bf}, {&m->k, Rz * hkv * d * bf},
+      {&m->v, Rz * hkv * d * bf}, {&m->o, Rz * hq * d * bf}, {&m->rows, Tz * 4 + 4}, {&m->toks, Tz * 4 + 4},
+      {&m->last, 8 * 4}, {&m->nf, static_cast<size_t>(8) * H * bf},
+      {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
+      {&m->tok_out, 8 * 4}};
+  bool grow = false;
+  for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
+  if (grow) {
+    e = hipStreamSynchronize(s);
+    for (const Need& nd : needs)
+      if (e == hipSuccess) e = nd.b->ensure(nd.bytes);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: activation buffers");
+  }
+  e = T > 0 ? hipMemcpyAsync(m->rows.p, h_rows, Tz * 4, hipMemcpyHostToDevice, s) : hipSuccess;
+  if (e == hipSuccess && T > 0) e = hipMemcpyAsync(m->toks.p, h_toks, Tz * 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && nh > 0) e = hipMemcpyAsync(m->last.p, h_last, static_cast<size_t>(nh) * 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipEventRecord(m->staged, s);
+  if (e != hipSuccess) return hip_err(e, "span_model_forward: row lists");
+
+  // ---- embeddings, then the layers
+  const int32_t* rows = m->rows.as<int32_t>();
+  e = launch_copy_rows(m->x.p, c.embed, m->toks.as<int32_t>(), T, H * 2, false, s);
+  if (e != hipSuccess) return hip_err(e, "span_model_forward: embedding");
+  for (int l = 0; l < n_layers; ++l) {
+    e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: attention norm");
+    rc = m->gemm.run(m->n.p, m->w_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
+    if (rc) return rc;
+    e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: q/k/v scatter");
+    rc = span_prefill_fragments(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
+    if (rc) return rc;
+    rc = span_cross_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
+    if (rc) return rc;
+    e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: attention output gather");
+    rc = m->gemm.run(m->oc.p, m->w_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
+    if (rc) return rc;
+    e = launch_rmsnorm(m->x.p, nullptr, m->ffn_norm[l], m->n.p, T, H, c.rms_eps, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: ffn norm");
+    rc = m->gemm.run(m->n.p, m->w_gate_up[l], m->gu.p, T, 2 * static_cast<int64_t>(F), H, false, s);
+    if (rc) return rc;
+    e = launch_swiglu(m->gu.p, m->act.p, T, F, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: swiglu");
+    rc = m->gemm.run(m->act.p, m->w_down[l], m->x.p, T, H, F, true, s);
+    if (rc) return rc;
+  }
+  if (hidden_out) {
+    e = launch_copy_rows(hidden_out, m->x.p, rows, T, H * 2, true, s);
+    if (e != hipSuccess) return hip_err(e, "span_model_forward: hidden state scatter");
+  }
+  if (first_tokens)
+    for (int qi = 0; qi < nq; ++qi) first_tokens[qi] = -1;
+  if ((first_tokens || logits_out) && nh > 0) {
+    std::vector<int32_t> toks(static_cast<size_t>(nh));
+    for (int g0 = 0; g0 < nh; g0 += 8) {
+      const int ng = std::min(8, nh - g0);
+      const int np = ng <= 1 ? 1 : ng <= 2 ? 2 : ng <= 4 ? 4 : 8;
+      // padded rows repeat the group's last row
+      e = launch_rmsnorm(m->x.p, m->last.as<int32_t>() + g0, c.final_norm, m->nf.p, ng, H, c.rms_eps, s);
+      for (int r = ng; e == hipSuccess && r < np; ++r)
+        e = hipMemcpyAsync(static_cast<char*>(m->nf.p) + static_cast<size_t>(r) * H * bf,
+                           static_cast<char*>(m->nf.p) + static_cast<size_t>(ng - 1) * H * bf, H * bf,
+                           hipMemcpyDeviceToDevice, s);
+      if (e == hipSuccess) e = launch_lm_head(m->nf.p, c.lm_head, m->part.as<float>(), np, H, V, s);
+      float* lg = logits_out ? logits_out + static_cast<size_t>(g0) * V : nullptr;
+      if (e == hipSuccess) e = launch_argmax(m->part.as<float>(), np, ng, H, V, lg, m->tok_out.as<int32_t>(), s);
+      if (e == hipSuccess && first_tokens)
+        e = hipMemcpyAsync(toks.data() + g0, m->tok_out.p, static_cast<size_t>(ng) * 4, hipMemcpyDeviceToHost, s);
+      if (e != hipSuccess) return hip_err(e, "span_model_forward: LM head");
+    }
+    if (first_tokens) {
+      e = hipStreamSynchronize(s);
+      if (e != hipSuccess) return hip_err(e, "span_model_forward: first tokens");
+      for (int i = 0; i < nh; ++i) first_tokens[q_of[i]] = toks[i];
+    }
+  }
+  return SPAN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,37 @@
+// Launchers of the decoder-stack kernels (stack_kernels.hip).  Activations are
+// bf16 bit patterns, row-major; row sizes are multiples of 16 bytes.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace spanq {
+
+// Row copy: dst[i] = src[idx[i]] (gather) or dst[idx[i]] = src[i] (scatter); idx
+// null = identity.  row_bytes a multiple of 16.
+hipError_t launch_copy_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows, int row_bytes, bool scatter,
+                            hipStream_t s);
+
+// Split rows of qkv [n][q_elems + 2 kv_elems] into q [.][q_elems], k and v
+// [.][kv_elems] at rows[i].
+hipError_t launch_scatter_qkv(const void* qkv, const int32_t* rows, int64_t n, int q_elems, int kv_elems, void* q,
+                              void* k, void* v, hipStream_t s);
+
+// y[i] = RMSNorm(x[sel[i]]) * gain (sel null = identity), hidden <= 8192, a multiple of 8.
+hipError_t launch_rmsnorm(const void* x, const int32_t* sel, const void* gain, void* y, int64_t n_rows, int hidden,
+                          float eps, hipStream_t s);
+
+// act[i] = silu(gu[i][0:ffn]) * gu[i][ffn:2 ffn].
+hipError_t launch_swiglu(const void* gu, void* act, int64_t n, int ffn, hipStream_t s);
+
+// LM head over nq (1, 2, 4 or 8) rows of nf [nq][hidden]: partial logits per chunk
+// of the hidden dimension into part [lm_head_chunks(hidden)][nq][vocab] (fp32).
+// launch_argmax sums the chunks (in chunk order) for the first n_rows rows into
+// logits [n_rows][vocab] (optional) and writes their argmax, lowest id on ties,
+// to token [n_rows].
+int lm_head_chunks(int hidden);
+hipError_t launch_lm_head(const void* nf, const void* w, float* part, int nq, int hidden, int vocab, hipStream_t s);
+hipError_t launch_argmax(const float* part, int nq, int n_rows, int hidden, int vocab, float* logits, int32_t* token,
+                         hipStream_t s);
+
+}  // namespace spanq

@@ -1,0 +1,284 @@
+// Kernels of the decoder stack around span attention (bf16 activations, fp32
+// arithmetic).  All of them are HBM-bound element or row operations; they move
+// 16-byte vectors of eight bf16 values so that every wave's accesses are whole
+// 1 KiB runs.  The GEMMs of the stack go to hipBLASLt (stack.cpp).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "stack_kernels.h"
+
+namespace spanq {
+namespace {
+
+using u16 = unsigned short;
+
+__device__ __forceinline__ float bf(u16 b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// float to bf16 bits, round to nearest even (finite inputs)
+__device__ __forceinline__ u16 to_bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<u16>(u >> 16);
+}
+
+__device__ __forceinline__ void unpack8(const uint4& v, float* f) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ uint4 pack8(const float* f) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = static_cast<uint32_t>(to_bf(f[2 * i])) | (static_cast<uint32_t>(to_bf(f[2 * i + 1])) << 16);
+  return uint4{w[0], w[1], w[2], w[3]};
+}
+
+// dst[i] = src[idx[i]] (gather, scatter = false) or dst[idx[i]] = src[i] (scatter), rows
+// of vec16 16-byte vectors; idx == nullptr is the identity.
+__global__ void copy_rows_kernel(uint4* __restrict__ dst, const uint4* __restrict__ src, const int32_t* __restrict__ idx,
+                                 int64_t n_rows, int vec16, bool scatter) {
+  const int64_t total = n_rows * vec16;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t i = e / vec16;
+    const int c = static_cast<int>(e - i * vec16);
+    const int64_t r = idx ? static_cast<int64_t>(idx[i]) : i;
+    if (scatter) {
+      dst[r * vec16 + c] = src[e];
+    } else {
+      dst[e] = src[r * vec16 + c];
+    }
+  }
+}
+
+// Split each row of qkv [T][(Hq + 2 Hkv) d] into q, k, v at caller row rows[i].
+__global__ void scatter_qkv_kernel(const uint4* __restrict__ qkv, const int32_t* __restrict__ rows, int64_t n,
+                                   int vq, int vkv, uint4* __restrict__ q, uint4* __restrict__ k,
+                                   uint4* __restrict__ v) {
+  const int vrow = vq + 2 * vkv;
+  const int64_t total = n * vrow;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t i = e / vrow;
+    const int c = static_cast<int>(e - i * vrow);
+    const int64_t r = rows[i];
+    const uint4 x = qkv[e];
+    if (c < vq) {
+      q[r * vq + c] = x;
+    } else if (c < vq + vkv) {
+      k[r * vkv + (c - vq)] = x;
+    } else {
+      v[r * vkv + (c - vq - vkv)] = x;
+    }
+  }
+}
+
+constexpr int kNormThreads = 256;
+constexpr int kNormVec = 4;  // 16-byte vectors per thread: hidden <= 256 * 4 * 8 = 8192
+
+// y[i] = x[sel[i]] / sqrt(mean(x^2) + eps) * gain, one work-group per row.
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const uint4* __restrict__ x,
+                                                               const int32_t* __restrict__ sel,
+                                                               const uint4* __restrict__ gain, uint4* __restrict__ y,
+                                                               int vec16, float eps) {
+  __shared__ float part[kNormThreads / 64];
+  const int64_t row = blockIdx.x;
+  const int64_t src = sel ? static_cast<int64_t>(sel[row]) : row;
+  float f[kNormVec][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int c = threadIdx.x + j * kNormThreads;
+    if (c < vec16) {
+      unpack8(x[src * vec16 + c], f[j]);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) ss = fmaf(f[j][t], f[j][t], ss);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormThreads / 64; ++w) tot += part[w];
+  const float scale = 1.0f / sqrtf(tot / static_cast<float>(vec16 * 8) + eps);
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int c = threadIdx.x + j * kNormThreads;
+    if (c < vec16) {
+      float g[8], o[8];
+      unpack8(gain[c], g);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t] = f[j][t] * scale * g[t];
+      y[row * vec16 + c] = pack8(o);
+    }
+  }
+}
+
+// act[i][j] = silu(gu[i][j]) * gu[i][F + j], silu(z) = z / (1 + e^-z).
+__global__ void swiglu_kernel(const uint4* __restrict__ gu, uint4* __restrict__ act, int64_t n, int vf) {
+  const int64_t total = n * vf;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t i = e / vf;
+    const int c = static_cast<int>(e - i * vf);
+    float g[8], u[8], o[8];
+    unpack8(gu[i * 2 * vf + c], g);
+    unpack8(gu[i * 2 * vf + vf + c], u);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = g[t] / (1.0f + expf(-g[t])) * u[t];
+    act[e] = pack8(o);
+  }
+}
+
+constexpr int kHeadThreads = 256;
+constexpr int kHeadCols = kHeadThreads * 8;  // vocab columns per work-group
+
+// Partial logits of nq rows over a chunk of the hidden dimension:
+// part[chunk][q][c] = sum over h in the chunk of n[q][h] * w[h][c].  Work-group
+// (column block, chunk); each thread owns 8 consecutive columns.
+template <int NQ>
+__global__ __launch_bounds__(kHeadThreads) void lm_head_kernel(const u16* __restrict__ n, const uint4* __restrict__ w,
+                                                               float* __restrict__ part, int hidden, int vocab,
+                                                               int chunk_rows) {
+  const int col0 = blockIdx.x * kHeadCols + threadIdx.x * 8;
+  const int h0 = blockIdx.y * chunk_rows;
+  const int h1 = min(hidden, h0 + chunk_rows);
+  float acc[NQ][8];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[q][t] = 0.f;
+  if (col0 < vocab) {
+    const int vrow = vocab / 8;
+    for (int h = h0; h < h1; ++h) {
+      float f[8];
+      unpack8(w[static_cast<int64_t>(h) * vrow + col0 / 8], f);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const float a = bf(n[static_cast<int64_t>(q) * hidden + h]);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[q][t] = fmaf(a, f[t], acc[q][t]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      float* p = part + (static_cast<int64_t>(blockIdx.y) * NQ + q) * vocab + col0;
+      *reinterpret_cast<float4*>(p) = float4{acc[q][0], acc[q][1], acc[q][2], acc[q][3]};
+      *reinterpret_cast<float4*>(p + 4) = float4{acc[q][4], acc[q][5], acc[q][6], acc[q][7]};
+    }
+  }
+}
+
+// Logits = the chunks' partials summed in chunk order; token = argmax, lowest id on
+// ties.  One work-group per row.
+__global__ __launch_bounds__(kHeadThreads) void argmax_kernel(const float* __restrict__ part, int n_chunks, int nq,
+                                                              int vocab, float* __restrict__ logits,
+                                                              int32_t* __restrict__ token) {
+  // nq is the partials' row stride; the grid covers only the rows wanted
+  __shared__ float bv[kHeadThreads];
+  __shared__ int bi[kHeadThreads];
+  const int q = blockIdx.x;
+  float best = -INFINITY;
+  int arg = 0x7fffffff;
+  for (int c = threadIdx.x; c < vocab; c += kHeadThreads) {
+    float s = 0.f;
+    for (int k = 0; k < n_chunks; ++k) s += part[(static_cast<int64_t>(k) * nq + q) * vocab + c];
+    if (logits) logits[static_cast<int64_t>(q) * vocab + c] = s;
+    if (s > best) {  // columns rise along the loop: a later equal value keeps the lower id
+      best = s;
+      arg = c;
+    }
+  }
+  bv[threadIdx.x] = best;
+  bi[threadIdx.x] = arg;
+  __syncthreads();
+  for (int off = kHeadThreads / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off) {
+      const float ov = bv[threadIdx.x + off];
+      const int oi = bi[threadIdx.x + off];
+      if (ov > bv[threadIdx.x] || (ov == bv[threadIdx.x] && oi < bi[threadIdx.x])) {
+        bv[threadIdx.x] = ov;
+        bi[threadIdx.x] = oi;
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) token[q] = bi[0];
+}
+
+int grid_for(int64_t items, int threads) {
+  int64_t g = (items + threads - 1) / threads;
+  if (g > 65536) g = 65536;
+  return static_cast<int>(g < 1 ? 1 : g);
+}
+
+}  // namespace
+
+hipError_t launch_copy_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows, int row_bytes, bool scatter,
+                            hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  const int vec16 = row_bytes / 16;
+  copy_rows_kernel<<<grid_for(n_rows * vec16, 256), 256, 0, s>>>(static_cast<uint4*>(dst),
+                                                                 static_cast<const uint4*>(src), idx, n_rows, vec16,
+                                                                 scatter);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_qkv(const void* qkv, const int32_t* rows, int64_t n, int q_elems, int kv_elems, void* q,
+                              void* k, void* v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int vq = q_elems / 8, vkv = kv_elems / 8;
+  scatter_qkv_kernel<<<grid_for(n * (vq + 2 * vkv), 256), 256, 0, s>>>(
+      static_cast<const uint4*>(qkv), rows, n, vq, vkv, static_cast<uint4*>(q), static_cast<uint4*>(k),
+      static_cast<uint4*>(v));
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const void* x, const int32_t* sel, const void* gain, void* y, int64_t n_rows, int hidden,
+                          float eps, hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  rmsnorm_kernel<<<static_cast<unsigned>(n_rows), kNormThreads, 0, s>>>(
+      static_cast<const uint4*>(x), sel, static_cast<const uint4*>(gain), static_cast<uint4*>(y), hidden / 8, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu(const void* gu, void* act, int64_t n, int ffn, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int vf = ffn / 8;
+  swiglu_kernel<<<grid_for(n * vf, 256), 256, 0, s>>>(static_cast<const uint4*>(gu), static_cast<uint4*>(act), n, vf);
+  return hipGetLastError();
+}
+
+int lm_head_chunks(int hidden) { return hidden >= 2048 ? 8 : 1; }
+
+hipError_t launch_lm_head(const void* nf, const void* w, float* part, int nq, int hidden, int vocab, hipStream_t s) {
+  const int chunks = lm_head_chunks(hidden);
+  const int rows = (hidden + chunks - 1) / chunks;
+  const dim3 grid((vocab + kHeadCols - 1) / kHeadCols, chunks);
+  const u16* n = static_cast<const u16*>(nf);
+  const uint4* wv = static_cast<const uint4*>(w);
+  switch (nq) {
+    case 1: lm_head_kernel<1><<<grid, kHeadThreads, 0, s>>>(n, wv, part, hidden, vocab, rows); break;
+    case 2: lm_head_kernel<2><<<grid, kHeadThreads, 0, s>>>(n, wv, part, hidden, vocab, rows); break;
+    case 4: lm_head_kernel<4><<<grid, kHeadThreads, 0, s>>>(n, wv, part, hidden, vocab, rows); break;
+    case 8: lm_head_kernel<8><<<grid, kHeadThreads, 0, s>>>(n, wv, part, hidden, vocab, rows); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax(const float* part, int nq, int n_rows, int hidden, int vocab, float* logits, int32_t* token,
+                         hipStream_t s) {
+  if (n_rows < 1 || n_rows > nq) return hipErrorInvalidValue;
+  argmax_kernel<<<n_rows, kHeadThreads, 0, s>>>(part, lm_head_chunks(hidden), nq, vocab, logits, token);
+  return hipGetLastError();
+}
+
+}  // namespace spanq

@@ -157,3 +157,100 @@ def assert_tables_match(plan, res, batch):
         ids, nh = plan.block_table(qi, len(q.frags))
         assert ids == qr.cross.page_ids and nh == 0
     assert plan.evicted() == res.evicted
+
+
+# ---------------------------------------------------------------- decoder stacks
+
+class _Bf16Layers:
+    """Per-layer bf16 bit arrays seen as float32 one layer at a time (the oracle
+    converts each to float64 when it uses it)."""
+
+    def __init__(self, arrs):
+        self.arrs = arrs
+
+    def __len__(self):
+        return len(self.arrs)
+
+    def __getitem__(self, l):
+        return (self.arrs[l].astype(np.uint32) << 16).view(np.float32)
+
+
+def oracle_weights(sw):
+    from oracle import stack as OS
+    f = lambda a: (a.astype(np.uint32) << 16).view(np.float32)  # noqa: E731
+    return OS.Weights(embed=f(sw.embed), attn_norm=_Bf16Layers(sw.attn_norm), w_qkv=_Bf16Layers(sw.w_qkv),
+                      w_o=_Bf16Layers(sw.w_o), ffn_norm=_Bf16Layers(sw.ffn_norm), w_gate_up=_Bf16Layers(sw.w_gate_up),
+                      w_down=_Bf16Layers(sw.w_down), final_norm=f(sw.final_norm), lm_head=f(sw.lm_head),
+                      n_q_heads=sw.n_q_heads, n_kv_heads=sw.n_kv_heads, head_dim=sw.head_dim)
+
+
+def stack_oracle(swl, query, keep, rows=None, Wt=None):
+    """Oracle hidden states of one query: {layer count: {caller row: [hidden]}} for the
+    counts in keep, and the float64 logits of its last cross row when the last count
+    is the whole stack and the query has a cross segment."""
+    from oracle import attention as OA
+    from oracle import stack as OS
+    Wt = Wt if Wt is not None else oracle_weights(swl.weights)
+    toks = OS.query_tokens(query.prefix.tokens, [f.tokens for f in query.frags], query.cross.tokens)
+    lay = OA.layout(query.prefix.n, [f.n for f in query.frags], query.cross.n)
+    hs = OS.stack_forward(toks, lay, Wt, max(keep), swl.rope_theta, swl.rms_eps, storage="bf16", keep=list(keep))
+    qrows = query_rows(query)
+    want = set(int(r) for r in (qrows if rows is None else rows))
+    out = {L: {int(r): hs[L][i] for i, r in enumerate(qrows) if int(r) in want} for L in keep}
+    logits = None
+    if max(keep) == swl.weights.n_layers and query.cross.n > 0:
+        logits = OS.final_logits(hs[max(keep)][-1], Wt, swl.rms_eps, storage="bf16")
+    return out, logits
+
+
+class StackRun:
+    """A pool and a decoder stack on cuda:0 for a stack workload."""
+
+    def __init__(self, swl, num_pages=None, timing=False, kernel="auto"):
+        import torch
+
+        import paper_2511_02749_amd as spanq
+        self.torch = torch
+        self.swl = swl
+        sw = swl.weights
+        if num_pages is None:
+            num_pages = 64 + sum(
+                (q.prefix.n + 15) // 16 + sum((f.n + 15) // 16 for f in q.frags) + (q.cross.n + 15) // 16
+                for b in swl.batches for q in b)
+        self.pool = spanq.Pool(num_q_heads=sw.n_q_heads, num_kv_heads=sw.n_kv_heads, head_dim=sw.head_dim,
+                               num_pages=num_pages, dtype="bf16", rope_theta=swl.rope_theta, num_layers=sw.n_layers,
+                               timing=timing, kernel=kernel, device=0)
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()  # noqa: E731
+        self.w = dict(embed=dev(sw.embed), final_norm=dev(sw.final_norm), lm_head=dev(sw.lm_head),
+                      attn_norm=[dev(a) for a in sw.attn_norm], w_qkv=[dev(a) for a in sw.w_qkv],
+                      w_o=[dev(a) for a in sw.w_o], ffn_norm=[dev(a) for a in sw.ffn_norm],
+                      w_gate_up=[dev(a) for a in sw.w_gate_up], w_down=[dev(a) for a in sw.w_down])
+        self.model = spanq.Model(self.pool, hidden=sw.hidden, ffn=sw.ffn, vocab=sw.vocab, rms_eps=swl.rms_eps,
+                                 **self.w)
+        self.n_rows = int(swl.row_tokens.shape[0])
+        self.hidden = torch.zeros((self.n_rows, sw.hidden), dtype=torch.int16, device="cuda")
+
+    def run(self, batch, n_layers=None, commit=True, logits=True):
+        """Plan a batch and run it through the stack; returns (plan, first tokens,
+        logits [queries with cross][vocab] float32 or None)."""
+        torch = self.torch
+        plan = self.pool.plan(batch)
+        n_cross = sum(1 for q in batch if q.cross.n > 0)
+        lg = None
+        full = n_layers is None or n_layers == self.swl.weights.n_layers
+        if logits and full and n_cross:
+            lg = torch.zeros((n_cross, self.swl.weights.vocab), dtype=torch.float32, device="cuda")
+        toks = self.model.forward(plan, self.swl.row_tokens, n_layers=n_layers, hidden_out=self.hidden,
+                                  logits_out=lg, first_tokens=full)
+        torch.cuda.synchronize()
+        if commit:
+            plan.commit()
+        return plan, toks, (lg.cpu().numpy() if lg is not None else None)
+
+    def hidden_rows(self, rows) -> np.ndarray:
+        h = self.hidden[self.torch.as_tensor(np.asarray(rows, np.int64), device="cuda")].cpu().numpy()
+        return (h.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+    def close(self):
+        self.model.close()
+        self.pool.close()
