@@ -79,19 +79,48 @@ class PlanResult:
 
 
 class PoolReplay:
-    def __init__(self, num_pages: int, page_size: int = 16, stock: bool = False):
+    """Replay of the page cache.  The eviction victim is the evictable page with the
+    smallest key (last use, -index in span, page id).  ``brute_force`` takes that
+    minimum over every evictable page at each eviction (the rule as stated); the
+    default pops it from a heap of keys with stale entries skipped, which gives the
+    same victims (pinned against brute force in the tests) in time fit for long
+    streams."""
+
+    def __init__(self, num_pages: int, page_size: int = 16, stock: bool = False, brute_force: bool = False):
         self.num_pages = num_pages
         self.page_size = page_size
         self.stock = stock
+        self.brute_force = brute_force
         self.free: List[int] = list(range(num_pages))
         heapq.heapify(self.free)
         self.index: Dict[int, int] = {}
         self.pages: Dict[int, PageInfo] = {}
         self.tick = 0
+        self.evictable_keys: Dict[int, tuple] = {}   # published, unpinned pages -> their key
+        self._heap: List[tuple] = []
 
     # --- helpers -------------------------------------------------------
     def _evictable(self):
-        return [p for p in self.pages.values() if p.published and p.pins == 0]
+        return [self.pages[pid] for pid in self.evictable_keys]
+
+    def _refresh(self, p: PageInfo):
+        """Record whether p is evictable (published and unpinned), with its current key."""
+        if p.published and p.pins == 0:
+            key = (p.last_use, -p.idx, p.page_id)
+            if self.evictable_keys.get(p.page_id) != key:
+                self.evictable_keys[p.page_id] = key
+                heapq.heappush(self._heap, key)
+        else:
+            self.evictable_keys.pop(p.page_id, None)
+
+    def _victim(self) -> int:
+        if self.brute_force:
+            return min(self.evictable_keys.values())[2]
+        while True:
+            key = self._heap[0]
+            if self.evictable_keys.get(key[2]) == key:
+                return key[2]
+            heapq.heappop(self._heap)
 
     def _lookup(self, h: int, parent: int, toks: tuple, idx: int) -> Optional[int]:
         pid = self.index.get(h)
@@ -165,9 +194,9 @@ class PoolReplay:
                     if kind == "hit" and x not in hit_pids:
                         hit_pids.append(x)
         need = len(new_specs)
-        evictable = [p for p in self._evictable() if p.page_id not in hit_pids]
-        if need > len(self.free) + len(evictable):
-            raise PoolFull(f"need {need} pages, {len(self.free)} free, {len(evictable)} evictable")
+        n_evictable = len(self.evictable_keys) - sum(1 for pid in hit_pids if pid in self.evictable_keys)
+        if need > len(self.free) + n_evictable:
+            raise PoolFull(f"need {need} pages, {len(self.free)} free, {n_evictable} evictable")
 
         # mutate
         self.tick = tick
@@ -175,6 +204,7 @@ class PoolReplay:
             p = self.pages[pid]
             p.pins += 1
             p.last_use = tick
+            self._refresh(p)
         evicted = []
         slot_pid: Dict[int, int] = {}
         order = []
@@ -186,8 +216,8 @@ class PoolReplay:
             order.extend(cross_slots)
         for slot in order:
             if not self.free:
-                victims = self._evictable()
-                v = min(victims, key=lambda p: (p.last_use, -p.idx, p.page_id))
+                v = self.pages[self._victim()]
+                del self.evictable_keys[v.page_id]
                 del self.index[v.hash]
                 del self.pages[v.page_id]
                 evicted.append(v.page_id)
@@ -235,8 +265,11 @@ class PoolReplay:
             if not p.published:
                 del self.pages[pid]
                 heapq.heappush(self.free, pid)
+            else:
+                self._refresh(p)
         for pid in plan.hits:
             self.pages[pid].pins -= 1
+            self._refresh(self.pages[pid])
         plan.committed = True
 
     def destroy(self, plan: PlanResult):
@@ -248,6 +281,7 @@ class PoolReplay:
             heapq.heappush(self.free, pid)
         for pid in plan.hits:
             self.pages[pid].pins -= 1
+            self._refresh(self.pages[pid])
         plan.destroyed = True
 
     def cached_pages(self) -> int:

@@ -156,3 +156,43 @@ def test_lru_stream_properties(seed):
             pool.destroy(r)
         _survivors_are_prefixes(pool)
         assert len(pool.free) + len(pool.pages) == pool.num_pages
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_heap_victims_equal_brute_force(seed):
+    """The heap-based victim search returns what the rule's definition (the minimum
+    key over all evictable pages) returns, on streams with many evictions."""
+    rnd = random.Random(100 + seed)
+    ps = 4
+    prefixes = [[rnd.randrange(40) for _ in range(rnd.randrange(0, 9))] for _ in range(3)]
+    frags = [[rnd.randrange(40) for _ in range(rnd.randrange(1, 18))] for _ in range(12)]
+    n_pages = rnd.randrange(10, 24)
+    fast, slow = PoolReplay(n_pages, ps), PoolReplay(n_pages, ps, brute_force=True)
+    evictions = 0
+    for step in range(120):
+        qs = []
+        for _ in range(rnd.randrange(1, 3)):
+            chosen = rnd.sample(range(12), rnd.randrange(0, 4))
+            qs.append((prefixes[rnd.randrange(3)], [frags[i] for i in chosen],
+                       [rnd.randrange(40) for _ in range(rnd.randrange(0, 6))]))
+        outs = []
+        for pool in (fast, slow):
+            try:
+                outs.append(pool.plan(qs))
+            except PoolFull:
+                outs.append(None)
+        a, b = outs
+        assert (a is None) == (b is None)
+        if a is None:
+            continue
+        assert a.evicted == b.evicted and a.new_pages == b.new_pages and a.hits == b.hits
+        for qa, qb in zip(a.queries, b.queries):
+            assert qa == qb
+        evictions += len(a.evicted)
+        if rnd.random() < 0.85:
+            fast.commit(a)
+            slow.commit(b)
+        else:
+            fast.destroy(a)
+            slow.destroy(b)
+    assert evictions > 20

@@ -438,3 +438,60 @@ def config_c4(seed: int = 0, n_layers: int = 32) -> StackWorkload:
     batches, rt = stack_queries(seed, VOCAB, 512, [1024] * 32, 256, [list(range(32))])
     return StackWorkload(name="c4", weights=w, batches=batches, row_tokens=rt,
                          meta=dict(prefix_len=512, n_frags=32, frag_len=1024, cross_len=256))
+
+
+KIND_C5 = 11
+
+
+@dataclass
+class StreamQuery:
+    """One query of a stream: its spans (rows numbered from 0 within the query:
+    prefix, fragments in order, cross) and the token id at each of those rows."""
+    query: Query
+    row_tokens: np.ndarray
+    frag_ids: List[int]
+
+
+def c5_stream(seed: int = 0, n_queries: int = 256, pool_size: int = 1024, len_lo: int = 128, len_hi: int = 2048,
+              zipf_s: float = 1.1, k_lo: int = 4, k_hi: int = 24, prefix_len: int = 256, cross_len: int = 128,
+              vocab: int = VOCAB) -> List[StreamQuery]:
+    """Agentic stream: a pool of fragments with lengths uniform on [len_lo, len_hi];
+    fragment popularity Zipf(zipf_s) over ranks, ranks mapped to fragments by a seeded
+    permutation; each query draws k ~ U{k_lo..k_hi} distinct fragments with
+    probability proportional to popularity (without replacement; draw order = the
+    query's order), behind one shared prefix, with its own cross segment."""
+    g = rng(seed, KIND_C5, 0)
+    lens = g.integers(len_lo, len_hi + 1, size=pool_size)
+    perm = rng(seed, KIND_C5, 1).permutation(pool_size)
+    pop = np.empty(pool_size, np.float64)
+    pop[perm] = np.arange(1, pool_size + 1, dtype=np.float64) ** -zipf_s
+    pop /= pop.sum()
+    tok = lambda kind, i, n: rng(seed, KIND_C5, 1_000_000 * kind + i).integers(  # noqa: E731
+        0, vocab, size=int(n), dtype=np.int64).astype(np.int32)
+    prefix_tokens = tok(KIND_PREFIX, 0, prefix_len)
+    frag_tokens = {}
+    out = []
+    for qi in range(n_queries):
+        gq = rng(seed, KIND_C5, 2_000_000 + qi)
+        k = int(gq.integers(k_lo, k_hi + 1))
+        ids = [int(x) for x in gq.choice(pool_size, size=k, replace=False, p=pop)]
+        at = 0
+        prefix = Span(tokens=prefix_tokens, row=at)
+        at += prefix_len
+        frags = []
+        for f in ids:
+            if f not in frag_tokens:
+                frag_tokens[f] = tok(KIND_FRAG, f, lens[f])
+            frags.append(Span(tokens=frag_tokens[f], row=at))
+            at += frag_tokens[f].shape[0]
+        cross = Span(tokens=tok(KIND_CROSS, qi, cross_len), row=at)
+        at += cross_len
+        rt = np.concatenate([prefix.tokens] + [s.tokens for s in frags] + [cross.tokens]).astype(np.int32)
+        out.append(StreamQuery(query=Query(prefix=prefix, frags=frags, cross=cross), row_tokens=rt, frag_ids=ids))
+    return out
+
+
+def llama3_8b_weights(seed: int = 0, n_layers: int = 32, threads: int = 16) -> StackWeights:
+    """Llama-3-8B-shaped random-init weights: hidden 4096, 32 query / 8 kv heads x 128,
+    SwiGLU 14336, vocab 128256."""
+    return stack_weights(seed, n_layers, 4096, 32, 8, 128, 14336, VOCAB, threads=threads)
