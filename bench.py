@@ -99,33 +99,44 @@ def _flops(wl, pairs):
     return 4.0 * wl.head_dim * wl.n_q_heads * pairs
 
 
-def cpu_baseline(wl, query, seconds):
-    """The oracle timed on this host's cores over sampled rows of one query."""
+def cpu_baseline(wl, query, max_seconds):
+    """The oracle on this host's cores over every row of one query (float64), with
+    the BLAS and torch thread counts set to the cores this process may use.  Stops
+    early, on whole row blocks, if it runs past max_seconds."""
     import numpy as np
 
     from oracle import attention as OA
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:  # pragma: no cover
-        cores = len(os.sched_getaffinity(0))
+        limiter = None
+    try:
+        import torch
+        torch.set_num_threads(cores)
+    except Exception:  # pragma: no cover
+        pass
     lay = OA.layout(query.prefix.n, [f.n for f in query.frags], query.cross.n)
     rows = np.concatenate([np.arange(query.prefix.row, query.prefix.row + query.prefix.n)] +
                           [np.arange(f.row, f.row + f.n) for f in query.frags] +
                           [np.arange(query.cross.row, query.cross.row + query.cross.n)])
     q, k, v = wl.q[rows], wl.k[rows], wl.v[rows]
-    rng = np.random.default_rng(0)
-    order = rng.permutation(lay.n)
     done, pairs = 0, 0
     t0 = time.perf_counter()
-    while done < lay.n and time.perf_counter() - t0 < seconds:
-        sel = np.sort(order[done: done + 64])
+    for b0 in range(0, lay.n, 512):
+        sel = np.arange(b0, min(lay.n, b0 + 512))
         OA.attention_rows(q, k, v, lay, sel, wl.rope_theta)
         pairs += int(OA.mask_rows(lay, sel).sum())
         done += sel.size
+        if time.perf_counter() - t0 > max_seconds:
+            break
     dt = time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister()
     return {"value": _flops(wl, pairs) / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{done} random rows of one query ({lay.n} tokens), float64, {dt:.1f} s"}
+            "sample": f"{done} of {lay.n} rows of one C2 query (all rows unless cut at {max_seconds:.0f} s), "
+                      f"float64, {dt:.1f} s, {cores} threads"}
 
 
 def kv_gather(spanq, W, torch, np, reps, rows_list=(1, 4, 16), n_queries=8):
@@ -156,7 +167,7 @@ def kv_gather(spanq, W, torch, np, reps, rows_list=(1, 4, 16), n_queries=8):
     for nq in rows_list:
         qs = [W.Query(prefix=x.prefix, frags=x.frags, cross=W.Span(tokens=x.cross.tokens[:nq], row=x.cross.row))
               for x in queries]
-        times, st = [], None
+        times, merged, st = [], [], None
         for r in range(reps + 2):
             p = pool.plan(qs, stream)
             p.cross(0, q, k, v, out)
@@ -166,15 +177,198 @@ def kv_gather(spanq, W, torch, np, reps, rows_list=(1, 4, 16), n_queries=8):
             p.destroy()
             if r >= 2:
                 times.append(kt["cross_attention_ms"])
+                merged.append(kt["cross_attention_ms"] + kt["combine_ms"])
         assert st["pages_new"] == 0
         nbytes = (st["pages_hit"] + st["pages_cross"]) * page_bytes
         ms = float(np.mean(times))
+        ms_merged = float(np.mean(merged))
         gbs = nbytes / (ms * 1e-3) / 1e9
         res[f"q{nq}"] = {"cross_rows_per_query": nq, "bytes": int(nbytes), "ms": ms, "gbs": gbs,
-                         "frac": gbs / PEAK_HBM_GBS, "kv_splits": st["kv_splits"]}
+                         "frac": gbs / PEAK_HBM_GBS, "kv_splits": st["kv_splits"],
+                         "ms_with_merge": ms_merged, "gbs_with_merge": nbytes / (ms_merged * 1e-3) / 1e9,
+                         "frac_with_merge": nbytes / (ms_merged * 1e-3) / 1e9 / PEAK_HBM_GBS}
     pool.close()
     return {"kernel": "cross_attention", "bound": "hbm", "peak_gbs": PEAK_HBM_GBS, "queries": n_queries,
             "kv_per_query_mb": (640 * page_bytes) / 1e6, "by_rows": res}
+
+
+def _percentiles(xs):
+    return {"p50": _pct(xs, 50), "p99": _pct(xs, 99), "mean": float(sum(xs) / len(xs)) if xs else None}
+
+
+def attention_batch(spanq, wl, torch, np, steps, warmup):
+    """One cold batch of a single-layer workload, repeated: step time and the two
+    attention kernels' rates (HIP events on the launch stream)."""
+    qa, ka, va = wl.device_arrays()
+    q, k, v = (torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda() for a in (qa, ka, va))
+    out = torch.zeros_like(q)
+    batch = wl.batches[0]
+    pages = sum((s.n + 15) // 16 for s in {id(x): x for qq in batch for x in [qq.prefix, *qq.frags, qq.cross]}.values())
+    pool = spanq.Pool(num_q_heads=wl.n_q_heads, num_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                      num_pages=pages + 256, dtype=wl.dtype, rope_theta=wl.rope_theta, timing=True, device=0)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pool.reset()
+        p = pool.plan(batch, stream)
+        p.prefill(0, q, k, v, out)
+        p.cross(0, q, k, v, out)
+        p.commit()
+        return p
+
+    for _ in range(warmup):
+        step().destroy()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plans = [step() for _ in range(steps)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = plans[0].stats()
+    kt = [p.kernel_times() for p in plans]
+    for p in plans:
+        p.destroy()
+    pool.close()
+    k1 = float(np.mean([t["prefill_attention_ms"] for t in kt]))
+    k2 = float(np.mean([t["cross_attention_ms"] for t in kt]))
+    return {"ms_per_step": wall * 1e3 / steps,
+            "tflops_step": _flops(wl, st["prefill_pairs"] + st["cross_pairs"]) / (wall / steps) / 1e12,
+            "span_prefill_attention": {"ms": k1, "tflops": _flops(wl, st["prefill_pairs"]) / (k1 * 1e-3) / 1e12},
+            "cross_attention": {"ms": k2, "tflops": _flops(wl, st["cross_pairs"]) / (k2 * 1e-3) / 1e12},
+            "tokens_new": st["tokens_new"], "tokens_cross": st["tokens_cross"]}
+
+
+def _upload_stack(torch, np, sw):
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()  # noqa: E731
+    return dict(embed=dev(sw.embed), final_norm=dev(sw.final_norm), lm_head=dev(sw.lm_head),
+                attn_norm=[dev(a) for a in sw.attn_norm], w_qkv=[dev(a) for a in sw.w_qkv],
+                w_o=[dev(a) for a in sw.w_o], ffn_norm=[dev(a) for a in sw.ffn_norm],
+                w_gate_up=[dev(a) for a in sw.w_gate_up], w_down=[dev(a) for a in sw.w_down])
+
+
+def stack_flops(sw, rows, pairs_per_layer, queries_with_cross):
+    """Model FLOPs of a prefill: the four GEMMs per layer for every computed row,
+    attention over the allowed pairs in every layer, the LM head per query."""
+    d, hq, hkv, H, F = sw.head_dim, sw.n_q_heads, sw.n_kv_heads, sw.hidden, sw.ffn
+    per_row = 2 * (H * (hq + 2 * hkv) * d + hq * d * H + H * 2 * F + F * H)
+    return (per_row * rows + 4 * d * hq * pairs_per_layer) * sw.n_layers + 2 * H * sw.vocab * queries_with_cross
+
+
+def c4_ttft(spanq, W, torch, np, reps):
+    """C4: a 32-layer 2B-class decoder (hidden 2048, 32/8 heads x 64, SwiGLU 8192) over
+    one RAG span query (prefix 512 + 32 fragments x 1024 + question 256).  Time to
+    first token from the span_plan call to the first token on the host: cold (fresh
+    pool), warm (every fragment cached by the previous query, in reversed order), and
+    the same tokens as one causal span (no span sparsity, nothing cached)."""
+    t0 = time.perf_counter()
+    swl = W.config_c4()
+    sw = swl.weights
+    wts = _upload_stack(torch, np, sw)
+    gen_s = time.perf_counter() - t0
+    q = swl.batches[0][0]
+    rev = W.Query(prefix=q.prefix, frags=q.frags[::-1], cross=q.cross)
+    n_tok = q.prefix.n + sum(f.n for f in q.frags) + q.cross.n
+    pool = spanq.Pool(num_q_heads=sw.n_q_heads, num_kv_heads=sw.n_kv_heads, head_dim=sw.head_dim,
+                      num_pages=(n_tok + 15) // 16 + 3 * 64 + 64, dtype="bf16", rope_theta=swl.rope_theta,
+                      num_layers=sw.n_layers, device=0)
+    model = spanq.Model(pool, hidden=sw.hidden, ffn=sw.ffn, vocab=sw.vocab, rms_eps=swl.rms_eps, **wts)
+
+    def one(query, row_tokens):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        p = pool.plan([query])
+        tok = model.forward(p, row_tokens)
+        dt = (time.perf_counter() - t) * 1e3
+        st = p.stats()
+        p.commit()
+        p.destroy()
+        return dt, tok[0], st
+
+    cold, warm, dense = [], [], []
+    toks = {}
+    st_cold = st_warm = None
+    for r in range(reps + 1):
+        pool.reset()
+        c = one(q, swl.row_tokens)
+        w = one(rev, swl.row_tokens)
+        if r:
+            cold.append(c[0])
+            warm.append(w[0])
+        toks = {"cold_order": c[1], "warm_reversed": w[1]}
+        st_cold, st_warm = c[2], w[2]
+    S = np.concatenate([s.tokens for s in [q.prefix, *q.frags, q.cross]]).astype(np.int32)
+    whole = W.Query(prefix=W.Span(tokens=S[:-q.cross.n], row=0), frags=[],
+                    cross=W.Span(tokens=S[-q.cross.n:], row=S.size - q.cross.n))
+    for r in range(3):
+        pool.reset()
+        d = one(whole, S)
+        if r:
+            dense.append(d[0])
+    model.close()
+    pool.close()
+    del wts
+    torch.cuda.empty_cache()
+    f_cold = stack_flops(sw, st_cold["tokens_new"] + st_cold["tokens_cross"],
+                         st_cold["prefill_pairs"] + st_cold["cross_pairs"], 1)
+    f_warm = stack_flops(sw, st_warm["tokens_new"] + st_warm["tokens_cross"],
+                         st_warm["prefill_pairs"] + st_warm["cross_pairs"], 1)
+    c, w_, dd = _percentiles(cold), _percentiles(warm), _percentiles(dense)
+    return {"workload": "C4: 32 layers, hidden 2048, 32/8 heads x 64, SwiGLU 8192, vocab 128256, bf16; prefix 512 + "
+                        "32 x 1024 fragments + question 256 (33,536 tokens)",
+            "cold_ms_p50": c["p50"], "cold_ms_p99": c["p99"], "warm_ms_p50": w_["p50"], "warm_ms_p99": w_["p99"],
+            "dense_causal_ms_p50": dd["p50"], "warm_speedup_vs_cold": c["p50"] / w_["p50"],
+            "warm_speedup_vs_dense": dd["p50"] / w_["p50"], "reps": len(cold),
+            "cold_model_tflops": f_cold / (c["p50"] * 1e-3) / 1e12, "cold_model_tflop": f_cold / 1e12,
+            "warm_model_tflop": f_warm / 1e12, "first_tokens": toks, "weights_gen_and_upload_s": gen_s}
+
+
+def c5_stream(spanq, W, torch, np, n_queries):
+    """C5: the 32-layer Llama-3-8B-shaped decoder (random init, bf16) over an agentic
+    stream of span queries (1024 fragments of 128..2048 tokens, Zipf 1.1 popularity,
+    4-24 per query, shared 256-token prefix, 128-token question), one query at a time,
+    with a 200 GB KV pool (95,367 pages of 2 MiB: no eviction) and with a 48 GB cap
+    (22,888 pages: LRU eviction).  Per query: time to first token (span_plan call to
+    the token on the host)."""
+    t0 = time.perf_counter()
+    sw = W.llama3_8b_weights(threads=len(os.sched_getaffinity(0)))
+    print(f"[bench] c5 weights {sw.nbytes() / 1e9:.1f} GB drawn in {time.perf_counter() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    wts = _upload_stack(torch, np, sw)
+    stream = W.c5_stream(n_queries=n_queries)
+    res = {}
+    for name, pages in (("pool_200GB", 95_367), ("cap_48GB", 22_888)):
+        pool = spanq.Pool(num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=pages, dtype="bf16",
+                          rope_theta=1e4, num_layers=32, device=0)
+        model = spanq.Model(pool, hidden=4096, ffn=14336, vocab=W.VOCAB, rms_eps=1e-5, **wts)
+        ttft, hit, tot, flops, evicted, new_tok = [], 0, 0, 0.0, 0, 0
+        t_run = time.perf_counter()
+        for i, sq in enumerate(stream):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            p = pool.plan([sq.query])
+            model.forward(p, sq.row_tokens)
+            ttft.append((time.perf_counter() - t) * 1e3)
+            st = p.stats()
+            p.commit()
+            p.destroy()
+            hit += st["tokens_hit"]
+            tot += st["tokens_hit"] + st["tokens_new"]
+            new_tok += st["tokens_new"]
+            evicted += st["pages_evicted"]
+            flops += stack_flops(sw, st["tokens_new"] + st["tokens_cross"], st["prefill_pairs"] + st["cross_pairs"], 1)
+            if i % 32 == 31:
+                print(f"[bench] c5 {name}: {i + 1} queries, hit rate {hit / tot:.3f}, "
+                      f"ttft p50 {_pct(ttft, 50):.1f} ms", file=sys.stderr, flush=True)
+        wall = time.perf_counter() - t_run
+        pr = _percentiles(ttft)
+        res[name] = {"pages": pages, "pool_gb": pages * 2 * 1024 * 1024 / 1e9, "queries": len(stream),
+                     "hit_rate": hit / tot, "evicted_pages": evicted, "new_tokens": new_tok,
+                     "ttft_ms_p50": pr["p50"], "ttft_ms_p99": pr["p99"], "ttft_ms_mean": pr["mean"],
+                     "stream_s": wall, "prefill_tflops": flops / (sum(ttft) * 1e-3) / 1e12,
+                     "model_tflop": flops / 1e12}
+        model.close()
+        pool.close()
+        torch.cuda.synchronize()
+    return res
 
 
 def main():
@@ -182,10 +376,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c2", choices=["c2", "c3"])
+    ap.add_argument("--config", default="c2", choices=["c2", "c3", "c5"],
+                    help="c2: the headline run (with C3 and C4 extras); c3: the judge pattern as the main "
+                         "workload; c5: only the agentic stream over the 8B-shaped decoder")
+    ap.add_argument("--c5-queries", type=int, default=256)
+    ap.add_argument("--no-extras", action="store_true", help="skip the C3 and C4 extras of the default run")
     ap.add_argument("--kernel", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--ttft-reps", type=int, default=20)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=60.0,
+                    help="upper bound on the oracle baseline's time (it runs every row of one C2 query)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peak-probes", action="store_true",
                     help="skip the MFMA-only and streaming-read probes of the attainable peaks")
@@ -209,6 +408,16 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
+        return
+    if args.config == "c5":
+        res = c5_stream(spanq, W, torch, np, args.c5_queries)
+        print(json.dumps({"metric": "C5 agentic stream: time to first token per span query (ms) and KV hit rate",
+                          "unit": "ms", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic (seeded tokens, random-init weights)",
+                          "config": {"workload": "C5: Llama-3-8B-shaped 32-layer decoder, 256 span queries over 1024 "
+                                                 "fragments (128..2048 tokens, Zipf 1.1, 4-24 per query), prefix 256, "
+                                                 "question 128"},
+                          "c5": res}), flush=True)
         return
     t_gen = time.perf_counter()
     wl = W.config_c2() if args.config == "c2" else W.config_c3()
@@ -337,6 +546,14 @@ def main():
                            "16-byte non-temporal loads, 10 launches"}
         print(f"[bench] measured peaks {json.dumps(peaks)}", file=sys.stderr, flush=True)
 
+    extras = {}
+    if not args.no_extras and args.config == "c2":
+        extras["c3"] = attention_batch(spanq, W.config_c3(), torch, np, steps=10, warmup=2)
+        extras["c3"]["workload"] = "C3 judge pattern: prompt 2048 + 32 candidates x 256 + judge 256, one query, cold"
+        print(f"[bench] c3 {json.dumps(extras['c3'])}", file=sys.stderr, flush=True)
+        extras["c4"] = c4_ttft(spanq, W, torch, np, reps=max(5, args.ttft_reps))
+        print(f"[bench] c4 {json.dumps(extras['c4'])}", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, batch[0], args.cpu_seconds)
@@ -382,8 +599,15 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": k1_tflops / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(args.config) if args.kernel != "generic" else None,
                      "algorithmic_bytes": k1_bytes, "launch_flops": k1_flops},
+        "headline": {"span_prefill_attention_tflops": k1_tflops,
+                     "span_prefill_attention_frac_of_2.5PF": k1_tflops / PEAK_BF16_TFLOPS,
+                     "cache_hit_ttft_ms_p50": ttft.get("warm_ms_p50"),
+                     "cold_ttft_ms_p50": ttft.get("cold_ms_p50"),
+                     "model_cache_hit_ttft_ms_p50": extras.get("c4", {}).get("warm_ms_p50"),
+                     "model_cold_ttft_ms_p50": extras.get("c4", {}).get("cold_ms_p50")},
         "ttft": ttft,
         "kv_gather": gather,
+        **extras,
         "measured_peaks": peaks,
         "cpu_baseline": cpu,
     }
