@@ -286,6 +286,27 @@ int span_plan_commit(span_plan_t* plan);
  * call itself does not wait for the device. */
 int span_plan_destroy(span_plan_t* plan);
 
+/* ---------------------------------------------------------------- serialized queries */
+
+typedef struct {
+  int64_t begin;  /* first token of the span in the serialized stream */
+  int64_t n;      /* tokens (special and pad tokens excluded) */
+} span_range;
+
+/* Parse a serialized span query (sections 5.2 and 5.3, Def. 4): the token stream of
+ * G(Cross(prefix, Plus(F_1, ..., F_n), cross)) as
+ *     prefix  OPEN F_1  SEP F_2 ... SEP F_n  CLOSE pos  cross
+ * where every special token starts a block of `block` tokens, PAD tokens fill the
+ * end of the block before it, and the token after CLOSE is the position of the OPEN
+ * (so no parsing stack is needed).  special = {PAD, OPEN, SEP, CLOSE} token ids.
+ * Writes the prefix and cross ranges and up to cap fragment ranges (in order);
+ * *n_frags = the number of fragments.  A stream with no OPEN is all cross segment.
+ * SPAN_EINVAL (with the offending position in span_last_error) for a special token
+ * off a block start, inside a span or after the join, a nested join, a missing CLOSE,
+ * or a CLOSE pointing elsewhere than its OPEN. */
+int span_parse_serialized(const int32_t* tokens, int64_t n, int32_t block, const int32_t special[4],
+                          span_range* frags, int32_t cap, int32_t* n_frags, span_range* prefix, span_range* cross);
+
 /* ---------------------------------------------------------------- decoder stack */
 
 /* A decoder stack that a span query's prefill runs through (the paper's latency

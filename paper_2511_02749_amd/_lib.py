@@ -29,6 +29,7 @@ EXPORTS = [
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
+    "span_parse_serialized",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -81,6 +82,10 @@ class KernelTimes(ctypes.Structure):
                                                             ("cross_calls", ctypes.c_int32)]
 
 
+class SpanRange(ctypes.Structure):
+    _fields_ = [("begin", ctypes.c_int64), ("n", ctypes.c_int64)]
+
+
 class ModelConfig(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
@@ -126,6 +131,8 @@ def load():
         "span_model_create": (I32, [VP, P(ModelConfig), P(VP)]),
         "span_model_destroy": (I32, [VP]),
         "span_model_forward": (I32, [VP, VP, P(I32), I64, I32, VP, VP, P(I32), VP]),
+        "span_parse_serialized": (I32, [P(I32), I64, I32, P(I32), P(SpanRange), I32, P(I32), P(SpanRange),
+                                        P(SpanRange)]),
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
