@@ -326,8 +326,9 @@ def c5_stream(spanq, W, torch, np, n_queries):
     stream of span queries (1024 fragments of 128..2048 tokens, Zipf 1.1 popularity,
     4-24 per query, shared 256-token prefix, 128-token question), one query at a time,
     with a 200 GB KV pool (95,367 pages of 2 MiB: no eviction) and with a 48 GB cap
-    (22,888 pages: LRU eviction).  Per query: time to first token (span_plan call to
-    the token on the host)."""
+    (22,888 pages: LRU eviction), the latter also in the order span_bulk_order gives the
+    whole stream as one bulk (section 5.8).  Per query: time to first token (span_plan
+    call to the token on the host)."""
     t0 = time.perf_counter()
     sw = W.llama3_8b_weights(threads=len(os.sched_getaffinity(0)))
     print(f"[bench] c5 weights {sw.nbytes() / 1e9:.1f} GB drawn in {time.perf_counter() - t0:.1f} s",
@@ -335,13 +336,18 @@ def c5_stream(spanq, W, torch, np, n_queries):
     wts = _upload_stack(torch, np, sw)
     stream = W.c5_stream(n_queries=n_queries)
     res = {}
-    for name, pages in (("pool_200GB", 95_367), ("cap_48GB", 22_888)):
+    for name, pages, bulk in (("pool_200GB", 95_367, False), ("cap_48GB", 22_888, False),
+                              ("cap_48GB_bulk_clustered", 22_888, True)):
         pool = spanq.Pool(num_q_heads=32, num_kv_heads=8, head_dim=128, num_pages=pages, dtype="bf16",
                           rope_theta=1e4, num_layers=32, device=0)
         model = spanq.Model(pool, hidden=4096, ffn=14336, vocab=W.VOCAB, rms_eps=1e-5, **wts)
         ttft, hit, tot, flops, evicted, new_tok = [], 0, 0, 0.0, 0, 0
+        # the whole stream as one bulk: executed in the order span_bulk_order gives
+        t_order = time.perf_counter()
+        order = pool.bulk_order([sq.query for sq in stream]) if bulk else list(range(len(stream)))
+        order_ms = (time.perf_counter() - t_order) * 1e3
         t_run = time.perf_counter()
-        for i, sq in enumerate(stream):
+        for i, sq in enumerate(stream[j] for j in order):
             torch.cuda.synchronize()
             t = time.perf_counter()
             p = pool.plan([sq.query])
@@ -364,7 +370,8 @@ def c5_stream(spanq, W, torch, np, n_queries):
                      "hit_rate": hit / tot, "evicted_pages": evicted, "new_tokens": new_tok,
                      "ttft_ms_p50": pr["p50"], "ttft_ms_p99": pr["p99"], "ttft_ms_mean": pr["mean"],
                      "stream_s": wall, "prefill_tflops": flops / (sum(ttft) * 1e-3) / 1e12,
-                     "model_tflop": flops / 1e12}
+                     "model_tflop": flops / 1e12, "order": "bulk clustered (span_bulk_order)" if bulk else "given",
+                     "bulk_order_ms": order_ms if bulk else 0.0}
         model.close()
         pool.close()
         torch.cuda.synchronize()

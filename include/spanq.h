@@ -286,6 +286,18 @@ int span_plan_commit(span_plan_t* plan);
  * call itself does not wait for the device. */
 int span_plan_destroy(span_plan_t* plan);
 
+/* ---------------------------------------------------------------- bulk scheduling */
+
+/* An execution order for a bulk of n_queries queries that clusters fragment reuse in
+ * time (section 5.8).  Greedy: the pool is simulated at span granularity (a prefix
+ * or fragment, keyed by its page-hash chain, is resident or not; spans the pool
+ * holds in full start resident; capacity = the pool's pages); each step takes the
+ * remaining query with the most pages in resident spans (ties: the lowest index),
+ * marks its spans used and evicts least recently used spans down to the capacity.
+ * order[0 .. n_queries) receives a permutation of 0 .. n_queries - 1.  The pool is
+ * only read.  O(n_queries^2 x spans per query). */
+int span_bulk_order(const span_pool* pool, const span_query* queries, int32_t n_queries, int32_t* order);
+
 /* ---------------------------------------------------------------- serialized queries */
 
 typedef struct {

@@ -29,7 +29,7 @@ EXPORTS = [
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
-    "span_parse_serialized",
+    "span_parse_serialized", "span_bulk_order",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -131,6 +131,7 @@ def load():
         "span_model_create": (I32, [VP, P(ModelConfig), P(VP)]),
         "span_model_destroy": (I32, [VP]),
         "span_model_forward": (I32, [VP, VP, P(I32), I64, I32, VP, VP, P(I32), VP]),
+        "span_bulk_order": (I32, [VP, P(SpanQuery), I32, P(I32)]),
         "span_parse_serialized": (I32, [P(I32), I64, I32, P(I32), P(SpanRange), I32, P(I32), P(SpanRange),
                                         P(SpanRange)]),
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
@@ -272,6 +273,15 @@ class Pool:
         _check(load().span_pool_read_page(self._h, layer, page_id, buf.ctypes.data, buf.nbytes))
         return buf
 
+    def bulk_order(self, queries: Iterable) -> List[int]:
+        """Execution order clustering fragment reuse (span_bulk_order)."""
+        qs = list(queries)
+        keep: list = []
+        arr = _query_array(qs, keep)
+        order = np.zeros(max(1, len(qs)), np.int32)
+        _check(load().span_bulk_order(self._h, arr, len(qs), _i32p(order)))
+        return [int(x) for x in order[: len(qs)]]
+
     def plan(self, queries: Iterable, stream=None, static: bool = False) -> "Plan":
         """queries: objects with .prefix, .frags, .cross; each span has .tokens (int32) and .row.
         static=True plans through span_plan_static (no device allocation)."""
@@ -286,17 +296,22 @@ def _span(s, keep: list) -> SpanTokens:
     return SpanTokens(t.ctypes.data if t.size else None, t.size, 0, int(s.row))
 
 
+def _query_array(queries: list, keep: list):
+    arr = (SpanQuery * max(1, len(queries)))()
+    for i, q in enumerate(queries):
+        fr = (SpanTokens * max(1, len(q.frags)))(*[_span(f, keep) for f in q.frags])
+        keep.append(fr)
+        arr[i] = SpanQuery(prefix=_span(q.prefix, keep), frags=fr, n_frags=len(q.frags), reserved=0,
+                           cross=_span(q.cross, keep))
+    return arr
+
+
 class Plan:
     def __init__(self, pool: Pool, queries: list, stream=None, static: bool = False):
         lib = load()
         self.pool = pool
         keep: list = []
-        arr = (SpanQuery * max(1, len(queries)))()
-        for i, q in enumerate(queries):
-            fr = (SpanTokens * max(1, len(q.frags)))(*[_span(f, keep) for f in q.frags])
-            keep.append(fr)
-            arr[i] = SpanQuery(prefix=_span(q.prefix, keep), frags=fr, n_frags=len(q.frags), reserved=0,
-                               cross=_span(q.cross, keep))
+        arr = _query_array(queries, keep)
         self.n_queries = len(queries)
         self.n_frags = [len(q.frags) for q in queries]
         self._h = ctypes.c_void_p()

@@ -158,6 +158,8 @@ int spanq::report(int code, const char* msg) { return fail(code, msg); }
 
 span_pool* spanq::plan_pool(const span_plan_t* plan) { return plan ? plan->pool : nullptr; }
 
+const PoolIndex* spanq::pool_index(const span_pool* pool) { return pool->index; }
+
 void spanq::pool_shape(const span_pool* pool, int32_t out[5]) {
   const span_pool_config& c = pool->cfg;
   out[0] = c.num_layers;

@@ -26,6 +26,9 @@ int pool_device(const span_pool* pool);
 // Record a failure for span_last_error and return its status.
 int report(int code, const char* msg);
 
+// The page index of a pool (host side).
+const class PoolIndex* pool_index(const span_pool* pool);
+
 // The pool a plan was made on.
 span_pool* plan_pool(const span_plan_t* plan);
 
