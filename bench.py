@@ -192,6 +192,76 @@ def kv_gather(spanq, W, torch, np, reps, rows_list=(1, 4, 16), n_queries=8):
             "kv_per_query_mb": (640 * page_bytes) / 1e6, "by_rows": res}
 
 
+def reposition_ab(spanq, W, torch, np, reps):
+    """Read-time rotation against materialised repositioning (every shifted page copied,
+    keys rotated to the final positions, as CIDRA does in place) on warm queries: the
+    RAG query with its 16 cached fragments reversed (15 shifted, 480 pages) and the
+    judge query with its 32 cached candidates reversed (31 shifted, 496 pages).  Both
+    pools plan the same query; a timed pass is plan + cross step (every fragment a hit),
+    wall time to stream sync, and kernel times from HIP events on the launch stream.
+    The move kernel's algorithmic bytes: each copied page read once and written once."""
+    res = {}
+    for name, wl in (("c2", W.config_c2()), ("c3", W.config_c3())):
+        q0 = wl.batches[0][0]
+        rev = W.Query(prefix=q0.prefix, frags=q0.frags[::-1], cross=q0.cross)
+        qa, ka, va = wl.device_arrays()
+        q, k, v = (torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda() for a in (qa, ka, va))
+        out = torch.zeros_like(q)
+        pages = 2 * sum((s.n + 15) // 16 for s in [q0.prefix, *q0.frags, q0.cross]) + 64
+        page_bytes = 2 * wl.n_kv_heads * 16 * wl.head_dim * 2
+        stream = torch.cuda.current_stream()
+        entry = {"query": f"prefix {q0.prefix.n} + {len(q0.frags)} x {q0.frags[0].n} (cached, reversed) + "
+                          f"cross {q0.cross.n}"}
+        for mode in ("read_time_rotation", "materialized"):
+            pool = spanq.Pool(num_q_heads=wl.n_q_heads, num_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
+                              num_pages=pages, dtype=wl.dtype, rope_theta=wl.rope_theta, timing=True,
+                              materialize=mode == "materialized", device=0)
+            p = pool.plan([q0], stream)
+            p.prefill(0, q, k, v, out)
+            p.cross(0, q, k, v, out)
+            p.commit()
+            p.destroy()
+            walls, kts, st = [], [], None
+            for r in range(reps + 2):
+                torch.cuda.synchronize()
+                t = time.perf_counter()
+                p = pool.plan([rev], stream)
+                p.prefill(0, q, k, v, out)
+                p.cross(0, q, k, v, out)
+                torch.cuda.synchronize()
+                dt = (time.perf_counter() - t) * 1e3
+                p.commit()
+                kt, st = p.kernel_times(), p.stats()
+                p.destroy()
+                if r >= 2:
+                    walls.append(dt)
+                    kts.append(kt)
+            pool.close()
+            assert st["tokens_new"] == 0
+            mean = {n: float(np.mean([x[n] for x in kts])) for n in spanq._lib.TIME_FIELDS}
+            e = {"warm_ms_p50": _pct(walls, 50),
+                 "cross_attention_ms": mean["cross_attention_ms"], "combine_ms": mean["combine_ms"],
+                 "cross_gpu_ms": mean["page_write_cross_ms"] + mean["page_move_ms"] + mean["cross_attention_ms"] +
+                 mean["combine_ms"]}
+            if mode == "materialized":
+                ms = mean["page_move_ms"]
+                nbytes = 2 * st["pages_moved"] * page_bytes
+                gbs = nbytes / (ms * 1e-3) / 1e9
+                e["page_move"] = {"kernel": "move_pages", "bound": "hbm", "ms": ms, "pages": st["pages_moved"],
+                                  "tokens": st["tokens_moved"], "algorithmic_bytes": nbytes, "gbs": gbs,
+                                  "frac": gbs / PEAK_HBM_GBS,
+                                  "tokens_per_ms_one_layer": st["tokens_moved"] / ms,
+                                  "tokens_per_ms_32_layers": st["tokens_moved"] / ms / 32}
+            entry[mode] = e
+        entry["materialized_over_read_time"] = {
+            "cross_gpu": entry["materialized"]["cross_gpu_ms"] / entry["read_time_rotation"]["cross_gpu_ms"],
+            "warm_ttft": entry["materialized"]["warm_ms_p50"] / entry["read_time_rotation"]["warm_ms_p50"]}
+        res[name] = entry
+        del q, k, v, out
+    res["paper_context"] = "CIDRA (section 5.5) repositions at most 500 tokens/ms on the paper's hardware"
+    return res
+
+
 def _percentiles(xs):
     return {"p50": _pct(xs, 50), "p99": _pct(xs, 99), "mean": float(sum(xs) / len(xs)) if xs else None}
 
@@ -383,9 +453,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c2", choices=["c2", "c3", "c5"],
-                    help="c2: the headline run (with C3 and C4 extras); c3: the judge pattern as the main "
-                         "workload; c5: only the agentic stream over the 8B-shaped decoder")
+    ap.add_argument("--config", default="c2", choices=["c2", "c3", "c5", "repos"],
+                    help="c2: the headline run (with C3, C4 and repositioning extras); c3: the judge pattern as "
+                         "the main workload; c5: only the agentic stream over the 8B-shaped decoder; repos: only "
+                         "the read-time vs materialised repositioning comparison")
     ap.add_argument("--c5-queries", type=int, default=256)
     ap.add_argument("--no-extras", action="store_true", help="skip the C3 and C4 extras of the default run")
     ap.add_argument("--kernel", default="auto", choices=["auto", "generic", "mfma"])
@@ -425,6 +496,14 @@ def main():
                                                  "fragments (128..2048 tokens, Zipf 1.1, 4-24 per query), prefix 256, "
                                                  "question 128"},
                           "c5": res}), flush=True)
+        return
+    if args.config == "repos":
+        res = reposition_ab(spanq, W, torch, np, reps=max(5, args.ttft_reps))
+        print(json.dumps({"metric": "repositioning: read-time rotation vs materialised copies, warm cross pass",
+                          "unit": "ms", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic (seeded tokens and activations)",
+                          "config": {"workload": "C2 and C3 first queries, fragments cached, reversed order"},
+                          "reposition": res}), flush=True)
         return
     t_gen = time.perf_counter()
     wl = W.config_c2() if args.config == "c2" else W.config_c3()
@@ -560,6 +639,8 @@ def main():
         print(f"[bench] c3 {json.dumps(extras['c3'])}", file=sys.stderr, flush=True)
         extras["c4"] = c4_ttft(spanq, W, torch, np, reps=max(5, args.ttft_reps))
         print(f"[bench] c4 {json.dumps(extras['c4'])}", file=sys.stderr, flush=True)
+        extras["reposition"] = reposition_ab(spanq, W, torch, np, reps=10)
+        print(f"[bench] reposition {json.dumps(extras['reposition'])}", file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu_baseline:

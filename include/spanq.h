@@ -78,6 +78,11 @@ extern "C" {
                                  num_kv_heads in {1, 2, 4, 8} (SPAN_EINVAL otherwise) */
 
 #define SPAN_FLAG_TIMING 1    /* bracket every kernel launch with HIP events (span_plan_kernel_times) */
+#define SPAN_FLAG_MATERIALIZE 2 /* materialised repositioning (the re-rotation of cached blocks of
+                                   section 5.5, CIDRA): plans copy every page that cross rows read at a shifted
+                                   position into a transient page whose keys sit at the final positions;
+                                   see span_plan.  Default (flag clear): cross attention rotates at read
+                                   time and nothing is copied. */
 
 typedef struct span_pool span_pool;
 typedef struct span_plan_t span_plan_t;
@@ -189,7 +194,12 @@ typedef struct {
  * first).  All pages the plan uses are pinned until commit (cache pages) or destroy
  * (cross pages).  The device work lists are copied once, on `stream`.
  * SPAN_ENOMEM (pool unchanged) if the batch needs more pages than are free or
- * evictable.  Host-only pools plan but cannot run attention. */
+ * evictable.  Host-only pools plan but cannot run attention.
+ * With SPAN_FLAG_MATERIALIZE the plan also allocates, after all other pages, one
+ * transient page per distinct (page, shift) that a query with a cross segment
+ * reads at a shifted position (a fragment page with final != canonical position;
+ * a page read at two shifts gets two copies, one read at the same shift by several
+ * queries one); they count in the capacity check and are freed like cross pages. */
 int span_plan(span_pool* pool, const span_query* queries, int32_t n_queries, void* stream,
               span_plan_t** out);
 
@@ -209,6 +219,8 @@ typedef struct {
   int64_t cross_kv_pages;   /* page reads of the cross pass per kv head */
   double host_plan_us;      /* host time of hashing, lookup, allocation and work lists */
   double host_upload_us;    /* host time of device metadata allocation + copy enqueue */
+  int64_t pages_moved;      /* SPAN_FLAG_MATERIALIZE: transient repositioned copies */
+  int64_t tokens_moved;     /* filled slots of those copies */
 } span_stats;
 int span_plan_stats(const span_plan_t* plan, span_stats* stats);
 
@@ -217,6 +229,11 @@ int span_plan_stats(const span_plan_t* plan, span_stats* stats);
  * leading pages that were hits. */
 int span_plan_block_table(const span_plan_t* plan, int32_t query, int32_t span, int32_t* page_ids,
                           int32_t cap, int32_t* n, int32_t* n_hit);
+
+/* Repositioned copies of a SPAN_FLAG_MATERIALIZE plan (none otherwise): record i
+ * is rec[4i..4i+3] = (source page, copy page, shift in positions, filled slots),
+ * for i < cap; *n = number of copies. */
+int span_plan_moves(const span_plan_t* plan, int32_t* rec, int32_t cap, int32_t* n);
 
 /* Page ids evicted by this plan, in eviction order. */
 int span_plan_evicted(const span_plan_t* plan, int32_t* page_ids, int32_t cap, int32_t* n);
@@ -270,7 +287,9 @@ int span_prefill_fragments(span_plan_t* plan, int32_t layer, const void* q, cons
  * prefix, to every fragment in this query's order and causally to the cross segment,
  * all at final positions (index in prefix | F_s1 | ... | F_sn | cross).  Cached
  * fragment keys are rotated by (final - canonical) position as they are read; pages
- * are never rewritten.  Must follow span_prefill_fragments for the same layer. */
+ * are never rewritten.  On a SPAN_FLAG_MATERIALIZE pool the layer's repositioned
+ * copies are written first (keys rotated by the shift, values copied) and the cross
+ * rows read those, unrotated.  Must follow span_prefill_fragments for the same layer. */
 int span_cross_attend(span_plan_t* plan, int32_t layer, const void* q, const void* k, const void* v,
                       void* out, void* stream);
 
@@ -392,6 +411,7 @@ typedef struct {
   float page_write_cross_ms;    /* K3 over cross pages */
   float cross_attention_ms;     /* cross attention (all KV splits) */
   float combine_ms;             /* KV-split merge */
+  float page_move_ms;           /* SPAN_FLAG_MATERIALIZE: repositioned copies */
   int32_t prefill_calls;
   int32_t cross_calls;
 } span_kernel_times;

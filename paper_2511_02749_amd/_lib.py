@@ -29,10 +29,11 @@ EXPORTS = [
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
-    "span_parse_serialized", "span_bulk_order",
+    "span_parse_serialized", "span_bulk_order", "span_plan_moves",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
+SPAN_FLAG_MATERIALIZE = 2
 
 
 class SpanError(RuntimeError):
@@ -70,11 +71,13 @@ STAT_FIELDS = ("pages_hit", "pages_new", "pages_cross", "pages_evicted", "tokens
 
 class SpanStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS] + [("host_plan_us", ctypes.c_double),
-                                                            ("host_upload_us", ctypes.c_double)]
+                                                            ("host_upload_us", ctypes.c_double),
+                                                            ("pages_moved", ctypes.c_int64),
+                                                            ("tokens_moved", ctypes.c_int64)]
 
 
 TIME_FIELDS = ("page_write_prefill_ms", "prefill_attention_ms", "page_write_cross_ms", "cross_attention_ms",
-               "combine_ms")
+               "combine_ms", "page_move_ms")
 
 
 class KernelTimes(ctypes.Structure):
@@ -137,6 +140,7 @@ def load():
         "span_plan_stats": (I32, [VP, P(SpanStats)]),
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
+        "span_plan_moves": (I32, [VP, P(I32), I32, P(I32)]),
         "span_plan_rows": (I32, [VP, P(I64), I64, P(I64), P(I64)]),
         "span_prefill_fragments": (I32, [VP, I32, VP, VP, VP, VP, VP]),
         "span_cross_attend": (I32, [VP, I32, VP, VP, VP, VP, VP]),
@@ -215,14 +219,15 @@ class Pool:
 
     def __init__(self, *, num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str = "bf16",
                  num_layers: int = 1, rope_theta: float = 1e4, page_size: int = 16, device: int = 0,
-                 hash_mode: str = "span", kernel: str = "auto", timing: bool = False):
+                 hash_mode: str = "span", kernel: str = "auto", timing: bool = False, materialize: bool = False):
         lib = load()
         self.cfg = PoolConfig(num_layers=num_layers, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                               head_dim=head_dim, page_size=page_size,
                               dtype=SPAN_BF16 if dtype == "bf16" else SPAN_F32,
                               hash_mode=SPAN_HASH_STOCK if hash_mode == "stock" else SPAN_HASH_SPAN,
                               kernel=SPAN_KERNEL[kernel], device=device,
-                              flags=SPAN_FLAG_TIMING if timing else 0, rope_theta=rope_theta,
+                              flags=(SPAN_FLAG_TIMING if timing else 0) | (SPAN_FLAG_MATERIALIZE if materialize else 0),
+                              rope_theta=rope_theta,
                               num_pages=num_pages, device_buf=None, device_bytes=0)
         self.dtype = dtype
         self._plans = weakref.WeakSet()
@@ -325,6 +330,7 @@ class Plan:
         _check(load().span_plan_stats(self._h, ctypes.byref(s)))
         d = {n: int(getattr(s, n)) for n in STAT_FIELDS}
         d["host_plan_us"], d["host_upload_us"] = float(s.host_plan_us), float(s.host_upload_us)
+        d["pages_moved"], d["tokens_moved"] = int(s.pages_moved), int(s.tokens_moved)
         return d
 
     def block_table(self, query: int, span: int):
@@ -335,6 +341,14 @@ class Plan:
         _check(load().span_plan_block_table(self._h, query, span, _i32p(ids), n.value, ctypes.byref(n),
                                             ctypes.byref(nh)))
         return [int(x) for x in ids[: n.value]], nh.value
+
+    def moves(self) -> List[tuple]:
+        """Repositioned copies (materialize pools): (source page, copy page, shift, filled slots)."""
+        n = ctypes.c_int32()
+        _check(load().span_plan_moves(self._h, None, 0, ctypes.byref(n)))
+        rec = np.zeros(max(4, 4 * n.value), np.int32)
+        _check(load().span_plan_moves(self._h, _i32p(rec), n.value, ctypes.byref(n)))
+        return [tuple(int(x) for x in rec[4 * i: 4 * i + 4]) for i in range(n.value)]
 
     def evicted(self) -> List[int]:
         n = ctypes.c_int32()

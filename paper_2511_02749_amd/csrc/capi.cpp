@@ -119,6 +119,7 @@ struct span_plan_t {
   const WorkTile* tp = nullptr;
   const WorkTile* tc = nullptr;
   const CombineTile* cb = nullptr;
+  const MovePage* mv = nullptr;
   const float2* rope = nullptr;
   // item counters of the span-prefill kernel: kSchedSlots pairs of words, zeroed at
   // upload and left zeroed by each launch; launches take them in turn, so up to
@@ -249,7 +250,8 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
   const bool device = pool->cfg.device >= 0;
   pl->mfma = device && pool->use_mfma;
   pl->bm = pl->mfma ? mfma_bm(pool->cfg.num_q_heads / pool->cfg.num_kv_heads) : kGenericBM;
-  const Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
+  Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
+  t.materialize = (pool->cfg.flags & SPAN_FLAG_MATERIALIZE) != 0;
   std::string msg;
   const auto t_plan0 = std::chrono::steady_clock::now();
   int rc = pool->index->plan(in, true, t, &pl->plan, &msg);
@@ -287,7 +289,8 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
     auto& hb = pl->host_meta;
     size_t o_kv = put(hb, P.kv), o_kt = put(hb, P.kv_tiles), o_k3p = put(hb, P.k3_prefill),
            o_k3c = put(hb, P.k3_cross);
-    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine);
+    size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine),
+           o_mv = put(hb, P.moves);
     size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
     pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
     const size_t part_bytes =
@@ -334,6 +337,7 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
     pl->tp = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tp);
     pl->tc = reinterpret_cast<const WorkTile*>(pl->dev_meta + o_tc);
     pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
+    pl->mv = reinterpret_cast<const MovePage*>(pl->dev_meta + o_mv);
     pl->sched = reinterpret_cast<unsigned*>(pl->dev_meta + o_sc);
   }
   *out = pl;
@@ -547,6 +551,23 @@ int span_plan_stats(const span_plan_t* pl, span_stats* s) {
   s->cross_kv_pages = P.cross_kv_pages;
   s->host_plan_us = pl->host_plan_us;
   s->host_upload_us = pl->host_upload_us;
+  s->pages_moved = static_cast<int64_t>(P.moves.size());
+  int64_t moved_tok = 0;
+  for (const MovePage& m : P.moves) moved_tok += m.n_valid;
+  s->tokens_moved = moved_tok;
+  return SPAN_OK;
+}
+
+int span_plan_moves(const span_plan_t* pl, int32_t* rec, int32_t cap, int32_t* n) {
+  if (!pl || !n || cap < 0 || (cap > 0 && !rec)) return fail(SPAN_EINVAL, "span_plan_moves: bad argument");
+  const auto& mv = pl->plan.moves;
+  *n = static_cast<int32_t>(mv.size());
+  for (int32_t i = 0; i < *n && i < cap; ++i) {
+    rec[4 * i] = mv[i].src_page;
+    rec[4 * i + 1] = mv[i].dst_page;
+    rec[4 * i + 2] = mv[i].delta;
+    rec[4 * i + 3] = mv[i].n_valid;
+  }
   return SPAN_OK;
 }
 
@@ -657,11 +678,16 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   rc = order_after_upload(pl, s, "span_cross_attend");
   if (rc) return rc;
   PoolGeom g = geom(pl, layer);
-  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 3, s, pl->pool->event_cache);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 4, s, pl->pool->event_cache);
   tm.mark(0);
   hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
   tm.mark(1);
+  // materialised repositioning: this layer's copies of shifted pages, keys rotated
+  // to the final positions (the cross key lists name the copies, delta 0)
+  e = launch_move_pages(g, pl->mv, static_cast<int>(P.moves.size()), pl->rope, s);
+  if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page moves");
+  tm.mark(2);
   float* po = pl->part;
   float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
   const int nt = static_cast<int>(P.t_cross.size());
@@ -674,10 +700,10 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
     e = launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
   }
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
-  tm.mark(2);
+  tm.mark(3);
   e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: combine");
-  tm.mark(3);
+  tm.mark(4);
   if (!tm.ev.empty()) pl->ev_cross.push_back(tm.ev);
   return SPAN_OK;
 }
@@ -698,8 +724,9 @@ int span_plan_kernel_times(const span_plan_t* pl, span_kernel_times* t) {
   }
   for (const auto& ev : pl->ev_cross) {
     t->page_write_cross_ms += elapsed(ev[0], ev[1]);
-    t->cross_attention_ms += elapsed(ev[1], ev[2]);
-    t->combine_ms += elapsed(ev[2], ev[3]);
+    t->page_move_ms += elapsed(ev[1], ev[2]);
+    t->cross_attention_ms += elapsed(ev[2], ev[3]);
+    t->combine_ms += elapsed(ev[3], ev[4]);
     t->cross_calls += 1;
   }
   return SPAN_OK;

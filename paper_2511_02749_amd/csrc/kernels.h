@@ -20,6 +20,11 @@ struct PoolGeom {
 hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n_pages, const void* k,
                              const void* v, const float2* rope, hipStream_t s);
 
+// Materialised repositioning: copy each move's source page to its destination
+// page with the keys rotated by the move's delta (values copied unchanged).
+hipError_t launch_move_pages(const PoolGeom& g, const MovePage* moves, int n_moves, const float2* rope,
+                             hipStream_t s);
+
 // Generic (vector ALU) span attention over work tiles of up to 64 rows.
 constexpr int kGenericBM = 64;
 hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,

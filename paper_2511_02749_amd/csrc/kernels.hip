@@ -134,6 +134,98 @@ hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, con
   return rope_write_t<float, 64>(g, pages, n, k, v, rope, s);
 }
 
+// ------------------------------------------------------------------ page moves
+// Materialised repositioning: one work-group per MovePage.  Keys of every kv head
+// and slot are rotated by the page's delta (rotations in one plane add, so a key
+// stored rotated at position p comes out rotated at p + delta); the transposed
+// values are copied as they are.  Slots past n_valid hold the zeros K3 wrote and
+// stay zero.  Loads of four items are issued before their stores.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void move_pages_kernel(const MovePage* __restrict__ moves, T* __restrict__ pool,
+                                                         int64_t layer_off, int hkv,
+                                                         const float2* __restrict__ rope) {
+  constexpr int E = Chunk16<T>::E;
+  constexpr int H = D / 2;
+  constexpr int U = 4;
+  const MovePage m = moves[blockIdx.x];
+  const int64_t page_elems = 2ll * hkv * kPage * D;
+  const T* src = pool + layer_off + static_cast<int64_t>(m.src_page) * page_elems;
+  T* dst = pool + layer_off + static_cast<int64_t>(m.dst_page) * page_elems;
+  const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(m.delta) * H);
+
+  // K: item e = (head, slot) row e / (H / E), chunk q = e % (H / E) of E pairs (i, i + H)
+  const int n_k = hkv * kPage * (H / E);
+  for (int e0 = threadIdx.x; e0 < n_k; e0 += U * blockDim.x) {
+    Chunk16<T> x0[U], x1[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int e = e0 + j * blockDim.x;
+      if (e < n_k) {
+        const int64_t off = static_cast<int64_t>(e / (H / E)) * D + (e % (H / E)) * E;
+        x0[j] = load16(src + off);
+        x1[j] = load16(src + off + H);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int e = e0 + j * blockDim.x;
+      if (e >= n_k) break;
+      const int q = e % (H / E);
+      const int64_t off = static_cast<int64_t>(e / (H / E)) * D + q * E;
+      Chunk16<T> y0, y1;
+#pragma unroll
+      for (int u2 = 0; u2 < E / 2; ++u2) {
+        const float4 w = cs4[q * (E / 2) + u2];  // (cos, sin) of pairs q*E + 2u2 and + 1
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int u = 2 * u2 + b;
+          const float cs = b ? w.z : w.x, sn = b ? w.w : w.y;
+          const float a0 = to_f32(x0[j].x[u]), a1 = to_f32(x1[j].x[u]);
+          y0.x[u] = from_f32<T>(a0 * cs - a1 * sn);
+          y1.x[u] = from_f32<T>(a1 * cs + a0 * sn);
+        }
+      }
+      store16(dst + off, y0);
+      store16(dst + off + H, y1);
+    }
+  }
+
+  // V: the [kv head][d][slot] block, copied
+  const uint4* vs = reinterpret_cast<const uint4*>(src + static_cast<int64_t>(hkv) * kPage * D);
+  uint4* vd = reinterpret_cast<uint4*>(dst + static_cast<int64_t>(hkv) * kPage * D);
+  const int n_v = hkv * kPage * D / E;
+  for (int e0 = threadIdx.x; e0 < n_v; e0 += 2 * U * blockDim.x) {
+    uint4 x[2 * U];
+#pragma unroll
+    for (int j = 0; j < 2 * U; ++j) {
+      const int e = e0 + j * blockDim.x;
+      if (e < n_v) x[j] = vs[e];
+    }
+#pragma unroll
+    for (int j = 0; j < 2 * U; ++j) {
+      const int e = e0 + j * blockDim.x;
+      if (e < n_v) vd[e] = x[j];
+    }
+  }
+}
+
+template <typename T, int D>
+static hipError_t move_pages_t(const PoolGeom& g, const MovePage* moves, int n, const float2* rope, hipStream_t s) {
+  hipLaunchKernelGGL((move_pages_kernel<T, D>), dim3(n), dim3(256), 0, s, moves, static_cast<T*>(g.base), g.layer_off,
+                     g.hkv, rope);
+  return hipGetLastError();
+}
+
+hipError_t launch_move_pages(const PoolGeom& g, const MovePage* moves, int n, const float2* rope, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (g.dtype == SPAN_BF16) {
+    if (g.d == 128) return move_pages_t<bf16_t, 128>(g, moves, n, rope, s);
+    return move_pages_t<bf16_t, 64>(g, moves, n, rope, s);
+  }
+  if (g.d == 128) return move_pages_t<float, 128>(g, moves, n, rope, s);
+  return move_pages_t<float, 64>(g, moves, n, rope, s);
+}
+
 // ------------------------------------------------------------------ generic attention
 // One wave per (tile, query head); lane r owns query row r of the tile.  Each
 // key page is staged in LDS (rotated by the page's delta when it is read from a

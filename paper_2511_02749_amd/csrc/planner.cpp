@@ -304,6 +304,48 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     walk.push_back(std::move(w));
   }
 
+  // Materialised repositioning (the alternative to rotating at read time: section
+  // 5.5 re-rotates cached blocks into place, CIDRA in place): every page
+  // of a fragment that a query's cross rows read at a shifted position gets a
+  // transient copy whose keys sit at the final positions.  A page read at the same
+  // shift by several queries of the batch is copied once; a page read at two
+  // shifts is copied twice (the duplication of a block with two targets).  Source
+  // pages are never rewritten, so the moves have no dependencies among them.
+  // Page identity: a hit's page id, or -1 - slot for a page this plan computes
+  // (a batch duplicate names the slot of its first occurrence).
+  struct MoveSrc {
+    int64_t page;
+    int32_t delta, n_valid;
+  };
+  std::vector<MoveSrc> moves;
+  std::vector<std::vector<int32_t>> move_of(walk.size());
+  if (tiling.materialize && hash_mode_ != SPAN_HASH_STOCK) {
+    std::unordered_map<uint64_t, int32_t> seen;
+    for (size_t qi = 0; qi < qs.size(); ++qi) {
+      if (qs[qi].cross.n == 0) continue;
+      const auto& ids = query_spans[qi];
+      int32_t shift = 0;  // final minus canonical position of the fragment's tokens
+      for (size_t c = 1; c + 1 < ids.size(); ++c) {
+        const SpanWalk& w = walk[ids[c]];
+        if (shift != 0) {
+          auto& mv = move_of[ids[c]];
+          for (size_t pg = 0; pg < w.entries.size(); ++pg) {
+            const Entry& e = w.entries[pg];
+            const int64_t page = e.hit ? e.x : -1 - static_cast<int64_t>(e.x);
+            const uint64_t key = (static_cast<uint64_t>(page) << 32) ^ static_cast<uint32_t>(shift);
+            auto it = seen.find(key);
+            if (it == seen.end()) {
+              it = seen.emplace(key, static_cast<int32_t>(moves.size())).first;
+              moves.push_back({page, shift, std::min(ps, w.in.n - static_cast<int32_t>(pg) * ps)});
+            }
+            mv.push_back(it->second);
+          }
+        }
+        shift += w.in.n;
+      }
+    }
+  }
+
   // distinct published pages this plan hits, in walk order
   std::vector<int32_t> hit_pids;
   const int64_t stamp = ++stamp_;
@@ -313,7 +355,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
         pages_[e.x].seen_stamp = stamp;
         hit_pids.push_back(e.x);
       }
-  int64_t need = static_cast<int64_t>(specs.size());
+  int64_t need = static_cast<int64_t>(specs.size() + moves.size());
   int64_t evictable = n_evictable_;
   for (int32_t pid : hit_pids)
     if (pages_[pid].published && pages_[pid].pins == 0) --evictable;
@@ -359,6 +401,19 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     for (int wi : query_spans[qi])
       for (const Entry& e : walk[wi].entries)
         if (!e.hit && !e.dup) alloc(e.x);
+  // repositioned copies last: transient like cross pages, never published
+  for (const MoveSrc& m : moves) {
+    if (free_count() == 0) evict_one(&P);
+    const int32_t pid = pop_free();
+    PageRec& r = pages_[pid];
+    r = PageRec{};
+    r.last_use = P.tick;
+    r.pins = 1;
+    r.used = true;
+    P.new_pages.push_back(pid);
+    const int32_t src = m.page >= 0 ? static_cast<int32_t>(m.page) : slot_pid[-1 - m.page];
+    P.moves.push_back(MovePage{src, pid, m.delta, m.n_valid});
+  }
 
   P.query_spans = query_spans;
   P.spans.resize(walk.size());
@@ -371,6 +426,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     sp.n_tok = w.in.n;
     sp.row = w.in.row;
     sp.n_hit = 0;
+    for (int32_t m : move_of[wi]) sp.moved.push_back(P.moves[m].dst_page);
     bool leading = true;
     for (const Entry& e : w.entries) {
       sp.pages.push_back(e.hit ? e.x : slot_pid[e.x]);
@@ -489,7 +545,10 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     const int32_t kv0 = static_cast<int32_t>(p->kv.size());
     for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
       const SpanPlan& s = p->spans[ids[c]];
-      append_span(p->kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, t.pad4);
+      if (!s.moved.empty())
+        append_span(p->kv, s.moved, s.n_tok, ps, s.final0, 0, t.pad4);  // copies at final positions
+      else
+        append_span(p->kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, t.pad4);
     }
     append_span(p->kv, cross.pages, cross.n_tok, ps, cross.final0, 0, t.pad4);
     const int32_t kv1 = static_cast<int32_t>(p->kv.size());

@@ -51,6 +51,8 @@ struct SpanPlan {
   int32_t final0 = 0;  // final position of token 0 in its query
   std::vector<int32_t> pages;
   int32_t n_hit = 0;
+  std::vector<int32_t> moved;  // materialised repositioning: copy of each page at
+                               // final positions (empty if the span is not shifted)
 };
 
 struct Tiling {
@@ -63,6 +65,8 @@ struct Tiling {
   int two_group_rows = 0;     // cross tiles of at most this many rows use kTwoKeyGroups
   int few_rows = 0;           // two-key-group tiles of at most this many rows go last
                               // in the cross list (the 16-row kernel takes them)
+  bool materialize = false;   // cross rows read re-rotated copies of shifted pages
+                              // (delta 0) instead of rotating at read time
 };
 
 // Work-list shape for the attention kernels.  The MFMA kernel is persistent, one
@@ -93,6 +97,8 @@ struct Plan {
   std::vector<SpanPlan> spans;
   std::vector<std::vector<int>> query_spans;  // per query: prefix, fragments..., cross
   std::vector<int32_t> evicted, new_pages, cross_pages, hits;
+  std::vector<MovePage> moves;  // materialised repositioning copies, one per distinct
+                                // (page, delta != 0) that cross rows read
   bool committed = false;
 
   // work lists

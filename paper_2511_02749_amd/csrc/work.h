@@ -38,6 +38,16 @@ struct NewPage {
   int32_t pos0;
 };
 
+// One repositioned copy (materialised repositioning): the keys of page src_page,
+// stored at positions p.., are written to page dst_page rotated to positions
+// p + delta..; the values are copied as they are.
+struct MovePage {
+  int32_t src_page;
+  int32_t dst_page;
+  int32_t delta;
+  int32_t n_valid;
+};
+
 // A tile of up to BM consecutive query rows of one span, against the key pages
 // kv[kv_begin, kv_end).  part < 0: write the normalised output; else write the
 // unnormalised partial (one KV split) into partial slot `part`.  With

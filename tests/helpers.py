@@ -39,7 +39,7 @@ def oracle_rows(wl, query, want_rows=None):
 class GpuRun:
     """A pool on cuda:0 holding a workload's activations; runs batches through the library."""
 
-    def __init__(self, wl, num_pages=None, kernel="auto", num_layers=1):
+    def __init__(self, wl, num_pages=None, kernel="auto", num_layers=1, materialize=False):
         import torch
 
         import paper_2511_02749_amd as spanq
@@ -51,7 +51,7 @@ class GpuRun:
                 for b in wl.batches for q in b)
         self.pool = spanq.Pool(num_q_heads=wl.n_q_heads, num_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                                num_pages=num_pages, dtype=wl.dtype, rope_theta=wl.rope_theta, kernel=kernel,
-                               num_layers=num_layers, device=0)
+                               num_layers=num_layers, materialize=materialize, device=0)
         qa, ka, va = wl.device_arrays()
         conv = (lambda a: torch.from_numpy(a.view(np.int16))) if wl.dtype == "bf16" else torch.from_numpy
         self.q, self.k, self.v = (conv(np.ascontiguousarray(a)).cuda() for a in (qa, ka, va))
