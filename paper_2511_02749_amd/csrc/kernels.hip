@@ -135,11 +135,12 @@ hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, con
 }
 
 // ------------------------------------------------------------------ page moves
-// Materialised repositioning: one work-group per MovePage.  Keys of every kv head
-// and slot are rotated by the page's delta (rotations in one plane add, so a key
-// stored rotated at position p comes out rotated at p + delta); the transposed
-// values are copied as they are.  Slots past n_valid hold the zeros K3 wrote and
-// stay zero.  Loads of four items are issued before their stores.
+// Materialised repositioning: two work-groups per MovePage, one for the keys
+// (blockIdx.y 0) and one for the values.  Keys of every kv head and slot are
+// rotated by the page's delta (rotations in one plane add, so a key stored rotated
+// at position p comes out rotated at p + delta); the transposed values are copied
+// as they are.  Slots past n_valid hold the zeros K3 wrote and stay zero.  Each
+// thread issues all its loads (four key items, eight value chunks) before storing.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void move_pages_kernel(const MovePage* __restrict__ moves, T* __restrict__ pool,
                                                          int64_t layer_off, int hkv,
@@ -151,6 +152,26 @@ __global__ __launch_bounds__(256) void move_pages_kernel(const MovePage* __restr
   const int64_t page_elems = 2ll * hkv * kPage * D;
   const T* src = pool + layer_off + static_cast<int64_t>(m.src_page) * page_elems;
   T* dst = pool + layer_off + static_cast<int64_t>(m.dst_page) * page_elems;
+  if (blockIdx.y != 0) {
+    // V: the [kv head][d][slot] block, copied
+    const uint4* vs = reinterpret_cast<const uint4*>(src + static_cast<int64_t>(hkv) * kPage * D);
+    uint4* vd = reinterpret_cast<uint4*>(dst + static_cast<int64_t>(hkv) * kPage * D);
+    const int n_v = hkv * kPage * D / E;
+    for (int e0 = threadIdx.x; e0 < n_v; e0 += 2 * U * blockDim.x) {
+      uint4 x[2 * U];
+#pragma unroll
+      for (int j = 0; j < 2 * U; ++j) {
+        const int e = e0 + j * blockDim.x;
+        if (e < n_v) x[j] = vs[e];
+      }
+#pragma unroll
+      for (int j = 0; j < 2 * U; ++j) {
+        const int e = e0 + j * blockDim.x;
+        if (e < n_v) vd[e] = x[j];
+      }
+    }
+    return;
+  }
   const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(m.delta) * H);
 
   // K: item e = (head, slot) row e / (H / E), chunk q = e % (H / E) of E pairs (i, i + H)
@@ -189,29 +210,11 @@ __global__ __launch_bounds__(256) void move_pages_kernel(const MovePage* __restr
       store16(dst + off + H, y1);
     }
   }
-
-  // V: the [kv head][d][slot] block, copied
-  const uint4* vs = reinterpret_cast<const uint4*>(src + static_cast<int64_t>(hkv) * kPage * D);
-  uint4* vd = reinterpret_cast<uint4*>(dst + static_cast<int64_t>(hkv) * kPage * D);
-  const int n_v = hkv * kPage * D / E;
-  for (int e0 = threadIdx.x; e0 < n_v; e0 += 2 * U * blockDim.x) {
-    uint4 x[2 * U];
-#pragma unroll
-    for (int j = 0; j < 2 * U; ++j) {
-      const int e = e0 + j * blockDim.x;
-      if (e < n_v) x[j] = vs[e];
-    }
-#pragma unroll
-    for (int j = 0; j < 2 * U; ++j) {
-      const int e = e0 + j * blockDim.x;
-      if (e < n_v) vd[e] = x[j];
-    }
-  }
 }
 
 template <typename T, int D>
 static hipError_t move_pages_t(const PoolGeom& g, const MovePage* moves, int n, const float2* rope, hipStream_t s) {
-  hipLaunchKernelGGL((move_pages_kernel<T, D>), dim3(n), dim3(256), 0, s, moves, static_cast<T*>(g.base), g.layer_off,
+  hipLaunchKernelGGL((move_pages_kernel<T, D>), dim3(n, 2), dim3(256), 0, s, moves, static_cast<T*>(g.base), g.layer_off,
                      g.hkv, rope);
   return hipGetLastError();
 }
