@@ -221,6 +221,8 @@ typedef struct {
   double host_upload_us;    /* host time of device metadata allocation + copy enqueue */
   int64_t pages_moved;      /* SPAN_FLAG_MATERIALIZE: transient repositioned copies */
   int64_t tokens_moved;     /* filled slots of those copies */
+  int64_t prefill_queues;   /* work queues of the last bf16 MFMA prefill launch: 8 (one per XCD,
+                               each reading one kv head of a group of spans), 1, or 0 (none yet) */
 } span_stats;
 int span_plan_stats(const span_plan_t* plan, span_stats* stats);
 

@@ -73,7 +73,8 @@ class SpanStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in STAT_FIELDS] + [("host_plan_us", ctypes.c_double),
                                                             ("host_upload_us", ctypes.c_double),
                                                             ("pages_moved", ctypes.c_int64),
-                                                            ("tokens_moved", ctypes.c_int64)]
+                                                            ("tokens_moved", ctypes.c_int64),
+                                                            ("prefill_queues", ctypes.c_int64)]
 
 
 TIME_FIELDS = ("page_write_prefill_ms", "prefill_attention_ms", "page_write_cross_ms", "cross_attention_ms",
@@ -331,6 +332,7 @@ class Plan:
         d = {n: int(getattr(s, n)) for n in STAT_FIELDS}
         d["host_plan_us"], d["host_upload_us"] = float(s.host_plan_us), float(s.host_upload_us)
         d["pages_moved"], d["tokens_moved"] = int(s.pages_moved), int(s.tokens_moved)
+        d["prefill_queues"] = int(s.prefill_queues)
         return d
 
     def block_table(self, query: int, span: int):

@@ -121,11 +121,13 @@ struct span_plan_t {
   const CombineTile* cb = nullptr;
   const MovePage* mv = nullptr;
   const float2* rope = nullptr;
-  // item counters of the span-prefill kernel: kSchedSlots pairs of words, zeroed at
-  // upload and left zeroed by each launch; launches take them in turn, so up to
-  // kSchedSlots launches of one plan may overlap (on different streams)
+  // item counters of the span-prefill kernel: kSchedSlots groups of kSchedWords
+  // words, zeroed at upload and left zeroed by each launch; launches take them in
+  // turn, so up to kSchedSlots launches of one plan may overlap (on different streams)
   static constexpr int kSchedSlots = 64;
   unsigned* sched = nullptr;
+  const int32_t* xch = nullptr;  // per-XCD chunk offsets of the prefill tiles
+  int prefill_queues = 0;         // queues of the last MFMA prefill launch (8: per XCD)
   unsigned sched_next = 0;
   int bm = kGenericBM;
   bool mfma = false;
@@ -291,7 +293,8 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
            o_k3c = put(hb, P.k3_cross);
     size_t o_tp = put(hb, P.t_prefill), o_tc = put(hb, P.t_cross), o_cb = put(hb, P.combine),
            o_mv = put(hb, P.moves);
-    size_t o_sc = put(hb, std::vector<unsigned>(2 * span_plan_t::kSchedSlots, 0u));
+    size_t o_sc = put(hb, std::vector<unsigned>(kSchedWords * span_plan_t::kSchedSlots, 0u));
+    size_t o_xc = put(hb, P.prefill_chunks);
     pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
     const size_t part_bytes =
         (pl->part_o_elems + static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2) * sizeof(float);
@@ -339,6 +342,7 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
     pl->cb = reinterpret_cast<const CombineTile*>(pl->dev_meta + o_cb);
     pl->mv = reinterpret_cast<const MovePage*>(pl->dev_meta + o_mv);
     pl->sched = reinterpret_cast<unsigned*>(pl->dev_meta + o_sc);
+    pl->xch = reinterpret_cast<const int32_t*>(pl->dev_meta + o_xc);
   }
   *out = pl;
   return SPAN_OK;
@@ -555,6 +559,7 @@ int span_plan_stats(const span_plan_t* pl, span_stats* s) {
   int64_t moved_tok = 0;
   for (const MovePage& m : P.moves) moved_tok += m.n_valid;
   s->tokens_moved = moved_tok;
+  s->prefill_queues = pl->prefill_queues;
   return SPAN_OK;
 }
 
@@ -658,8 +663,10 @@ int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const 
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: page write");
   tm.mark(1);
   const int nt = static_cast<int>(P.t_prefill.size());
-  unsigned* sched = pl->sched + 2 * (pl->sched_next++ % span_plan_t::kSchedSlots);
-  e = pl->mfma ? launch_prefill_mfma(g, pl->tp, nt, pl->kt, q, out, pl->rope, sched, s)
+  unsigned* sched = pl->sched + kSchedWords * (pl->sched_next++ % span_plan_t::kSchedSlots);
+  const int nch = P.prefill_chunks.empty() ? 0 : static_cast<int>(P.prefill_chunks.size()) - 1;
+  e = pl->mfma ? launch_prefill_mfma(g, pl->tp, nt, pl->kt, q, out, pl->rope, sched, P.prefill_chunks.data(),
+                                     pl->xch, nch, &pl->prefill_queues, s)
                : launch_attn_generic(g, pl->tp, nt, pl->kv, q, out, nullptr, nullptr, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_prefill_fragments: attention");
   tm.mark(2);

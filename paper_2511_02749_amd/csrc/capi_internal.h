@@ -1,7 +1,5 @@
 // Internal entries shared by the C-ABI sources (not part of the public ABI).
 #pragma once
-#include <hip/hip_runtime.h>
-
 #include <cstddef>
 #include <cstdint>
 #include <vector>

@@ -55,11 +55,20 @@ hipError_t launch_few_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles
                            float* part_o, float* part_ml, const float2* rope, hipStream_t s);
 
 // Span prefill (no repositioning, no key splits), the software-pipelined kernel.
-// Every tile must have at least one key tile.  `sched` is two zeroed device words,
-// the launch's item counter; the kernel leaves them at zero when it ends, so
-// launches that run one after another may share them and overlapping ones may not.
+// Every tile must have at least one key tile.  `sched` is kSchedWords zeroed device
+// words, the launch's queue counters (words 0..7) and finish count (word
+// kQueueDone); the kernel leaves them at zero when it ends, so launches that run
+// one after another may share them and overlapping ones may not.  chunks_host /
+// chunks_dev: the n_chunks + 1 offsets of the per-XCD tile chunks (n_chunks = 8 /
+// kv heads), or n_chunks = 0 for one queue; the launch falls back to one queue when
+// a chunk is too short for the grid.  *queues (if given) receives the queue count
+// the launch used (8 or 1).
+constexpr int kQueueDone = 8;
+constexpr int kSchedWords = 16;
 hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt,
-                               const void* q, void* out, const float2* rope, unsigned* sched, hipStream_t s);
+                               const void* q, void* out, const float2* rope, unsigned* sched,
+                               const int32_t* chunks_host, const int32_t* chunks_dev, int n_chunks, int* queues,
+                               hipStream_t s);
 
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,

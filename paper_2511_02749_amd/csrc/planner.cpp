@@ -23,11 +23,23 @@ uint64_t mix64(uint64_t x) {
   return z ^ (z >> 31);
 }
 
+// A page hash as the index stores it.  Test builds of the host code may define
+// SPANQ_TEST_HASH_BITS to keep only that many low bits, so that unrelated pages
+// collide often and the content check behind every index hit is exercised; the
+// library is never built so.
+static inline uint64_t stored_hash(uint64_t h) {
+#ifdef SPANQ_TEST_HASH_BITS
+  return h & ((1ull << SPANQ_TEST_HASH_BITS) - 1);
+#else
+  return h;
+#endif
+}
+
 uint64_t page_hash(uint64_t prev, const int32_t* tok, int32_t n, int32_t page_idx) {
   uint64_t h = prev;
   for (int32_t i = 0; i < n; ++i) h = mix64(h ^ static_cast<uint64_t>(static_cast<uint32_t>(tok[i])));
-  return mix64(h ^ (static_cast<uint64_t>(static_cast<uint32_t>(n)) << 32) ^
-               static_cast<uint64_t>(static_cast<uint32_t>(page_idx)));
+  return stored_hash(mix64(h ^ (static_cast<uint64_t>(static_cast<uint32_t>(n)) << 32) ^
+                           static_cast<uint64_t>(static_cast<uint32_t>(page_idx))));
 }
 
 uint64_t fragment_seed(uint64_t prefix_last_or_root) { return mix64(prefix_last_or_root ^ SPAN_HASH_FRAG_TAG); }
@@ -59,8 +71,8 @@ void chains4(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t p
     for (int c = 0; c < 4; ++c)
       if (base < n[c]) {
         const int32_t m = std::min(ps, n[c] - base);
-        h[c] = mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(m)) << 32) ^
-                     static_cast<uint64_t>(static_cast<uint32_t>(p)));
+        h[c] = stored_hash(mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(m)) << 32) ^
+                                 static_cast<uint64_t>(static_cast<uint32_t>(p))));
         out[c].push_back(h[c]);
       }
   }
@@ -478,6 +490,83 @@ int32_t list_end(const std::vector<KvPage>& kv, int32_t kv0, int32_t kv1, int32_
   if (pad4) end = std::min(kv1, kv0 + ((end - kv0 + 3) / 4) * 4);
   return end;
 }
+
+// Order of the prefill row tiles.
+// Generic kernel: longest key lists first, so the launch ends on short tiles.
+// MFMA kernel with 1, 2, 4 or 8 kv heads: queues for the chip's eight L2 domains
+// (XCDs).  The tiles are cut into R = 8 / kv_heads chunks; queue x serves chunk
+// x / kv_heads for kv head x mod kv_heads, so the work-groups of one XCD read the
+// K/V of one kv head of one group of spans and find the pages the span's other row
+// tiles fetched in their L2.  In a chunk the long tiles come span by span (a span's
+// tiles together, longest first), then its share of the shortest tiles (an eighth
+// of the work), longest first, so that a queue ends on short items.  chunks receives
+// the R + 1 chunk offsets (empty for the generic order).
+void order_prefill(std::vector<WorkTile>& tiles, const std::vector<int32_t>& span_of, const Tiling& t,
+                   std::vector<int32_t>* chunks) {
+  chunks->clear();
+  auto work = [](const WorkTile& w) { return static_cast<int64_t>(w.kv_end - w.kv_begin); };
+  const int hkv = t.kv_heads;
+  if (!t.pad4 || !(hkv == 1 || hkv == 2 || hkv == 4 || hkv == 8) || tiles.empty()) {
+    std::stable_sort(tiles.begin(), tiles.end(),
+                     [&](const WorkTile& a, const WorkTile& b) { return work(a) > work(b); });
+    return;
+  }
+  const int R = 8 / hkv;
+  const size_t n = tiles.size();
+  int64_t total = 0;
+  for (const WorkTile& w : tiles) total += work(w);
+  // the shortest tiles, an eighth of the work
+  std::vector<size_t> by_work(n);
+  for (size_t i = 0; i < n; ++i) by_work[i] = i;
+  std::stable_sort(by_work.begin(), by_work.end(), [&](size_t a, size_t b) { return work(tiles[a]) < work(tiles[b]); });
+  std::vector<char> is_short(n, 0);
+  int64_t short_work = 0;
+  for (size_t i : by_work) {
+    if (8 * short_work >= total) break;
+    is_short[i] = 1;
+    short_work += work(tiles[i]);
+  }
+  // long tiles span by span (spans with more long work first), longest first in a span
+  std::unordered_map<int32_t, int64_t> span_work;
+  for (size_t i = 0; i < n; ++i)
+    if (!is_short[i]) span_work[span_of[i]] += work(tiles[i]);
+  std::vector<size_t> long_list;
+  for (size_t i = 0; i < n; ++i)
+    if (!is_short[i]) long_list.push_back(i);
+  std::stable_sort(long_list.begin(), long_list.end(), [&](size_t a, size_t b) {
+    const int64_t wa = span_work[span_of[a]], wb = span_work[span_of[b]];
+    if (wa != wb) return wa > wb;
+    if (span_of[a] != span_of[b]) return span_of[a] < span_of[b];
+    return work(tiles[a]) > work(tiles[b]);
+  });
+  std::vector<std::vector<size_t>> part(R);
+  const int64_t long_work = total - short_work;
+  int64_t acc = 0;
+  int rho = 0;
+  for (size_t i : long_list) {
+    while (rho + 1 < R && acc * R >= long_work * (rho + 1)) ++rho;
+    part[rho].push_back(i);
+    acc += work(tiles[i]);
+  }
+  // the short tiles, longest first, dealt to the chunk with the least work so far
+  std::vector<int64_t> part_work(R, 0);
+  for (int c = 0; c < R; ++c)
+    for (size_t i : part[c]) part_work[c] += work(tiles[i]);
+  for (auto it = by_work.rbegin(); it != by_work.rend(); ++it) {
+    if (!is_short[*it]) continue;
+    const int c = static_cast<int>(std::min_element(part_work.begin(), part_work.end()) - part_work.begin());
+    part[c].push_back(*it);
+    part_work[c] += work(tiles[*it]);
+  }
+  std::vector<WorkTile> out;
+  out.reserve(n);
+  chunks->push_back(0);
+  for (int c = 0; c < R; ++c) {
+    for (size_t i : part[c]) out.push_back(tiles[i]);
+    chunks->push_back(static_cast<int32_t>(out.size()));
+  }
+  tiles.swap(out);
+}
 }  // namespace
 
 void PoolIndex::build_work(Plan* p, const Tiling& t) {
@@ -502,6 +591,7 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     p->max_pos = std::max(p->max_pos, at + cross.n_tok);
   }
   // ---- prefill: new pages and row tiles of every span that computes pages
+  std::vector<int32_t> tile_span;  // per prefill tile: the span it belongs to
   for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
     const auto& ids = p->query_spans[qi];
     const SpanPlan& prefix = p->spans[ids[0]];
@@ -521,16 +611,14 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
         int32_t n = std::min(t.bm_prefill, s.n_tok - j0);
         int32_t end = list_end(p->kv, kv0, kv1, s.canon0 + j0 + n - 1, t.pad4);
         p->t_prefill.push_back(WorkTile{static_cast<int32_t>(s.row + j0), n, s.canon0 + j0, kv0, end, -1, 0, 0});
+        tile_span.push_back(ids[c]);
         p->rows_prefill.push_back(Plan::RowRun{s.row + j0, n});
         // rows j0..j0+n-1 see pre + j + 1 keys each
         p->prefill_pairs += static_cast<int64_t>(n) * (pre + 1) + static_cast<int64_t>(n) * (2 * j0 + n - 1) / 2;
       }
     }
   }
-  // longest key lists first, so the tail of the launch is short tiles
-  std::stable_sort(p->t_prefill.begin(), p->t_prefill.end(), [](const WorkTile& a, const WorkTile& b) {
-    return (a.kv_end - a.kv_begin) > (b.kv_end - b.kv_begin);
-  });
+  order_prefill(p->t_prefill, tile_span, t, &p->prefill_chunks);
   // ---- cross: pages, key list in query order, split-KV row tiles
   struct CrossTile { int32_t row0, n, pos0, kv0, kv1; };
   std::vector<CrossTile> ct;

@@ -106,6 +106,8 @@ struct Plan {
   std::vector<TileRec> kv_tiles;  // pad4 plans: kv in tiles of four pages
   std::vector<NewPage> k3_prefill, k3_cross;
   std::vector<WorkTile> t_prefill, t_cross;
+  std::vector<int32_t> prefill_chunks;  // MFMA prefill: offsets of the 8 / H_kv tile chunks of
+                                        // the per-XCD queues (empty: one queue)
   std::vector<CombineTile> combine;
   struct RowRun {
     int64_t row0;

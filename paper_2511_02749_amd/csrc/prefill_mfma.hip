@@ -88,8 +88,8 @@ struct PGeo {
   static constexpr bool STAGE_IN_V = D == 128;
   static constexpr int SROW = STAGE_IN_V ? VBYTES / kNW / 32 : 2 * D;
   static constexpr int STOFF = BROFF + BRBYTES;
-  static constexpr int SCHOFF = STOFF + (STAGE_IN_V ? 0 : kNW * 32 * SROW);  // two item indices
-  static constexpr int LDS = SCHOFF + 16;
+  static constexpr int SCHOFF = STOFF + (STAGE_IN_V ? 0 : kNW * 32 * SROW);  // schedule words
+  static constexpr int LDS = SCHOFF + 64;
   static_assert(SROW % 64 == 0 && (2 * D) % SROW == 0, "a pass covers whole 32-dim blocks");
 };
 
@@ -121,7 +121,8 @@ template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void prefill_mfma_kernel(
     const WorkTile* __restrict__ tiles, int n_items, const TileRec* __restrict__ kt, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
-    const float2* __restrict__ rope, unsigned* __restrict__ sched) {
+    const float2* __restrict__ rope, unsigned* __restrict__ sched, const int32_t* __restrict__ xchunks,
+    int n_chunks) {
   using GE = PGeo<D>;
   constexpr int KS = GE::KS, DB = GE::DB, NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
@@ -139,34 +140,86 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   unsigned char* const rt_lds = lds + GE::RTOFF;
   unsigned char* const br_lds = lds + GE::BROFF + wave * 4 * D;
 
-  // ---------------- item schedule.  Item e is (row tile e / hkv, kv head e mod hkv);
-  // row tiles come sorted by key count, longest first.  Work-group b takes items b
-  // and b + grid, then one item at a time from the launch's counter sched[0], so
-  // compute units that run faster take more items (the XCDs of one chip do not run
-  // this kernel equally fast).  The grab for item k + 3 is issued during the last
-  // block of item k and published at the first barrier of item k + 1: while it
-  // computes item k a work-group knows items k .. k + 2, which is as far as the key
-  // tile stream runs ahead.  Item indices at or past n_total stand for "none"; the
-  // counter only grows, so once one grab comes back empty all later ones would too.
+  // ---------------- item schedule.  Item e is (row tile e / hkv, kv head e mod hkv).
+  // Items come from queues, each with its own counter sched[x]:
+  // - one queue (n_chunks == 0): every item, e = r, row tiles longest first;
+  // - eight queues, one per XCD (n_chunks == 8 / hkv): queue x holds the tiles of
+  //   chunk x / hkv for kv head x mod hkv, e = (chunk start + r) hkv + x mod hkv.
+  //   Work-groups are dispatched to the eight XCDs in turn, so work-group b is on
+  //   XCD b mod 8 and takes from queue b mod 8: a queue's K/V pages stay in one L2.
+  // Work-group b takes the first two items of its queue statically (its position
+  // among the queue's work-groups, and that plus their count), then one item at a
+  // time from the queue's counter, so compute units that run faster take more items.
+  // A work-group whose queue runs dry moves on to the next queue (the XCDs of one
+  // chip do not run this kernel equally fast); items are "none" once every queue is
+  // dry.  Counters only grow, so a dry queue stays dry.  (The host uses eight queues
+  // only when every queue holds at least its two static items per work-group.)
   // The grab for item k + 3 is issued right after the first barrier of item k and
   // its result is first read at the first barrier of item k + 1, after that
-  // barrier's full wait: the atomic's latency hides behind a whole item.  (The
-  // build turns off the compiler's atomic optimizer, whose broadcast of the result
-  // would read it, and so wait for it, right after the atomic.)
+  // barrier's full wait: the atomic's latency hides behind a whole item.  Only a
+  // move to another queue waits for an atomic.  (The build turns off the compiler's
+  // atomic optimizer, whose broadcast of the result would read it, and so wait for
+  // it, right after the atomic.)
   const int n_total = n_items * hkv;
   const int grid = gridDim.x;
-  int ec0 = blockIdx.x;                                        // compute item k
-  int ec1 = min(n_total, static_cast<int>(blockIdx.x) + grid);  // item k + 1
-  int ec2 = n_total;                                           // item k + 2, read at item k's first barrier
+  const int n_queues = n_chunks > 0 ? 8 : 1;
+  const int home = n_chunks > 0 ? static_cast<int>(blockIdx.x & 7) : 0;
+  const int q_wgs = n_chunks > 0 ? (grid - home + 7) >> 3 : grid;             // work-groups of the home queue
+  const int q_pos = n_chunks > 0 ? static_cast<int>(blockIdx.x >> 3) : static_cast<int>(blockIdx.x);
+  int h_tile0 = 0, h_head = 0, h_len = n_total;
+  if (n_chunks > 0) {
+    const int c = home / hkv;
+    h_tile0 = xchunks[c];
+    h_len = xchunks[c + 1] - h_tile0;
+    h_head = home - c * hkv;
+  }
+  auto home_item = [&](int r) __attribute__((always_inline)) {
+    return n_chunks > 0 ? (h_tile0 + r) * hkv + h_head : r;
+  };
+  int ec0 = home_item(q_pos);                                          // compute item k
+  int ec1 = q_pos + q_wgs < h_len ? home_item(q_pos + q_wgs) : n_total;  // item k + 1
+  int ec2 = n_total;                                  // item k + 2, read at item k's first barrier
   unsigned grab_raw = 0;   // thread 0: counter value the last grab returned
   bool grabbed = false;    // the last grab was issued (not skipped as known empty)
   int* const sched_lds = reinterpret_cast<int*>(lds + GE::SCHOFF);  // two slots, by item parity
+  // Thread 0's current queue, kept in LDS (only thread 0 touches it), so that it holds
+  // no registers across the key loop: index, first tile, kv head, length, first
+  // counted item, queue moves so far.
+  int* const qs = sched_lds + 4;
+  auto set_queue = [&](int x) __attribute__((always_inline)) {  // thread 0
+    int tile0 = 0, head = 0, len = n_total, first = 2 * grid;
+    if (n_chunks > 0) {
+      const int c = x / hkv;
+      tile0 = xchunks[c];
+      len = xchunks[c + 1] - tile0;
+      head = x - c * hkv;
+      first = 2 * ((grid - x + 7) >> 3);
+    }
+    qs[0] = x;
+    qs[1] = tile0;
+    qs[2] = head;
+    qs[3] = len;
+    qs[4] = first;
+  };
+  if (threadIdx.x == 0) {
+    set_queue(home);
+    qs[5] = 0;
+  }
   auto grab = [&](int last_known) __attribute__((always_inline)) {
     grabbed = last_known < n_total;
-    if (grabbed && threadIdx.x == 0) grab_raw = atomicAdd(sched, 1u);
+    if (grabbed && threadIdx.x == 0) grab_raw = atomicAdd(sched + qs[0], 1u);
   };
-  auto grabbed_item = [&]() __attribute__((always_inline)) {
-    return grabbed ? min(n_total, 2 * grid + static_cast<int>(grab_raw)) : n_total;
+  auto grabbed_item = [&]() __attribute__((always_inline)) {  // thread 0
+    if (!grabbed) return n_total;
+    int r = qs[4] + static_cast<int>(grab_raw);
+    while (r >= qs[3]) {
+      const int moves = qs[5] + 1;
+      qs[5] = moves;
+      if (moves >= n_queues) return n_total;
+      set_queue(qs[0] == 7 ? 0 : qs[0] + 1);
+      r = qs[4] + static_cast<int>(atomicAdd(sched + qs[0], 1u));
+    }
+    return n_chunks > 0 ? (qs[1] + r) * hkv + qs[2] : r;
   };
 
   // ---------------- DMA side: the stream's next tile is tile dk_j of item dk_e, which
@@ -733,16 +786,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // launch; the fence orders this work-group's grabs before its count.
   if (threadIdx.x == 0) {
     __threadfence();
-    if (atomicAdd(sched + 1, 1u) == gridDim.x - 1) {
-      atomicExch(sched, 0u);
-      atomicExch(sched + 1, 0u);
+    if (atomicAdd(sched + kQueueDone, 1u) == gridDim.x - 1) {
+      for (int x = 0; x < n_queues; ++x) atomicExch(sched + x, 0u);
+      atomicExch(sched + kQueueDone, 0u);
     }
   }
 }
 
 template <int D, int G>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           const float2* rope, unsigned* sched, int cus, hipStream_t s) {
+                           const float2* rope, unsigned* sched, const int32_t* chunks_host,
+                           const int32_t* chunks_dev, int n_chunks, int cus, int* queues, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = PGeo<D>::LDS;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_mfma_kernel<D, G>),
@@ -752,33 +806,45 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
   if (items >= (1ll << 30)) return hipErrorInvalidValue;
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus)));
+  // per-XCD queues only if each holds the two static items of each of its work-groups
+  bool xcd = n_chunks > 0 && n_chunks * g.hkv == 8 && grid >= 8 && chunks_host && chunks_dev &&
+             chunks_host[0] == 0 && chunks_host[n_chunks] == n;
+  for (int x = 0; xcd && x < 8; ++x) {
+    const int c = x / g.hkv;
+    xcd = chunks_host[c + 1] - chunks_host[c] >= 2 * ((grid - x + 7) / 8);
+  }
+  if (queues) *queues = xcd ? 8 : 1;
   hipLaunchKernelGGL((prefill_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
-                     g.layer_off, g.hq, g.hkv, scale_log2, rope, sched);
+                     g.layer_off, g.hq, g.hkv, scale_log2, rope, sched, chunks_dev, xcd ? n_chunks : 0);
   return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           const float2* rope, unsigned* sched, int cus, hipStream_t s) {
+                           const float2* rope, unsigned* sched, const int32_t* ch, const int32_t* cd, int nc, int cus,
+                           int* queues, hipStream_t s) {
   switch (g.hq / g.hkv) {
-    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, rope, sched, cus, s);
-    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, rope, sched, cus, s);
-    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, rope, sched, cus, s);
-    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, rope, sched, cus, s);
+    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, rope, sched, ch, cd, nc, cus, queues, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, rope, sched, ch, cd, nc, cus, queues, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, rope, sched, ch, cd, nc, cus, queues, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, rope, sched, ch, cd, nc, cus, queues, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
-                               void* out, const float2* rope, unsigned* sched, hipStream_t s) {
+                               void* out, const float2* rope, unsigned* sched, const int32_t* chunks_host,
+                               const int32_t* chunks_dev, int n_chunks, int* queues, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype) || sched == nullptr) return hipErrorInvalidValue;
   int cus = 0;
   const hipError_t e = cu_count(&cus);
   if (e != hipSuccess) return e;
-  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, rope, sched, cus, s)
-                    : launch_d<64>(g, tiles, n, kt, q, out, rope, sched, cus, s);
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, rope, sched, chunks_host, chunks_dev, n_chunks, cus,
+                                    queues, s)
+                    : launch_d<64>(g, tiles, n, kt, q, out, rope, sched, chunks_host, chunks_dev, n_chunks, cus,
+                                   queues, s);
 }
 
 }  // namespace spanq

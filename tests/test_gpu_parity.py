@@ -228,6 +228,40 @@ def test_c3_full_size_sampled():
     run.close()
 
 
+# (query heads, kv heads, head dim, fragments): enough row tiles that every one of
+# the eight per-XCD queues of the span-prefill kernel holds its work-groups' first
+# two items, for each chunking (8 / kv heads chunks of the tiles)
+XCD_CASES = [(32, 8, 128, 64), (32, 4, 64, 64), (16, 2, 64, 64), (8, 1, 128, 72)]
+
+
+@pytest.mark.parametrize("hq,hkv,d,nf", XCD_CASES, ids=[f"kv{c[1]}" for c in XCD_CASES])
+def test_prefill_per_xcd_queues(hq, hkv, d, nf):
+    """The span-prefill kernel's per-XCD queues (one kv head of one group of spans per
+    queue, work-groups moving on to other queues when theirs runs dry), against the
+    oracle on rows sampled evenly over every query and fragment."""
+    per = nf // 8
+    wl = W.rag_workload("xcd", seed=5, n_q_heads=hq, n_kv_heads=hkv, head_dim=d, hidden=64, prefix_len=64,
+                        pool_size=nf, frag_lens=256, n_queries=8, cross_len=16, mode="direct",
+                        orders=[[per * q + i for i in range(per)] for q in range(8)])
+    run = GpuRun(wl)
+    batch = wl.batches[0]
+    plan = run.run_batch(batch)
+    assert plan.stats()["prefill_queues"] == 8
+    pre, cross = plan.rows()
+    _check_rows(run, batch, pre, TOL["bf16"], limit=512)
+    _check_rows(run, batch, cross, TOL["bf16"], limit=64)
+    run.close()
+
+
+def test_prefill_small_launch_uses_one_queue():
+    wl = W.small_workload()
+    run = GpuRun(wl)
+    plan = run.run_batch(wl.batches[0])
+    assert plan.stats()["prefill_queues"] == 1
+    _check_rows(run, wl.batches[0], _computed_rows(plan), TOL["bf16"])
+    run.close()
+
+
 @pytest.mark.parametrize("cross_len", [1, 4, 16])
 def test_few_cross_rows_over_many_pages(cross_len):
     """The KV page-gather regime: a handful of cross rows per query over a long
