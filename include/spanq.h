@@ -223,6 +223,10 @@ typedef struct {
   int64_t tokens_moved;     /* filled slots of those copies */
   int64_t prefill_queues;   /* work queues of the last bf16 MFMA prefill launch: 8 (one per XCD,
                                each reading one kv head of a group of spans), 1, or 0 (none yet) */
+  int64_t decode_steps;     /* span_plan_decode calls so far */
+  int64_t decode_tokens;    /* tokens they appended */
+  int64_t decode_pages;     /* transient pages they allocated */
+  int64_t decode_pairs;     /* (query, key) pairs of the last decode step's rows */
 } span_stats;
 int span_plan_stats(const span_plan_t* plan, span_stats* stats);
 
@@ -306,6 +310,32 @@ int span_plan_commit(span_plan_t* plan);
  * the work enqueued so far on every stream the plan's attention calls used; the
  * call itself does not wait for the device. */
 int span_plan_destroy(span_plan_t* plan);
+
+/* ---------------------------------------------------------------- nested generation */
+
+/* Decode steps after the first token (section 5.7: a generate G over a cross
+ * segment; section 6: the judge steps of a tree reduction).  A step appends
+ * n_new[q] tokens (caller rows rows[q] .. rows[q] + n_new[q] - 1; 0 for a query
+ * that is not decoding) to the end of each query's cross segment: they take the
+ * positions after it, their keys and values go into the cross segment's pages
+ * (new transient pages as the last one fills, allocated and evicted for like
+ * span_plan's, freed at commit or destroy), and each new row attends to the
+ * prefix, every fragment at its final position and causally to the whole cross
+ * segment, as a cross row would.  The step's work lists are copied on `stream`.
+ * Call after the plan's span_prefill_fragments / span_cross_attend calls for
+ * every layer: once a step is planned those two return SPAN_ESTATE.
+ * SPAN_ENOMEM (plan and pool unchanged) if the pages do not fit; SPAN_ESTATE after
+ * commit; SPAN_EINVAL for plans of span_plan_static (a step allocates).  Host-only
+ * pools plan the step (pages, positions) without device work. */
+int span_plan_decode(span_plan_t* plan, const int32_t* n_new, const int64_t* rows, void* stream);
+
+/* The last decode step for one layer: write the new tokens' keys (rotated at their
+ * positions) and values into their pages, then out[row] = attention of each new
+ * row as span_plan_decode describes.  q, k, v, out as for span_cross_attend (rows
+ * are caller rows).  Calls on a stream other than the step's wait for its upload;
+ * the next step and destroy wait for them. */
+int span_decode_attend(span_plan_t* plan, int32_t layer, const void* q, const void* k, const void* v, void* out,
+                       void* stream);
 
 /* ---------------------------------------------------------------- bulk scheduling */
 
@@ -414,8 +444,10 @@ typedef struct {
   float cross_attention_ms;     /* cross attention (all KV splits) */
   float combine_ms;             /* KV-split merge */
   float page_move_ms;           /* SPAN_FLAG_MATERIALIZE: repositioned copies */
+  float decode_ms;              /* decode steps: page writes, attention and merge */
   int32_t prefill_calls;
   int32_t cross_calls;
+  int32_t decode_calls;
 } span_kernel_times;
 int span_plan_kernel_times(const span_plan_t* plan, span_kernel_times* times);
 

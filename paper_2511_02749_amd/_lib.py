@@ -29,7 +29,7 @@ EXPORTS = [
     "span_plan_evicted", "span_plan_rows", "span_prefill_fragments", "span_cross_attend",
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
-    "span_parse_serialized", "span_bulk_order", "span_plan_moves",
+    "span_parse_serialized", "span_bulk_order", "span_plan_moves", "span_plan_decode", "span_decode_attend",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -74,16 +74,21 @@ class SpanStats(ctypes.Structure):
                                                             ("host_upload_us", ctypes.c_double),
                                                             ("pages_moved", ctypes.c_int64),
                                                             ("tokens_moved", ctypes.c_int64),
-                                                            ("prefill_queues", ctypes.c_int64)]
+                                                            ("prefill_queues", ctypes.c_int64),
+                                                            ("decode_steps", ctypes.c_int64),
+                                                            ("decode_tokens", ctypes.c_int64),
+                                                            ("decode_pages", ctypes.c_int64),
+                                                            ("decode_pairs", ctypes.c_int64)]
 
 
 TIME_FIELDS = ("page_write_prefill_ms", "prefill_attention_ms", "page_write_cross_ms", "cross_attention_ms",
-               "combine_ms", "page_move_ms")
+               "combine_ms", "page_move_ms", "decode_ms")
 
 
 class KernelTimes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in TIME_FIELDS] + [("prefill_calls", ctypes.c_int32),
-                                                            ("cross_calls", ctypes.c_int32)]
+                                                            ("cross_calls", ctypes.c_int32),
+                                                            ("decode_calls", ctypes.c_int32)]
 
 
 class SpanRange(ctypes.Structure):
@@ -142,6 +147,8 @@ def load():
         "span_plan_block_table": (I32, [VP, I32, I32, P(I32), I32, P(I32), P(I32)]),
         "span_plan_evicted": (I32, [VP, P(I32), I32, P(I32)]),
         "span_plan_moves": (I32, [VP, P(I32), I32, P(I32)]),
+        "span_plan_decode": (I32, [VP, P(I32), P(I64), VP]),
+        "span_decode_attend": (I32, [VP, I32, VP, VP, VP, VP, VP]),
         "span_plan_rows": (I32, [VP, P(I64), I64, P(I64), P(I64)]),
         "span_prefill_fragments": (I32, [VP, I32, VP, VP, VP, VP, VP]),
         "span_cross_attend": (I32, [VP, I32, VP, VP, VP, VP, VP]),
@@ -332,7 +339,8 @@ class Plan:
         d = {n: int(getattr(s, n)) for n in STAT_FIELDS}
         d["host_plan_us"], d["host_upload_us"] = float(s.host_plan_us), float(s.host_upload_us)
         d["pages_moved"], d["tokens_moved"] = int(s.pages_moved), int(s.tokens_moved)
-        d["prefill_queues"] = int(s.prefill_queues)
+        for n in ("prefill_queues", "decode_steps", "decode_tokens", "decode_pages", "decode_pairs"):
+            d[n] = int(getattr(s, n))
         return d
 
     def block_table(self, query: int, span: int):
@@ -376,11 +384,24 @@ class Plan:
         _check(load().span_cross_attend(self._h, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                         _stream(stream) if stream is not None else self._stream))
 
+    def decode(self, n_new, rows, stream=None):
+        """Plan a decode step: n_new[q] tokens appended to query q's cross segment, taken
+        from caller rows rows[q] .. (span_plan_decode)."""
+        n = np.ascontiguousarray(n_new, np.int32)
+        r = np.ascontiguousarray(rows, np.int64)
+        _check(load().span_plan_decode(self._h, _i32p(n), r.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                       _stream(stream) if stream is not None else self._stream))
+
+    def decode_attend(self, layer: int, q, k, v, out, stream=None):
+        _check(load().span_decode_attend(self._h, layer, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                         _stream(stream) if stream is not None else self._stream))
+
     def kernel_times(self) -> dict:
         t = KernelTimes()
         _check(load().span_plan_kernel_times(self._h, ctypes.byref(t)))
         d = {n: float(getattr(t, n)) for n in TIME_FIELDS}
         d["prefill_calls"], d["cross_calls"] = int(t.prefill_calls), int(t.cross_calls)
+        d["decode_calls"] = int(t.decode_calls)
         return d
 
     def commit(self):

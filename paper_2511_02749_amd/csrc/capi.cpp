@@ -146,6 +146,29 @@ struct span_plan_t {
   // allocations: nothing to free at destroy, and the region is released for the
   // next such plan on the device.
   bool in_scratch = false;
+  // Nested generation (span_plan_decode, span_decode_attend).  The last decode
+  // step's device data (metadata and split-KV partials, allocated on the decode
+  // stream), its host copy (kept until that copy is known to be done), and the
+  // events of decode attention calls made on other streams: the next step and
+  // destroy make the decode stream wait for them before the data are freed.
+  struct DecodeDev {
+    unsigned char* meta = nullptr;
+    float* part = nullptr;
+    size_t part_o_elems = 0;
+    const SlotWrite* writes = nullptr;
+    const KvPage* kv = nullptr;
+    const TileRec* kt = nullptr;
+    const WorkTile* tiles = nullptr;
+    const CombineTile* cb = nullptr;
+    const float2* rope = nullptr;
+  } dec;
+  std::vector<unsigned char> dec_host;
+  hipEvent_t dec_copied = nullptr;  // recorded after the upload of dec_host
+  hipStream_t dec_stream = nullptr;
+  hipEvent_t dec_ready = nullptr;   // recorded on dec_stream after the upload
+  std::vector<hipEvent_t> dec_pending;
+  bool decoding = false;            // decode steps planned: prefill and cross calls are over
+  std::vector<std::vector<hipEvent_t>> ev_decode;
 };
 
 namespace {
@@ -560,6 +583,10 @@ int span_plan_stats(const span_plan_t* pl, span_stats* s) {
   for (const MovePage& m : P.moves) moved_tok += m.n_valid;
   s->tokens_moved = moved_tok;
   s->prefill_queues = pl->prefill_queues;
+  s->decode_steps = P.decode_steps;
+  s->decode_tokens = P.decode_tokens;
+  s->decode_pages = P.decode_pages;
+  s->decode_pairs = P.dec.pairs;
   return SPAN_OK;
 }
 
@@ -650,6 +677,7 @@ int span_prefill_fragments(span_plan_t* pl, int32_t layer, const void* q, const 
                            void* stream) {
   int rc = attention_common(pl, layer, "span_prefill_fragments");
   if (rc) return rc;
+  if (pl->decoding) return fail(SPAN_ESTATE, "span_prefill_fragments: the plan has decode steps");
   const Plan& P = pl->plan;
   if (P.k3_prefill.empty() && P.t_prefill.empty()) return SPAN_OK;
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_prefill_fragments: null activation pointer");
@@ -678,6 +706,7 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
                       void* stream) {
   int rc = attention_common(pl, layer, "span_cross_attend");
   if (rc) return rc;
+  if (pl->decoding) return fail(SPAN_ESTATE, "span_cross_attend: the plan has decode steps");
   const Plan& P = pl->plan;
   if (P.t_cross.empty()) return SPAN_OK;
   if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_cross_attend: null activation pointer");
@@ -715,6 +744,135 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   return SPAN_OK;
 }
 
+// Make stream s wait for the decode data's last readers: attention calls on other
+// streams (their events) and the previous decode stream.
+static int decode_drain(span_plan_t* pl, hipStream_t s, const char* who) {
+  for (hipEvent_t ev : pl->dec_pending) {
+    hipError_t e = hipStreamWaitEvent(s, ev, 0);
+    pl->pool->order_cache.push_back(ev);
+    if (e != hipSuccess) {
+      pl->dec_pending.clear();
+      return hip_fail(e, who);
+    }
+  }
+  pl->dec_pending.clear();
+  if (pl->dec_stream && pl->dec_stream != s) {
+    hipEvent_t ev = take_order_event(pl->pool);
+    if (!ev) return fail(SPAN_EHIP, std::string(who) + ": event creation");
+    hipError_t e = hipEventRecord(ev, pl->dec_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, ev, 0);
+    pl->pool->order_cache.push_back(ev);
+    if (e != hipSuccess) return hip_fail(e, who);
+  }
+  return SPAN_OK;
+}
+
+int span_plan_decode(span_plan_t* pl, const int32_t* n_new, const int64_t* rows, void* stream) {
+  if (!pl) return fail(SPAN_EINVAL, "span_plan_decode: null plan");
+  if (pl->committed) return fail(SPAN_ESTATE, "span_plan_decode: plan already committed");
+  if (pl->in_scratch) return fail(SPAN_EINVAL, "span_plan_decode: decode steps allocate; not for span_plan_static plans");
+  Plan& P = pl->plan;
+  const size_t nq = P.query_spans.size();
+  if (nq > 0 && (!n_new || !rows)) return fail(SPAN_EINVAL, "span_plan_decode: null argument");
+  std::vector<int32_t> n(n_new, n_new + nq);
+  std::vector<int64_t> r(rows, rows + nq);
+  span_pool* pool = pl->pool;
+  Tiling t = tiling_for(pl->mfma, pl->bm, pool->cfg.num_q_heads, pool->cfg.num_kv_heads);
+  t.materialize = (pool->cfg.flags & SPAN_FLAG_MATERIALIZE) != 0;
+  std::string msg;
+  int rc = pool->index->decode(&P, n, r, t, &msg);
+  if (rc) return fail(rc, "span_plan_decode: " + msg);
+  pl->decoding = true;
+  if (pool->cfg.device < 0) return SPAN_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSetDevice(pool->cfg.device);
+  if (e != hipSuccess) return hip_fail(e, "span_plan_decode: hipSetDevice");
+  // the previous step's device data are freed once their readers are done
+  rc = decode_drain(pl, s, "span_plan_decode");
+  if (rc) return rc;
+  if (pl->dec.meta) (void)hipFreeAsync(pl->dec.meta, s);
+  if (pl->dec.part) (void)hipFreeAsync(pl->dec.part, s);
+  pl->dec = span_plan_t::DecodeDev{};
+  rc = ensure_rope_table(pool, P.max_pos + 1, s);
+  if (rc) return rc;
+  // the host copy of the previous upload is reused once that upload is done
+  if (pl->dec_copied && hipEventSynchronize(pl->dec_copied) != hipSuccess)
+    return fail(SPAN_EHIP, "span_plan_decode: wait for the previous upload");
+  const Plan::DecodeStep& d = P.dec;
+  auto& hb = pl->dec_host;
+  hb.clear();
+  const size_t o_w = put(hb, d.writes), o_kv = put(hb, d.kv), o_kt = put(hb, d.kv_tiles), o_t = put(hb, d.tiles),
+               o_cb = put(hb, d.combine);
+  hb.resize((hb.size() + 255) & ~static_cast<size_t>(255));
+  e = hipMallocAsync(reinterpret_cast<void**>(&pl->dec.meta), hb.size(), s);
+  if (e == hipSuccess) e = hipMemcpyAsync(pl->dec.meta, hb.data(), hb.size(), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !pl->dec_copied) e = hipEventCreateWithFlags(&pl->dec_copied, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(pl->dec_copied, s);
+  pl->dec.part_o_elems = static_cast<size_t>(d.n_parts) * pool->cfg.num_q_heads * pl->bm * pool->cfg.head_dim;
+  const size_t part_bytes =
+      (pl->dec.part_o_elems + static_cast<size_t>(d.n_parts) * pool->cfg.num_q_heads * pl->bm * 2) * sizeof(float);
+  if (e == hipSuccess && d.n_parts > 0) e = hipMallocAsync(reinterpret_cast<void**>(&pl->dec.part), part_bytes, s);
+  if (e == hipSuccess && !pl->dec_ready) {
+    pl->dec_ready = take_order_event(pool);
+    if (!pl->dec_ready) e = hipErrorOutOfMemory;
+  }
+  if (e == hipSuccess) e = hipEventRecord(pl->dec_ready, s);
+  if (e != hipSuccess) return hip_fail(e, "span_plan_decode: device metadata");
+  pl->dec_stream = s;
+  pl->dec.writes = reinterpret_cast<const SlotWrite*>(pl->dec.meta + o_w);
+  pl->dec.kv = reinterpret_cast<const KvPage*>(pl->dec.meta + o_kv);
+  pl->dec.kt = reinterpret_cast<const TileRec*>(pl->dec.meta + o_kt);
+  pl->dec.tiles = reinterpret_cast<const WorkTile*>(pl->dec.meta + o_t);
+  pl->dec.cb = reinterpret_cast<const CombineTile*>(pl->dec.meta + o_cb);
+  pl->dec.rope = pool->rope_tab;
+  return SPAN_OK;
+}
+
+int span_decode_attend(span_plan_t* pl, int32_t layer, const void* q, const void* k, const void* v, void* out,
+                       void* stream) {
+  int rc = attention_common(pl, layer, "span_decode_attend");
+  if (rc) return rc;
+  if (!pl->dec.meta) return fail(SPAN_ESTATE, "span_decode_attend: no decode step planned");
+  const Plan::DecodeStep& d = pl->plan.dec;
+  if (d.tokens == 0) return SPAN_OK;
+  if (!q || !k || !v || !out) return fail(SPAN_EINVAL, "span_decode_attend: null activation pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool foreign = s != pl->dec_stream;
+  if (foreign) {
+    hipError_t e = hipStreamWaitEvent(s, pl->dec_ready, 0);
+    if (e != hipSuccess) return hip_fail(e, "span_decode_attend: stream order");
+  }
+  PoolGeom g = geom(pl, layer);
+  Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 1, s, pl->pool->event_cache);
+  tm.mark(0);
+  hipError_t e = launch_append_kv(g, pl->dec.writes, static_cast<int>(d.writes.size()), k, v, pl->dec.rope, s);
+  if (e != hipSuccess) return hip_fail(e, "span_decode_attend: page write");
+  float* po = pl->dec.part;
+  float* pml = po ? po + pl->dec.part_o_elems : nullptr;
+  const int nt = static_cast<int>(d.tiles.size());
+  if (pl->mfma) {
+    const int nf = d.n_few;
+    e = launch_attn_mfma(g, pl->dec.tiles, nt - nf, pl->dec.kt, q, out, po, pml, pl->dec.rope, s);
+    if (e == hipSuccess && nf > 0)
+      e = launch_few_mfma(g, pl->dec.tiles + (nt - nf), nf, pl->dec.kt, q, po, pml, pl->dec.rope, s);
+  } else {
+    e = launch_attn_generic(g, pl->dec.tiles, nt, pl->dec.kv, q, out, po, pml, pl->dec.rope, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "span_decode_attend: attention");
+  e = launch_combine(g, pl->dec.cb, static_cast<int>(d.combine.size()), po, pml, pl->bm, out, s);
+  if (e != hipSuccess) return hip_fail(e, "span_decode_attend: combine");
+  tm.mark(1);
+  if (!tm.ev.empty()) pl->ev_decode.push_back(tm.ev);
+  if (foreign) {
+    hipEvent_t ev = take_order_event(pl->pool);
+    if (!ev) return fail(SPAN_EHIP, "span_decode_attend: event creation");
+    e = hipEventRecord(ev, s);
+    pl->dec_pending.push_back(ev);
+    if (e != hipSuccess) return hip_fail(e, "span_decode_attend: stream order");
+  }
+  return SPAN_OK;
+}
+
 static float elapsed(hipEvent_t a, hipEvent_t b) {
   float ms = 0.f;
   if (!a || !b || hipEventSynchronize(b) != hipSuccess || hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.f;
@@ -736,6 +894,10 @@ int span_plan_kernel_times(const span_plan_t* pl, span_kernel_times* t) {
     t->combine_ms += elapsed(ev[3], ev[4]);
     t->cross_calls += 1;
   }
+  for (const auto& ev : pl->ev_decode) {
+    t->decode_ms += elapsed(ev[0], ev[1]);
+    t->decode_calls += 1;
+  }
   return SPAN_OK;
 }
 
@@ -752,6 +914,16 @@ int span_plan_destroy(span_plan_t* pl) {
   if (!pl->committed) pl->pool->index->release(&pl->plan);
   release_events(pl->ev_prefill, pl->pool->event_cache);
   release_events(pl->ev_cross, pl->pool->event_cache);
+  release_events(pl->ev_decode, pl->pool->event_cache);
+  // decode data: wait for their readers on the plan's stream, then free there
+  if (pl->dec.meta || !pl->dec_pending.empty()) (void)decode_drain(pl, pl->stream, "span_plan_destroy");
+  if (pl->dec.meta) (void)hipFreeAsync(pl->dec.meta, pl->stream);
+  if (pl->dec.part) (void)hipFreeAsync(pl->dec.part, pl->stream);
+  if (pl->dec_ready) pl->pool->order_cache.push_back(pl->dec_ready);
+  if (pl->dec_copied) {
+    (void)hipEventSynchronize(pl->dec_copied);
+    (void)hipEventDestroy(pl->dec_copied);
+  }
   // work enqueued on other streams must end before the plan's memory is released
   for (hipStream_t s : pl->foreign) {
     hipEvent_t ev = take_order_event(pl->pool);

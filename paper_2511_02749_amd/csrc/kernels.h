@@ -20,6 +20,11 @@ struct PoolGeom {
 hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n_pages, const void* k,
                              const void* v, const float2* rope, hipStream_t s);
 
+// Nested generation: write decoded tokens' keys (rotated at their positions) and
+// values into slots of their cross pages, leaving the pages' other slots as they are.
+hipError_t launch_append_kv(const PoolGeom& g, const SlotWrite* writes, int n_writes, const void* k, const void* v,
+                            const float2* rope, hipStream_t s);
+
 // Materialised repositioning: copy each move's source page to its destination
 // page with the keys rotated by the move's delta (values copied unchanged).
 hipError_t launch_move_pages(const PoolGeom& g, const MovePage* moves, int n_moves, const float2* rope,

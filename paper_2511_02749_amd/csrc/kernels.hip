@@ -134,6 +134,78 @@ hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, con
   return rope_write_t<float, 64>(g, pages, n, k, v, rope, s);
 }
 
+// ------------------------------------------------------------------ decode writes
+// Decoded tokens into their cross pages: one work-group per SlotWrite.  Keys are
+// rotated at their positions into slots slot0 .., values go to the transposed slot
+// positions; the page's other slots are not touched (earlier tokens of the page,
+// and the zeros past the end that K3 or an earlier write left).
+template <typename T, int D>
+__global__ __launch_bounds__(256) void append_kv_kernel(const SlotWrite* __restrict__ writes,
+                                                        const T* __restrict__ k, const T* __restrict__ v,
+                                                        T* __restrict__ pool, int64_t layer_off, int hkv,
+                                                        const float2* __restrict__ rope) {
+  constexpr int E = Chunk16<T>::E;
+  constexpr int H = D / 2;
+  const SlotWrite w = writes[blockIdx.x];
+  const int64_t page_elems = 2ll * hkv * kPage * D;
+  T* kp = pool + layer_off + static_cast<int64_t>(w.page_id) * page_elems;
+  T* vp = kp + static_cast<int64_t>(hkv) * kPage * D;
+  // K: item (head, token j, chunk of E pairs (i, i + H))
+  for (int e = threadIdx.x; e < hkv * w.n * (H / E); e += blockDim.x) {
+    const int qc = e % (H / E);
+    const int hj = e / (H / E);
+    const int j = hj % w.n;
+    const int h = hj / w.n;
+    const T* src = k + (static_cast<int64_t>(w.src_row + j) * hkv + h) * D + qc * E;
+    const Chunk16<T> x0 = load16(src), x1 = load16(src + H);
+    const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(w.pos0 + j) * H + qc * E);
+    Chunk16<T> y0, y1;
+#pragma unroll
+    for (int u2 = 0; u2 < E / 2; ++u2) {
+      const float4 c = cs4[u2];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int u = 2 * u2 + b;
+        const float cs = b ? c.z : c.x, sn = b ? c.w : c.y;
+        const float a0 = to_f32(x0.x[u]), a1 = to_f32(x1.x[u]);
+        y0.x[u] = from_f32<T>(a0 * cs - a1 * sn);
+        y1.x[u] = from_f32<T>(a1 * cs + a0 * sn);
+      }
+    }
+    T* dst = kp + (static_cast<int64_t>(h) * kPage + w.slot0 + j) * D + qc * E;
+    store16(dst, y0);
+    store16(dst + H, y1);
+  }
+  // V: element (head, d, token j) to [head][d][v_pos(slot0 + j)]
+  for (int e = threadIdx.x; e < hkv * D * w.n; e += blockDim.x) {
+    const int j = e % w.n;
+    const int hd = e / w.n;
+    const int d = hd % D;
+    const int h = hd / D;
+    vp[(static_cast<int64_t>(h) * D + d) * kPage + v_pos(w.slot0 + j)] =
+        v[(static_cast<int64_t>(w.src_row + j) * hkv + h) * D + d];
+  }
+}
+
+template <typename T, int D>
+static hipError_t append_kv_t(const PoolGeom& g, const SlotWrite* w, int n, const void* k, const void* v,
+                              const float2* rope, hipStream_t s) {
+  hipLaunchKernelGGL((append_kv_kernel<T, D>), dim3(n), dim3(256), 0, s, w, static_cast<const T*>(k),
+                     static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv, rope);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_kv(const PoolGeom& g, const SlotWrite* writes, int n, const void* k, const void* v,
+                            const float2* rope, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (g.dtype == SPAN_BF16) {
+    if (g.d == 128) return append_kv_t<bf16_t, 128>(g, writes, n, k, v, rope, s);
+    return append_kv_t<bf16_t, 64>(g, writes, n, k, v, rope, s);
+  }
+  if (g.d == 128) return append_kv_t<float, 128>(g, writes, n, k, v, rope, s);
+  return append_kv_t<float, 64>(g, writes, n, k, v, rope, s);
+}
+
 // ------------------------------------------------------------------ page moves
 // Materialised repositioning: two work-groups per MovePage, one for the keys
 // (blockIdx.y 0) and one for the values.  Keys of every kv head and slot are

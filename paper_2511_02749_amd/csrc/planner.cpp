@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <limits>
 
 #include "../../include/spanq.h"
 
@@ -569,6 +570,84 @@ void order_prefill(std::vector<WorkTile>& tiles, const std::vector<int32_t>& spa
 }
 }  // namespace
 
+namespace {
+// Row tiles of cross attention (cross and decode rows) before the KV split.
+struct CrossTile {
+  int32_t row0, n, pos0, kv0, kv1;
+};
+
+// The key list a query's cross (and decode) rows read: the prefix, each fragment
+// at its final positions (its repositioned copies at delta 0 when it has them, else
+// its pages with the delta still to apply) and the cross segment's pages.
+void append_query_keys(const Plan& p, const std::vector<int>& ids, int32_t ps, bool pad4, std::vector<KvPage>& kv) {
+  for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
+    const SpanPlan& s = p.spans[ids[c]];
+    if (!s.moved.empty())
+      append_span(kv, s.moved, s.n_tok, ps, s.final0, 0, pad4);  // copies at final positions
+    else
+      append_span(kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, pad4);
+  }
+  const SpanPlan& cross = p.spans[ids.back()];
+  append_span(kv, cross.pages, cross.n_tok, ps, cross.final0, 0, pad4);
+}
+
+// Split the keys of the row tiles into the same number of parts (enough work items
+// for the launch, at least min_split_pages per part), tiles with more than one part
+// (or two key groups) writing partials that a combine tile merges; few-row
+// two-key-group tiles go last.
+void tile_cross(const std::vector<CrossTile>& ct, int32_t max_pages, const Tiling& t, std::vector<WorkTile>* tiles,
+                std::vector<CombineTile>* combine, int32_t* n_parts, int32_t* n_few, int32_t* kv_splits) {
+  int32_t splits = 1;
+  if (!ct.empty()) {
+    int64_t items = static_cast<int64_t>(ct.size()) * t.kv_heads;
+    int64_t want = (t.target_items + items - 1) / items;
+    int64_t cap = std::max<int64_t>(1, max_pages / t.min_split_pages);
+    splits = static_cast<int32_t>(std::max<int64_t>(1, std::min(want, cap)));
+  }
+  *kv_splits = splits;
+  const int32_t align = t.pad4 ? 4 : 1;
+  for (const CrossTile& c : ct) {
+    int32_t n_pages = c.kv1 - c.kv0;
+    int32_t chunk = (n_pages + splits - 1) / splits;
+    chunk = ((chunk + align - 1) / align) * align;   // splits cut at whole tiles
+    int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
+    const bool two = c.n <= t.two_group_rows;     // each split writes two partials
+    if (parts <= 1 && !two) {
+      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});
+      continue;
+    }
+    int32_t part0 = *n_parts;
+    for (int32_t s = 0; s < parts; ++s) {
+      int32_t b = c.kv0 + s * chunk;
+      int32_t e = std::min(c.kv1, b + chunk);
+      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, b, e, *n_parts, two ? kTwoKeyGroups : 0, 0});
+      *n_parts += two ? 2 : 1;
+    }
+    combine->push_back(CombineTile{c.row0, c.n, part0, *n_parts - part0});
+  }
+  // Few-row two-key-group tiles last, for the kernel that takes them.
+  *n_few = 0;
+  if (t.few_rows > 0) {
+    auto few = [&](const WorkTile& w) { return (w.flags & kTwoKeyGroups) != 0 && w.n_rows <= t.few_rows; };
+    std::stable_partition(tiles->begin(), tiles->end(), [&](const WorkTile& w) { return !few(w); });
+    *n_few = static_cast<int32_t>(std::count_if(tiles->begin(), tiles->end(), few));
+  }
+}
+
+// Tiled key lists: every list (and every split of one) starts at a multiple of four
+// pages, so kv[4i .. 4i + 3] is a tile.
+void tile_records(const std::vector<KvPage>& kv, bool pad4, std::vector<TileRec>* out) {
+  out->clear();
+  if (!pad4) return;
+  out->reserve(kv.size() / 4);
+  for (size_t i = 0; i + 3 < kv.size(); i += 4) {
+    const KvPage* k = &kv[i];
+    out->push_back(TileRec{{k[0].page_id, k[1].page_id, k[2].page_id, k[3].page_id}, k[0].pos0,
+                           k[0].n_valid + k[1].n_valid + k[2].n_valid + k[3].n_valid, k[0].delta, 0});
+  }
+}
+}  // namespace
+
 void PoolIndex::build_work(Plan* p, const Tiling& t) {
   const int32_t ps = page_size_;
   p->bm_cross = t.bm_cross;
@@ -620,7 +699,6 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
   }
   order_prefill(p->t_prefill, tile_span, t, &p->prefill_chunks);
   // ---- cross: pages, key list in query order, split-KV row tiles
-  struct CrossTile { int32_t row0, n, pos0, kv0, kv1; };
   std::vector<CrossTile> ct;
   int32_t max_pages = 0;
   for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
@@ -631,14 +709,7 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
       p->k3_cross.push_back(NewPage{cross.pages[pg], std::min<int32_t>(ps, cross.n_tok - static_cast<int32_t>(pg) * ps),
                                     static_cast<int32_t>(cross.row + pg * ps), cross.final0 + static_cast<int32_t>(pg) * ps});
     const int32_t kv0 = static_cast<int32_t>(p->kv.size());
-    for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
-      const SpanPlan& s = p->spans[ids[c]];
-      if (!s.moved.empty())
-        append_span(p->kv, s.moved, s.n_tok, ps, s.final0, 0, t.pad4);  // copies at final positions
-      else
-        append_span(p->kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, t.pad4);
-    }
-    append_span(p->kv, cross.pages, cross.n_tok, ps, cross.final0, 0, t.pad4);
+    append_query_keys(*p, ids, ps, t.pad4, p->kv);
     const int32_t kv1 = static_cast<int32_t>(p->kv.size());
     p->cross_kv_pages += kv1 - kv0;
     for (int32_t j0 = 0; j0 < cross.n_tok; j0 += t.bm_cross) {
@@ -650,52 +721,85 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
       p->cross_pairs += static_cast<int64_t>(n) * (cross.final0 + 1) + static_cast<int64_t>(n) * (2 * j0 + n - 1) / 2;
     }
   }
-  int32_t splits = 1;
-  if (!ct.empty()) {
-    int64_t items = static_cast<int64_t>(ct.size()) * t.kv_heads;
-    int64_t want = (t.target_items + items - 1) / items;
-    int64_t cap = std::max<int64_t>(1, max_pages / t.min_split_pages);
-    splits = static_cast<int32_t>(std::max<int64_t>(1, std::min(want, cap)));
+  tile_cross(ct, max_pages, t, &p->t_cross, &p->combine, &p->n_parts, &p->n_cross_few, &p->kv_splits);
+  tile_records(p->kv, t.pad4, &p->kv_tiles);
+}
+
+int PoolIndex::decode(Plan* p, const std::vector<int32_t>& n_new, const std::vector<int64_t>& rows,
+                      const Tiling& t, std::string* msg) {
+  const int32_t ps = page_size_;
+  const size_t nq = p->query_spans.size();
+  if (n_new.size() != nq || rows.size() != nq) {
+    *msg = "decode: one token count and one row per query";
+    return SPAN_EINVAL;
   }
-  p->kv_splits = splits;
-  const int32_t align = t.pad4 ? 4 : 1;
-  for (const CrossTile& c : ct) {
-    int32_t n_pages = c.kv1 - c.kv0;
-    int32_t chunk = (n_pages + splits - 1) / splits;
-    chunk = ((chunk + align - 1) / align) * align;   // splits cut at whole tiles
-    int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
-    const bool two = c.n <= t.two_group_rows;     // each split writes two partials
-    if (parts <= 1 && !two) {
-      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});
-      continue;
+  int64_t need = 0, total = 0;
+  for (size_t q = 0; q < nq; ++q) {
+    const SpanPlan& cross = p->spans[p->query_spans[q].back()];
+    const int64_t n = n_new[q];
+    if (n < 0 || (n > 0 && (rows[q] < 0 || rows[q] + n > std::numeric_limits<int32_t>::max())) ||
+        static_cast<int64_t>(cross.final0) + cross.n_tok + n >= std::numeric_limits<int32_t>::max() / 2) {
+      *msg = "decode: bad token count or row";
+      return SPAN_EINVAL;
     }
-    int32_t part0 = p->n_parts;
-    for (int32_t s = 0; s < parts; ++s) {
-      int32_t b = c.kv0 + s * chunk;
-      int32_t e = std::min(c.kv1, b + chunk);
-      p->t_cross.push_back(WorkTile{c.row0, c.n, c.pos0, b, e, p->n_parts, two ? kTwoKeyGroups : 0, 0});
-      p->n_parts += two ? 2 : 1;
+    need += (cross.n_tok + n + ps - 1) / ps - (cross.n_tok + ps - 1) / ps;
+    total += n;
+  }
+  if (need > free_count() + n_evictable_) {
+    *msg = "pool exhausted: decode needs " + std::to_string(need) + " pages, " + std::to_string(free_count()) +
+           " free, " + std::to_string(n_evictable_) + " evictable";
+    return SPAN_ENOMEM;
+  }
+  Plan::DecodeStep& d = p->dec;
+  d = Plan::DecodeStep{};
+  std::vector<CrossTile> ct;
+  int32_t max_pages = 0;
+  for (size_t q = 0; q < nq; ++q) {
+    const int32_t n = n_new[q];
+    if (n == 0) continue;
+    const auto& ids = p->query_spans[q];
+    SpanPlan& cross = p->spans[ids.back()];
+    const int32_t cur = cross.n_tok;
+    while (static_cast<int64_t>(cross.pages.size()) * ps < static_cast<int64_t>(cur) + n) {
+      if (free_count() == 0) evict_one(p);
+      const int32_t pid = pop_free();
+      PageRec& r = pages_[pid];
+      r = PageRec{};
+      r.last_use = p->tick;
+      r.pins = 1;
+      r.used = true;
+      p->new_pages.push_back(pid);
+      p->cross_pages.push_back(pid);
+      cross.pages.push_back(pid);
+      ++d.pages_new;
     }
-    p->combine.push_back(CombineTile{c.row0, c.n, part0, p->n_parts - part0});
-  }
-  // Few-row two-key-group tiles last, for the kernel that takes them.
-  p->n_cross_few = 0;
-  if (t.few_rows > 0) {
-    auto few = [&](const WorkTile& w) { return (w.flags & kTwoKeyGroups) != 0 && w.n_rows <= t.few_rows; };
-    std::stable_partition(p->t_cross.begin(), p->t_cross.end(), [&](const WorkTile& w) { return !few(w); });
-    p->n_cross_few = static_cast<int32_t>(std::count_if(p->t_cross.begin(), p->t_cross.end(), few));
-  }
-  // Tiled key lists: every list (and every split of one) starts at a multiple of
-  // four pages, so kv[4i .. 4i + 3] is a tile.
-  p->kv_tiles.clear();
-  if (t.pad4) {
-    p->kv_tiles.reserve(p->kv.size() / 4);
-    for (size_t i = 0; i + 3 < p->kv.size(); i += 4) {
-      const KvPage* k = &p->kv[i];
-      p->kv_tiles.push_back(TileRec{{k[0].page_id, k[1].page_id, k[2].page_id, k[3].page_id}, k[0].pos0,
-                                    k[0].n_valid + k[1].n_valid + k[2].n_valid + k[3].n_valid, k[0].delta, 0});
+    const int32_t pos_first = cross.final0 + cur;
+    for (int32_t i = 0; i < n;) {
+      const int32_t pg = (cur + i) / ps, s0 = (cur + i) % ps, m = std::min(ps - s0, n - i);
+      d.writes.push_back(SlotWrite{cross.pages[pg], s0, m, static_cast<int32_t>(rows[q] + i), pos_first + i, {0, 0, 0}});
+      i += m;
+    }
+    cross.n_tok = cur + n;
+    p->max_pos = std::max(p->max_pos, cross.final0 + cross.n_tok);
+    const int32_t kv0 = static_cast<int32_t>(d.kv.size());
+    append_query_keys(*p, ids, ps, t.pad4, d.kv);
+    const int32_t kv1 = static_cast<int32_t>(d.kv.size());
+    for (int32_t j0 = 0; j0 < n; j0 += t.bm_cross) {
+      const int32_t nn = std::min(t.bm_cross, n - j0);
+      const int32_t end = list_end(d.kv, kv0, kv1, pos_first + j0 + nn - 1, t.pad4);
+      ct.push_back(CrossTile{static_cast<int32_t>(rows[q] + j0), nn, pos_first + j0, kv0, end});
+      max_pages = std::max(max_pages, end - kv0);
+      d.rows.push_back(Plan::RowRun{rows[q] + j0, nn});
+      d.pairs += static_cast<int64_t>(nn) * (pos_first + j0 + 1) + static_cast<int64_t>(nn) * (nn - 1) / 2;
     }
   }
+  tile_cross(ct, max_pages, t, &d.tiles, &d.combine, &d.n_parts, &d.n_few, &d.kv_splits);
+  tile_records(d.kv, t.pad4, &d.kv_tiles);
+  d.tokens = total;
+  p->decode_steps += 1;
+  p->decode_tokens += total;
+  p->decode_pages += d.pages_new;
+  return SPAN_OK;
 }
 
 void PoolIndex::commit(Plan* p) {

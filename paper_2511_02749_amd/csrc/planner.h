@@ -122,6 +122,20 @@ struct Plan {
 
   int64_t pages_hit = 0, pages_new = 0, tokens_hit = 0, tokens_new = 0, tokens_cross = 0;
   int64_t prefill_pairs = 0, cross_pairs = 0, cross_kv_pages = 0;
+
+  // Nested generation: the work of the last decode step (tokens appended to each
+  // query's cross segment), and totals over all steps.
+  struct DecodeStep {
+    std::vector<SlotWrite> writes;
+    std::vector<KvPage> kv;
+    std::vector<TileRec> kv_tiles;
+    std::vector<WorkTile> tiles;
+    std::vector<CombineTile> combine;
+    std::vector<RowRun> rows;
+    int32_t n_parts = 0, n_few = 0, kv_splits = 1;
+    int64_t tokens = 0, pages_new = 0, pairs = 0;
+  } dec;
+  int64_t decode_steps = 0, decode_tokens = 0, decode_pages = 0;
 };
 
 class PoolIndex {
@@ -131,6 +145,11 @@ class PoolIndex {
   // Returns 0, or -2 (pool full, unchanged), -1 (bad input) with msg set.
   int plan(const std::vector<QueryIn>& qs, bool build_work, const Tiling& tiling, Plan* out,
            std::string* msg);
+  // Append n_new[q] decoded tokens (caller rows rows[q] ..) to each query's cross
+  // segment: pages for them (transient, like cross pages) and the decode step's
+  // work lists in p->dec.  Returns 0, -2 (pool full; plan and pool unchanged) or -1.
+  int decode(Plan* p, const std::vector<int32_t>& n_new, const std::vector<int64_t>& rows, const Tiling& tiling,
+             std::string* msg);
   void commit(Plan* p);
   void release(Plan* p);  // destroy without commit
   void reset();

@@ -44,9 +44,11 @@
 // 3-slot K ring and a 4-slot V ring (132 KiB of LDS at head dim 128 with the rotary
 // rows).  Both tiles' LDS layouts are read conflict-free by 16 consecutive lanes.
 //
-// Work-groups take items from a per-launch counter (three items ahead), so compute
-// units that run slower take fewer; an item's output rows leave through an LDS
-// staging area as whole row segments at the next item's first barrier.
+// Work-groups take items from queue counters (three items ahead), so compute units
+// that run slower take fewer; with eight queues, one per XCD, the work-groups of an
+// XCD share one kv head of a group of spans, so pages that a span's row tiles all
+// read are fetched into that XCD's L2 once.  An item's output rows leave through an
+// LDS staging area as whole row segments at the next item's first barrier.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

@@ -48,6 +48,18 @@ struct MovePage {
   int32_t n_valid;
 };
 
+// Decoded tokens to write into a page: slots slot0 .. slot0 + n - 1 from caller rows
+// src_row .., keys rotated at positions pos0 ..; the page's other slots are left as
+// they are.
+struct SlotWrite {
+  int32_t page_id;
+  int32_t slot0;
+  int32_t n;
+  int32_t src_row;
+  int32_t pos0;
+  int32_t pad[3];
+};
+
 // A tile of up to BM consecutive query rows of one span, against the key pages
 // kv[kv_begin, kv_end).  part < 0: write the normalised output; else write the
 // unnormalised partial (one KV split) into partial slot `part`.  With
