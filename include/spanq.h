@@ -432,6 +432,17 @@ int span_model_destroy(span_model* model);
 int span_model_forward(span_model* model, span_plan_t* plan, const int32_t* row_tokens, int64_t n_rows,
                        int32_t n_layers, void* hidden_out, float* logits_out, int32_t* first_tokens, void* stream);
 
+/* One greedy decode step of nested generation (sections 5.7 and 6), after
+ * span_model_forward on the same plan: every query q with tokens[q] >= 0 feeds that
+ * token (typically the one it generated last) as the next token of its cross
+ * segment; it runs through every layer, attending as span_plan_decode describes
+ * (which this calls, one token per decoding query), and the final norm, LM head and
+ * argmax give next_tokens[q] (-1 for queries with tokens[q] < 0).  logits_out, if
+ * not NULL, receives [decoding queries][vocab] float32, in query order.  The
+ * model's own buffers hold the step's activations. */
+int span_model_decode(span_model* model, span_plan_t* plan, const int32_t* tokens, float* logits_out,
+                      int32_t* next_tokens, void* stream);
+
 /* ---------------------------------------------------------------- debug */
 
 /* Kernel durations of a plan's launches on a pool created with SPAN_FLAG_TIMING,

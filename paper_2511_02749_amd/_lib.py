@@ -30,6 +30,7 @@ EXPORTS = [
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
     "span_parse_serialized", "span_bulk_order", "span_plan_moves", "span_plan_decode", "span_decode_attend",
+    "span_model_decode",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -140,6 +141,7 @@ def load():
         "span_model_create": (I32, [VP, P(ModelConfig), P(VP)]),
         "span_model_destroy": (I32, [VP]),
         "span_model_forward": (I32, [VP, VP, P(I32), I64, I32, VP, VP, P(I32), VP]),
+        "span_model_decode": (I32, [VP, VP, P(I32), VP, P(I32), VP]),
         "span_bulk_order": (I32, [VP, P(SpanQuery), I32, P(I32)]),
         "span_parse_serialized": (I32, [P(I32), I64, I32, P(I32), P(SpanRange), I32, P(I32), P(SpanRange),
                                         P(SpanRange)]),
@@ -227,7 +229,10 @@ class Pool:
 
     def __init__(self, *, num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str = "bf16",
                  num_layers: int = 1, rope_theta: float = 1e4, page_size: int = 16, device: int = 0,
-                 hash_mode: str = "span", kernel: str = "auto", timing: bool = False, materialize: bool = False):
+                 hash_mode: str = "span", kernel: str = "auto", timing: bool = False, materialize: bool = False,
+                 device_buf=None):
+        """device_buf: optional caller-owned device memory for the pages (a torch tensor of
+        at least span_pool_bytes bytes, kept referenced by the pool)."""
         lib = load()
         self.cfg = PoolConfig(num_layers=num_layers, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                               head_dim=head_dim, page_size=page_size,
@@ -236,7 +241,9 @@ class Pool:
                               kernel=SPAN_KERNEL[kernel], device=device,
                               flags=(SPAN_FLAG_TIMING if timing else 0) | (SPAN_FLAG_MATERIALIZE if materialize else 0),
                               rope_theta=rope_theta,
-                              num_pages=num_pages, device_buf=None, device_bytes=0)
+                              num_pages=num_pages, device_buf=_ptr(device_buf),
+                              device_bytes=0 if device_buf is None else device_buf.numel() * device_buf.element_size())
+        self._buf = device_buf
         self.dtype = dtype
         self._plans = weakref.WeakSet()
         self._h = ctypes.c_void_p()
@@ -458,6 +465,15 @@ class Model:
                                          _i32p(toks) if toks is not None else None,
                                          _stream(stream) if stream is not None else plan._stream))
         return [int(t) for t in toks[: plan.n_queries]] if toks is not None else None
+
+    def decode(self, plan: "Plan", tokens, logits_out=None, stream=None):
+        """One greedy decode step (span_model_decode): tokens[q] >= 0 is fed to query q;
+        returns the next token of each query (-1 where tokens[q] < 0)."""
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        nxt = np.zeros(max(1, plan.n_queries), np.int32)
+        _check(load().span_model_decode(self._h, plan._h, _i32p(t), _ptr(logits_out), _i32p(nxt),
+                                        _stream(stream) if stream is not None else plan._stream))
+        return [int(x) for x in nxt[: plan.n_queries]]
 
     def close(self):
         if self._h:

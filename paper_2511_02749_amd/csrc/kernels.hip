@@ -137,8 +137,10 @@ hipError_t launch_rope_write(const PoolGeom& g, const NewPage* pages, int n, con
 // ------------------------------------------------------------------ decode writes
 // Decoded tokens into their cross pages: one work-group per SlotWrite.  Keys are
 // rotated at their positions into slots slot0 .., values go to the transposed slot
-// positions; the page's other slots are not touched (earlier tokens of the page,
-// and the zeros past the end that K3 or an earlier write left).
+// positions.  A write at slot 0 opens a page fresh from the free list, whatever it
+// held before: it also zeroes the slots past its tokens, as K3 does, so that masked
+// keys never feed a stale NaN into the P.V product.  Other writes leave the page's
+// other slots alone (earlier tokens, and the zeros past the end).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void append_kv_kernel(const SlotWrite* __restrict__ writes,
                                                         const T* __restrict__ k, const T* __restrict__ v,
@@ -184,6 +186,23 @@ __global__ __launch_bounds__(256) void append_kv_kernel(const SlotWrite* __restr
     const int h = hd / D;
     vp[(static_cast<int64_t>(h) * D + d) * kPage + v_pos(w.slot0 + j)] =
         v[(static_cast<int64_t>(w.src_row + j) * hkv + h) * D + d];
+  }
+  if (w.slot0 == 0 && w.n < kPage) {
+    const int rest = kPage - w.n;  // slots n .. 15
+    Chunk16<T> zero;
+#pragma unroll
+    for (int u = 0; u < E; ++u) zero.x[u] = from_f32<T>(0.f);
+    for (int e = threadIdx.x; e < hkv * rest * (D / E); e += blockDim.x) {
+      const int c = e % (D / E);
+      const int hs = e / (D / E);
+      const int h = hs / rest, slot = w.n + hs % rest;
+      store16(kp + (static_cast<int64_t>(h) * kPage + slot) * D + c * E, zero);
+    }
+    for (int e = threadIdx.x; e < hkv * D * rest; e += blockDim.x) {
+      const int slot = w.n + e % rest;
+      const int hd = e / rest;
+      vp[static_cast<int64_t>(hd) * kPage + v_pos(slot)] = from_f32<T>(0.f);
+    }
   }
 }
 

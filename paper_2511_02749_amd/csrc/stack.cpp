@@ -188,6 +188,126 @@ int check_config(span_pool* pool, const span_model_config* c) {
   return SPAN_OK;
 }
 
+// The pinned staging area for a call's row lists, at least n words, once the
+// previous call's upload from it is done.
+int stage_area(span_model* m, size_t n, int32_t** out, const char* who) {
+  hipError_t e = hipEventSynchronize(m->staged);  // the previous upload has left the staging area
+  if (e == hipSuccess && n > m->host_stage_cap) {
+    if (m->host_stage) e = hipHostFree(m->host_stage);
+    m->host_stage = nullptr;
+    m->host_stage_cap = 0;
+    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->host_stage), n * sizeof(int32_t), 0);
+    if (e == hipSuccess) m->host_stage_cap = n;
+  }
+  if (e != hipSuccess) return hip_err(e, std::string(who) + ": pinned staging");
+  *out = m->host_stage;
+  return SPAN_OK;
+}
+
+// Buffers for T compact rows whose attention rows lie in [0, R), then the upload of
+// the row list (compact row i -> attention row), the tokens and the LM-head rows.
+// Buffers grow with the stream drained, so no launch still reads the old ones.
+int prepare(span_model* m, int64_t T, int64_t R, const int32_t* h_rows, const int32_t* h_toks, const int32_t* h_last,
+            int nh, hipStream_t s, const char* who) {
+  const span_model_config& c = m->cfg;
+  const int H = c.hidden, hq = c.num_q_heads, hkv = c.num_kv_heads, d = c.head_dim, F = c.ffn, V = c.vocab;
+  const int64_t qkv_w = static_cast<int64_t>(hq + 2 * hkv) * d;
+  const size_t bf = 2;
+  const size_t Tz = static_cast<size_t>(T), Rz = static_cast<size_t>(R);
+  struct Need {
+    Buf* b;
+    size_t bytes;
+  } needs[] = {
+      {&m->x, Tz * H * bf}, {&m->n, Tz * H * bf}, {&m->qkv, Tz * qkv_w * bf}, {&m->oc, Tz * hq * d * bf},
+      {&m->gu, Tz * 2 * F * bf}, {&m->act, Tz * F * bf}, {&m->q, Rz * hq * d * bf}, {&m->k, Rz * hkv * d * bf},
+      {&m->v, Rz * hkv * d * bf}, {&m->o, Rz * hq * d * bf}, {&m->rows, Tz * 4 + 4}, {&m->toks, Tz * 4 + 4},
+      {&m->last, static_cast<size_t>(nh) * 4 + 32}, {&m->nf, static_cast<size_t>(8) * H * bf},
+      {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
+      {&m->tok_out, 8 * 4}};
+  bool grow = false;
+  for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
+  hipError_t e = hipSuccess;
+  if (grow) {
+    e = hipStreamSynchronize(s);
+    for (const Need& nd : needs)
+      if (e == hipSuccess) e = nd.b->ensure(nd.bytes);
+    if (e != hipSuccess) return hip_err(e, std::string(who) + ": activation buffers");
+  }
+  e = T > 0 ? hipMemcpyAsync(m->rows.p, h_rows, Tz * 4, hipMemcpyHostToDevice, s) : hipSuccess;
+  if (e == hipSuccess && T > 0) e = hipMemcpyAsync(m->toks.p, h_toks, Tz * 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && nh > 0) e = hipMemcpyAsync(m->last.p, h_last, static_cast<size_t>(nh) * 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipEventRecord(m->staged, s);
+  if (e != hipSuccess) return hip_err(e, std::string(who) + ": row lists");
+  return SPAN_OK;
+}
+
+// Embeddings of the T compact rows, then n_layers decoder layers; attn(l) runs the
+// span attention of layer l on the q/k/v/o buffers.
+template <class Attn>
+int run_layers(span_model* m, int64_t T, int n_layers, hipStream_t s, const char* who, Attn attn) {
+  const span_model_config& c = m->cfg;
+  const int H = c.hidden, hq = c.num_q_heads, hkv = c.num_kv_heads, d = c.head_dim, F = c.ffn;
+  const int64_t qkv_w = static_cast<int64_t>(hq + 2 * hkv) * d;
+  const int32_t* rows = m->rows.as<int32_t>();
+  const std::string w(who);
+  hipError_t e = launch_copy_rows(m->x.p, c.embed, m->toks.as<int32_t>(), T, H * 2, false, s);
+  if (e != hipSuccess) return hip_err(e, w + ": embedding");
+  for (int l = 0; l < n_layers; ++l) {
+    e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
+    if (e != hipSuccess) return hip_err(e, w + ": attention norm");
+    int rc = m->gemm.run(m->n.p, m->w_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
+    if (rc) return rc;
+    e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
+    if (e != hipSuccess) return hip_err(e, w + ": q/k/v scatter");
+    rc = attn(l);
+    if (rc) return rc;
+    e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
+    if (e != hipSuccess) return hip_err(e, w + ": attention output gather");
+    rc = m->gemm.run(m->oc.p, m->w_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
+    if (rc) return rc;
+    e = launch_rmsnorm(m->x.p, nullptr, m->ffn_norm[l], m->n.p, T, H, c.rms_eps, s);
+    if (e != hipSuccess) return hip_err(e, w + ": ffn norm");
+    rc = m->gemm.run(m->n.p, m->w_gate_up[l], m->gu.p, T, 2 * static_cast<int64_t>(F), H, false, s);
+    if (rc) return rc;
+    e = launch_swiglu(m->gu.p, m->act.p, T, F, s);
+    if (e != hipSuccess) return hip_err(e, w + ": swiglu");
+    rc = m->gemm.run(m->act.p, m->w_down[l], m->x.p, T, H, F, true, s);
+    if (rc) return rc;
+  }
+  return SPAN_OK;
+}
+
+// Final RMSNorm, LM head and argmax of the nh compact rows listed in m->last, in
+// groups of up to 8 (a group padded to 1, 2, 4 or 8 rows repeats its last row).
+// Logits to logits_out [nh][vocab] if given; tokens to *toks if given (waits).
+int lm_head(span_model* m, int nh, float* logits_out, std::vector<int32_t>* toks, hipStream_t s, const char* who) {
+  const span_model_config& c = m->cfg;
+  const int H = c.hidden, V = c.vocab;
+  const size_t bf = 2;
+  if (toks) toks->assign(static_cast<size_t>(nh), -1);
+  hipError_t e = hipSuccess;
+  for (int g0 = 0; g0 < nh; g0 += 8) {
+    const int ng = std::min(8, nh - g0);
+    const int np = ng <= 1 ? 1 : ng <= 2 ? 2 : ng <= 4 ? 4 : 8;
+    e = launch_rmsnorm(m->x.p, m->last.as<int32_t>() + g0, c.final_norm, m->nf.p, ng, H, c.rms_eps, s);
+    for (int r = ng; e == hipSuccess && r < np; ++r)
+      e = hipMemcpyAsync(static_cast<char*>(m->nf.p) + static_cast<size_t>(r) * H * bf,
+                         static_cast<char*>(m->nf.p) + static_cast<size_t>(ng - 1) * H * bf, H * bf,
+                         hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = launch_lm_head(m->nf.p, c.lm_head, m->part.as<float>(), np, H, V, s);
+    float* lg = logits_out ? logits_out + static_cast<size_t>(g0) * V : nullptr;
+    if (e == hipSuccess) e = launch_argmax(m->part.as<float>(), np, ng, H, V, lg, m->tok_out.as<int32_t>(), s);
+    if (e == hipSuccess && toks)
+      e = hipMemcpyAsync(toks->data() + g0, m->tok_out.p, static_cast<size_t>(ng) * 4, hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_err(e, std::string(who) + ": LM head");
+  }
+  if (toks) {
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_err(e, std::string(who) + ": tokens");
+  }
+  return SPAN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -271,20 +391,9 @@ int span_model_forward(span_model* m, span_plan_t* plan, const int32_t* row_toke
   std::unordered_map<int64_t, int32_t> last_at;
   for (int64_t r : last_rows)
     if (r >= 0) last_at.emplace(r, -1);
-  const size_t stage_n = 2 * static_cast<size_t>(T) + static_cast<size_t>(nq) + 8;
-  if (stage_n > m->host_stage_cap) {
-    e = hipEventSynchronize(m->staged);
-    if (e == hipSuccess && m->host_stage) e = hipHostFree(m->host_stage);
-    m->host_stage = nullptr;
-    m->host_stage_cap = 0;
-    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&m->host_stage), stage_n * sizeof(int32_t), 0);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: pinned staging");
-    m->host_stage_cap = stage_n;
-  } else {
-    e = hipEventSynchronize(m->staged);  // the previous upload has left the staging area
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: staging");
-  }
-  int32_t* h_rows = m->host_stage;
+  int32_t* h_rows = nullptr;
+  rc = stage_area(m, 2 * static_cast<size_t>(T) + static_cast<size_t>(nq) + 8, &h_rows, "span_model_forward");
+  if (rc) return rc;
   int32_t* h_toks = h_rows + T;
   int32_t* h_last = h_toks + T;
   for (int64_t i = 0; i < T; ++i) {
@@ -306,94 +415,80 @@ int span_model_forward(span_model* m, span_plan_t* plan, const int32_t* row_toke
       q_of.push_back(qi);
     }
   const int nh = static_cast<int>(q_of.size());
-
-  // ---- buffers (grown with the stream drained, so no launch still reads the old ones)
-  const int H = c.hidden, hq = c.num_q_heads, hkv = c.num_kv_heads, d = c.head_dim, F = c.ffn, V = c.vocab;
-  const int64_t qkv_w = static_cast<int64_t>(hq + 2 * hkv) * d;
-  const size_t bf = 2;
-  const size_t Tz = static_cast<size_t>(T), Rz = static_cast<size_t>(n_rows);
-  struct Need {
-    Buf* b;
-    size_t bytes;
-  } needs[] = {
-      {&m->x, Tz * H * bf}, {&m->n, Tz * H * bf}, {&m->qkv, Tz * qkv_w * bf}, {&m->oc, Tz * hq * d * bf},
-      {&m->gu, Tz * 2 * F * bf}, {&m->act, Tz * F * bf}, {&m->q, Rz * hq * d * bf}, {&m->k, Rz * hkv * d * bf},
-      {&m->v, Rz * hkv * d * bf}, {&m->o, Rz * hq * d * bf}, {&m->rows, Tz * 4 + 4}, {&m->toks, Tz * 4 + 4},
-      {&m->last, 8 * 4}, {&m->nf, static_cast<size_t>(8) * H * bf},
-      {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
-      {&m->tok_out, 8 * 4}};
-  bool grow = false;
-  for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
-  if (grow) {
-    e = hipStreamSynchronize(s);
-    for (const Need& nd : needs)
-      if (e == hipSuccess) e = nd.b->ensure(nd.bytes);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: activation buffers");
-  }
-  e = T > 0 ? hipMemcpyAsync(m->rows.p, h_rows, Tz * 4, hipMemcpyHostToDevice, s) : hipSuccess;
-  if (e == hipSuccess && T > 0) e = hipMemcpyAsync(m->toks.p, h_toks, Tz * 4, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess && nh > 0) e = hipMemcpyAsync(m->last.p, h_last, static_cast<size_t>(nh) * 4, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipEventRecord(m->staged, s);
-  if (e != hipSuccess) return hip_err(e, "span_model_forward: row lists");
-
-  // ---- embeddings, then the layers
-  const int32_t* rows = m->rows.as<int32_t>();
-  e = launch_copy_rows(m->x.p, c.embed, m->toks.as<int32_t>(), T, H * 2, false, s);
-  if (e != hipSuccess) return hip_err(e, "span_model_forward: embedding");
-  for (int l = 0; l < n_layers; ++l) {
-    e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: attention norm");
-    rc = m->gemm.run(m->n.p, m->w_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
-    if (rc) return rc;
-    e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: q/k/v scatter");
-    rc = span_prefill_fragments(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
-    if (rc) return rc;
-    rc = span_cross_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
-    if (rc) return rc;
-    e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: attention output gather");
-    rc = m->gemm.run(m->oc.p, m->w_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
-    if (rc) return rc;
-    e = launch_rmsnorm(m->x.p, nullptr, m->ffn_norm[l], m->n.p, T, H, c.rms_eps, s);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: ffn norm");
-    rc = m->gemm.run(m->n.p, m->w_gate_up[l], m->gu.p, T, 2 * static_cast<int64_t>(F), H, false, s);
-    if (rc) return rc;
-    e = launch_swiglu(m->gu.p, m->act.p, T, F, s);
-    if (e != hipSuccess) return hip_err(e, "span_model_forward: swiglu");
-    rc = m->gemm.run(m->act.p, m->w_down[l], m->x.p, T, H, F, true, s);
-    if (rc) return rc;
-  }
+  rc = prepare(m, T, n_rows, h_rows, h_toks, h_last, nh, s, "span_model_forward");
+  if (rc) return rc;
+  rc = run_layers(m, T, n_layers, s, "span_model_forward", [&](int l) {
+    int r = span_prefill_fragments(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
+    if (!r) r = span_cross_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
+    return r;
+  });
+  if (rc) return rc;
   if (hidden_out) {
-    e = launch_copy_rows(hidden_out, m->x.p, rows, T, H * 2, true, s);
+    e = launch_copy_rows(hidden_out, m->x.p, m->rows.as<int32_t>(), T, c.hidden * 2, true, s);
     if (e != hipSuccess) return hip_err(e, "span_model_forward: hidden state scatter");
   }
   if (first_tokens)
     for (int qi = 0; qi < nq; ++qi) first_tokens[qi] = -1;
   if ((first_tokens || logits_out) && nh > 0) {
-    std::vector<int32_t> toks(static_cast<size_t>(nh));
-    for (int g0 = 0; g0 < nh; g0 += 8) {
-      const int ng = std::min(8, nh - g0);
-      const int np = ng <= 1 ? 1 : ng <= 2 ? 2 : ng <= 4 ? 4 : 8;
-      // padded rows repeat the group's last row
-      e = launch_rmsnorm(m->x.p, m->last.as<int32_t>() + g0, c.final_norm, m->nf.p, ng, H, c.rms_eps, s);
-      for (int r = ng; e == hipSuccess && r < np; ++r)
-        e = hipMemcpyAsync(static_cast<char*>(m->nf.p) + static_cast<size_t>(r) * H * bf,
-                           static_cast<char*>(m->nf.p) + static_cast<size_t>(ng - 1) * H * bf, H * bf,
-                           hipMemcpyDeviceToDevice, s);
-      if (e == hipSuccess) e = launch_lm_head(m->nf.p, c.lm_head, m->part.as<float>(), np, H, V, s);
-      float* lg = logits_out ? logits_out + static_cast<size_t>(g0) * V : nullptr;
-      if (e == hipSuccess) e = launch_argmax(m->part.as<float>(), np, ng, H, V, lg, m->tok_out.as<int32_t>(), s);
-      if (e == hipSuccess && first_tokens)
-        e = hipMemcpyAsync(toks.data() + g0, m->tok_out.p, static_cast<size_t>(ng) * 4, hipMemcpyDeviceToHost, s);
-      if (e != hipSuccess) return hip_err(e, "span_model_forward: LM head");
-    }
-    if (first_tokens) {
-      e = hipStreamSynchronize(s);
-      if (e != hipSuccess) return hip_err(e, "span_model_forward: first tokens");
+    std::vector<int32_t> toks;
+    rc = lm_head(m, nh, logits_out, first_tokens ? &toks : nullptr, s, "span_model_forward");
+    if (rc) return rc;
+    if (first_tokens)
       for (int i = 0; i < nh; ++i) first_tokens[q_of[i]] = toks[i];
-    }
   }
+  return SPAN_OK;
+}
+
+int span_model_decode(span_model* m, span_plan_t* plan, const int32_t* tokens, float* logits_out, int32_t* next_tokens,
+                      void* stream) {
+  if (!m || !plan) return report(SPAN_EINVAL, "span_model_decode: null argument");
+  if (plan_pool(plan) != m->pool) return report(SPAN_EINVAL, "span_model_decode: the plan belongs to another pool");
+  const span_model_config& c = m->cfg;
+  std::vector<int64_t> last_rows;
+  plan_last_cross_rows(plan, &last_rows);
+  const int nq = static_cast<int>(last_rows.size());
+  if (nq > 0 && !tokens) return report(SPAN_EINVAL, "span_model_decode: null token list");
+  std::vector<int> q_of;  // decoding queries, in order
+  std::vector<int32_t> n_new(static_cast<size_t>(nq), 0);
+  std::vector<int64_t> rows(static_cast<size_t>(nq), 0);
+  for (int qi = 0; qi < nq; ++qi) {
+    if (tokens[qi] < 0) continue;
+    if (tokens[qi] >= c.vocab) return report(SPAN_EINVAL, "span_model_decode: token id outside the vocabulary");
+    n_new[qi] = 1;
+    rows[qi] = static_cast<int64_t>(q_of.size());
+    q_of.push_back(qi);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSetDevice(m->device);
+  if (e != hipSuccess) return hip_err(e, "span_model_decode: hipSetDevice");
+  if (next_tokens)
+    for (int qi = 0; qi < nq; ++qi) next_tokens[qi] = -1;
+  const int nd = static_cast<int>(q_of.size());
+  if (nd == 0) return SPAN_OK;
+  int rc = span_plan_decode(plan, n_new.data(), rows.data(), s);
+  if (rc) return rc;
+  // one compact row per decoding query; its attention row is the same index
+  int32_t* h_rows = nullptr;
+  rc = stage_area(m, 3 * static_cast<size_t>(nd) + 8, &h_rows, "span_model_decode");
+  if (rc) return rc;
+  int32_t* h_toks = h_rows + nd;
+  int32_t* h_last = h_toks + nd;
+  for (int i = 0; i < nd; ++i) {
+    h_rows[i] = i;
+    h_toks[i] = tokens[q_of[i]];
+    h_last[i] = i;
+  }
+  rc = prepare(m, nd, nd, h_rows, h_toks, h_last, nd, s, "span_model_decode");
+  if (rc) return rc;
+  rc = run_layers(m, nd, c.num_layers, s, "span_model_decode",
+                  [&](int l) { return span_decode_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s); });
+  if (rc) return rc;
+  if (!next_tokens && !logits_out) return SPAN_OK;
+  std::vector<int32_t> toks;
+  rc = lm_head(m, nd, logits_out, next_tokens ? &toks : nullptr, s, "span_model_decode");
+  if (rc) return rc;
+  if (next_tokens)
+    for (int i = 0; i < nd; ++i) next_tokens[q_of[i]] = toks[i];
   return SPAN_OK;
 }
 

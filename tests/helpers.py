@@ -39,7 +39,7 @@ def oracle_rows(wl, query, want_rows=None):
 class GpuRun:
     """A pool on cuda:0 holding a workload's activations; runs batches through the library."""
 
-    def __init__(self, wl, num_pages=None, kernel="auto", num_layers=1, materialize=False):
+    def __init__(self, wl, num_pages=None, kernel="auto", num_layers=1, materialize=False, nan_pool=False):
         import torch
 
         import paper_2511_02749_amd as spanq
@@ -49,9 +49,15 @@ class GpuRun:
             num_pages = 64 + sum(
                 (q.prefix.n + 15) // 16 + sum((f.n + 15) // 16 for f in q.frags) + (q.cross.n + 15) // 16
                 for b in wl.batches for q in b)
+        buf = None
+        if nan_pool:  # page memory full of NaN bit patterns, as memory reused from other work may be
+            elem = 2 if wl.dtype == "bf16" else 4
+            n = num_layers * num_pages * 2 * wl.n_kv_heads * 16 * wl.head_dim
+            buf = (torch.full((n,), 0x7FC0, dtype=torch.int16, device="cuda") if elem == 2 else
+                   torch.full((n,), 0x7FC00000, dtype=torch.int32, device="cuda"))
         self.pool = spanq.Pool(num_q_heads=wl.n_q_heads, num_kv_heads=wl.n_kv_heads, head_dim=wl.head_dim,
                                num_pages=num_pages, dtype=wl.dtype, rope_theta=wl.rope_theta, kernel=kernel,
-                               num_layers=num_layers, materialize=materialize, device=0)
+                               num_layers=num_layers, materialize=materialize, device=0, device_buf=buf)
         qa, ka, va = wl.device_arrays()
         conv = (lambda a: torch.from_numpy(a.view(np.int16))) if wl.dtype == "bf16" else torch.from_numpy
         self.q, self.k, self.v = (conv(np.ascontiguousarray(a)).cuda() for a in (qa, ka, va))

@@ -176,6 +176,26 @@ def test_decode_over_repositioned_fragments(materialize):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("dtype,kernel,materialize", [("bf16", "auto", False), ("bf16", "auto", True),
+                                                      ("f32", "generic", False)])
+def test_decode_on_a_pool_of_nan_garbage(dtype, kernel, materialize):
+    """Page memory that starts as NaN bit patterns (memory reused from other work):
+    prefill, cross and decode steps must never read a slot they did not write, or must
+    read it as a masked key over a zeroed value.  Decode pages come from the free list
+    as they are; the step that opens one zeroes its unfilled slots."""
+    _need_gpu()
+    wl = W.small_workload(dtype=dtype, cross_len=40, orders=[[0, 1, 2], [2, 3, 1]], n_queries=2)
+    run = GpuRun(wl, kernel=kernel, materialize=materialize, nan_pool=True)
+    full = wl.batches[0]
+    plan = run.run_batch([_cut(q, 3) for q in full], commit=False)
+    _, cross = plan.rows()
+    check_rows(run, full, cross, TOL[dtype])
+    _decode_through(run, plan, full, 3, [[1], [13], [1], [2], [40]])
+    plan.destroy()
+    run.close()
+
+
+@pytest.mark.gpu
 def test_decode_on_another_stream():
     torch = _need_gpu()
     wl = W.small_workload(cross_len=30)

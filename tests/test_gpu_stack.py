@@ -213,3 +213,76 @@ def test_c4_fragment_rows_and_warm_equals_cold():
     assert pc.stats()["tokens_hit"] == 0
     _warm_vs_cold(hw, cold.hidden_rows(cross), lw, lc, tw, tc, "c4")
     cold.close()
+
+
+def _cut_cross(q, c0):
+    return W.Query(prefix=q.prefix, frags=q.frags, cross=W.Span(tokens=q.cross.tokens[:c0], row=q.cross.row))
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_model_decode_teacher_forced(head_dim):
+    """span_model_decode fed the seeded cross tokens past a cut (teacher forcing): the
+    logits of every decoded row against the oracle stack's logits of that row of the
+    uncut query, and each step's token is an argmax of the oracle logits within the
+    logit tolerance (section 5.7's generate after the join, one token per step)."""
+    from oracle import stack as OS
+    swl = W.stack_small(head_dim=head_dim)
+    run = StackRun(swl)
+    Wt = oracle_weights(swl.weights)
+    full = swl.batches[0]
+    steps = 6
+    c0 = full[0].cross.n - steps
+    plan, toks, _ = run.run([_cut_cross(q, c0) for q in full], commit=False)
+    refs = []
+    for q in full:
+        rows = [q.cross.row + c0 + t for t in range(steps)]
+        hid, _ = stack_oracle(swl, q, [swl.weights.n_layers], rows=rows, Wt=Wt)
+        refs.append([OS.final_logits(hid[swl.weights.n_layers][r], Wt, swl.rms_eps) for r in rows])
+    for t in range(steps):
+        feed = [int(q.cross.tokens[c0 + t]) for q in full]
+        lg = torch.zeros((len(full), swl.weights.vocab), dtype=torch.float32, device="cuda")
+        nxt = run.model.decode(plan, feed, logits_out=lg)
+        torch.cuda.synchronize()
+        lg = lg.cpu().numpy()
+        for qi in range(len(full)):
+            ref = refs[qi][t]
+            err = float(np.max(np.abs(lg[qi].astype(np.float64) - ref)))
+            print(f"d{head_dim} step {t} query {qi}: logits max abs err {err:.4g}; token {nxt[qi]} oracle "
+                  f"{int(np.argmax(ref))}", flush=True)
+            assert err <= LOGIT_TOL
+            assert ref[nxt[qi]] >= ref.max() - LOGIT_TOL
+            assert int(np.argmax(lg[qi])) == nxt[qi]
+    assert plan.stats()["decode_tokens"] == steps * len(full)
+    plan.destroy()
+    run.close()
+
+
+def test_model_decode_greedy_and_partial():
+    """Greedy decoding of some queries only: queries fed -1 get -1 and no rows; the
+    returned tokens are the argmax of the returned logits; commit frees the pages the
+    steps took."""
+    swl = W.stack_small()
+    run = StackRun(swl)
+    batch = swl.batches[0]
+    plan, toks, _ = run.run(batch, commit=False)
+    free0 = run.pool.info()["free_pages"]
+    cur = list(toks)
+    for step in range(20):
+        feed = [cur[0], -1] + cur[2:] if len(cur) > 2 else [cur[0], -1]
+        n_dec = sum(1 for f in feed if f >= 0)
+        lg = torch.zeros((n_dec, swl.weights.vocab), dtype=torch.float32, device="cuda")
+        nxt = run.model.decode(plan, feed, logits_out=lg)
+        torch.cuda.synchronize()
+        lg = lg.cpu().numpy()
+        assert nxt[1] == -1
+        dec = [i for i, f in enumerate(feed) if f >= 0]
+        for j, qi in enumerate(dec):
+            assert 0 <= nxt[qi] < swl.weights.vocab and int(np.argmax(lg[j])) == nxt[qi]
+        cur = [nxt[i] if feed[i] >= 0 else cur[i] for i in range(len(cur))]
+    st = plan.stats()
+    assert st["decode_tokens"] == 20 * (len(batch) - 1)
+    assert run.pool.info()["free_pages"] == free0 - st["decode_pages"]
+    plan.commit()
+    assert run.pool.info()["free_pages"] == run.pool.info()["num_pages"] - run.pool.info()["cached_pages"]
+    plan.destroy()
+    run.close()
