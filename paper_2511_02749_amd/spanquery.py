@@ -23,6 +23,10 @@ runs once per child, and its output is presented prefixed by that child's input
 (the "dual output" of section 2: what the cache holds is input followed by
 output), so a later reader of the outputs reads exactly what is cached.
 
+Attention locality (section 6, ``attention_locality``): a judge over n candidates
+becomes a tree reduction of k-way judges, so that no generate attends to more than k
+candidates at once.
+
 Lowering (``to_spans``) maps an optimized RAG / judge-shaped tree
 G(Cross(before.., Plus(children..), after..)) to the library's span query:
 the messages before the join are the shared prefix, each child of the join is a
@@ -194,14 +198,70 @@ def optimize(n: Node, rules=RULES, max_steps: int = 10_000) -> Node:
     raise RuntimeError("the rewrite did not converge")
 
 
+# ---------------------------------------------------------------- attention locality
+
+def _is_join(n: Node) -> bool:
+    """A commutative join, plain or inside a distributed generate G(Plus(..))."""
+    return n.op == "Plus" or (n.op == "G" and not is_prepare(n) and n.children[0].op == "Plus")
+
+
+def attention_locality(tree: Node, k: int = 2) -> Node:
+    """Section 6: a judge over n candidates, G(Cross(before.., join, after..)), becomes
+    a tree reduction of k-way judges: the candidates are judged k at a time (each
+    judge G(Cross(before.., join of k candidates, after..)) with the root's
+    max_tokens), then the judgments k at a time, and so on, ceil(log_k n) plies in
+    all, the last one being the root.  A judge reads the judgments of the ply below
+    as plain outputs (A(out) once the generates have run), so every generate attends
+    to at most k candidates.  A group of one judgment passes through unjudged.
+    Apply it to a tree at the fixed point of the section 5.1 rules and do not
+    optimize the result again: plus distribution would turn the judgments' join back
+    into one generate.  Trees of another shape, or with at most k candidates, come
+    back unchanged."""
+    if k < 2:
+        raise ValueError("k must be at least 2")
+    if tree.op != "G" or is_prepare(tree):
+        return tree
+    body = tree.children[0]
+    parts = list(body.children) if body.op == "Cross" else [body]
+    joins = [i for i, c in enumerate(parts) if _is_join(c)]
+    if len(joins) != 1:
+        return tree
+    j = joins[0]
+    before, join, after = parts[:j], parts[j], parts[j + 1:]
+    if join.op == "G":  # the candidates are generated: each group stays one distributed generate
+        items = list(join.children[0].children)
+        group = lambda xs: G(Plus(*xs), max_tokens=join.max_tokens)  # noqa: E731
+    else:
+        items = list(join.children)
+        group = lambda xs: Plus(*xs)  # noqa: E731
+    if len(items) <= k:
+        return tree
+    judge = lambda inner: G(Cross(*before, inner, *after), max_tokens=tree.max_tokens)  # noqa: E731
+    level = [judge(group(items[i:i + k])) for i in range(0, len(items), k)]
+    while len(level) > k:
+        level = [judge(Plus(*level[i:i + k])) if len(level[i:i + k]) > 1 else level[i]
+                 for i in range(0, len(level), k)]
+    return judge(Plus(*level)) if len(level) > 1 else level[0]
+
+
+def plies(tree: Node) -> int:
+    """Generates on the longest root-to-leaf path (the root counts; Prepare does not)."""
+    own = 1 if tree.op == "G" and not is_prepare(tree) else 0
+    return own + max((plies(c) for c in tree.children), default=0)
+
+
 # ---------------------------------------------------------------- inner generates
 
-def expand_generates(tree: Node, generate) -> Node:
+def expand_generates(tree: Node, generate, generate_join=None) -> Node:
     """Run the generates nested inside the root (innermost first) with
     ``generate(tokens, max_tokens) -> output tokens`` and splice in what their readers
     see: for a distributed G(Plus(x1..xn)), Plus(Cross(x1, A(out1)) .. Cross(xn,
     A(outn))), each child's output prefixed by its input; for any other inner G(x),
-    A(out) alone.  Prepare nodes are left for the lowering (their output is never read)."""
+    A(out) alone.  An inner generate whose body holds a join (a judge of a tree
+    reduction) is a span query of its own: it runs as
+    ``generate_join(spans, max_tokens)`` on its lowering, or, without that callback,
+    through ``generate`` on its tokens in sequence order.  Prepare nodes are left for
+    the lowering (their output is never read)."""
     def walk(n: Node, root: bool) -> Node:
         kids = tuple(walk(c, False) for c in n.children)
         n = Node(n.op, children=kids, tokens=n.tokens, max_tokens=n.max_tokens)
@@ -210,6 +270,11 @@ def expand_generates(tree: Node, generate) -> Node:
         body = n.children[0]
         if body.op == "Plus":
             return Plus(*[Cross(c, A(generate(_message_tokens(c), n.max_tokens))) for c in body.children])
+        if body.op == "Cross" and any(c.op == "Plus" for c in body.children):
+            sp = to_spans(n)
+            if generate_join is not None:
+                return A(generate_join(sp, n.max_tokens))
+            return A(generate(sp.prefix + [t for f in sp.fragments for t in f] + sp.cross, n.max_tokens))
         return A(generate(_message_tokens(body), n.max_tokens))
     return walk(tree, True)
 

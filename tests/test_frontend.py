@@ -223,3 +223,93 @@ def test_rag_through_front_end_and_planner():
         plan.commit()
         replay.commit(res)
     pool.close()
+
+
+def _judge_tree(n, gen_tokens=3, judge_tokens=2):
+    """A judge over n generated candidates (section 6's judge/generator), at the fixed
+    point of the rewrite rules: G(Cross(S, G(Plus(Cross(S1, U_i)..)), U))."""
+    cands = [sq.C(S1, sq.U([100 + i])) for i in range(n)]
+    tree = sq.C(S2, sq.Plus(*[sq.G(sq.Cross(*c.children), gen_tokens) for c in cands]), U3)
+    tree = sq.G(tree.children[0] if tree.op == "G" else sq.Cross(*tree.children), judge_tokens)
+    return _fixed_point(tree)
+
+
+def test_attention_locality_eight_way_judge_becomes_three_two_way_plies():
+    tree = _judge_tree(8)
+    assert tree.op == "G" and sq.plies(tree) == 2          # the judge, then the distributed candidates
+    out = sq.attention_locality(tree, 2)
+    assert sq.plies(out) == 4                               # 3 judge plies over the candidates' generate
+    # every judge reads at most two candidates or judgments, with the judge's own messages around them
+    judges = []
+
+    def walk(n, depth):
+        if n.op == "G" and n.children[0].op == "Cross":
+            parts = n.children[0].children
+            assert parts[0] == S2 and parts[-1] == U3 and len(parts) == 3
+            join = parts[1]
+            kids = join.children[0].children if join.op == "G" else join.children
+            assert 1 <= len(kids) <= 2
+            judges.append(depth)
+        for c in n.children:
+            walk(c, depth + 1)
+    walk(out, 0)
+    assert len(judges) == 4 + 2 + 1
+    # the candidates keep their order across the ply-1 judges
+    leaves = []
+
+    def cand(n):
+        if n.op == "U" and n.tokens[0] >= 100:
+            leaves.append(n.tokens[0])
+        for c in n.children:
+            cand(c)
+    cand(out)
+    assert leaves == [100 + i for i in range(8)]
+
+
+@pytest.mark.parametrize("n,k,expect", [(8, 2, 3), (8, 3, 2), (9, 3, 2), (10, 3, 3), (24, 2, 5), (24, 24, 1)])
+def test_attention_locality_plies(n, k, expect):
+    out = sq.attention_locality(_judge_tree(n), k)
+    assert sq.plies(out) - 1 == expect                      # judge plies (the candidates' generate aside)
+    if n <= k:
+        assert out == _judge_tree(n)
+
+
+def test_attention_locality_runs_judges_on_outputs_alone():
+    """Executed with expand_generates: 8 candidate generates (each read as input then
+    output), then 4 + 2 judges as span queries of their own whose fragments are, in
+    ply 1, the candidates' input and output and, in ply 2, the ply-1 judgments alone;
+    the root lowers to a query over the two ply-2 judgments."""
+    out = sq.attention_locality(_judge_tree(8), 2)
+    gens, joins = [], []
+
+    def generate(tokens, max_tokens):
+        gens.append((list(tokens), max_tokens))
+        return [500 + len(gens)] * max_tokens
+
+    def generate_join(spans, max_tokens):
+        joins.append(spans)
+        return [900 + len(joins)] * max_tokens
+
+    ex = sq.expand_generates(out, generate, generate_join)
+    assert len(gens) == 8 and all(m == 3 for _, m in gens)
+    assert [g[0] for g in gens] == [[1, 2, 3, 100 + i] for i in range(8)]
+    assert len(joins) == 6
+    # innermost first, one sub-tree after the other: ply-1 judges 0 and 1, the ply-2
+    # judge over them, ply-1 judges 2 and 3, the ply-2 judge over those
+    ply1 = [joins[0], joins[1], joins[3], joins[4]]
+    for j, sp in enumerate(ply1):
+        assert sp.prefix == [4, 5] and sp.cross == [9, 10, 11]
+        assert sp.fragments == [[1, 2, 3, 100 + 2 * j] + [501 + 2 * j] * 3, [1, 2, 3, 101 + 2 * j] + [502 + 2 * j] * 3]
+    assert joins[2].fragments == [[901, 901], [902, 902]] and joins[5].fragments == [[904, 904], [905, 905]]
+    root = sq.to_spans(ex)
+    assert root.fragments == [[903, 903], [906, 906]] and root.max_tokens == 2
+
+
+def test_attention_locality_leaves_other_shapes_alone():
+    chat = _fixed_point(sq.C(S1, U1))
+    assert sq.attention_locality(chat, 2) == chat
+    rag = _fixed_point(sq.C(S1, sq.R(F1, F2, F3), U1))
+    out = sq.attention_locality(rag, 2)                     # plain fragments: judged two at a time
+    assert sq.plies(out) == 2 and sq.attention_locality(rag, 3) == rag   # ceil(log2 3) judge plies
+    with pytest.raises(ValueError):
+        sq.attention_locality(rag, 1)

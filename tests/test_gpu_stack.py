@@ -286,3 +286,41 @@ def test_model_decode_greedy_and_partial():
     assert run.pool.info()["free_pages"] == run.pool.info()["num_pages"] - run.pool.info()["cached_pages"]
     plan.destroy()
     run.close()
+
+
+def _judge(n, k=None):
+    """A judge over n generated candidates with small token ids (vocab 1000), at the
+    fixed point of the section 5.1 rules; with k, rewritten for attention locality."""
+    from paper_2511_02749_amd import spanquery as sq
+    sys_c, sys_j, ask = sq.S([11, 12, 13]), sq.S(list(range(40, 80))), sq.U([21, 22, 23, 24])
+    cands = [sq.G(sq.Cross(sys_c, sq.U([300 + 7 * i + j for j in range(5)])), 3) for i in range(n)]
+    tree = sq.optimize(sq.G(sq.Cross(sys_j, sq.Plus(*cands), ask), 4))
+    return sq.attention_locality(tree, k) if k else tree
+
+
+@pytest.mark.parametrize("k", [None, 2])
+def test_engine_runs_a_judge_tree(k):
+    """Nested generation end to end on the GPU (sections 5.7 and 6): 8 candidates
+    generated greedily (first token by span_model_forward, the rest by decode steps),
+    then the judge, or the tree of 2-way judges.  Every call returns its token count
+    of valid ids; the judges after the first find the judge prompt's prefix pages in
+    the cache."""
+    from paper_2511_02749_amd import spanquery as sq
+    from paper_2511_02749_amd.engine import Engine
+    swl = W.stack_small()
+    run = StackRun(swl, num_pages=1024)
+    eng = Engine(run.pool, run.model)
+    tree = _judge(8, k)
+    out = eng.run(tree)
+    assert len(out) == 4 and all(0 <= t < swl.weights.vocab for t in out)
+    n_judges = 1 if k is None else 7
+    assert len(eng.calls) == 8 + n_judges
+    assert all(c.decode_steps == 2 for c in eng.calls[:2])             # candidates: 3 tokens
+    judges = [c for c in eng.calls if c.decode_steps == 3]
+    assert len(judges) == n_judges
+    if k:
+        assert sq.plies(tree) == 4
+        assert all(c.pages_hit >= 2 for c in judges[1:])              # the 40-token judge prompt
+    print(f"k={k}: output {out}; calls {[(c.pages_hit, c.tokens_new, c.decode_steps) for c in eng.calls]}",
+          flush=True)
+    run.close()
