@@ -323,7 +323,7 @@ def stack_flops(sw, rows, pairs_per_layer, queries_with_cross):
     return (per_row * rows + 4 * d * hq * pairs_per_layer) * sw.n_layers + 2 * H * sw.vocab * queries_with_cross
 
 
-def c4_ttft(spanq, W, torch, np, reps):
+def c4_ttft(spanq, W, torch, np, reps, decode_steps=16):
     """C4: a 32-layer 2B-class decoder (hidden 2048, 32/8 heads x 64, SwiGLU 8192) over
     one RAG span query (prefix 512 + 32 fragments x 1024 + question 256).  Time to
     first token from the span_plan call to the first token on the host: cold (fresh
@@ -365,6 +365,29 @@ def c4_ttft(spanq, W, torch, np, reps):
             warm.append(w[0])
         toks = {"cold_order": c[1], "warm_reversed": w[1]}
         st_cold, st_warm = c[2], w[2]
+    # nested generation: the warm query's first token, then greedy decode steps through
+    # all 32 layers (span_model_decode), each timed from the call to its token on the host
+    p = pool.plan([rev])
+    cur = model.forward(p, swl.row_tokens)
+    step_ms = []
+    for i in range(decode_steps + 2):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        cur = model.decode(p, cur)
+        if i >= 2:
+            step_ms.append((time.perf_counter() - t) * 1e3)
+    ctx_pages = sum(len(p.block_table(0, s)[0]) for s in range(-1, len(rev.frags) + 1))
+    p.commit()
+    p.destroy()
+    page_bytes = 2 * sw.n_kv_heads * 16 * sw.head_dim * 2
+    w_bytes = sum(a.nbytes for a in [*sw.w_qkv, *sw.w_o, *sw.w_gate_up, *sw.w_down]) + sw.lm_head.nbytes
+    kv_bytes = ctx_pages * page_bytes * sw.n_layers
+    dstep = _percentiles(step_ms)
+    decode = {"steps": len(step_ms), "ms_per_token_p50": dstep["p50"], "ms_per_token_p99": dstep["p99"],
+              "context_tokens": n_tok + decode_steps + 2, "weight_bytes": int(w_bytes), "kv_bytes": int(kv_bytes),
+              "hbm_gbs_p50": (w_bytes + kv_bytes) / (dstep["p50"] * 1e-3) / 1e9,
+              "note": "one query; per step every weight matrix and every cached K/V page of the context is read "
+                      "once (the bytes above), plus the host round trip for the token"}
     S = np.concatenate([s.tokens for s in [q.prefix, *q.frags, q.cross]]).astype(np.int32)
     whole = W.Query(prefix=W.Span(tokens=S[:-q.cross.n], row=0), frags=[],
                     cross=W.Span(tokens=S[-q.cross.n:], row=S.size - q.cross.n))
@@ -388,7 +411,8 @@ def c4_ttft(spanq, W, torch, np, reps):
             "dense_causal_ms_p50": dd["p50"], "warm_speedup_vs_cold": c["p50"] / w_["p50"],
             "warm_speedup_vs_dense": dd["p50"] / w_["p50"], "reps": len(cold),
             "cold_model_tflops": f_cold / (c["p50"] * 1e-3) / 1e12, "cold_model_tflop": f_cold / 1e12,
-            "warm_model_tflop": f_warm / 1e12, "first_tokens": toks, "weights_gen_and_upload_s": gen_s}
+            "warm_model_tflop": f_warm / 1e12, "first_tokens": toks, "decode": decode,
+            "weights_gen_and_upload_s": gen_s}
 
 
 def c5_stream(spanq, W, torch, np, n_queries):
@@ -453,10 +477,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c2", choices=["c2", "c3", "c5", "repos"],
+    ap.add_argument("--config", default="c2", choices=["c2", "c3", "c4", "c5", "repos"],
                     help="c2: the headline run (with C3, C4 and repositioning extras); c3: the judge pattern as "
-                         "the main workload; c5: only the agentic stream over the 8B-shaped decoder; repos: only "
-                         "the read-time vs materialised repositioning comparison")
+                         "the main workload; c4: only the 2B-class decoder's TTFT and decode steps; c5: only the "
+                         "agentic stream over the 8B-shaped decoder; repos: only the read-time vs materialised "
+                         "repositioning comparison")
     ap.add_argument("--c5-queries", type=int, default=256)
     ap.add_argument("--no-extras", action="store_true", help="skip the C3 and C4 extras of the default run")
     ap.add_argument("--kernel", default="auto", choices=["auto", "generic", "mfma"])
@@ -496,6 +521,13 @@ def main():
                                                  "fragments (128..2048 tokens, Zipf 1.1, 4-24 per query), prefix 256, "
                                                  "question 128"},
                           "c5": res}), flush=True)
+        return
+    if args.config == "c4":
+        res = c4_ttft(spanq, W, torch, np, reps=max(5, args.ttft_reps))
+        print(json.dumps({"metric": "C4 decoder: time to first token (ms), cold / warm / dense, and decode steps",
+                          "unit": "ms", "higher_is_better": False, "n_gpus": 1, "dtype": "bf16",
+                          "data": "synthetic (seeded tokens, random-init weights)",
+                          "config": {"workload": res["workload"]}, "c4": res}), flush=True)
         return
     if args.config == "repos":
         res = reposition_ab(spanq, W, torch, np, reps=max(5, args.ttft_reps))

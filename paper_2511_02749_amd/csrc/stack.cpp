@@ -158,7 +158,7 @@ struct span_model {
   // caller-row activations the attention entry points read and write
   Buf q, k, v, o;
   // row lists, LM head
-  Buf rows, toks, last, nf, part, logits, tok_out;
+  Buf rows, toks, last, nf, part, logits, tok_out, best;
   int32_t* host_stage = nullptr;  // pinned staging of the row lists
   size_t host_stage_cap = 0;
   hipEvent_t staged = nullptr;     // the last upload from host_stage
@@ -223,7 +223,7 @@ int prepare(span_model* m, int64_t T, int64_t R, const int32_t* h_rows, const in
       {&m->v, Rz * hkv * d * bf}, {&m->o, Rz * hq * d * bf}, {&m->rows, Tz * 4 + 4}, {&m->toks, Tz * 4 + 4},
       {&m->last, static_cast<size_t>(nh) * 4 + 32}, {&m->nf, static_cast<size_t>(8) * H * bf},
       {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
-      {&m->tok_out, 8 * 4}};
+      {&m->tok_out, 8 * 4}, {&m->best, argmax_scratch_bytes(8, V)}};
   bool grow = false;
   for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
   hipError_t e = hipSuccess;
@@ -296,7 +296,7 @@ int lm_head(span_model* m, int nh, float* logits_out, std::vector<int32_t>* toks
                          hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess) e = launch_lm_head(m->nf.p, c.lm_head, m->part.as<float>(), np, H, V, s);
     float* lg = logits_out ? logits_out + static_cast<size_t>(g0) * V : nullptr;
-    if (e == hipSuccess) e = launch_argmax(m->part.as<float>(), np, ng, H, V, lg, m->tok_out.as<int32_t>(), s);
+    if (e == hipSuccess) e = launch_argmax(m->part.as<float>(), np, ng, H, V, lg, m->tok_out.as<int32_t>(), m->best.p, s);
     if (e == hipSuccess && toks)
       e = hipMemcpyAsync(toks->data() + g0, m->tok_out.p, static_cast<size_t>(ng) * 4, hipMemcpyDeviceToHost, s);
     if (e != hipSuccess) return hip_err(e, std::string(who) + ": LM head");
@@ -355,7 +355,7 @@ int span_model_destroy(span_model* m) {
   (void)hipDeviceSynchronize();
   m->gemm.destroy();
   for (Buf* b : {&m->x, &m->n, &m->qkv, &m->oc, &m->gu, &m->act, &m->q, &m->k, &m->v, &m->o, &m->rows, &m->toks,
-                 &m->last, &m->nf, &m->part, &m->logits, &m->tok_out})
+                 &m->last, &m->nf, &m->part, &m->logits, &m->tok_out, &m->best})
     b->release();
   if (m->host_stage) (void)hipHostFree(m->host_stage);
   if (m->staged) (void)hipEventDestroy(m->staged);

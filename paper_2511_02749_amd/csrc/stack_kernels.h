@@ -28,10 +28,11 @@ hipError_t launch_swiglu(const void* gu, void* act, int64_t n, int ffn, hipStrea
 // of the hidden dimension into part [lm_head_chunks(hidden)][nq][vocab] (fp32).
 // launch_argmax sums the chunks (in chunk order) for the first n_rows rows into
 // logits [n_rows][vocab] (optional) and writes their argmax, lowest id on ties,
-// to token [n_rows].
+// to token [n_rows]; scratch holds argmax_scratch_bytes(nq, vocab) of device memory.
 int lm_head_chunks(int hidden);
 hipError_t launch_lm_head(const void* nf, const void* w, float* part, int nq, int hidden, int vocab, hipStream_t s);
+size_t argmax_scratch_bytes(int nq, int vocab);
 hipError_t launch_argmax(const float* part, int nq, int n_rows, int hidden, int vocab, float* logits, int32_t* token,
-                         hipStream_t s);
+                         void* scratch, hipStream_t s);
 
 }  // namespace spanq

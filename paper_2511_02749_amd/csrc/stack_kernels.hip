@@ -177,40 +177,92 @@ __global__ __launch_bounds__(kHeadThreads) void lm_head_kernel(const u16* __rest
 }
 
 // Logits = the chunks' partials summed in chunk order; token = argmax, lowest id on
-// ties.  One work-group per row.
-__global__ __launch_bounds__(kHeadThreads) void argmax_kernel(const float* __restrict__ part, int n_chunks, int nq,
-                                                              int vocab, float* __restrict__ logits,
-                                                              int32_t* __restrict__ token) {
+// ties, in two passes.  Pass 1, one work-group per (block of kArgCols columns, row):
+// the sums (stored as logits if asked) and the block's best value with its lowest
+// id.  Pass 2, one work-group per row: the best of the blocks' bests, lower block
+// first on ties.  A NaN never wins; a row of NaNs gives id 0x7fffffff.
+constexpr int kArgThreads = 256;
+constexpr int kArgCols = kArgThreads * 4;
+
+__device__ __forceinline__ void better(float& bv, int& bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+__global__ __launch_bounds__(kArgThreads) void argmax_blocks_kernel(const float* __restrict__ part, int n_chunks,
+                                                                    int nq, int vocab, float* __restrict__ logits,
+                                                                    float* __restrict__ best_v,
+                                                                    int* __restrict__ best_i) {
   // nq is the partials' row stride; the grid covers only the rows wanted
-  __shared__ float bv[kHeadThreads];
-  __shared__ int bi[kHeadThreads];
-  const int q = blockIdx.x;
+  __shared__ float sv[kArgThreads];
+  __shared__ int si[kArgThreads];
+  const int q = blockIdx.y;
+  const int c0 = blockIdx.x * kArgCols + threadIdx.x * 4;
   float best = -INFINITY;
   int arg = 0x7fffffff;
-  for (int c = threadIdx.x; c < vocab; c += kHeadThreads) {
-    float s = 0.f;
-    for (int k = 0; k < n_chunks; ++k) s += part[(static_cast<int64_t>(k) * nq + q) * vocab + c];
-    if (logits) logits[static_cast<int64_t>(q) * vocab + c] = s;
-    if (s > best) {  // columns rise along the loop: a later equal value keeps the lower id
-      best = s;
-      arg = c;
+  if (c0 < vocab) {  // vocab is a multiple of 8: four columns are all in or all out
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < n_chunks; ++k) {
+      const float4 p = *reinterpret_cast<const float4*>(part + (static_cast<int64_t>(k) * nq + q) * vocab + c0);
+      acc.x += p.x;
+      acc.y += p.y;
+      acc.z += p.z;
+      acc.w += p.w;
     }
-  }
-  bv[threadIdx.x] = best;
-  bi[threadIdx.x] = arg;
-  __syncthreads();
-  for (int off = kHeadThreads / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off) {
-      const float ov = bv[threadIdx.x + off];
-      const int oi = bi[threadIdx.x + off];
-      if (ov > bv[threadIdx.x] || (ov == bv[threadIdx.x] && oi < bi[threadIdx.x])) {
-        bv[threadIdx.x] = ov;
-        bi[threadIdx.x] = oi;
+    if (logits) *reinterpret_cast<float4*>(logits + static_cast<int64_t>(q) * vocab + c0) = acc;
+    const float v[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (v[j] > best) {  // columns rise: an equal later value keeps the lower id
+        best = v[j];
+        arg = c0 + j;
       }
+  }
+  sv[threadIdx.x] = best;
+  si[threadIdx.x] = arg;
+  __syncthreads();
+  for (int off = kArgThreads / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off) {
+      float bv = sv[threadIdx.x];
+      int bi = si[threadIdx.x];
+      better(bv, bi, sv[threadIdx.x + off], si[threadIdx.x + off]);
+      sv[threadIdx.x] = bv;
+      si[threadIdx.x] = bi;
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) token[q] = bi[0];
+  if (threadIdx.x == 0) {
+    best_v[static_cast<int64_t>(q) * gridDim.x + blockIdx.x] = sv[0];
+    best_i[static_cast<int64_t>(q) * gridDim.x + blockIdx.x] = si[0];
+  }
+}
+
+__global__ __launch_bounds__(kArgThreads) void argmax_rows_kernel(const float* __restrict__ best_v,
+                                                                  const int* __restrict__ best_i, int n_blocks,
+                                                                  int32_t* __restrict__ token) {
+  __shared__ float sv[kArgThreads];
+  __shared__ int si[kArgThreads];
+  const int q = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int b = threadIdx.x; b < n_blocks; b += kArgThreads)
+    better(bv, bi, best_v[static_cast<int64_t>(q) * n_blocks + b], best_i[static_cast<int64_t>(q) * n_blocks + b]);
+  sv[threadIdx.x] = bv;
+  si[threadIdx.x] = bi;
+  __syncthreads();
+  for (int off = kArgThreads / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off) {
+      float v = sv[threadIdx.x];
+      int i = si[threadIdx.x];
+      better(v, i, sv[threadIdx.x + off], si[threadIdx.x + off]);
+      sv[threadIdx.x] = v;
+      si[threadIdx.x] = i;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) token[q] = si[0];
 }
 
 int grid_for(int64_t items, int threads) {
@@ -274,10 +326,20 @@ hipError_t launch_lm_head(const void* nf, const void* w, float* part, int nq, in
   return hipGetLastError();
 }
 
+size_t argmax_scratch_bytes(int nq, int vocab) {
+  return static_cast<size_t>(nq) * ((vocab + kArgCols - 1) / kArgCols) * (sizeof(float) + sizeof(int));
+}
+
 hipError_t launch_argmax(const float* part, int nq, int n_rows, int hidden, int vocab, float* logits, int32_t* token,
-                         hipStream_t s) {
-  if (n_rows < 1 || n_rows > nq) return hipErrorInvalidValue;
-  argmax_kernel<<<n_rows, kHeadThreads, 0, s>>>(part, lm_head_chunks(hidden), nq, vocab, logits, token);
+                         void* scratch, hipStream_t s) {
+  if (n_rows < 1 || n_rows > nq || vocab % 8 != 0 || !scratch) return hipErrorInvalidValue;
+  const int nb = (vocab + kArgCols - 1) / kArgCols;
+  float* bv = static_cast<float*>(scratch);
+  int* bi = reinterpret_cast<int*>(bv + static_cast<size_t>(nq) * nb);
+  argmax_blocks_kernel<<<dim3(nb, n_rows), kArgThreads, 0, s>>>(part, lm_head_chunks(hidden), nq, vocab, logits, bv, bi);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  argmax_rows_kernel<<<n_rows, kArgThreads, 0, s>>>(bv, bi, nb, token);
   return hipGetLastError();
 }
 
