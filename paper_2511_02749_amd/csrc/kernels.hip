@@ -453,68 +453,122 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, 
 }
 
 // ------------------------------------------------------------------ K4 combine
-// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.  One
-// work-group per (tile, query head); a thread merges 8 consecutive dims of a row.
-// K4: one thread per (row, 8 output dims) of one head; a work-group covers
-// kCombineRows rows of one (tile, head).  The partials' maxima are read first
-// (independent loads), then the weighted sum over parts, four parts per step so
-// their loads are in flight together.
-constexpr int kCombineRows = 16;
+// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.  One work-group
+// per (tile, query head, block of 256 / (D / 8) rows): its threads cover the block's
+// (row, 8 output dims) pairs.  With fewer pairs than threads (a few rows over many
+// KV splits: decode steps and the page gather), S threads share a pair and each
+// takes every S-th part (S a power of two, at most 32 and at most the part count),
+// merging as it goes: a running max, the sums so far rescaled when it rises.  The S
+// merges then meet in LDS in a tree.  Loads of four parts are in flight at once.  A
+// part that saw no key of the row (max -inf) is skipped; a row that no part saw
+// comes out 0.
+struct Merge {
+  float m, l;
+  float a[8];
+};
+
+__device__ __forceinline__ void merge_into(Merge& x, float m2, float l2, const float* a2) {
+  if (m2 == -INFINITY) return;
+  if (x.m == -INFINITY) {
+    x.m = m2;
+    x.l = l2;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x.a[i] = a2[i];
+    return;
+  }
+  const float mn = fmaxf(x.m, m2);
+  const float f1 = exp2f(x.m - mn), f2 = exp2f(m2 - mn);
+  x.m = mn;
+  x.l = x.l * f1 + l2 * f2;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x.a[i] = x.a[i] * f1 + a2[i] * f2;
+}
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restrict__ tiles,
                                                       const float* __restrict__ part_o,
                                                       const float* __restrict__ part_ml, int bm, int hq,
                                                       T* __restrict__ out) {
+  constexpr int C8 = D / 8;
+  constexpr int R = 256 / C8;  // rows per work-group
+  __shared__ float sh_m[256], sh_l[256], sh_a[8][256];
   const CombineTile t = tiles[blockIdx.x];
   const int h = blockIdx.y;
-  constexpr int C8 = D / 8;
-  const int r = blockIdx.z * kCombineRows + threadIdx.x / C8;
-  const int c = threadIdx.x % C8;
-  if (threadIdx.x >= kCombineRows * C8 || r >= t.n_rows) return;
-  auto slot_of = [&](int p) { return (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r; };
-  float M = -INFINITY;
-  for (int p = 0; p < t.n_parts; ++p) M = fmaxf(M, part_ml[slot_of(p) * 2]);
-  float L = 0.f;
-  float acc[8];
+  const int row0 = blockIdx.z * R;
+  if (row0 >= t.n_rows) return;
+  const int pairs = min(R, t.n_rows - row0) * C8;
+  int S = 1;
+  while (S < 32 && 2 * S * pairs <= 256 && 2 * S <= t.n_parts) S *= 2;
+  const int per_pass = 256 / S;
+  const int s = threadIdx.x % S;
+  for (int base = 0; base < pairs; base += per_pass) {
+    const int pi = base + threadIdx.x / S;
+    Merge x;
+    x.m = -INFINITY;
+    x.l = 0.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  if (M != -INFINITY) {
-    for (int p0 = 0; p0 < t.n_parts; p0 += 4) {
-      float2 ml[4];
-      float4 a[4], b[4];
+    for (int i = 0; i < 8; ++i) x.a[i] = 0.f;
+    const int r = row0 + pi / C8, c = pi % C8;
+    if (pi < pairs) {
+      auto slot_of = [&](int p) { return (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r; };
+      for (int p0 = s; p0 < t.n_parts; p0 += 4 * S) {
+        float2 ml[4];
+        float4 lo[4], hi[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (p0 + u < t.n_parts) {
-          const int64_t sl = slot_of(p0 + u);
-          ml[u] = *reinterpret_cast<const float2*>(part_ml + sl * 2);
-          a[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c);
-          b[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c + 4);
-        } else {
-          ml[u] = float2{-INFINITY, 0.f};
-          a[u] = b[u] = float4{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < 4; ++u) {
+          const int p = p0 + u * S;
+          if (p < t.n_parts) {
+            const int64_t sl = slot_of(p);
+            ml[u] = *reinterpret_cast<const float2*>(part_ml + sl * 2);
+            lo[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c);
+            hi[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c + 4);
+          } else {
+            ml[u] = float2{-INFINITY, 0.f};
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float a2[8] = {lo[u].x, lo[u].y, lo[u].z, lo[u].w, hi[u].x, hi[u].y, hi[u].z, hi[u].w};
+          merge_into(x, ml[u].x, ml[u].y, a2);
         }
       }
+    }
+    if (S > 1) {  // tree over the S threads of a pair (consecutive threads)
+      sh_m[threadIdx.x] = x.m;
+      sh_l[threadIdx.x] = x.l;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (ml[u].x == -INFINITY) continue;  // a split that saw no key of this row
-        const float w = exp2f(ml[u].x - M);
-        L += ml[u].y * w;
-        acc[0] += a[u].x * w; acc[1] += a[u].y * w; acc[2] += a[u].z * w; acc[3] += a[u].w * w;
-        acc[4] += b[u].x * w; acc[5] += b[u].y * w; acc[6] += b[u].z * w; acc[7] += b[u].w * w;
+      for (int i = 0; i < 8; ++i) sh_a[i][threadIdx.x] = x.a[i];
+      __syncthreads();
+      for (int st = S / 2; st >= 1; st /= 2) {
+        if (s < st) {
+          const int o = threadIdx.x + st;
+          float a2[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) a2[i] = sh_a[i][o];
+          merge_into(x, sh_m[o], sh_l[o], a2);
+          sh_m[threadIdx.x] = x.m;
+          sh_l[threadIdx.x] = x.l;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) sh_a[i][threadIdx.x] = x.a[i];
+        }
+        __syncthreads();
       }
     }
-  }
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  T* dst = out + (static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + 8 * c;
+    if (pi < pairs && s == 0) {
+      const float inv = x.l > 0.f ? 1.f / x.l : 0.f;
+      T* dst = out + (static_cast<int64_t>(t.q_row0 + r) * hq + h) * D + 8 * c;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dst[i] = from_f32<T>(acc[i] * inv);
+      for (int i = 0; i < 8; ++i) dst[i] = from_f32<T>(x.a[i] * inv);
+    }
+    __syncthreads();  // the LDS of this pass is read before the next one writes
+  }
 }
 
 hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n, const float* part_o,
                           const float* part_ml, int bm, void* out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  dim3 grid(n, g.hq, (bm + kCombineRows - 1) / kCombineRows);
+  const int rows_per_group = 256 / (g.d / 8);
+  dim3 grid(n, g.hq, (bm + rows_per_group - 1) / rows_per_group);
   if (g.dtype == SPAN_BF16) {
     if (g.d == 128)
       hipLaunchKernelGGL((combine_kernel<bf16_t, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,

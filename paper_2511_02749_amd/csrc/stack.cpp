@@ -9,7 +9,9 @@
 //   x = x + (silu(gate) * up) W_down                 SwiGLU kernel, GEMM with residual
 //
 // then the final RMSNorm of each query's last cross row, the LM head and the
-// argmax (the first generated token).  Rows that hit the cache are never
+// argmax (the first generated token).  GEMMs of at most 8 rows (decode steps) run
+// on GEMV kernels of our own (HBM-bound: each weight read once), the rest on
+// hipBLASLt.  Rows that hit the cache are never
 // computed: their keys and values are already in the pool's pages, which is the
 // point of the method (section 5.6).
 #include <hip/hip_runtime.h>
@@ -83,6 +85,9 @@ struct Gemm {
     size_t ws = 0;
   };
   std::map<std::tuple<int64_t, int64_t, int64_t, bool>, Plan> plans;
+  // Up to 8 rows (decode steps) go to the GEMV kernels instead, with this fp32
+  // scratch for their partial sums (sized by the caller before the launches).
+  Buf gemv_part;
 
   int init() {
     hipblasStatus_t st = hipblasLtCreate(&h);
@@ -106,6 +111,7 @@ struct Gemm {
       hipblasLtMatrixLayoutDestroy(kv.second.c);
     }
     plans.clear();
+    gemv_part.release();
     if (pref) hipblasLtMatmulPreferenceDestroy(pref);
     if (desc) hipblasLtMatmulDescDestroy(desc);
     if (h) hipblasLtDestroy(h);
@@ -114,6 +120,13 @@ struct Gemm {
 
   int run(const void* x, const void* w, void* y, int64_t M, int64_t N, int64_t K, bool residual, hipStream_t s) {
     if (M == 0) return SPAN_OK;
+    if (M <= 8 && N % 8 == 0 && gemv_part_bytes(static_cast<int>(M), static_cast<int>(N), static_cast<int>(K)) <=
+                                    gemv_part.cap) {
+      hipError_t e = launch_gemv(x, w, y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), residual,
+                                 gemv_part.as<float>(), gemv_part.cap, s);
+      if (e != hipSuccess) return hip_err(e, "GEMV");
+      return SPAN_OK;
+    }
     auto key = std::make_tuple(M, N, K, residual);
     auto it = plans.find(key);
     if (it == plans.end()) {
@@ -204,6 +217,15 @@ int stage_area(span_model* m, size_t n, int32_t** out, const char* who) {
   return SPAN_OK;
 }
 
+// Scratch of the GEMV path for T <= 8 rows: the largest of the four GEMMs' partials.
+size_t gemv_scratch(const span_model_config& c, int T) {
+  const int qkv_w = (c.num_q_heads + 2 * c.num_kv_heads) * c.head_dim;
+  size_t b = gemv_part_bytes(T, qkv_w, c.hidden);
+  b = std::max(b, gemv_part_bytes(T, c.hidden, c.num_q_heads * c.head_dim));
+  b = std::max(b, gemv_part_bytes(T, 2 * c.ffn, c.hidden));
+  return std::max(b, gemv_part_bytes(T, c.hidden, c.ffn));
+}
+
 // Buffers for T compact rows whose attention rows lie in [0, R), then the upload of
 // the row list (compact row i -> attention row), the tokens and the LM-head rows.
 // Buffers grow with the stream drained, so no launch still reads the old ones.
@@ -223,7 +245,8 @@ int prepare(span_model* m, int64_t T, int64_t R, const int32_t* h_rows, const in
       {&m->v, Rz * hkv * d * bf}, {&m->o, Rz * hq * d * bf}, {&m->rows, Tz * 4 + 4}, {&m->toks, Tz * 4 + 4},
       {&m->last, static_cast<size_t>(nh) * 4 + 32}, {&m->nf, static_cast<size_t>(8) * H * bf},
       {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
-      {&m->tok_out, 8 * 4}, {&m->best, argmax_scratch_bytes(8, V)}};
+      {&m->tok_out, 8 * 4}, {&m->best, argmax_scratch_bytes(8, V)},
+      {&m->gemm.gemv_part, T <= 8 ? gemv_scratch(c, static_cast<int>(T)) : 0}};
   bool grow = false;
   for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
   hipError_t e = hipSuccess;

@@ -24,6 +24,13 @@ hipError_t launch_rmsnorm(const void* x, const int32_t* sel, const void* gain, v
 // act[i] = silu(gu[i][0:ffn]) * gu[i][ffn:2 ffn].
 hipError_t launch_swiglu(const void* gu, void* act, int64_t n, int ffn, hipStream_t s);
 
+// Y[M][N] = X[M][K] W[K][N] (+ Y when residual) for 1 <= M <= 8 rows, bf16 row-major
+// in and out, fp32 sums in a fixed order; N a multiple of 8.  part: fp32 scratch of
+// at least gemv_part_bytes(M, N, K).  HBM-bound (W read once).
+size_t gemv_part_bytes(int M, int N, int K);
+hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
+                       size_t part_bytes, hipStream_t s);
+
 // LM head over nq (1, 2, 4 or 8) rows of nf [nq][hidden]: partial logits per chunk
 // of the hidden dimension into part [lm_head_chunks(hidden)][nq][vocab] (fp32).
 // launch_argmax sums the chunks (in chunk order) for the first n_rows rows into

@@ -4,6 +4,7 @@
 // 1 KiB runs.  The GEMMs of the stack go to hipBLASLt (stack.cpp).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "stack_kernels.h"
@@ -265,6 +266,96 @@ __global__ __launch_bounds__(kArgThreads) void argmax_rows_kernel(const float* _
   if (threadIdx.x == 0) token[q] = si[0];
 }
 
+// GEMV for a few rows (decode steps): Y[M][N] = X[M][K] W[K][N] (+ Y), M <= 8,
+// bf16 in and out, fp32 sums.  Pass 1, work-group (64 columns, one of kGemvChunks
+// slices of K): thread (row group g = 0..31, column lane) takes rows g, g + 32, ..
+// of the slice and 8 consecutive columns (a wave reads 8 whole 128-byte row
+// segments per load); the row groups meet in LDS and the work-group writes fp32
+// partials for its slice.  Pass 2, one thread per output element: the slices'
+// partials summed in slice order, the residual added, rounded once.  (A last
+// work-group per column block finishing the sum in pass 1 would need a device-scope
+// release per work-group; across this chip's eight L2s that costs more than the
+// second launch.)  Bound: HBM (W read once; partials of kGemvChunks x 4 bytes per
+// output element).
+constexpr int kGemvCols = 64;
+constexpr int kGemvChunks = 16;
+
+template <int MP>
+__global__ __launch_bounds__(256) void gemv_partial_kernel(const u16* __restrict__ x, const uint4* __restrict__ w,
+                                                           float* __restrict__ part, int M, int N, int K,
+                                                           int rows_per_chunk) {
+  __shared__ float red[32][MP][kGemvCols];
+  const int cl = threadIdx.x & 7;
+  const int rg = threadIdx.x >> 3;
+  const int c0 = blockIdx.x * kGemvCols + cl * 8;
+  const int k0 = blockIdx.y * rows_per_chunk;
+  const int k1 = min(K, k0 + rows_per_chunk);
+  float acc[MP][8];
+#pragma unroll
+  for (int m = 0; m < MP; ++m)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[m][j] = 0.f;
+  if (c0 < N) {
+    const int64_t vrow = N / 8;
+    int k = k0 + rg;
+    for (; k + 96 < k1; k += 128) {  // four rows in flight
+      uint4 wv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) wv[u] = w[static_cast<int64_t>(k + 32 * u) * vrow + c0 / 8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float f[8];
+        unpack8(wv[u], f);
+#pragma unroll
+        for (int m = 0; m < MP; ++m) {
+          if (m >= M) break;
+          const float a = bf(x[static_cast<int64_t>(m) * K + k + 32 * u]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[m][j] = fmaf(a, f[j], acc[m][j]);
+        }
+      }
+    }
+    for (; k < k1; k += 32) {
+      float f[8];
+      unpack8(w[static_cast<int64_t>(k) * vrow + c0 / 8], f);
+#pragma unroll
+      for (int m = 0; m < MP; ++m) {
+        if (m >= M) break;
+        const float a = bf(x[static_cast<int64_t>(m) * K + k]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[m][j] = fmaf(a, f[j], acc[m][j]);
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < MP; ++m)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) red[rg][m][cl * 8 + j] = acc[m][j];
+  __syncthreads();
+  // thread t sums column t % 64 of rows t / 64, t / 64 + 4, .. over the row groups
+  const int col = threadIdx.x % kGemvCols;
+  const int n_t = blockIdx.x * kGemvCols + col;
+  if (n_t < N)
+    for (int m = threadIdx.x / kGemvCols; m < M; m += 256 / kGemvCols) {
+      float sum = 0.f;
+#pragma unroll 8
+      for (int g = 0; g < 32; ++g) sum += red[g][m][col];
+      part[(static_cast<int64_t>(blockIdx.y) * M + m) * N + n_t] = sum;
+    }
+}
+
+__global__ __launch_bounds__(256) void gemv_reduce_kernel(const float* __restrict__ part, int chunks, int M, int N,
+                                                          u16* __restrict__ y, bool residual) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;  // element m * N + n
+  const int64_t MN = static_cast<int64_t>(M) * N;
+  if (i >= MN) return;
+  float sum = 0.f;
+#pragma unroll 4
+  for (int c = 0; c < chunks; ++c) sum += part[static_cast<int64_t>(c) * MN + i];
+  if (residual) sum += bf(y[i]);
+  y[i] = to_bf(sum);
+}
+
 int grid_for(int64_t items, int threads) {
   int64_t g = (items + threads - 1) / threads;
   if (g > 65536) g = 65536;
@@ -323,6 +414,31 @@ hipError_t launch_lm_head(const void* nf, const void* w, float* part, int nq, in
     case 8: lm_head_kernel<8><<<grid, kHeadThreads, 0, s>>>(n, wv, part, hidden, vocab, rows); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+size_t gemv_part_bytes(int M, int N, int K) {
+  (void)K;
+  return static_cast<size_t>(kGemvChunks) * M * N * sizeof(float);
+}
+
+hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
+                       size_t part_bytes, hipStream_t s) {
+  if (M < 1 || M > 8 || N % 8 != 0 || K < 1 || gemv_part_bytes(M, N, K) > part_bytes) return hipErrorInvalidValue;
+  const int chunks = std::min(kGemvChunks, (K + 31) / 32);
+  const int rows = (K + chunks - 1) / chunks;
+  const dim3 grid((N + kGemvCols - 1) / kGemvCols, chunks);
+  const u16* xx = static_cast<const u16*>(x);
+  const uint4* ww = static_cast<const uint4*>(w);
+  if (M == 1) gemv_partial_kernel<1><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
+  else if (M == 2) gemv_partial_kernel<2><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
+  else if (M <= 4) gemv_partial_kernel<4><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
+  else gemv_partial_kernel<8><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t items = static_cast<int64_t>(M) * N;
+  gemv_reduce_kernel<<<static_cast<int>((items + 255) / 256), 256, 0, s>>>(part, chunks, M, N, static_cast<u16*>(y),
+                                                                           residual);
   return hipGetLastError();
 }
 
