@@ -308,18 +308,35 @@ class Pool:
         return Plan(self, list(queries), stream, static)
 
 
+# Data addresses of int32 token arrays already marshalled, by id: the entry holds the
+# array itself, so its id cannot be reused while the entry lives, and an array whose
+# buffer this cache references cannot be resized in place.  Bounded; cleared when full.
+_ADDR: dict = {}
+_ADDR_CAP = 1 << 14
+
+
 def _span(s, keep: list) -> SpanTokens:
     t = s.tokens
+    hit = _ADDR.get(id(t))
+    if hit is not None and hit[0] is t:
+        return SpanTokens(hit[1], hit[2], 0, int(s.row))
     if not (isinstance(t, np.ndarray) and t.dtype == np.int32 and t.flags.c_contiguous):
         t = np.ascontiguousarray(t, dtype=np.int32)
         keep.append(t)
-    return SpanTokens(t.ctypes.data if t.size else None, t.size, 0, int(s.row))
+        return SpanTokens(t.ctypes.data if t.size else None, t.size, 0, int(s.row))
+    addr = t.ctypes.data if t.size else None
+    if len(_ADDR) >= _ADDR_CAP:
+        _ADDR.clear()
+    _ADDR[id(t)] = (t, addr, t.size)
+    return SpanTokens(addr, t.size, 0, int(s.row))
 
 
 def _query_array(queries: list, keep: list):
     arr = (SpanQuery * max(1, len(queries)))()
     for i, q in enumerate(queries):
-        fr = (SpanTokens * max(1, len(q.frags)))(*[_span(f, keep) for f in q.frags])
+        fr = (SpanTokens * max(1, len(q.frags)))()
+        for j, f in enumerate(q.frags):
+            fr[j] = _span(f, keep)
         keep.append(fr)
         arr[i] = SpanQuery(prefix=_span(q.prefix, keep), frags=fr, n_frags=len(q.frags), reserved=0,
                            cross=_span(q.cross, keep))

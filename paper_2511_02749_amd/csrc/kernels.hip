@@ -38,7 +38,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restrict__ pages,
                                                          const T* __restrict__ k, const T* __restrict__ v,
                                                          T* __restrict__ pool, int64_t layer_off, int hkv,
-                                                         const float2* __restrict__ rope) {
+                                                         int heads_per_group, const float2* __restrict__ rope) {
   constexpr int E = Chunk16<T>::E;
   constexpr int H = D / 2;
   constexpr int HG = 32768 / (kPage * D * static_cast<int>(sizeof(T)));  // kv heads per LDS pass
@@ -49,13 +49,16 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
   const int64_t page_elems = 2ll * hkv * kPage * D;
   T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems;
   T* vp = kp + static_cast<int64_t>(hkv) * kPage * D;
+  // this work-group's kv heads (all of them, or one group when the pages are few)
+  const int hb = blockIdx.y * heads_per_group;
+  const int he = min(hkv, hb + heads_per_group);
 
   // K: item (head, slot, chunk of E rotary pairs (i, i + H))
-  for (int e = threadIdx.x; e < hkv * kPage * (H / E); e += blockDim.x) {
+  for (int e = threadIdx.x; e < (he - hb) * kPage * (H / E); e += blockDim.x) {
     const int q = e % (H / E);
     const int hs = e / (H / E);
     const int s = hs % kPage;
-    const int h = hs / kPage;
+    const int h = hb + hs / kPage;
     Chunk16<T> y0, y1;
     if (s < pg.n_valid) {
       const T* src = k + (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + q * E;
@@ -83,8 +86,8 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
   }
 
   // V: rows [slot][d] of a group of heads into LDS, then transposed rows out
-  for (int h0 = 0; h0 < hkv; h0 += HG) {
-    const int hn = min(HG, hkv - h0);
+  for (int h0 = hb; h0 < he; h0 += HG) {
+    const int hn = min(HG, he - h0);
     for (int e = threadIdx.x; e < kPage * hn * (D / E); e += blockDim.x) {
       const int qd = e % (D / E);
       const int sh = e / (D / E);
@@ -118,8 +121,12 @@ __global__ __launch_bounds__(256) void rope_write_kernel(const NewPage* __restri
 template <typename T, int D>
 static hipError_t rope_write_t(const PoolGeom& g, const NewPage* pages, int n, const void* k, const void* v,
                                const float2* rope, hipStream_t s) {
-  hipLaunchKernelGGL((rope_write_kernel<T, D>), dim3(n), dim3(256), 0, s, pages, static_cast<const T*>(k),
-                     static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv, rope);
+  // few pages (cross segments): a work-group per (page, kv head), so the write is not
+  // left to a handful of compute units
+  const int hpg = n >= 256 ? g.hkv : 1;
+  hipLaunchKernelGGL((rope_write_kernel<T, D>), dim3(n, (g.hkv + hpg - 1) / hpg), dim3(256), 0, s, pages,
+                     static_cast<const T*>(k), static_cast<const T*>(v), static_cast<T*>(g.base), g.layer_off, g.hkv,
+                     hpg, rope);
   return hipGetLastError();
 }
 

@@ -89,6 +89,16 @@ __device__ __forceinline__ void dma16_m0(const void* g, uint32_t lds_wave) {
   __asm__ volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_wave) : "memory");
 }
 __device__ __forceinline__ void dma16(const void* g, void* lds_wave) { dma16_m0(g, lds_byte(lds_wave)); }
+// The same from a wave-uniform base (scalar registers) plus a 32-bit per-lane byte
+// offset: no 64-bit address arithmetic on the vector ALU.
+__device__ __forceinline__ void dma16_s(const void* base, uint32_t ofs, uint32_t lds_wave) {
+  __asm__ volatile("global_load_lds_dwordx4 %0, %1" ::"v"(ofs), "s"(base), "{m0}"(lds_wave) : "memory");
+}
+// Four bytes per lane to LDS at lds_wave + 4 * lane: used only to bring lines into the
+// caches ahead of a later load (the LDS bytes are never read).
+__device__ __forceinline__ void touch4_m0(const void* g, uint32_t lds_wave) {
+  __asm__ volatile("global_load_lds_dword %0, off" ::"v"(g), "{m0}"(lds_wave) : "memory");
+}
 
 // s_waitcnt with vmcnt = N (bits 3:0 and 15:14); expcnt and lgkmcnt left at their
 // maximum, so only vector-memory operations are waited for.

@@ -46,15 +46,17 @@ uint64_t page_hash(uint64_t prev, const int32_t* tok, int32_t n, int32_t page_id
 uint64_t fragment_seed(uint64_t prefix_last_or_root) { return mix64(prefix_last_or_root ^ SPAN_HASH_FRAG_TAG); }
 
 namespace {
-// The page-hash chains of up to four spans, advanced in lockstep: the chains are
-// independent, so their multiply latencies overlap.  out[c] is exactly the chain
-// page_hash gives for span c from seeds[c].
-void chains4(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps, std::vector<uint64_t>* out) {
-  uint64_t h[4];
-  int32_t n[4];
-  const int32_t* t[4];
+// The page-hash chains of up to kLanes spans, advanced in lockstep: the chains are
+// independent, so their multiply latencies overlap (one chain leaves the multiplier
+// idle most of the time; eight keep it busy).  out[c] is exactly the chain page_hash
+// gives for span c from seeds[c].
+constexpr int kLanes = 8;
+void chains(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps, std::vector<uint64_t>* out) {
+  uint64_t h[kLanes];
+  int32_t n[kLanes];
+  const int32_t* t[kLanes];
   int32_t nmax = 0;
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < kLanes; ++c) {
     h[c] = c < k ? seeds[c] : 0;
     n[c] = c < k ? spans[c]->n : 0;
     t[c] = c < k ? spans[c]->tok : nullptr;
@@ -67,9 +69,9 @@ void chains4(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t p
   for (int32_t p = 0; p * ps < nmax; ++p) {
     const int32_t base = p * ps;
     for (int32_t i = 0; i < ps; ++i)
-      for (int c = 0; c < 4; ++c)
+      for (int c = 0; c < kLanes; ++c)
         if (base + i < n[c]) h[c] = mix64(h[c] ^ static_cast<uint64_t>(static_cast<uint32_t>(t[c][base + i])));
-    for (int c = 0; c < 4; ++c)
+    for (int c = 0; c < kLanes; ++c)
       if (base < n[c]) {
         const int32_t m = std::min(ps, n[c] - base);
         h[c] = stored_hash(mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(m)) << 32) ^
@@ -257,7 +259,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     } else {
       const std::vector<uint64_t>& ph = chain_of(SPAN_HASH_ROOT, q.prefix);
       uint64_t fs = fragment_seed(ph.empty() ? SPAN_HASH_ROOT : ph.back());
-      // the fragments' chains (all from seed fs), four at a time
+      // the fragments' chains (all from seed fs), kLanes at a time
       std::vector<const SpanIn*> todo;
       for (const SpanIn& f : q.frags)
         if (memo.find(MemoKey{f.tok, f.n, fs}) == memo.end()) {
@@ -265,11 +267,12 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
           for (const SpanIn* o : todo) dup |= (o->tok == f.tok && o->n == f.n);
           if (!dup) todo.push_back(&f);
         }
-      for (size_t i = 0; i < todo.size(); i += 4) {
-        const int k = static_cast<int>(std::min<size_t>(4, todo.size() - i));
-        const uint64_t seeds[4] = {fs, fs, fs, fs};
-        std::vector<uint64_t> hs[4];
-        chains4(seeds, &todo[i], k, ps, hs);
+      for (size_t i = 0; i < todo.size(); i += kLanes) {
+        const int k = static_cast<int>(std::min<size_t>(kLanes, todo.size() - i));
+        uint64_t seeds[kLanes];
+        std::fill(seeds, seeds + kLanes, fs);
+        std::vector<uint64_t> hs[kLanes];
+        chains(seeds, &todo[i], k, ps, hs);
         for (int c = 0; c < k; ++c) memo.emplace(MemoKey{todo[i + c]->tok, todo[i + c]->n, fs}, std::move(hs[c]));
       }
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, true});

@@ -37,8 +37,11 @@
 //
 // K/V stream: the key tiles of a work-group's items form one stream.  Before the
 // QK of stream tile x every wave waits for its own DMA of tiles <= x, passes one
-// barrier, and issues the DMA of tile x + 2 (HBM to LDS, global_load_lds, no
-// register staging).  K(x) is read only by QK(x), before the barrier of tile x + 1,
+// barrier, and prepares the DMA of tile x + 2 (HBM to LDS, global_load_lds from a
+// scalar page address, no register staging), whose instructions it issues one per
+// chunk of the block that follows, so the eight waves do not queue them at once.
+// When the stream enters an item, each wave also touches the query rows it will load
+// for it two tiles later, so that load finds them in the caches.  K(x) is read only by QK(x), before the barrier of tile x + 1,
 // and V(x) only by PV(x), before the barrier of tile x + 2; so the fetch at the
 // barrier of tile x may overwrite the K of tile x - 1 and the V of tile x - 2: a
 // 3-slot K ring and a 4-slot V ring (132 KiB of LDS at head dim 128 with the rotary
@@ -91,7 +94,8 @@ struct PGeo {
   static constexpr int SROW = STAGE_IN_V ? VBYTES / kNW / 32 : 2 * D;
   static constexpr int STOFF = BROFF + BRBYTES;
   static constexpr int SCHOFF = STOFF + (STAGE_IN_V ? 0 : kNW * 32 * SROW);  // schedule words
-  static constexpr int LDS = SCHOFF + 64;
+  static constexpr int TOFF = SCHOFF + 64;  // per wave 256 bytes that cache-warming loads land in
+  static constexpr int LDS = TOFF + kNW * 256;
   static_assert(SROW % 64 == 0 && (2 * D) % SROW == 0, "a pass covers whole 32-dim blocks");
 };
 
@@ -237,17 +241,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // KPW + u: keys 4q.. (head dim 128) of one page, chunk c of key k stored at chunk
   // c ^ kswz(k).  V instruction u fills 1024 bytes of the V tile, which is laid out
   // [page][d][two 16-byte halves], half h of row d stored at h ^ (d >> 3 & 1): rows
-  // 32b .. 32b + 31 of one page.  So every instruction reads a single page, and a
-  // tile's fetch is a scalar page base plus these offsets.
+  // 32b .. 32b + 31 of one page.  Every instruction of wave w reads page w / 2 of the
+  // tile, so a fetch is one scalar page address plus these 32-bit offsets.
   constexpr int CPK = D / 8;  // 16-byte chunks per key row
+  static_assert(GE::KPW * (64 / CPK) * 2 == 16 && GE::VPW * 2 == D / 32, "one page per wave");
+  const int wpage = wave / 2;
   uint32_t dk_ofs[GE::KPW], dv_ofs[GE::VPW];
-  int dk_page[GE::KPW], dv_page[GE::VPW];
 #pragma unroll
   for (int u = 0; u < GE::KPW; ++u) {
     const int qi = wave * GE::KPW + u;
     const int key = qi * (64 / CPK) + lane / CPK;
     const int c = (lane % CPK) ^ kswz<D>(key);
-    dk_page[u] = (qi * (64 / CPK)) >> 4;  // the instruction's keys share one page
     dk_ofs[u] = 2u * static_cast<uint32_t>((key & 15) * D + 8 * c);
   }
 #pragma unroll
@@ -255,13 +259,20 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int qi = wave * GE::VPW + u;
     const int d = 32 * (qi % (D / 32)) + (lane >> 1);
     const int h = (lane & 1) ^ ((d >> 3) & 1);
-    dv_page[u] = qi / (D / 32);
     dv_ofs[u] = 2u * static_cast<uint32_t>(hkv * kPage * D + d * kPage + 8 * h);
   }
   // (position of key 0, real keys) of stream tiles x, x + 1, x + 2 after the fetch
   // at the barrier of tile x
   int mp0 = 0, mn0 = 0, mp1 = 0, mn1 = 0, mp2 = 0, mn2 = 0;
-  auto fetch_next = [&]() __attribute__((always_inline)) -> int {  // DMA instructions this wave issued
+  // A fetch is prepared at a barrier (tile record, page address, LDS slots) and its
+  // NDMA instructions are issued either at once or one per chunk of the block that
+  // follows the barrier, so that the eight waves do not all queue their DMA at the
+  // same moment.
+  const unsigned char* f_base = nullptr;  // the wave's page of the prepared tile
+  uint32_t f_mk = 0, f_mv = 0;           // LDS destinations of its K and V instructions
+  const unsigned char* const pool_b = reinterpret_cast<const unsigned char*>(pool + layer_off);
+  unsigned char* const touch_lds = lds + GE::TOFF + wave * 256;
+  auto fetch_prep = [&]() __attribute__((always_inline)) -> int {  // DMA instructions to issue
     if (dk_ok && dk_j >= dk.n) {  // every item has at least one key tile
       ++dk_k;
       dk_e = dk_k == 1 ? ec1 : ec2;
@@ -270,6 +281,15 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       if (dk_ok) {
         load_item_keys(tiles, dk_e / hkv, dk);
         dk_kvh = dk_e % hkv;
+        // the query rows this wave will load for the new item, two tiles from now,
+        // brought into the caches now (lines of 128 bytes, D / 64 per row)
+        const WorkTile* tn = tiles + __builtin_amdgcn_readfirstlane(dk_e / hkv);
+        const int rows = tn->n_rows, row0 = tn->q_row0;
+        constexpr int LPR = D / 64;
+        const int trow = 32 * rb + lane / LPR;
+        if (lane < 32 * LPR && trow < rows)
+          touch4_m0(q + (static_cast<int64_t>(row0 + trow) * hq + dk_kvh * G + hsub) * D + 64 * (lane % LPR),
+                    lds_byte(touch_lds));
       }
     }
     mp0 = mp1;
@@ -283,19 +303,28 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     mn2 = tp.nk;
     // the kv head's K rows of a page start kvh * 16 * D elements in, its V rows as many
     // elements past the page's V half
-    const unsigned char* pg = reinterpret_cast<const unsigned char*>(pool + layer_off + dk_kvh * kPage * D);
-#pragma unroll
-    for (int u = 0; u < GE::KPW; ++u)
-      dma16_m0(pg + static_cast<int64_t>(pick4(tp.id, dk_page[u])) * (page_elems * 2) + dk_ofs[u],
-               lds_byte(kring + fk * GE::KBYTES + (wave * GE::KPW + u) * 1024));
-#pragma unroll
-    for (int u = 0; u < GE::VPW; ++u)
-      dma16_m0(pg + static_cast<int64_t>(pick4(tp.id, dv_page[u])) * (page_elems * 2) + dv_ofs[u],
-               lds_byte(vring + fv * GE::VBYTES + (wave * GE::VPW + u) * 1024));
+    f_base = pool_b + (static_cast<int64_t>(pick4(tp.id, wpage)) * page_elems + dk_kvh * kPage * D) * 2;
+    f_mk = lds_byte(kring + fk * GE::KBYTES + wave * GE::KPW * 1024);
+    f_mv = lds_byte(vring + fv * GE::VBYTES + wave * GE::VPW * 1024);
     ++dk_j;
     fk = (fk == GE::NK - 1) ? 0 : fk + 1;
     fv = (fv == GE::NV - 1) ? 0 : fv + 1;
     return NDMA;
+  };
+  int last_ops = 0;  // DMA instructions of the most recent fetch group
+  auto issue_dma = [&](int u) __attribute__((always_inline)) {  // instruction u of the prepared fetch
+    if (u < GE::KPW)
+      dma16_s(f_base, dk_ofs[u], f_mk + u * 1024);
+    else
+      dma16_s(f_base, dv_ofs[u - GE::KPW], f_mv + (u - GE::KPW) * 1024);
+  };
+  auto fetch_next = [&]() __attribute__((always_inline)) -> int {  // prepared and issued at once
+    const int n = fetch_prep();
+    if (n) {
+#pragma unroll
+      for (int u = 0; u < NDMA; ++u) issue_dma(u);
+    }
+    return n;
   };
 
   // ---------------- compute-side state
@@ -420,20 +449,21 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // (lazily raised max, P = 2^(S - m) packed into pk_out, its row sum) runs in KS
   // chunks; chunk t also issues the QK MFMA of step t of the next key block (WQK, K
   // tile at byte kaddr) and the PV MFMA t of the previous block (WPV, V of pages
-  // vaddr.., operand pk_prev), and the LDS reads of the operands two chunks ahead.
-  // The operands of chunks 0 and 1 come from the previous block (pre.v always;
+  // vaddr.., operand pk_prev), the LDS reads of the operands two chunks ahead and,
+  // in the block after a barrier (WDMA), one DMA instruction of the fetch prepared
+  // there.  The operands of chunks 0 and 1 come from the previous block (pre.v always;
   // pre.k if PREK, else K is read here, right after the barrier that made it
   // valid), and the last two chunks read those of the next block (K at nkaddr if
   // NXK, V at nvaddr if NXV), so the MFMAs of chunk 0 need not wait for LDS.  Chunk
   // 0 issues its MFMAs before the row max, which they do not depend on.  The chunks
   // are fenced, so the compiler keeps this order and at most four operand reads (16
   // registers) are in flight.
-  auto block = [&](auto wqk, auto wpv, auto prek, auto nxk, auto nxv, const f32x16_t& s_in,
+  auto block = [&](auto wqk, auto wpv, auto prek, auto nxk, auto nxv, auto wdma, const f32x16_t& s_in,
                    bf16x8_t (&pk_out)[2], uint32_t kaddr, f32x16_t& s_out, uint32_t vaddr,
                    const bf16x8_t (&pk_prev)[2], Pre& pre, uint32_t nkaddr, uint32_t nvaddr, float& corr,
                    float& tsum) __attribute__((always_inline)) -> bool {
     constexpr bool WQK = decltype(wqk)::value, WPV = decltype(wpv)::value, PREK = decltype(prek)::value;
-    constexpr bool NXK = decltype(nxk)::value, NXV = decltype(nxv)::value;
+    constexpr bool NXK = decltype(nxk)::value, NXV = decltype(nxv)::value, WDMA = decltype(wdma)::value;
     constexpr int WPC = 8 / KS;  // packed words of P per chunk (8 words per block)
     auto rdk = [&](uint32_t base, int t) __attribute__((always_inline)) { return *lds_at(base, kofs[t]); };
     auto rdv = [&](uint32_t base, int t) __attribute__((always_inline)) {
@@ -458,6 +488,9 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         if (PREK || t > 0) qk_mfma(t);
       }
       if constexpr (WPV) o[t % DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[t], pk_prev[t / DB], o[t % DB], 0, 0, 0);
+      if constexpr (WDMA) {  // one DMA instruction of the fetch prepared at the barrier
+        if (t < NDMA && last_ops) issue_dma(t);
+      }
       if (t + 2 < KS) {
         if constexpr (WQK) ak[t + 2] = rdk(kaddr, t + 2);
         if constexpr (WPV) av[t + 2] = rdv(vaddr, t + 2);
@@ -641,9 +674,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
     st_rows = 0;
   };
-
   // ---------------- kernel prologue: rotary rows 0..31, stream tiles 0 and 1, first query
-  int last_ops = 0;  // DMA instructions of the most recent fetch group
   // raw query rows of the next item: loaded during an item's last block and rotated
   // at the next item's first barrier, after the previous item's rows are stored
   bf16x8_t qn[KS];
@@ -702,10 +733,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     l = 0.f;
 
     // the barrier before the QK of a stream tile, then the fetch of the tile two ahead
+    // (its DMA instructions go out one per chunk of the block after the barrier)
     auto sync_fetch = [&]() __attribute__((always_inline)) {
       wait_group<NDMA>(last_ops);
       block_sync();
-      last_ops = fetch_next();
+      last_ops = fetch_prep();
     };
 
     // Key blocks u = 0 .. 2n-1 of the item (block u&1 of tile u/2), processed as
@@ -721,7 +753,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     auto step_even = [&](auto with_pv, auto prek, uint32_t kslot0, uint32_t vprev,
                          uint32_t vnext) __attribute__((always_inline)) {
       float corr, tsum;
-      const bool up = block(T_{}, with_pv, prek, F_{}, T_{}, S[0], P[0], kslot0 + 32 * D * 2, S[1],
+      const bool up = block(T_{}, with_pv, prek, F_{}, T_{}, F_{}, S[0], P[0], kslot0 + 32 * D * 2, S[1],
                             vprev + 2 * D * 32, P[1], pre, 0u, vnext, corr, tsum);
       rescale(up, corr, tsum);
       mask(S[1], 1, mp0, mn0);
@@ -732,7 +764,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       sync_fetch();
       __builtin_amdgcn_sched_barrier(0);
       float corr, tsum;
-      const bool up = block(T_{}, T_{}, F_{}, T_{}, T_{}, S[1], P[1], knext, S[0], vcur, P[0], pre,
+      const bool up = block(T_{}, T_{}, F_{}, T_{}, T_{}, T_{}, S[1], P[1], knext, S[0], vcur, P[0], pre,
                             knext + 32 * D * 2, vcur + 2 * D * 32, corr, tsum);
       rescale(up, corr, tsum);
       mask(S[0], 0, mp0, mn0);
@@ -741,7 +773,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     auto last_odd = [&](uint32_t vcur) __attribute__((always_inline)) {
       if (has_next) prefetch(ec1, qn);  // the next item's query rows
       float corr, tsum;
-      const bool up = block(F_{}, T_{}, F_{}, F_{}, F_{}, S[1], P[1], 0u, S[0], vcur, P[0], pre, 0u, 0u, corr, tsum);
+      const bool up = block(F_{}, T_{}, F_{}, F_{}, F_{}, F_{}, S[1], P[1], 0u, S[0], vcur, P[0], pre, 0u, 0u, corr, tsum);
       rescale(up, corr, tsum);
       pv(vcur, 1, P[1]);
     };
