@@ -98,7 +98,7 @@ template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
     const WorkTile* __restrict__ tiles, int n_tiles_total, const TileRec* __restrict__ kt, const bf16_t* __restrict__ q,
     bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
-    const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    const float2* __restrict__ rope, f16_t* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = Geo<D>;
   constexpr int BM = 32 * (kNW / G);
   // Two key groups (cross attention, four query heads per kv head): a few-row item
@@ -516,14 +516,16 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           }
       } else {
         const int64_t slot = (static_cast<int64_t>(t.part + grp) * hq + head) * BM + irow;
-        float* po = part_o + slot * D;
+        f16_t* po = part_o + slot * D;
+        const float inv = l_row > 0.f ? 1.f / l_row : 0.f;  // O / l in fp16
 #pragma unroll
         for (int db = 0; db < GE::DB; ++db)
 #pragma unroll
           for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = 32 * db + 8 * g4 + 4 * h2;
-            *reinterpret_cast<float4*>(po + d0) =
-                float4{o[db][4 * g4], o[db][4 * g4 + 1], o[db][4 * g4 + 2], o[db][4 * g4 + 3]};
+            *reinterpret_cast<f16x4_t*>(po + d0) =
+                f16x4_t{static_cast<f16_t>(o[db][4 * g4] * inv), static_cast<f16_t>(o[db][4 * g4 + 1] * inv),
+                        static_cast<f16_t>(o[db][4 * g4 + 2] * inv), static_cast<f16_t>(o[db][4 * g4 + 3] * inv)};
           }
         if (h2 == 0) {  // a row that saw no key: max -inf, as the merge expects
           part_ml[slot * 2] = l_row > 0.f ? m : -INFINITY;
@@ -567,7 +569,7 @@ hipError_t cu_count(int* n) {
 
 template <int D, int G>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                           void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = Geo<D>::LDS;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<D, G>),
@@ -581,13 +583,13 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
   hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt,
                      static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
-                     g.layer_off, g.hq, g.hkv, scale_log2, rope, part_o, part_ml);
+                     g.layer_off, g.hq, g.hkv, scale_log2, rope, static_cast<f16_t*>(part_o), part_ml);
   return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           float* po, float* pml, const float2* rope, hipStream_t s) {
+                           void* po, float* pml, const float2* rope, hipStream_t s) {
   switch (g.hq / g.hkv) {
     case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, po, pml, rope, s);
     case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, po, pml, rope, s);
@@ -598,7 +600,7 @@ static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, cons
 }
 
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
-                            void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                            void* out, void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype)) return hipErrorInvalidValue;
   return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, part_o, part_ml, rope, s)

@@ -57,6 +57,19 @@ struct span_pool {
 };
 
 namespace {
+int max_parts(const std::vector<CombineTile>& c) {
+  int m = 0;
+  for (const CombineTile& t : c) m = std::max(m, static_cast<int>(t.n_parts));
+  return m;
+}
+
+// The (m, l) half of a split-KV partial buffer, after its part_o_elems O elements.
+float* part_ml_of(const span_pool* p, float* part, size_t part_o_elems) {
+  if (!part) return nullptr;
+  return reinterpret_cast<float*>(reinterpret_cast<unsigned char*>(part) +
+                                  part_o_elems * part_elem_bytes(p->cfg.dtype == SPAN_BF16));
+}
+
 // Make the rotary table cover positions [0, need).  Computed on the host in double
 // precision (angle reduced to [-pi, pi] before cos/sin), rounded once to float, and
 // copied on `stream`: kernels of this plan on that stream follow the copy, and
@@ -109,7 +122,7 @@ struct span_plan_t {
   hipStream_t stream = nullptr;
   std::vector<unsigned char> host_meta;
   unsigned char* dev_meta = nullptr;
-  float* part = nullptr;  // partial O then partial (m, l)
+  float* part = nullptr;  // partial O (fp16 O / l for bf16 pools, fp32 O otherwise) then partial (m, l)
   size_t part_o_elems = 0;
   // device views
   const KvPage* kv = nullptr;
@@ -319,8 +332,8 @@ int spanq::plan_impl(span_pool* pool, const span_query* qs, int32_t nq, void* st
     size_t o_sc = put(hb, std::vector<unsigned>(kSchedWords * span_plan_t::kSchedSlots, 0u));
     size_t o_xc = put(hb, P.prefill_chunks);
     pl->part_o_elems = static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * d;
-    const size_t part_bytes =
-        (pl->part_o_elems + static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2) * sizeof(float);
+    const size_t part_bytes = pl->part_o_elems * part_elem_bytes(pool->cfg.dtype == SPAN_BF16) +
+                              static_cast<size_t>(P.n_parts) * pool->cfg.num_q_heads * pl->bm * 2 * sizeof(float);
     if (region) {
       const size_t meta_bytes = (hb.size() + 255) & ~static_cast<size_t>(255);
       if (meta_bytes + part_bytes > region_bytes) {
@@ -724,8 +737,8 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   e = launch_move_pages(g, pl->mv, static_cast<int>(P.moves.size()), pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page moves");
   tm.mark(2);
-  float* po = pl->part;
-  float* pml = pl->part ? pl->part + pl->part_o_elems : nullptr;
+  void* po = pl->part;
+  float* pml = part_ml_of(pl->pool, pl->part, pl->part_o_elems);
   const int nt = static_cast<int>(P.t_cross.size());
   if (pl->mfma) {
     // the last n_cross_few tiles (few rows, two key groups) on the 16-row kernel
@@ -737,7 +750,7 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   }
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: attention");
   tm.mark(3);
-  e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, out, s);
+  e = launch_combine(g, pl->cb, static_cast<int>(P.combine.size()), po, pml, pl->bm, max_parts(P.combine), out, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: combine");
   tm.mark(4);
   if (!tm.ev.empty()) pl->ev_cross.push_back(tm.ev);
@@ -809,8 +822,8 @@ int span_plan_decode(span_plan_t* pl, const int32_t* n_new, const int64_t* rows,
   if (e == hipSuccess && !pl->dec_copied) e = hipEventCreateWithFlags(&pl->dec_copied, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventRecord(pl->dec_copied, s);
   pl->dec.part_o_elems = static_cast<size_t>(d.n_parts) * pool->cfg.num_q_heads * pl->bm * pool->cfg.head_dim;
-  const size_t part_bytes =
-      (pl->dec.part_o_elems + static_cast<size_t>(d.n_parts) * pool->cfg.num_q_heads * pl->bm * 2) * sizeof(float);
+  const size_t part_bytes = pl->dec.part_o_elems * part_elem_bytes(pool->cfg.dtype == SPAN_BF16) +
+                            static_cast<size_t>(d.n_parts) * pool->cfg.num_q_heads * pl->bm * 2 * sizeof(float);
   if (e == hipSuccess && d.n_parts > 0) e = hipMallocAsync(reinterpret_cast<void**>(&pl->dec.part), part_bytes, s);
   if (e == hipSuccess && !pl->dec_ready) {
     pl->dec_ready = take_order_event(pool);
@@ -847,8 +860,8 @@ int span_decode_attend(span_plan_t* pl, int32_t layer, const void* q, const void
   tm.mark(0);
   hipError_t e = launch_append_kv(g, pl->dec.writes, static_cast<int>(d.writes.size()), k, v, pl->dec.rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_decode_attend: page write");
-  float* po = pl->dec.part;
-  float* pml = po ? po + pl->dec.part_o_elems : nullptr;
+  void* po = pl->dec.part;
+  float* pml = part_ml_of(pl->pool, pl->dec.part, pl->dec.part_o_elems);
   const int nt = static_cast<int>(d.tiles.size());
   if (pl->mfma) {
     const int nf = d.n_few;
@@ -859,7 +872,7 @@ int span_decode_attend(span_plan_t* pl, int32_t layer, const void* q, const void
     e = launch_attn_generic(g, pl->dec.tiles, nt, pl->dec.kv, q, out, po, pml, pl->dec.rope, s);
   }
   if (e != hipSuccess) return hip_fail(e, "span_decode_attend: attention");
-  e = launch_combine(g, pl->dec.cb, static_cast<int>(d.combine.size()), po, pml, pl->bm, out, s);
+  e = launch_combine(g, pl->dec.cb, static_cast<int>(d.combine.size()), po, pml, pl->bm, max_parts(d.combine), out, s);
   if (e != hipSuccess) return hip_fail(e, "span_decode_attend: combine");
   tm.mark(1);
   if (!tm.ev.empty()) pl->ev_decode.push_back(tm.ev);

@@ -26,6 +26,26 @@ __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <>
 __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
 
+// A split-KV partial of one (row, head), written by the attention kernels and merged
+// by the combine pass, with (m, l) in fp32 beside it.  bf16 pools store O / l in fp16:
+// a convex combination of V rows, so bounded by the largest |V| (fp16 holds up to
+// 65504), with 11 significant bits against the output's 8, at half the bytes of fp32.
+// fp32 pools store the unnormalised O in fp32.
+typedef _Float16 f16_t;
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+template <typename T>
+struct PartOf;
+template <>
+struct PartOf<bf16_t> {
+  using type = f16_t;
+  static constexpr bool normalized = true;
+};
+template <>
+struct PartOf<float> {
+  using type = float;
+  static constexpr bool normalized = false;
+};
+
 // Position of key slot s (0..15) inside a page's transposed V rows: bits 2 and 3
 // swapped, i.e. quads ordered {0-3, 8-11, 4-7, 12-15}.  A P.V operand of the MFMA
 // kernel then covers 8 consecutive positions (one 16-byte LDS read).

@@ -94,7 +94,7 @@ template <int D>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void few_mfma_kernel(
     const WorkTile* __restrict__ tiles, int n_tiles_total, const TileRec* __restrict__ kt,
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, int bm,
-    float scale_log2, const float2* __restrict__ rope, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    float scale_log2, const float2* __restrict__ rope, f16_t* __restrict__ part_o, float* __restrict__ part_ml) {
   using GE = FGeo<D>;
   constexpr int KS = GE::KS, DB = GE::DB, NDMA = GE::NDMA;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
@@ -435,7 +435,7 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       j += sz;
     }
 
-    // ---- epilogue: this group's partial (unnormalised O, running max, row sum).
+    // ---- epilogue: this group's partial (O / l in fp16, running max, row sum).
     // The next item's query is rotated first, so the stores do not sit in front of
     // that wait.
     const float l_row = row_sum4(l);
@@ -446,10 +446,13 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
     if (r < t.n_rows && t.part >= 0) {
       const int64_t slot = (static_cast<int64_t>(t.part + kg) * hq + head) * bm + r;
-      float* po = part_o + slot * D;
+      f16_t* po = part_o + slot * D;
+      const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<float4*>(po + 16 * db + 4 * g) = float4{o[db][0], o[db][1], o[db][2], o[db][3]};
+        *reinterpret_cast<f16x4_t*>(po + 16 * db + 4 * g) =
+            f16x4_t{static_cast<f16_t>(o[db][0] * inv), static_cast<f16_t>(o[db][1] * inv),
+                    static_cast<f16_t>(o[db][2] * inv), static_cast<f16_t>(o[db][3] * inv)};
       if (g == 0) {  // a row that saw no key: max -inf, as the merge expects
         part_ml[slot * 2] = l_row > 0.f ? m : -INFINITY;
         part_ml[slot * 2 + 1] = l_row;
@@ -466,7 +469,7 @@ bool few_supported(int hq, int hkv, int d, int dtype) {
 
 template <int D>
 static hipError_t launch_few_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
-                               float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                               void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = FGeo<D>::LDS;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&few_mfma_kernel<D>),
@@ -480,12 +483,12 @@ static hipError_t launch_few_d(const PoolGeom& g, const WorkTile* tiles, int n, 
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
   hipLaunchKernelGGL((few_mfma_kernel<D>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt, static_cast<const bf16_t*>(q),
                      static_cast<const bf16_t*>(g.base), g.layer_off, g.hq, g.hkv, mfma_bm(kFG), scale_log2, rope,
-                     part_o, part_ml);
+                     static_cast<f16_t*>(part_o), part_ml);
   return hipGetLastError();
 }
 
 hipError_t launch_few_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
-                           float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                           void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!few_supported(g.hq, g.hkv, g.d, g.dtype) || part_o == nullptr || part_ml == nullptr)
     return hipErrorInvalidValue;

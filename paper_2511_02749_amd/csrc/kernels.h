@@ -33,7 +33,7 @@ hipError_t launch_move_pages(const PoolGeom& g, const MovePage* moves, int n_mov
 // Generic (vector ALU) span attention over work tiles of up to 64 rows.
 constexpr int kGenericBM = 64;
 hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const KvPage* kv,
-                               const void* q, void* out, float* part_o, float* part_ml,
+                               const void* q, void* out, void* part_o, float* part_ml,
                                const float2* rope, hipStream_t s);
 
 // bf16 MFMA attention kernels: eight waves per work-group, work items (row tile,
@@ -47,9 +47,9 @@ int mfma_bm(int g);
 hipError_t cu_count(int* n);
 
 // Cross attention: the query is rotated by each tile's delta; tiles with
-// part >= 0 write fp32 partials for the combine pass.
+// part >= 0 write partials (fp16 O / l and fp32 (m, l)) for the combine pass.
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt,
-                            const void* q, void* out, float* part_o, float* part_ml,
+                            const void* q, void* out, void* part_o, float* part_ml,
                             const float2* rope, hipStream_t s);
 
 // Cross attention for two-key-group tiles of at most 16 rows (four query heads per
@@ -57,7 +57,7 @@ hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tile
 // part + 1 of each tile, like the two-key-group mode of launch_attn_mfma.
 bool few_supported(int hq, int hkv, int d, int dtype);
 hipError_t launch_few_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt, const void* q,
-                           float* part_o, float* part_ml, const float2* rope, hipStream_t s);
+                           void* part_o, float* part_ml, const float2* rope, hipStream_t s);
 
 // Span prefill (no repositioning, no key splits), the software-pipelined kernel.
 // Every tile must have at least one key tile.  `sched` is kSchedWords zeroed device
@@ -75,9 +75,14 @@ hipError_t launch_prefill_mfma(const PoolGeom& g, const WorkTile* tiles, int n_t
                                const int32_t* chunks_host, const int32_t* chunks_dev, int n_chunks, int* queues,
                                hipStream_t s);
 
+// Split-KV partial buffers: n_parts x H_q x bm slots of D elements (O / l in fp16
+// for bf16 pools, the unnormalised O in fp32 for fp32 pools), then the slots' (m, l)
+// as fp32 pairs.  Bytes of one O element:
+constexpr int part_elem_bytes(bool bf16_pool) { return bf16_pool ? 2 : 4; }
+
 // K4: merge KV-split partials (bm = rows per tile of the producing kernel).
-hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const float* part_o,
-                          const float* part_ml, int bm, void* out, hipStream_t s);
+hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n_tiles, const void* part_o,
+                          const float* part_ml, int bm, int max_parts, void* out, hipStream_t s);
 
 // Machine-peak probes (probes.hip): an MFMA-only loop on every compute unit (two
 // waves per SIMD, probe_mfma_flops(iters, n_cu) flops per launch) and a streaming

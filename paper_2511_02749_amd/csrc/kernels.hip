@@ -4,6 +4,7 @@
 // at angle pos * theta^(-2i/d); cos/sin come from the pool's position table.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
                                                           const T* __restrict__ pool, int64_t layer_off, int hq,
                                                           int hkv, float scale_log2,
                                                           const float2* __restrict__ rope,
-                                                          float* __restrict__ part_o, float* __restrict__ part_ml) {
+                                                          void* __restrict__ part_o, float* __restrict__ part_ml) {
   constexpr int H = D / 2;
   __shared__ float ks[kPage][D + 1];
   __shared__ float vs[D][kPage + 1];
@@ -430,9 +431,11 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
     for (int i = 0; i < D; ++i) o[i] = from_f32<T>(acc[i] * inv);
   } else {
     const int64_t slot = (static_cast<int64_t>(t.part) * hq + h) * kGenericBM + lane;
-    float* po = part_o + slot * D;
+    using P = typename PartOf<T>::type;
+    P* po = static_cast<P*>(part_o) + slot * D;
+    const float inv = !PartOf<T>::normalized ? 1.f : (l > 0.f ? 1.f / l : 0.f);
 #pragma unroll
-    for (int i = 0; i < D; ++i) po[i] = acc[i];
+    for (int i = 0; i < D; ++i) po[i] = static_cast<P>(acc[i] * inv);
     part_ml[slot * 2 + 0] = m;
     part_ml[slot * 2 + 1] = l;
   }
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(const WorkTile* __rest
 
 template <typename T, int D>
 static hipError_t attn_generic_t(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                                 void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                                 void* out, void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   hipLaunchKernelGGL((attn_generic_kernel<T, D>), dim3(n, g.hq), dim3(64), 0, s, tiles, kv,
                      static_cast<const T*>(q), static_cast<T*>(out), static_cast<const T*>(g.base), g.layer_off,
@@ -449,7 +452,7 @@ static hipError_t attn_generic_t(const PoolGeom& g, const WorkTile* tiles, int n
 }
 
 hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, const KvPage* kv, const void* q,
-                               void* out, float* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                               void* out, void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (g.dtype == SPAN_BF16) {
     if (g.d == 128) return attn_generic_t<bf16_t, 128>(g, tiles, n, kv, q, out, part_o, part_ml, rope, s);
@@ -460,7 +463,8 @@ hipError_t launch_attn_generic(const PoolGeom& g, const WorkTile* tiles, int n, 
 }
 
 // ------------------------------------------------------------------ K4 combine
-// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p.  One work-group
+// out = sum_p o_p 2^(m_p - M) / sum_p l_p 2^(m_p - M), M = max_p m_p, with o_p the
+// unnormalised partial (l_p times the stored O / l for bf16 pools).  One work-group
 // per (tile, query head, block of 256 / (D / 8) rows): its threads cover the block's
 // (row, 8 output dims) pairs.  With fewer pairs than threads (a few rows over many
 // KV splits: decode steps and the page gather), S threads share a pair and each
@@ -493,11 +497,10 @@ __device__ __forceinline__ void merge_into(Merge& x, float m2, float l2, const f
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restrict__ tiles,
-                                                      const float* __restrict__ part_o,
-                                                      const float* __restrict__ part_ml, int bm, int hq,
+                                                      const void* __restrict__ part_o,
+                                                      const float* __restrict__ part_ml, int bm, int hq, int R,
                                                       T* __restrict__ out) {
-  constexpr int C8 = D / 8;
-  constexpr int R = 256 / C8;  // rows per work-group
+  constexpr int C8 = D / 8;  // R: rows per work-group, at most 256 / C8
   __shared__ float sh_m[256], sh_l[256], sh_a[8][256];
   const CombineTile t = tiles[blockIdx.x];
   const int h = blockIdx.y;
@@ -520,24 +523,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restr
       auto slot_of = [&](int p) { return (static_cast<int64_t>(t.part0 + p) * hq + h) * bm + r; };
       for (int p0 = s; p0 < t.n_parts; p0 += 4 * S) {
         float2 ml[4];
-        float4 lo[4], hi[4];
+        float a2[4][8];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int p = p0 + u * S;
           if (p < t.n_parts) {
             const int64_t sl = slot_of(p);
             ml[u] = *reinterpret_cast<const float2*>(part_ml + sl * 2);
-            lo[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c);
-            hi[u] = *reinterpret_cast<const float4*>(part_o + sl * D + 8 * c + 4);
+            if constexpr (PartOf<T>::normalized) {  // O / l in fp16: back to O
+              typedef f16_t f16x8_t __attribute__((ext_vector_type(8)));
+              const f16x8_t v = *reinterpret_cast<const f16x8_t*>(static_cast<const f16_t*>(part_o) + sl * D + 8 * c);
+#pragma unroll
+              for (int i = 0; i < 8; ++i) a2[u][i] = static_cast<float>(v[i]) * ml[u].y;
+            } else {
+              const float* po = static_cast<const float*>(part_o) + sl * D + 8 * c;
+              const float4 lo = *reinterpret_cast<const float4*>(po), hi = *reinterpret_cast<const float4*>(po + 4);
+              a2[u][0] = lo.x, a2[u][1] = lo.y, a2[u][2] = lo.z, a2[u][3] = lo.w;
+              a2[u][4] = hi.x, a2[u][5] = hi.y, a2[u][6] = hi.z, a2[u][7] = hi.w;
+            }
           } else {
             ml[u] = float2{-INFINITY, 0.f};
           }
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float a2[8] = {lo[u].x, lo[u].y, lo[u].z, lo[u].w, hi[u].x, hi[u].y, hi[u].z, hi[u].w};
-          merge_into(x, ml[u].x, ml[u].y, a2);
-        }
+        for (int u = 0; u < 4; ++u) merge_into(x, ml[u].x, ml[u].y, a2[u]);
       }
     }
     if (S > 1) {  // tree over the S threads of a pair (consecutive threads)
@@ -571,24 +580,28 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineTile* __restr
   }
 }
 
-hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n, const float* part_o,
-                          const float* part_ml, int bm, void* out, hipStream_t s) {
+hipError_t launch_combine(const PoolGeom& g, const CombineTile* tiles, int n, const void* part_o,
+                          const float* part_ml, int bm, int max_parts, void* out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int rows_per_group = 256 / (g.d / 8);
+  // Fewer rows per work-group when tiles have many parts, so that about four parts
+  // fall to each thread: one round of loads in flight instead of a chain of rounds.
+  int share = 1;
+  while (share < 32 && 8 * share <= max_parts) share *= 2;
+  const int rows_per_group = std::max(1, 256 / (g.d / 8) / share);
   dim3 grid(n, g.hq, (bm + rows_per_group - 1) / rows_per_group);
   if (g.dtype == SPAN_BF16) {
     if (g.d == 128)
-      hipLaunchKernelGGL((combine_kernel<bf16_t, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+      hipLaunchKernelGGL((combine_kernel<bf16_t, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq, rows_per_group,
                          static_cast<bf16_t*>(out));
     else
-      hipLaunchKernelGGL((combine_kernel<bf16_t, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+      hipLaunchKernelGGL((combine_kernel<bf16_t, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq, rows_per_group,
                          static_cast<bf16_t*>(out));
   } else {
     if (g.d == 128)
-      hipLaunchKernelGGL((combine_kernel<float, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+      hipLaunchKernelGGL((combine_kernel<float, 128>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq, rows_per_group,
                          static_cast<float*>(out));
     else
-      hipLaunchKernelGGL((combine_kernel<float, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq,
+      hipLaunchKernelGGL((combine_kernel<float, 64>), grid, dim3(256), 0, s, tiles, part_o, part_ml, bm, g.hq, rows_per_group,
                          static_cast<float*>(out));
   }
   return hipGetLastError();

@@ -62,7 +62,7 @@ struct SlotWrite {
 
 // A tile of up to BM consecutive query rows of one span, against the key pages
 // kv[kv_begin, kv_end).  part < 0: write the normalised output; else write the
-// unnormalised partial (one KV split) into partial slot `part`.  With
+// partial of one KV split (O / l, m, l) into partial slot `part`.  With
 // kTwoKeyGroups (MFMA kernel, rows <= 32, four query heads per kv head) the two
 // 32-row wave groups of the work-group take alternate key tiles instead of two
 // row blocks, and write partial slots part and part + 1.
