@@ -50,6 +50,7 @@
 #include "dev_common.h"
 #include "kernels.h"
 #include "mfma_common.h"
+#include "page_write.h"
 
 namespace spanq {
 
@@ -97,8 +98,9 @@ __device__ __forceinline__ void wait_tiles(int k) {
 template <int D, int G>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mfma_kernel(
     const WorkTile* __restrict__ tiles, int n_tiles_total, const TileRec* __restrict__ kt, const bf16_t* __restrict__ q,
-    bf16_t* __restrict__ out, const bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
-    const float2* __restrict__ rope, f16_t* __restrict__ part_o, float* __restrict__ part_ml) {
+    bf16_t* __restrict__ out, bf16_t* __restrict__ pool, int64_t layer_off, int hq, int hkv, float scale_log2,
+    const float2* __restrict__ rope, f16_t* __restrict__ part_o, float* __restrict__ part_ml,
+    const bf16_t* __restrict__ kin, const bf16_t* __restrict__ vin, const NewPage* __restrict__ wpages) {
   using GE = Geo<D>;
   constexpr int BM = 32 * (kNW / G);
   // Two key groups (cross attention, four query heads per kv head): a few-row item
@@ -183,6 +185,25 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     ++is_j;
     ++n_issued;
   };
+  // The cross-segment pages in this work-group's key ranges (wpages given), written
+  // here for its kv head before the tile stream starts, while the LDS is still free.
+  // Every work-group that reads such a page writes it; their writes agree, and each
+  // reads only after its own have completed.
+  if (wpages) {
+    bool wrote = false;
+    for (int ti = t0; ti < n_tiles_total; ti += tstride) {
+      const WorkTile* tw = tiles + __builtin_amdgcn_readfirstlane(ti);
+      const int cnt = tw->flags >> kWriteShift, w0 = tw->w_first;
+      if (cnt > 0)
+        write_pages_one_head<bf16_t, D>(wpages + w0, cnt, kvh, kin, vin, pool, layer_off, hkv, rope,
+                                        reinterpret_cast<bf16_t*>(lds), static_cast<int>(threadIdx.x), kNT);
+      wrote |= cnt > 0;
+    }
+    if (wrote) {
+      wait_vm_all();  // this wave's page stores are done
+      block_sync();   // and every other wave's
+    }
+  }
   for (int k = 0; k < kStages - 2; ++k) issue_next();
 
   bf16x8_t qf[GE::KS];                // Q^T operand of the current item
@@ -569,7 +590,7 @@ hipError_t cu_count(int* n) {
 
 template <int D, int G>
 static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                           void* part_o, float* part_ml, const float2* rope, const CrossWrites& w, hipStream_t s) {
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
   const size_t lds = Geo<D>::LDS;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<D, G>),
@@ -582,29 +603,32 @@ static hipError_t launch_t(const PoolGeom& g, const WorkTile* tiles, int n, cons
   const int64_t items = static_cast<int64_t>(n) * g.hkv;
   const int grid = static_cast<int>(std::min<int64_t>(items, std::max(1, cus / g.hkv) * g.hkv));
   hipLaunchKernelGGL((attn_mfma_kernel<D, G>), dim3(grid), dim3(kNT), lds, s, tiles, n, kt,
-                     static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<const bf16_t*>(g.base),
-                     g.layer_off, g.hq, g.hkv, scale_log2, rope, static_cast<f16_t*>(part_o), part_ml);
+                     static_cast<const bf16_t*>(q), static_cast<bf16_t*>(out), static_cast<bf16_t*>(g.base),
+                     g.layer_off, g.hq, g.hkv, scale_log2, rope, static_cast<f16_t*>(part_o), part_ml,
+                     static_cast<const bf16_t*>(w.k), static_cast<const bf16_t*>(w.v), w.pages);
   return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q, void* out,
-                           void* po, float* pml, const float2* rope, hipStream_t s) {
+                           void* po, float* pml, const float2* rope, const CrossWrites& w, hipStream_t s) {
   switch (g.hq / g.hkv) {
-    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, po, pml, rope, s);
-    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, po, pml, rope, s);
-    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, po, pml, rope, s);
-    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, po, pml, rope, s);
+    case 1: return launch_t<D, 1>(g, tiles, n, kt, q, out, po, pml, rope, w, s);
+    case 2: return launch_t<D, 2>(g, tiles, n, kt, q, out, po, pml, rope, w, s);
+    case 4: return launch_t<D, 4>(g, tiles, n, kt, q, out, po, pml, rope, w, s);
+    case 8: return launch_t<D, 8>(g, tiles, n, kt, q, out, po, pml, rope, w, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n, const TileRec* kt, const void* q,
-                            void* out, void* part_o, float* part_ml, const float2* rope, hipStream_t s) {
+                            void* out, void* part_o, float* part_ml, const float2* rope, const CrossWrites& w,
+                            hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (!mfma_supported(g.hq, g.hkv, g.d, g.dtype)) return hipErrorInvalidValue;
-  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, part_o, part_ml, rope, s)
-                    : launch_d<64>(g, tiles, n, kt, q, out, part_o, part_ml, rope, s);
+  if (w.pages && (!w.k || !w.v)) return hipErrorInvalidValue;
+  return g.d == 128 ? launch_d<128>(g, tiles, n, kt, q, out, part_o, part_ml, rope, w, s)
+                    : launch_d<64>(g, tiles, n, kt, q, out, part_o, part_ml, rope, w, s);
 }
 
 }  // namespace spanq

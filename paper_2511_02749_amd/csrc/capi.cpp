@@ -729,7 +729,11 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   PoolGeom g = geom(pl, layer);
   Timer tm((pl->pool->cfg.flags & SPAN_FLAG_TIMING) != 0, 4, s, pl->pool->event_cache);
   tm.mark(0);
-  hipError_t e = launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->rope, s);
+  // The MFMA cross kernel writes the cross-segment pages itself when every cross tile
+  // is its own (none on the 16-row kernel); otherwise they are written first.
+  const bool fused = pl->mfma && P.n_cross_few == 0 && !P.k3_cross.empty();
+  hipError_t e =
+      fused ? hipSuccess : launch_rope_write(g, pl->k3c, static_cast<int>(P.k3_cross.size()), k, v, pl->rope, s);
   if (e != hipSuccess) return hip_fail(e, "span_cross_attend: page write");
   tm.mark(1);
   // materialised repositioning: this layer's copies of shifted pages, keys rotated
@@ -743,7 +747,9 @@ int span_cross_attend(span_plan_t* pl, int32_t layer, const void* q, const void*
   if (pl->mfma) {
     // the last n_cross_few tiles (few rows, two key groups) on the 16-row kernel
     const int nf = P.n_cross_few;
-    e = launch_attn_mfma(g, pl->tc, nt - nf, pl->kt, q, out, po, pml, pl->rope, s);
+    CrossWrites w;
+    if (fused) w = CrossWrites{pl->k3c, k, v};
+    e = launch_attn_mfma(g, pl->tc, nt - nf, pl->kt, q, out, po, pml, pl->rope, w, s);
     if (e == hipSuccess && nf > 0) e = launch_few_mfma(g, pl->tc + (nt - nf), nf, pl->kt, q, po, pml, pl->rope, s);
   } else {
     e = launch_attn_generic(g, pl->tc, nt, pl->kv, q, out, po, pml, pl->rope, s);
@@ -865,7 +871,7 @@ int span_decode_attend(span_plan_t* pl, int32_t layer, const void* q, const void
   const int nt = static_cast<int>(d.tiles.size());
   if (pl->mfma) {
     const int nf = d.n_few;
-    e = launch_attn_mfma(g, pl->dec.tiles, nt - nf, pl->dec.kt, q, out, po, pml, pl->dec.rope, s);
+    e = launch_attn_mfma(g, pl->dec.tiles, nt - nf, pl->dec.kt, q, out, po, pml, pl->dec.rope, CrossWrites{}, s);
     if (e == hipSuccess && nf > 0)
       e = launch_few_mfma(g, pl->dec.tiles + (nt - nf), nf, pl->dec.kt, q, po, pml, pl->dec.rope, s);
   } else {

@@ -48,9 +48,18 @@ hipError_t cu_count(int* n);
 
 // Cross attention: the query is rotated by each tile's delta; tiles with
 // part >= 0 write partials (fp16 O / l and fp32 (m, l)) for the combine pass.
+// With w.pages given, the kernel also writes the cross-segment pages that each tile
+// names (WorkTile::w_first, flags >> kWriteShift) from the caller's k, v rows, as
+// launch_rope_write would, before reading them: the separate page-write launch and
+// its gap disappear from the cross pass.
+struct CrossWrites {
+  const NewPage* pages = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+};
 hipError_t launch_attn_mfma(const PoolGeom& g, const WorkTile* tiles, int n_tiles, const TileRec* kt,
                             const void* q, void* out, void* part_o, float* part_ml,
-                            const float2* rope, hipStream_t s);
+                            const float2* rope, const CrossWrites& w, hipStream_t s);
 
 // Cross attention for two-key-group tiles of at most 16 rows (four query heads per
 // kv head, bf16, d 64 or 128) on 16x16x32 MFMAs; writes partial slots part and

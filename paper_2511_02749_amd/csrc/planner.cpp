@@ -577,12 +577,16 @@ namespace {
 // Row tiles of cross attention (cross and decode rows) before the KV split.
 struct CrossTile {
   int32_t row0, n, pos0, kv0, kv1;
+  // the query's cross-segment pages: key-list entries wkv0 .. wkv0 + wn, cross page
+  // writes wk3 .. wk3 + wn (wn = 0: none to write, e.g. decode rows)
+  int32_t wkv0 = 0, wk3 = 0, wn = 0;
 };
 
 // The key list a query's cross (and decode) rows read: the prefix, each fragment
 // at its final positions (its repositioned copies at delta 0 when it has them, else
 // its pages with the delta still to apply) and the cross segment's pages.
-void append_query_keys(const Plan& p, const std::vector<int>& ids, int32_t ps, bool pad4, std::vector<KvPage>& kv) {
+// Returns the key-list index where the cross segment's pages begin.
+int32_t append_query_keys(const Plan& p, const std::vector<int>& ids, int32_t ps, bool pad4, std::vector<KvPage>& kv) {
   for (int c = 0; c + 1 < static_cast<int>(ids.size()); ++c) {
     const SpanPlan& s = p.spans[ids[c]];
     if (!s.moved.empty())
@@ -591,7 +595,9 @@ void append_query_keys(const Plan& p, const std::vector<int>& ids, int32_t ps, b
       append_span(kv, s.pages, s.n_tok, ps, s.final0, s.final0 - s.canon0, pad4);
   }
   const SpanPlan& cross = p.spans[ids.back()];
+  const int32_t at = static_cast<int32_t>(kv.size());
   append_span(kv, cross.pages, cross.n_tok, ps, cross.final0, 0, pad4);
+  return at;
 }
 
 // Split the keys of the row tiles into the same number of parts (enough work items
@@ -615,15 +621,25 @@ void tile_cross(const std::vector<CrossTile>& ct, int32_t max_pages, const Tilin
     chunk = ((chunk + align - 1) / align) * align;   // splits cut at whole tiles
     int32_t parts = (chunk > 0) ? (n_pages + chunk - 1) / chunk : 1;
     const bool two = c.n <= t.two_group_rows;     // each split writes two partials
+    // the cross pages among key-list entries [b, e): (first write, count << kWriteShift)
+    auto writes = [&](int32_t b, int32_t e, int32_t* first) {
+      const int32_t lo = std::max(b, c.wkv0), hi = std::min(e, c.wkv0 + c.wn);
+      *first = hi > lo ? c.wk3 + (lo - c.wkv0) : 0;
+      return hi > lo ? (hi - lo) << kWriteShift : 0;
+    };
     if (parts <= 1 && !two) {
-      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, 0, 0});
+      int32_t wf = 0;
+      const int32_t wfl = writes(c.kv0, c.kv1, &wf);
+      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, c.kv0, c.kv1, -1, wfl, wf});
       continue;
     }
     int32_t part0 = *n_parts;
     for (int32_t s = 0; s < parts; ++s) {
       int32_t b = c.kv0 + s * chunk;
       int32_t e = std::min(c.kv1, b + chunk);
-      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, b, e, *n_parts, two ? kTwoKeyGroups : 0, 0});
+      int32_t wf = 0;
+      const int32_t wfl = writes(b, e, &wf);
+      tiles->push_back(WorkTile{c.row0, c.n, c.pos0, b, e, *n_parts, (two ? kTwoKeyGroups : 0) | wfl, wf});
       *n_parts += two ? 2 : 1;
     }
     combine->push_back(CombineTile{c.row0, c.n, part0, *n_parts - part0});
@@ -708,17 +724,19 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
     const auto& ids = p->query_spans[qi];
     const SpanPlan& cross = p->spans[ids.back()];
     if (cross.n_tok == 0) continue;
+    const int32_t wk3 = static_cast<int32_t>(p->k3_cross.size());
     for (size_t pg = 0; pg < cross.pages.size(); ++pg)
       p->k3_cross.push_back(NewPage{cross.pages[pg], std::min<int32_t>(ps, cross.n_tok - static_cast<int32_t>(pg) * ps),
                                     static_cast<int32_t>(cross.row + pg * ps), cross.final0 + static_cast<int32_t>(pg) * ps});
     const int32_t kv0 = static_cast<int32_t>(p->kv.size());
-    append_query_keys(*p, ids, ps, t.pad4, p->kv);
+    const int32_t wkv0 = append_query_keys(*p, ids, ps, t.pad4, p->kv);
     const int32_t kv1 = static_cast<int32_t>(p->kv.size());
     p->cross_kv_pages += kv1 - kv0;
     for (int32_t j0 = 0; j0 < cross.n_tok; j0 += t.bm_cross) {
       int32_t n = std::min(t.bm_cross, cross.n_tok - j0);
       int32_t end = list_end(p->kv, kv0, kv1, cross.final0 + j0 + n - 1, t.pad4);
-      ct.push_back(CrossTile{static_cast<int32_t>(cross.row + j0), n, cross.final0 + j0, kv0, end});
+      ct.push_back(CrossTile{static_cast<int32_t>(cross.row + j0), n, cross.final0 + j0, kv0, end, wkv0, wk3,
+                             static_cast<int32_t>(cross.pages.size())});
       max_pages = std::max(max_pages, end - kv0);
       p->rows_cross.push_back(Plan::RowRun{cross.row + j0, n});
       p->cross_pairs += static_cast<int64_t>(n) * (cross.final0 + 1) + static_cast<int64_t>(n) * (2 * j0 + n - 1) / 2;

@@ -66,7 +66,11 @@ struct SlotWrite {
 // kTwoKeyGroups (MFMA kernel, rows <= 32, four query heads per kv head) the two
 // 32-row wave groups of the work-group take alternate key tiles instead of two
 // row blocks, and write partial slots part and part + 1.
+// Cross tiles also name the cross-segment pages of their key range (flags >> 8 of
+// them, from entry w_first of the plan's cross page writes), which the MFMA cross
+// kernel writes itself before reading them when the launch asks it to.
 constexpr int32_t kTwoKeyGroups = 1;
+constexpr int kWriteShift = 8;
 struct WorkTile {
   int32_t q_row0;
   int32_t n_rows;
@@ -75,7 +79,7 @@ struct WorkTile {
   int32_t kv_end;
   int32_t part;
   int32_t flags;
-  int32_t pad1;
+  int32_t w_first;
 };
 
 // Merge partial slots part0..part0+n_parts-1 into output rows q_row0...

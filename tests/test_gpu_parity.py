@@ -163,6 +163,34 @@ def test_pages_hold_canonical_kv(dtype):
     run.close()
 
 
+@pytest.mark.parametrize("dtype,cross_len", [("bf16", 10), ("bf16", 23), ("bf16", 100), ("f32", 23)])
+def test_cross_pages_hold_final_kv(dtype, cross_len):
+    """The cross segment's pages hold its keys rotated at their final positions and its
+    values, unfilled slots zero, whichever launch writes them: the page-write kernel
+    (few-row cross tiles, fp32 pools) or the MFMA cross kernel itself (the others)."""
+    wl = W.small_workload(dtype=dtype, cross_len=cross_len)
+    run = GpuRun(wl)
+    batch = wl.batches[0]
+    plan = run.run_batch(batch)
+    for qi, q in enumerate(batch):
+        ids, n_hit = plan.block_table(qi, len(q.frags))
+        assert n_hit == 0 and len(ids) == (q.cross.n + 15) // 16
+        final0 = q.prefix.n + sum(f.n for f in q.frags)
+        rows = np.arange(q.cross.row, q.cross.row + q.cross.n)
+        kc = OA.rope(wl.k[rows].astype(np.float64), final0 + np.arange(q.cross.n), wl.rope_theta)
+        vc = wl.v[rows].astype(np.float64)
+        for p, pid in enumerate(ids):
+            k, v = _page_kv(run, pid, wl)
+            n = min(16, q.cross.n - 16 * p)
+            kr, vr = kc[16 * p: 16 * p + n].transpose(1, 0, 2), vc[16 * p: 16 * p + n].transpose(1, 0, 2)
+            rtol = 2.0 ** -8 if dtype == "bf16" else 1e-6
+            np.testing.assert_allclose(k[:, :n], kr, rtol=rtol, atol=1e-5)
+            np.testing.assert_array_equal(v[:, :n], vr.astype(np.float32))
+            assert not np.any(k[:, n:]) and not np.any(v[:, n:])   # unfilled slots are zero
+    _check_rows(run, batch, _computed_rows(plan), TOL[dtype])
+    run.close()
+
+
 def test_permutation_keeps_pages_and_rows_bit_identical():
     wl = W.small_workload(orders=[[0, 1, 2, 3], [3, 1, 0, 2]], n_queries=2, frags_per_query=4,
                           batch_split=[1, 1])
