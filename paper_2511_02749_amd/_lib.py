@@ -3,6 +3,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import struct
 import weakref
 from typing import Iterable, List, Optional, Sequence
 
@@ -314,33 +315,51 @@ class Pool:
 _ADDR: dict = {}
 _ADDR_CAP = 1 << 14
 
+# span_tokens and span_query (include/spanq.h) as packed little-endian records
+_SPAN_REC = struct.Struct("<QiiQ")
+_QUERY_REC = struct.Struct("<QiiQ" "Qii" "QiiQ")
+assert _SPAN_REC.size == ctypes.sizeof(SpanTokens) and _QUERY_REC.size == ctypes.sizeof(SpanQuery)
 
-def _span(s, keep: list) -> SpanTokens:
-    t = s.tokens
+
+def _tokens(t, keep: list):
+    """(array, data address or 0, length) of a span's int32 tokens."""
     hit = _ADDR.get(id(t))
     if hit is not None and hit[0] is t:
-        return SpanTokens(hit[1], hit[2], 0, int(s.row))
+        return hit
     if not (isinstance(t, np.ndarray) and t.dtype == np.int32 and t.flags.c_contiguous):
         t = np.ascontiguousarray(t, dtype=np.int32)
         keep.append(t)
-        return SpanTokens(t.ctypes.data if t.size else None, t.size, 0, int(s.row))
-    addr = t.ctypes.data if t.size else None
+        return t, (t.ctypes.data if t.size else 0), t.size
     if len(_ADDR) >= _ADDR_CAP:
         _ADDR.clear()
-    _ADDR[id(t)] = (t, addr, t.size)
-    return SpanTokens(addr, t.size, 0, int(s.row))
+    hit = _ADDR[id(t)] = (t, t.ctypes.data if t.size else 0, t.size)
+    return hit
 
 
 def _query_array(queries: list, keep: list):
-    arr = (SpanQuery * max(1, len(queries)))()
+    """A span_query array over the queries (the buffers it points into go to keep)."""
+    n = max(1, len(queries))
+    qb = bytearray(_QUERY_REC.size * n)
+    pack_span, pack_query, get = _SPAN_REC.pack_into, _QUERY_REC.pack_into, _ADDR.get
     for i, q in enumerate(queries):
-        fr = (SpanTokens * max(1, len(q.frags)))()
-        for j, f in enumerate(q.frags):
-            fr[j] = _span(f, keep)
-        keep.append(fr)
-        arr[i] = SpanQuery(prefix=_span(q.prefix, keep), frags=fr, n_frags=len(q.frags), reserved=0,
-                           cross=_span(q.cross, keep))
-    return arr
+        frags = q.frags
+        fb = bytearray(_SPAN_REC.size * max(1, len(frags)))
+        o = 0
+        for f in frags:
+            t = f.tokens
+            hit = get(id(t))  # the cached entry inline: this loop runs once per fragment
+            if hit is None or hit[0] is not t:
+                hit = _tokens(t, keep)
+            pack_span(fb, o, hit[1], hit[2], 0, int(f.row))
+            o += _SPAN_REC.size
+        keep.append(fb)
+        p, c = q.prefix, q.cross
+        _, pa, pm = _tokens(p.tokens, keep)
+        _, ca, cm = _tokens(c.tokens, keep)
+        pack_query(qb, _QUERY_REC.size * i, pa, pm, 0, int(p.row), ctypes.addressof(ctypes.c_char.from_buffer(fb)),
+                   len(frags), 0, ca, cm, 0, int(c.row))
+    keep.append(qb)
+    return (SpanQuery * n).from_buffer(qb)
 
 
 class Plan:

@@ -51,22 +51,36 @@ namespace {
 // idle most of the time; eight keep it busy).  out[c] is exactly the chain page_hash
 // gives for span c from seeds[c].
 constexpr int kLanes = 8;
-void chains(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps, std::vector<uint64_t>* out) {
+// Lanes beyond k hash lane 0's tokens and their results are dropped, so that the
+// pages every span has in full take one loop without per-lane conditions.
+void chains(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps, std::vector<uint64_t>* const* out) {
   uint64_t h[kLanes];
   int32_t n[kLanes];
   const int32_t* t[kLanes];
-  int32_t nmax = 0;
+  int32_t nmax = 0, nmin = spans[0]->n;
   for (int c = 0; c < kLanes; ++c) {
     h[c] = c < k ? seeds[c] : 0;
     n[c] = c < k ? spans[c]->n : 0;
-    t[c] = c < k ? spans[c]->tok : nullptr;
+    t[c] = c < k ? spans[c]->tok : spans[0]->tok;
     nmax = std::max(nmax, n[c]);
     if (c < k) {
-      out[c].clear();
-      out[c].reserve(static_cast<size_t>((n[c] + ps - 1) / ps));
+      nmin = std::min(nmin, n[c]);
+      out[c]->clear();
+      out[c]->reserve(static_cast<size_t>((n[c] + ps - 1) / ps));
     }
   }
-  for (int32_t p = 0; p * ps < nmax; ++p) {
+  int32_t p = 0;
+  for (; (p + 1) * ps <= nmin; ++p) {
+    const int32_t base = p * ps;
+    for (int32_t i = 0; i < ps; ++i)
+      for (int c = 0; c < kLanes; ++c) h[c] = mix64(h[c] ^ static_cast<uint64_t>(static_cast<uint32_t>(t[c][base + i])));
+    for (int c = 0; c < kLanes; ++c) {
+      h[c] = stored_hash(mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(ps)) << 32) ^
+                               static_cast<uint64_t>(static_cast<uint32_t>(p))));
+      if (c < k) out[c]->push_back(h[c]);
+    }
+  }
+  for (; p * ps < nmax; ++p) {
     const int32_t base = p * ps;
     for (int32_t i = 0; i < ps; ++i)
       for (int c = 0; c < kLanes; ++c)
@@ -76,7 +90,7 @@ void chains(const uint64_t* seeds, const SpanIn* const* spans, int k, int32_t ps
         const int32_t m = std::min(ps, n[c] - base);
         h[c] = stored_hash(mix64(h[c] ^ (static_cast<uint64_t>(static_cast<uint32_t>(m)) << 32) ^
                                  static_cast<uint64_t>(static_cast<uint32_t>(p))));
-        out[c].push_back(h[c]);
+        out[c]->push_back(h[c]);
       }
   }
 }
@@ -119,9 +133,44 @@ bool PoolIndex::content_equal(int32_t pid, const Spec& s) const {
                      sizeof(int32_t) * s.n_tok) == 0;
 }
 
+void PoolIndex::pending_begin(size_t n) {
+  size_t cap = 64;
+  while (cap < 2 * n) cap *= 2;
+  if (cap > pend_key_.size()) {
+    pend_key_.assign(cap, 0);
+    pend_val_.assign(cap, 0);
+    pend_stamp_.assign(cap, 0);
+    pend_gen_ = 0;
+  }
+  pend_mask_ = pend_key_.size() - 1;
+  if (++pend_gen_ == 0) {  // stamps wrapped: clear them all
+    std::fill(pend_stamp_.begin(), pend_stamp_.end(), 0u);
+    pend_gen_ = 1;
+  }
+}
+
+int32_t PoolIndex::pending_find(uint64_t h) const {
+  for (size_t i = static_cast<size_t>(h ^ (h >> 29)) & pend_mask_;; i = (i + 1) & pend_mask_) {
+    if (pend_stamp_[i] != pend_gen_) return -1;
+    if (pend_key_[i] == h) return pend_val_[i];
+  }
+}
+
+void PoolIndex::pending_insert(uint64_t h, int32_t v) {
+  for (size_t i = static_cast<size_t>(h ^ (h >> 29)) & pend_mask_;; i = (i + 1) & pend_mask_) {
+    if (pend_stamp_[i] != pend_gen_) {
+      pend_stamp_[i] = pend_gen_;
+      pend_key_[i] = h;
+      pend_val_[i] = v;
+      return;
+    }
+    if (pend_key_[i] == h) return;
+  }
+}
+
 bool PoolIndex::spec_equal(const Spec& a, const Spec& b) const {
   return a.idx == b.idx && a.n_tok == b.n_tok && a.parent == b.parent &&
-         std::memcmp(a.tok, b.tok, sizeof(int32_t) * a.n_tok) == 0;
+         (a.tok == b.tok || std::memcmp(a.tok, b.tok, sizeof(int32_t) * a.n_tok) == 0);
 }
 
 int32_t PoolIndex::pop_free() {
@@ -205,8 +254,8 @@ struct Entry {
 int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& tiling, Plan* out,
                     std::string* msg) {
   const int32_t ps = page_size_;
-  std::vector<Spec> specs;
-  std::unordered_map<uint64_t, int32_t> pending;
+  std::vector<Spec>& specs = specs_;
+  specs.clear();
   {
     size_t pages_in = 0;
     for (const QueryIn& q : qs) {
@@ -214,7 +263,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
       for (const SpanIn& f : q.frags) pages_in += (f.n + ps - 1) / ps;
     }
     specs.reserve(pages_in);
-    pending.reserve(pages_in);
+    pending_begin(pages_in);  // at most half full: every probe ends
   }
   struct SpanWalk {
     int kind, query, child;
@@ -250,6 +299,38 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     return memo.emplace(MemoKey{in.tok, in.n, seed}, std::move(hs)).first->second;
   };
 
+  // Every fragment chain of the batch first, kLanes at a time: a fragment's chain
+  // starts from a seed its query's prefix chain gives.
+  std::vector<uint64_t> frag_seed(qs.size(), SPAN_HASH_ROOT);
+  if (hash_mode_ != SPAN_HASH_STOCK) {
+    struct Todo {
+      const SpanIn* in;
+      uint64_t seed;
+      std::vector<uint64_t>* out;
+    };
+    std::vector<Todo> todo;
+    for (size_t qi = 0; qi < qs.size(); ++qi) {
+      const std::vector<uint64_t>& ph = chain_of(SPAN_HASH_ROOT, qs[qi].prefix);
+      const uint64_t fs = fragment_seed(ph.empty() ? SPAN_HASH_ROOT : ph.back());
+      frag_seed[qi] = fs;
+      for (const SpanIn& f : qs[qi].frags) {
+        auto ins = memo.try_emplace(MemoKey{f.tok, f.n, fs});
+        if (ins.second) todo.push_back({&f, fs, &ins.first->second});  // node values stay put
+      }
+    }
+    for (size_t i = 0; i < todo.size(); i += kLanes) {
+      const int k = static_cast<int>(std::min<size_t>(kLanes, todo.size() - i));
+      uint64_t seeds[kLanes];
+      const SpanIn* in[kLanes];
+      std::vector<uint64_t>* out[kLanes];
+      for (int c = 0; c < k; ++c) {
+        seeds[c] = todo[i + c].seed;
+        in[c] = todo[i + c].in;
+        out[c] = todo[i + c].out;
+      }
+      chains(seeds, in, k, ps, out);
+    }
+  }
   for (size_t qi = 0; qi < qs.size(); ++qi) {
     const QueryIn& q = qs[qi];
     struct Src { uint64_t seed; SpanIn in; int kind, child; bool partial_ok; };
@@ -257,38 +338,22 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     if (hash_mode_ == SPAN_HASH_STOCK) {
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, false});
     } else {
-      const std::vector<uint64_t>& ph = chain_of(SPAN_HASH_ROOT, q.prefix);
-      uint64_t fs = fragment_seed(ph.empty() ? SPAN_HASH_ROOT : ph.back());
-      // the fragments' chains (all from seed fs), kLanes at a time
-      std::vector<const SpanIn*> todo;
-      for (const SpanIn& f : q.frags)
-        if (memo.find(MemoKey{f.tok, f.n, fs}) == memo.end()) {
-          bool dup = false;
-          for (const SpanIn* o : todo) dup |= (o->tok == f.tok && o->n == f.n);
-          if (!dup) todo.push_back(&f);
-        }
-      for (size_t i = 0; i < todo.size(); i += kLanes) {
-        const int k = static_cast<int>(std::min<size_t>(kLanes, todo.size() - i));
-        uint64_t seeds[kLanes];
-        std::fill(seeds, seeds + kLanes, fs);
-        std::vector<uint64_t> hs[kLanes];
-        chains(seeds, &todo[i], k, ps, hs);
-        for (int c = 0; c < k; ++c) memo.emplace(MemoKey{todo[i + c]->tok, todo[i + c]->n, fs}, std::move(hs[c]));
-      }
       srcs.push_back({SPAN_HASH_ROOT, q.prefix, 0, 0, true});
-      for (size_t c = 0; c < q.frags.size(); ++c) srcs.push_back({fs, q.frags[c], 1, static_cast<int>(c), true});
+      for (size_t c = 0; c < q.frags.size(); ++c)
+        srcs.push_back({frag_seed[qi], q.frags[c], 1, static_cast<int>(c), true});
     }
     for (const Src& s : srcs) {
       SpanWalk w{s.kind, static_cast<int>(qi), s.child, s.in, {}};
       const std::vector<uint64_t>& hs = chain_of(s.seed, s.in);
+      w.entries.reserve(hs.size());
       bool missed = false;
       for (int32_t p = 0; p * ps < s.in.n; ++p) {
         int32_t n = std::min(ps, s.in.n - p * ps);
         Spec sp{hs[p], p == 0 ? s.seed : hs[p - 1], p, n, s.in.tok + p * ps, n == ps || s.partial_ok, false};
         if (!missed && sp.cacheable) {
-          auto it = pending.find(sp.hash);
-          if (it != pending.end() && spec_equal(specs[it->second], sp)) {
-            w.entries.push_back({false, true, it->second});
+          const int32_t pj = pending_find(sp.hash);
+          if (pj >= 0 && spec_equal(specs[pj], sp)) {
+            w.entries.push_back({false, true, pj});
             continue;
           }
           auto jt = index_.find(sp.hash);
@@ -300,7 +365,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
         missed = true;
         int32_t slot = static_cast<int32_t>(specs.size());
         specs.push_back(sp);
-        if (sp.cacheable && pending.find(sp.hash) == pending.end()) pending[sp.hash] = slot;
+        if (sp.cacheable) pending_insert(sp.hash, slot);
         w.entries.push_back({false, false, slot});
       }
       query_spans[qi].push_back(static_cast<int>(walk.size()));
@@ -393,6 +458,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   }
   P.hits = hit_pids;
   std::vector<int32_t> slot_pid(specs.size(), -1);
+  P.new_pages.reserve(static_cast<size_t>(need));
   auto alloc = [&](int32_t slot) {
     if (free_count() == 0) evict_one(&P);
     int32_t pid = pop_free();
@@ -443,6 +509,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
     sp.row = w.in.row;
     sp.n_hit = 0;
     for (int32_t m : move_of[wi]) sp.moved.push_back(P.moves[m].dst_page);
+    sp.pages.reserve(w.entries.size());
     bool leading = true;
     for (const Entry& e : w.entries) {
       sp.pages.push_back(e.hit ? e.x : slot_pid[e.x]);
@@ -479,20 +546,23 @@ namespace {
 void append_span(std::vector<KvPage>& kv, const std::vector<int32_t>& pages, int32_t n_tok, int32_t ps,
                  int32_t pos_base, int32_t delta, bool pad4) {
   const int32_t np = static_cast<int32_t>(pages.size());
+  const int32_t padded = (pad4 && np > 0) ? (np + 3) / 4 * 4 : np;
+  const size_t at = kv.size();
+  kv.resize(at + padded);
+  KvPage* out = kv.data() + at;
   for (int32_t pg = 0; pg < np; ++pg)
-    kv.push_back(KvPage{pages[pg], std::min(ps, n_tok - pg * ps), pos_base + pg * ps, delta});
-  if (pad4 && np > 0)
-    for (int32_t pg = np; pg % 4 != 0; ++pg) kv.push_back(KvPage{pages[np - 1], 0, pos_base + (np - 1) * ps, delta});
+    out[pg] = KvPage{pages[pg], std::min(ps, n_tok - pg * ps), pos_base + pg * ps, delta};
+  for (int32_t pg = np; pg < padded; ++pg) out[pg] = KvPage{pages[np - 1], 0, pos_base + (np - 1) * ps, delta};
 }
 
 // One past the last page of kv[kv0, kv1) whose first position is <= last_pos
 // (positions are non-decreasing along a list); rounded up to whole 4-page tiles
 // with pad4 (the extra pages are masked by position or are empty).
 int32_t list_end(const std::vector<KvPage>& kv, int32_t kv0, int32_t kv1, int32_t last_pos, bool pad4) {
-  int32_t end = kv0;
-  while (end < kv1 && kv[end].pos0 <= last_pos) ++end;
-  if (pad4) end = std::min(kv1, kv0 + ((end - kv0 + 3) / 4) * 4);
-  return end;
+  const int32_t end = static_cast<int32_t>(
+      std::upper_bound(kv.begin() + kv0, kv.begin() + kv1, last_pos,
+                       [](int32_t pos, const KvPage& k) { return pos < k.pos0; }) - kv.begin());
+  return pad4 ? std::min(kv1, kv0 + ((end - kv0 + 3) / 4) * 4) : end;
 }
 
 // Order of the prefill row tiles.
@@ -531,10 +601,11 @@ void order_prefill(std::vector<WorkTile>& tiles, const std::vector<int32_t>& spa
     short_work += work(tiles[i]);
   }
   // long tiles span by span (spans with more long work first), longest first in a span
-  std::unordered_map<int32_t, int64_t> span_work;
+  std::vector<int64_t> span_work(static_cast<size_t>(*std::max_element(span_of.begin(), span_of.end())) + 1, 0);
   for (size_t i = 0; i < n; ++i)
     if (!is_short[i]) span_work[span_of[i]] += work(tiles[i]);
   std::vector<size_t> long_list;
+  long_list.reserve(n);
   for (size_t i = 0; i < n; ++i)
     if (!is_short[i]) long_list.push_back(i);
   std::stable_sort(long_list.begin(), long_list.end(), [&](size_t a, size_t b) {
@@ -690,6 +761,28 @@ void PoolIndex::build_work(Plan* p, const Tiling& t) {
   }
   // ---- prefill: new pages and row tiles of every span that computes pages
   std::vector<int32_t> tile_span;  // per prefill tile: the span it belongs to
+  {
+    // room for every list (each padded by at most 3 pages per span)
+    size_t kv_n = 0, new_n = 0, tile_n = 0;
+    for (const auto& ids : p->query_spans) {
+      const size_t pre = p->spans[ids[0]].pages.size() + 3;
+      size_t all = 0;
+      for (size_t c = 0; c < ids.size(); ++c) {
+        const SpanPlan& s = p->spans[ids[c]];
+        all += s.pages.size() + 3;
+        if (c + 1 == ids.size() || s.n_hit >= static_cast<int32_t>(s.pages.size())) continue;
+        kv_n += s.pages.size() + 3 + (s.kind == 1 ? pre : 0);
+        new_n += s.pages.size() - s.n_hit;
+        tile_n += (static_cast<size_t>(s.n_tok - s.n_hit * ps) + t.bm_prefill - 1) / t.bm_prefill;
+      }
+      kv_n += all;
+    }
+    p->kv.reserve(kv_n);
+    p->k3_prefill.reserve(new_n);
+    p->t_prefill.reserve(tile_n);
+    p->rows_prefill.reserve(tile_n);
+    tile_span.reserve(tile_n);
+  }
   for (size_t qi = 0; qi < p->query_spans.size(); ++qi) {
     const auto& ids = p->query_spans[qi];
     const SpanPlan& prefix = p->spans[ids[0]];
@@ -826,8 +919,7 @@ int PoolIndex::decode(Plan* p, const std::vector<int32_t>& n_new, const std::vec
 void PoolIndex::commit(Plan* p) {
   for (int32_t pid : p->new_pages) {
     PageRec& r = pages_[pid];
-    if (!r.cacheable || index_.count(r.hash)) continue;
-    index_[r.hash] = pid;
+    if (!r.cacheable || !index_.try_emplace(r.hash, pid).second) continue;
     r.published = true;
   }
   for (int32_t pid : p->new_pages) {

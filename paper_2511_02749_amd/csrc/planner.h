@@ -172,6 +172,18 @@ class PoolIndex {
     const int32_t* tok;
     bool cacheable, cross;
   };
+  // Working storage of plan(), kept from call to call so that planning a batch does
+  // not allocate it again: the page specs, and the batch's own pages by hash (open
+  // addressing; a slot is live iff its stamp is the current call's).
+  std::vector<Spec> specs_;
+  std::vector<uint64_t> pend_key_;
+  std::vector<int32_t> pend_val_;
+  std::vector<uint32_t> pend_stamp_;
+  uint32_t pend_gen_ = 0;
+  size_t pend_mask_ = 0;
+  void pending_begin(size_t n);
+  int32_t pending_find(uint64_t h) const;
+  void pending_insert(uint64_t h, int32_t v);  // keeps an existing entry
   bool content_equal(int32_t pid, const Spec& s) const;
   bool spec_equal(const Spec& a, const Spec& b) const;
   int32_t pop_free();
