@@ -382,7 +382,11 @@ int span_parse_serialized(const int32_t* tokens, int64_t n, int32_t block, const
  * its logits (lowest id on ties) as the first generated token.
  * Weights are caller-owned device memory, bf16, row-major, x @ W convention
  * (W is [in][out]); the per-layer tables are host arrays of num_layers pointers.
- * The model copies the tables; the weights must outlive it. */
+ * The model copies the tables; the weights must outlive it.  At creation it also
+ * makes a transposed copy of each layer matrix that its few-row GEMM kernel takes (a
+ * reduction K at least 4 times the output width N, N a multiple of 64, K of 256:
+ * the down projection of usual FFNs), read by forward calls of 129..256 rows, so
+ * weights changed after span_model_create are not seen by those calls. */
 typedef struct span_model span_model;
 
 
@@ -408,7 +412,8 @@ typedef struct {
 } span_model_config;
 
 /* Bind a model to a bf16 device pool of the same layers and heads.  Allocates a
- * GEMM workspace; activation buffers are allocated by the first forward call and
+ * GEMM workspace and the transposed weight copies (waits for the transposition on
+ * the null stream); activation buffers are allocated by the first forward call and
  * grown when a later one needs more.  SPAN_EINVAL on a shape mismatch. */
 int span_model_create(span_pool* pool, const span_model_config* cfg, span_model** out);
 int span_model_destroy(span_model* model);
@@ -487,6 +492,19 @@ int span_probe_mfma_peak(int32_t iters, int32_t reps, void* stream, double* tflo
  * (1 GiB or more) measures HBM.  Stores GB/s (10^9 bytes per second) in *gbs.
  * SPAN_EINVAL also for a buffer that is not 16-byte aligned. */
 int span_probe_read_peak(const void* buf, size_t bytes, int32_t reps, void* stream, double* gbs);
+
+/* The model stack's GEMM on caller buffers: Y[M][N] = X[M][K] W[K][N] (+ Y when
+ * residual != 0), bf16 row-major device memory (16-byte aligned), fp32 accumulation,
+ * through the same dispatch span_model_forward uses for M rows: the GEMV kernels for
+ * M <= 8, the skinny MFMA kernel for 129..256 rows when K >= 4 N, N is a multiple of
+ * 64 and K of 256 (from a transposed copy of W this call makes), hipBLASLt otherwise.  N and K
+ * multiples of 8.  *kernel (if given) receives 1 (GEMV), 2 (skinny) or 0 (hipBLASLt).
+ * With reps > 0 and sec_per_call given, reps more calls into a scratch copy of Y are
+ * timed between two events and the mean seconds per call stored.  Waits for `stream`
+ * before returning.  Allocates its scratch; SPAN_EINVAL on a bad argument, SPAN_EHIP
+ * on a HIP or hipBLASLt error. */
+int span_probe_gemm(const void* x, const void* w, void* y, int64_t M, int64_t N, int64_t K, int32_t residual,
+                    int32_t reps, void* stream, int32_t* kernel, double* sec_per_call);
 
 #ifdef __cplusplus
 }

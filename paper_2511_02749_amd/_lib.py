@@ -31,7 +31,7 @@ EXPORTS = [
     "span_plan_commit", "span_plan_destroy", "span_plan_kernel_times", "span_probe_mfma_peak",
     "span_probe_read_peak", "span_plan_static", "span_model_create", "span_model_destroy", "span_model_forward",
     "span_parse_serialized", "span_bulk_order", "span_plan_moves", "span_plan_decode", "span_decode_attend",
-    "span_model_decode",
+    "span_model_decode", "span_probe_gemm",
 ]
 SPAN_STATIC_SCRATCH_BYTES = 64 << 20
 SPAN_FLAG_TIMING = 1
@@ -160,6 +160,7 @@ def load():
         "span_plan_kernel_times": (I32, [VP, P(KernelTimes)]),
         "span_probe_mfma_peak": (I32, [I32, I32, VP, P(ctypes.c_double)]),
         "span_probe_read_peak": (I32, [VP, ctypes.c_size_t, I32, VP, P(ctypes.c_double)]),
+        "span_probe_gemm": (I32, [VP, VP, VP, I64, I64, I64, I32, I32, VP, P(I32), P(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -209,6 +210,18 @@ def probe_read_peak(buf, reps: int = 5, stream=None) -> float:
     nbytes = buf.numel() * buf.element_size()
     _check(load().span_probe_read_peak(_ptr(buf), nbytes - nbytes % 16, reps, _stream(stream), ctypes.byref(out)))
     return float(out.value)
+
+
+def probe_gemm(x, w, y, residual: bool = False, reps: int = 0, stream=None):
+    """The model stack's GEMM y = x @ w (+ y) on bf16 device tensors (span_probe_gemm).
+    Returns (kernel, seconds per call): kernel 1 GEMV, 2 skinny MFMA, 0 hipBLASLt."""
+    M, K = x.shape
+    K2, N = w.shape
+    assert K2 == K and tuple(y.shape) == (M, N)
+    kern, sec = ctypes.c_int32(), ctypes.c_double()
+    _check(load().span_probe_gemm(_ptr(x), _ptr(w), _ptr(y), M, N, K, 1 if residual else 0, reps, _stream(stream),
+                                  ctypes.byref(kern), ctypes.byref(sec)))
+    return int(kern.value), float(sec.value)
 
 
 def hash_mix(x: int) -> int:

@@ -10,8 +10,10 @@
 //
 // then the final RMSNorm of each query's last cross row, the LM head and the
 // argmax (the first generated token).  GEMMs of at most 8 rows (decode steps) run
-// on GEMV kernels of our own (HBM-bound: each weight read once), the rest on
-// hipBLASLt.  Rows that hit the cache are never
+// on GEMV kernels of our own (HBM-bound: each weight read once), long reductions
+// (the down projection) of 129..256 rows (a cache-hit query's question) on an MFMA
+// kernel of our own that streams a transposed copy of the weights once with K split
+// over the chip, the rest on hipBLASLt.  Rows that hit the cache are never
 // computed: their keys and values are already in the pool's pages, which is the
 // point of the method (section 5.6).
 #include <hip/hip_runtime.h>
@@ -86,8 +88,10 @@ struct Gemm {
   };
   std::map<std::tuple<int64_t, int64_t, int64_t, bool>, Plan> plans;
   // Up to 8 rows (decode steps) go to the GEMV kernels instead, with this fp32
-  // scratch for their partial sums (sized by the caller before the launches).
-  Buf gemv_part;
+  // scratch for their partial sums (sized by the caller before the launches); the
+  // shapes skinny_gemm_fits takes to the skinny MFMA kernel when the weight has a
+  // transposed copy, with sk_part for its K-slice partials.
+  Buf gemv_part, sk_part;
 
   int init() {
     hipblasStatus_t st = hipblasLtCreate(&h);
@@ -112,14 +116,24 @@ struct Gemm {
     }
     plans.clear();
     gemv_part.release();
+    sk_part.release();
     if (pref) hipblasLtMatmulPreferenceDestroy(pref);
     if (desc) hipblasLtMatmulDescDestroy(desc);
     if (h) hipblasLtDestroy(h);
     ws.release();
   }
 
-  int run(const void* x, const void* w, void* y, int64_t M, int64_t N, int64_t K, bool residual, hipStream_t s) {
+  // wt: W^T [N][K], or null when the weight has no transposed copy
+  int run(const void* x, const void* w, const void* wt, void* y, int64_t M, int64_t N, int64_t K, bool residual,
+          hipStream_t s) {
     if (M == 0) return SPAN_OK;
+    if (wt && skinny_gemm_fits(M, N, K) &&
+        skinny_gemm_part_bytes(static_cast<int>(M), static_cast<int>(N), static_cast<int>(K)) <= sk_part.cap) {
+      hipError_t e = launch_skinny_gemm(x, wt, y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+                                        residual, sk_part.as<float>(), sk_part.cap, s);
+      if (e != hipSuccess) return hip_err(e, "skinny GEMM");
+      return SPAN_OK;
+    }
     if (M <= 8 && N % 8 == 0 && gemv_part_bytes(static_cast<int>(M), static_cast<int>(N), static_cast<int>(K)) <=
                                     gemv_part.cap) {
       hipError_t e = launch_gemv(x, w, y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), residual,
@@ -165,6 +179,10 @@ struct span_model {
   int device = 0;
   span_model_config cfg{};
   std::vector<const void*> attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
+  // transposed copies (W^T [N][K]) for the skinny GEMM, all in wt_buf; null where a
+  // matrix's shape does not suit that kernel
+  std::vector<const void*> wt_qkv, wt_o, wt_gate_up, wt_down;
+  Buf wt_buf;
   Gemm gemm;
   // compact activations over the computed rows
   Buf x, n, qkv, oc, gu, act;
@@ -226,6 +244,19 @@ size_t gemv_scratch(const span_model_config& c, int T) {
   return std::max(b, gemv_part_bytes(T, c.hidden, c.ffn));
 }
 
+// Scratch of the skinny GEMM for T rows: the largest of the four GEMMs' K-slice partials.
+size_t skinny_scratch(const span_model_config& c, int64_t T) {
+  const int64_t shapes[4][2] = {{(c.num_q_heads + 2 * c.num_kv_heads) * c.head_dim, c.hidden},
+                                {c.hidden, c.num_q_heads * c.head_dim},
+                                {2 * c.ffn, c.hidden},
+                                {c.hidden, c.ffn}};
+  size_t b = 0;
+  for (const auto& nk : shapes)
+    if (skinny_gemm_fits(T, nk[0], nk[1]))
+      b = std::max(b, skinny_gemm_part_bytes(static_cast<int>(T), static_cast<int>(nk[0]), static_cast<int>(nk[1])));
+  return b;
+}
+
 // Buffers for T compact rows whose attention rows lie in [0, R), then the upload of
 // the row list (compact row i -> attention row), the tokens and the LM-head rows.
 // Buffers grow with the stream drained, so no launch still reads the old ones.
@@ -246,7 +277,8 @@ int prepare(span_model* m, int64_t T, int64_t R, const int32_t* h_rows, const in
       {&m->last, static_cast<size_t>(nh) * 4 + 32}, {&m->nf, static_cast<size_t>(8) * H * bf},
       {&m->part, static_cast<size_t>(lm_head_chunks(H)) * 8 * V * 4}, {&m->logits, static_cast<size_t>(8) * V * 4},
       {&m->tok_out, 8 * 4}, {&m->best, argmax_scratch_bytes(8, V)},
-      {&m->gemm.gemv_part, T <= 8 ? gemv_scratch(c, static_cast<int>(T)) : 0}};
+      {&m->gemm.gemv_part, T <= 8 ? gemv_scratch(c, static_cast<int>(T)) : 0},
+      {&m->gemm.sk_part, skinny_scratch(c, T)}};
   bool grow = false;
   for (const Need& nd : needs) grow |= nd.bytes > nd.b->cap;
   hipError_t e = hipSuccess;
@@ -278,7 +310,7 @@ int run_layers(span_model* m, int64_t T, int n_layers, hipStream_t s, const char
   for (int l = 0; l < n_layers; ++l) {
     e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
     if (e != hipSuccess) return hip_err(e, w + ": attention norm");
-    int rc = m->gemm.run(m->n.p, m->w_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
+    int rc = m->gemm.run(m->n.p, m->w_qkv[l], m->wt_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
     if (rc) return rc;
     e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
     if (e != hipSuccess) return hip_err(e, w + ": q/k/v scatter");
@@ -286,15 +318,15 @@ int run_layers(span_model* m, int64_t T, int n_layers, hipStream_t s, const char
     if (rc) return rc;
     e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
     if (e != hipSuccess) return hip_err(e, w + ": attention output gather");
-    rc = m->gemm.run(m->oc.p, m->w_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
+    rc = m->gemm.run(m->oc.p, m->w_o[l], m->wt_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
     if (rc) return rc;
     e = launch_rmsnorm(m->x.p, nullptr, m->ffn_norm[l], m->n.p, T, H, c.rms_eps, s);
     if (e != hipSuccess) return hip_err(e, w + ": ffn norm");
-    rc = m->gemm.run(m->n.p, m->w_gate_up[l], m->gu.p, T, 2 * static_cast<int64_t>(F), H, false, s);
+    rc = m->gemm.run(m->n.p, m->w_gate_up[l], m->wt_gate_up[l], m->gu.p, T, 2 * static_cast<int64_t>(F), H, false, s);
     if (rc) return rc;
     e = launch_swiglu(m->gu.p, m->act.p, T, F, s);
     if (e != hipSuccess) return hip_err(e, w + ": swiglu");
-    rc = m->gemm.run(m->act.p, m->w_down[l], m->x.p, T, H, F, true, s);
+    rc = m->gemm.run(m->act.p, m->w_down[l], m->wt_down[l], m->x.p, T, H, F, true, s);
     if (rc) return rc;
   }
   return SPAN_OK;
@@ -331,6 +363,38 @@ int lm_head(span_model* m, int nh, float* logits_out, std::vector<int32_t>* toks
   return SPAN_OK;
 }
 
+// W^T copies of every layer matrix whose shape the skinny GEMM takes (at 256 rows; the
+// row range does not change which shapes fit), in one allocation, made once.
+int make_transposed(span_model* m) {
+  const span_model_config& c = m->cfg;
+  const int L = c.num_layers;
+  const int64_t dims[4][2] = {{c.hidden, (c.num_q_heads + 2 * c.num_kv_heads) * c.head_dim},
+                              {c.num_q_heads * c.head_dim, c.hidden},
+                              {c.hidden, 2 * c.ffn},
+                              {c.ffn, c.hidden}};  // K x N of W
+  std::vector<const void*>* src[4] = {&m->w_qkv, &m->w_o, &m->w_gate_up, &m->w_down};
+  std::vector<const void*>* dst[4] = {&m->wt_qkv, &m->wt_o, &m->wt_gate_up, &m->wt_down};
+  size_t total = 0;
+  for (int i = 0; i < 4; ++i)
+    if (skinny_gemm_fits(256, dims[i][1], dims[i][0])) total += static_cast<size_t>(L) * dims[i][0] * dims[i][1] * 2;
+  for (int i = 0; i < 4; ++i) dst[i]->assign(static_cast<size_t>(L), nullptr);
+  if (total == 0) return SPAN_OK;
+  hipError_t e = m->wt_buf.ensure(total);
+  if (e != hipSuccess) return hip_err(e, "span_model_create: transposed weights");
+  char* at = m->wt_buf.as<char>();
+  for (int i = 0; i < 4 && e == hipSuccess; ++i) {
+    if (!skinny_gemm_fits(256, dims[i][1], dims[i][0])) continue;
+    for (int l = 0; l < L && e == hipSuccess; ++l) {
+      e = launch_transpose_bf16((*src[i])[l], at, dims[i][0], dims[i][1], nullptr);
+      (*dst[i])[l] = at;
+      at += static_cast<size_t>(dims[i][0]) * dims[i][1] * 2;
+    }
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) return hip_err(e, "span_model_create: transposing the weights");
+  return SPAN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -363,8 +427,11 @@ int span_model_create(span_pool* pool, const span_model_config* cfg, span_model*
     e = hipEventCreateWithFlags(&m->staged, hipEventDisableTiming);
     if (e != hipSuccess) rc = hip_err(e, "span_model_create: event");
   }
+  if (rc == SPAN_OK) rc = make_transposed(m);
   if (rc) {
     m->gemm.destroy();
+    m->wt_buf.release();
+    if (m->staged) (void)hipEventDestroy(m->staged);
     delete m;
     return rc;
   }
@@ -377,6 +444,7 @@ int span_model_destroy(span_model* m) {
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
   m->gemm.destroy();
+  m->wt_buf.release();
   for (Buf* b : {&m->x, &m->n, &m->qkv, &m->oc, &m->gu, &m->act, &m->q, &m->k, &m->v, &m->o, &m->rows, &m->toks,
                  &m->last, &m->nf, &m->part, &m->logits, &m->tok_out, &m->best})
     b->release();
@@ -513,6 +581,60 @@ int span_model_decode(span_model* m, span_plan_t* plan, const int32_t* tokens, f
   if (next_tokens)
     for (int i = 0; i < nd; ++i) next_tokens[q_of[i]] = toks[i];
   return SPAN_OK;
+}
+
+int span_probe_gemm(const void* x, const void* w, void* y, int64_t M, int64_t N, int64_t K, int32_t residual,
+                    int32_t reps, void* stream, int32_t* kernel, double* sec_per_call) {
+  if (!x || !w || !y || M < 1 || N < 8 || N % 8 != 0 || K < 8 || K % 8 != 0 || reps < 0 || M > (int64_t{1} << 24) ||
+      N > (int64_t{1} << 24) || K > (int64_t{1} << 24))
+    return report(SPAN_EINVAL, "span_probe_gemm: bad argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Gemm g;
+  Buf wt, y2;
+  auto done = [&](int rc) {
+    (void)hipStreamSynchronize(s);
+    g.destroy();
+    wt.release();
+    y2.release();
+    return rc;
+  };
+  int rc = g.init();
+  if (rc) return done(rc);
+  const int Mi = static_cast<int>(M), Ni = static_cast<int>(N), Ki = static_cast<int>(K);
+  const bool skinny = skinny_gemm_fits(M, N, K);
+  hipError_t e = hipSuccess;
+  if (skinny) {
+    e = wt.ensure(static_cast<size_t>(N) * K * 2);
+    if (e == hipSuccess) e = launch_transpose_bf16(w, wt.p, K, N, s);
+    if (e == hipSuccess) e = g.sk_part.ensure(std::max<size_t>(16, skinny_gemm_part_bytes(Mi, Ni, Ki)));
+  } else if (M <= 8) {
+    e = g.gemv_part.ensure(gemv_part_bytes(Mi, Ni, Ki));
+  }
+  if (e != hipSuccess) return done(hip_err(e, "span_probe_gemm: set-up"));
+  rc = g.run(x, w, skinny ? wt.p : nullptr, y, M, N, K, residual != 0, s);
+  if (rc) return done(rc);
+  if (kernel) *kernel = skinny ? 2 : (M <= 8 ? 1 : 0);
+  if (sec_per_call && reps > 0) {
+    e = y2.ensure(static_cast<size_t>(M) * N * 2);
+    if (e == hipSuccess) e = hipMemcpyAsync(y2.p, y, static_cast<size_t>(M) * N * 2, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return done(hip_err(e, "span_probe_gemm: timing buffer"));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    if (e == hipSuccess) e = hipEventRecord(e0, s);
+    for (int i = 0; e == hipSuccess && rc == SPAN_OK && i < reps; ++i)
+      rc = g.run(x, w, skinny ? wt.p : nullptr, y2.p, M, N, K, residual != 0, s);
+    if (e == hipSuccess && rc == SPAN_OK) e = hipEventRecord(e1, s);
+    if (e == hipSuccess && rc == SPAN_OK) e = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (e == hipSuccess && rc == SPAN_OK) e = hipEventElapsedTime(&ms, e0, e1);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (rc) return done(rc);
+    if (e != hipSuccess) return done(hip_err(e, "span_probe_gemm: timing"));
+    *sec_per_call = 1e-3 * ms / reps;
+  }
+  return done(SPAN_OK);
 }
 
 }  // extern "C"

@@ -31,6 +31,19 @@ size_t gemv_part_bytes(int M, int N, int K);
 hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
                        size_t part_bytes, hipStream_t s);
 
+// Y[M][N] = X[M][K] W[K][N] (+ Y when residual) for 129..256 rows and K >= 4 N from
+// the transposed weights wt = W^T [N][K] (bf16 row-major), N a multiple of 64, K a
+// multiple of 256 (skinny_gemm_fits).  Split-K launches need part: fp32 scratch of at least
+// skinny_gemm_part_bytes(M, N, K) bytes (0 when the launch does not split).  The slices
+// are summed in a fixed order.
+bool skinny_gemm_fits(int64_t M, int64_t N, int64_t K);
+int skinny_gemm_slices(int M, int N, int K);
+size_t skinny_gemm_part_bytes(int M, int N, int K);
+hipError_t launch_skinny_gemm(const void* x, const void* wt, void* y, int M, int N, int K, bool residual, float* part,
+                              size_t part_bytes, hipStream_t s);
+// out[c][r] = in[r][c] for an R x C bf16 matrix.
+hipError_t launch_transpose_bf16(const void* in, void* out, int64_t R, int64_t C, hipStream_t s);
+
 // LM head over nq (1, 2, 4 or 8) rows of nf [nq][hidden]: partial logits per chunk
 // of the hidden dimension into part [lm_head_chunks(hidden)][nq][vocab] (fp32).
 // launch_argmax sums the chunks (in chunk order) for the first n_rows rows into
