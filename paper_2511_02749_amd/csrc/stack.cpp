@@ -297,9 +297,11 @@ int prepare(span_model* m, int64_t T, int64_t R, const int32_t* h_rows, const in
 }
 
 // Embeddings of the T compact rows, then n_layers decoder layers; attn(l) runs the
-// span attention of layer l on the q/k/v/o buffers.
+// span attention of layer l on the q/k/v/o buffers.  base >= 0: compact row i is
+// attention row base + i for every i, so the output projection reads the attention
+// output in place instead of through a gather.
 template <class Attn>
-int run_layers(span_model* m, int64_t T, int n_layers, hipStream_t s, const char* who, Attn attn) {
+int run_layers(span_model* m, int64_t T, int n_layers, int64_t base, hipStream_t s, const char* who, Attn attn) {
   const span_model_config& c = m->cfg;
   const int H = c.hidden, hq = c.num_q_heads, hkv = c.num_kv_heads, d = c.head_dim, F = c.ffn;
   const int64_t qkv_w = static_cast<int64_t>(hq + 2 * hkv) * d;
@@ -316,9 +318,14 @@ int run_layers(span_model* m, int64_t T, int n_layers, hipStream_t s, const char
     if (e != hipSuccess) return hip_err(e, w + ": q/k/v scatter");
     rc = attn(l);
     if (rc) return rc;
-    e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
-    if (e != hipSuccess) return hip_err(e, w + ": attention output gather");
-    rc = m->gemm.run(m->oc.p, m->w_o[l], m->wt_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
+    const void* oc = m->oc.p;
+    if (base >= 0) {
+      oc = static_cast<const char*>(m->o.p) + base * hq * d * 2;
+    } else {
+      e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
+      if (e != hipSuccess) return hip_err(e, w + ": attention output gather");
+    }
+    rc = m->gemm.run(oc, m->w_o[l], m->wt_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
     if (rc) return rc;
     e = launch_rmsnorm(m->x.p, nullptr, m->ffn_norm[l], m->n.p, T, H, c.rms_eps, s);
     if (e != hipSuccess) return hip_err(e, w + ": ffn norm");
@@ -506,9 +513,12 @@ int span_model_forward(span_model* m, span_plan_t* plan, const int32_t* row_toke
       q_of.push_back(qi);
     }
   const int nh = static_cast<int>(q_of.size());
+  int64_t base = T > 0 ? h_rows[0] : -1;
+  for (int64_t i = 1; i < T && base >= 0; ++i)
+    if (h_rows[i] != base + i) base = -1;
   rc = prepare(m, T, n_rows, h_rows, h_toks, h_last, nh, s, "span_model_forward");
   if (rc) return rc;
-  rc = run_layers(m, T, n_layers, s, "span_model_forward", [&](int l) {
+  rc = run_layers(m, T, n_layers, base, s, "span_model_forward", [&](int l) {
     int r = span_prefill_fragments(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
     if (!r) r = span_cross_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s);
     return r;
@@ -571,7 +581,7 @@ int span_model_decode(span_model* m, span_plan_t* plan, const int32_t* tokens, f
   }
   rc = prepare(m, nd, nd, h_rows, h_toks, h_last, nd, s, "span_model_decode");
   if (rc) return rc;
-  rc = run_layers(m, nd, c.num_layers, s, "span_model_decode",
+  rc = run_layers(m, nd, c.num_layers, 0, s, "span_model_decode",
                   [&](int l) { return span_decode_attend(plan, l, m->q.p, m->k.p, m->v.p, m->o.p, s); });
   if (rc) return rc;
   if (!next_tokens && !logits_out) return SPAN_OK;
