@@ -124,6 +124,17 @@ struct Gemm {
   }
 
   // wt: W^T [N][K], or null when the weight has no transposed copy
+  // every GEMV of a layer of M rows fits the scratch (decode-sized M)
+  bool gemv_layer(int64_t M, int64_t qkv_w, int64_t H, int64_t F, int64_t attn_w) const {
+    if (M < 1 || M > 8) return false;
+    const int m = static_cast<int>(M);
+    return qkv_w % 8 == 0 && H % 8 == 0 && F % 8 == 0 &&
+           gemv_part_bytes(m, static_cast<int>(qkv_w), static_cast<int>(H)) <= gemv_part.cap &&
+           gemv_part_bytes(m, static_cast<int>(H), static_cast<int>(attn_w)) <= gemv_part.cap &&
+           gemv_part_bytes(m, static_cast<int>(2 * F), static_cast<int>(H)) <= gemv_part.cap &&
+           gemv_part_bytes(m, static_cast<int>(H), static_cast<int>(F)) <= gemv_part.cap;
+  }
+
   int run(const void* x, const void* w, const void* wt, void* y, int64_t M, int64_t N, int64_t K, bool residual,
           hipStream_t s) {
     if (M == 0) return SPAN_OK;
@@ -309,13 +320,29 @@ int run_layers(span_model* m, int64_t T, int n_layers, int64_t base, hipStream_t
   const std::string w(who);
   hipError_t e = launch_copy_rows(m->x.p, c.embed, m->toks.as<int32_t>(), T, H * 2, false, s);
   if (e != hipSuccess) return hip_err(e, w + ": embedding");
-  for (int l = 0; l < n_layers; ++l) {
-    e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
+  // Up to 8 rows: every GEMM is a GEMV whose second pass also does the step after it
+  // (q/k/v split, SwiGLU, the next RMSNorm), bit for bit the separate kernels' result.
+  const bool gv = m->gemm.gemv_layer(T, qkv_w, H, F, static_cast<int64_t>(hq) * d);
+  float* gp = m->gemm.gemv_part.as<float>();
+  const size_t gcap = m->gemm.gemv_part.cap;
+  const int Ti = static_cast<int>(T);
+  if (gv && n_layers > 0) {
+    e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[0], m->n.p, T, H, c.rms_eps, s);
     if (e != hipSuccess) return hip_err(e, w + ": attention norm");
-    int rc = m->gemm.run(m->n.p, m->w_qkv[l], m->wt_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
-    if (rc) return rc;
-    e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
-    if (e != hipSuccess) return hip_err(e, w + ": q/k/v scatter");
+  }
+  for (int l = 0; l < n_layers; ++l) {
+    int rc;
+    if (gv) {
+      e = launch_gemv_qkv(m->n.p, m->w_qkv[l], Ti, H, rows, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, gp, gcap, s);
+      if (e != hipSuccess) return hip_err(e, w + ": q/k/v GEMV");
+    } else {
+      e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
+      if (e != hipSuccess) return hip_err(e, w + ": attention norm");
+      rc = m->gemm.run(m->n.p, m->w_qkv[l], m->wt_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
+      if (rc) return rc;
+      e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
+      if (e != hipSuccess) return hip_err(e, w + ": q/k/v scatter");
+    }
     rc = attn(l);
     if (rc) return rc;
     const void* oc = m->oc.p;
@@ -324,6 +351,22 @@ int run_layers(span_model* m, int64_t T, int n_layers, int64_t base, hipStream_t
     } else {
       e = launch_copy_rows(m->oc.p, m->o.p, rows, T, hq * d * 2, false, s);
       if (e != hipSuccess) return hip_err(e, w + ": attention output gather");
+    }
+    if (gv) {
+      e = launch_gemv_residual_norm(oc, m->w_o[l], m->x.p, Ti, H, hq * d, m->ffn_norm[l], m->n.p, c.rms_eps, gp, gcap,
+                                    s);
+      if (e != hipSuccess) return hip_err(e, w + ": output GEMV");
+      e = launch_gemv_swiglu(m->n.p, m->w_gate_up[l], m->act.p, Ti, F, H, gp, gcap, s);
+      if (e != hipSuccess) return hip_err(e, w + ": gate/up GEMV");
+      if (l + 1 < n_layers) {
+        e = launch_gemv_residual_norm(m->act.p, m->w_down[l], m->x.p, Ti, H, F, m->attn_norm[l + 1], m->n.p,
+                                      c.rms_eps, gp, gcap, s);
+        if (e != hipSuccess) return hip_err(e, w + ": down GEMV");
+      } else {
+        rc = m->gemm.run(m->act.p, m->w_down[l], m->wt_down[l], m->x.p, T, H, F, true, s);
+        if (rc) return rc;
+      }
+      continue;
     }
     rc = m->gemm.run(oc, m->w_o[l], m->wt_o[l], m->x.p, T, H, static_cast<int64_t>(hq) * d, true, s);
     if (rc) return rc;

@@ -30,6 +30,17 @@ hipError_t launch_swiglu(const void* gu, void* act, int64_t n, int ffn, hipStrea
 size_t gemv_part_bytes(int M, int N, int K);
 hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
                        size_t part_bytes, hipStream_t s);
+// The same GEMV with the layer's next step fused into its second pass, bit for bit
+// what the separate kernels give: q|k|v rows (N = q_elems + 2 kv_elems) written
+// straight to caller rows rows[m] of q, k, v (launch_scatter_qkv); gate|up (N = 2 ffn)
+// into act = silu(gate) * up (launch_swiglu); a projection added to the residual
+// stream y (N = hidden <= 8192) followed by nout = RMSNorm(y) * gain (launch_rmsnorm).
+hipError_t launch_gemv_qkv(const void* x, const void* w, int M, int K, const int32_t* rows, int q_elems,
+                           int kv_elems, void* q, void* k, void* v, float* part, size_t part_bytes, hipStream_t s);
+hipError_t launch_gemv_swiglu(const void* x, const void* w, void* act, int M, int ffn, int K, float* part,
+                              size_t part_bytes, hipStream_t s);
+hipError_t launch_gemv_residual_norm(const void* x, const void* w, void* y, int M, int N, int K, const void* gain,
+                                     void* nout, float eps, float* part, size_t part_bytes, hipStream_t s);
 
 // Y[M][N] = X[M][K] W[K][N] (+ Y when residual) for 129..256 rows and K >= 4 N from
 // the transposed weights wt = W^T [N][K] (bf16 row-major), N a multiple of 64, K a

@@ -356,6 +356,114 @@ __global__ __launch_bounds__(256) void gemv_reduce_kernel(const float* __restric
   y[i] = to_bf(sum);
 }
 
+// Fused second passes for the decode-sized GEMVs.  Each forms every sum exactly as
+// gemv_reduce_kernel does (slices in order, one rounding to bf16) and then does the
+// next small step of the layer on it, so that the results are the bits the separate
+// kernels give:
+// - q|k|v: the rounded values go straight to caller row rows[m] of q, k or v;
+__global__ __launch_bounds__(256) void gemv_reduce_qkv_kernel(const float* __restrict__ part, int chunks, int M,
+                                                              int N, const int32_t* __restrict__ rows, int nq,
+                                                              int nkv, u16* __restrict__ q, u16* __restrict__ k,
+                                                              u16* __restrict__ v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t MN = static_cast<int64_t>(M) * N;
+  if (i >= MN) return;
+  float sum = 0.f;
+#pragma unroll 4
+  for (int c = 0; c < chunks; ++c) sum += part[static_cast<int64_t>(c) * MN + i];
+  const u16 b = to_bf(sum);
+  const int m = static_cast<int>(i / N), n = static_cast<int>(i - static_cast<int64_t>(m) * N);
+  const int64_t r = rows[m];
+  if (n < nq) {
+    q[r * nq + n] = b;
+  } else if (n < nq + nkv) {
+    k[r * nkv + (n - nq)] = b;
+  } else {
+    v[r * nkv + (n - nq - nkv)] = b;
+  }
+}
+
+// - gate|up: act[m][f] = silu(gate) * up of the two rounded sums, as swiglu_kernel;
+__global__ __launch_bounds__(256) void gemv_reduce_swiglu_kernel(const float* __restrict__ part, int chunks, int M,
+                                                                 int F, u16* __restrict__ act) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;  // m * F + f
+  if (i >= static_cast<int64_t>(M) * F) return;
+  const int64_t N = 2 * static_cast<int64_t>(F), MN = static_cast<int64_t>(M) * N;
+  const int64_t m = i / F, f = i - m * F;
+  float sg = 0.f, su = 0.f;
+#pragma unroll 4
+  for (int c = 0; c < chunks; ++c) {
+    sg += part[static_cast<int64_t>(c) * MN + m * N + f];
+    su += part[static_cast<int64_t>(c) * MN + m * N + F + f];
+  }
+  const float g = bf(to_bf(sg)), u = bf(to_bf(su));
+  act[i] = to_bf(g / (1.0f + expf(-g)) * u);
+}
+
+// - a projection into the residual stream: y += the rounded sums (one rounding of the
+//   sum with the residual, as gemv_reduce_kernel), then the RMSNorm of the new row
+//   with `gain`, formed exactly as rmsnorm_kernel forms it; one work-group per row.
+__global__ __launch_bounds__(kNormThreads) void gemv_reduce_norm_kernel(const float* __restrict__ part, int chunks,
+                                                                        int M, int N, u16* __restrict__ y,
+                                                                        const uint4* __restrict__ gain,
+                                                                        uint4* __restrict__ nout, float eps) {
+  __shared__ float red[kNormThreads / 64];
+  const int64_t row = blockIdx.x;
+  const int64_t MN = static_cast<int64_t>(M) * N;
+  const int vec16 = N / 8;
+  float f[kNormVec][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int c = threadIdx.x + j * kNormThreads;
+    if (c < vec16) {
+      const int64_t i0 = row * N + 8 * c;
+      float sum[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) sum[t] = 0.f;
+#pragma unroll 4
+      for (int cc = 0; cc < chunks; ++cc) {
+        const float4* pp = reinterpret_cast<const float4*>(part + static_cast<int64_t>(cc) * MN + i0);
+        const float4 a = pp[0], b = pp[1];
+        sum[0] += a.x;
+        sum[1] += a.y;
+        sum[2] += a.z;
+        sum[3] += a.w;
+        sum[4] += b.x;
+        sum[5] += b.y;
+        sum[6] += b.z;
+        sum[7] += b.w;
+      }
+      float res[8];
+      unpack8(reinterpret_cast<const uint4*>(y)[row * vec16 + c], res);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) f[j][t] = bf(to_bf(sum[t] + res[t]));
+      reinterpret_cast<uint4*>(y)[row * vec16 + c] = pack8(f[j]);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) ss = fmaf(f[j][t], f[j][t], ss);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormThreads / 64; ++w) tot += red[w];
+  const float scale = 1.0f / sqrtf(tot / static_cast<float>(vec16 * 8) + eps);
+#pragma unroll
+  for (int j = 0; j < kNormVec; ++j) {
+    const int c = threadIdx.x + j * kNormThreads;
+    if (c < vec16) {
+      float g[8], o[8];
+      unpack8(gain[c], g);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t] = f[j][t] * scale * g[t];
+      nout[row * vec16 + c] = pack8(o);
+    }
+  }
+}
+
 int grid_for(int64_t items, int threads) {
   int64_t g = (items + threads - 1) / threads;
   if (g > 65536) g = 65536;
@@ -422,9 +530,9 @@ size_t gemv_part_bytes(int M, int N, int K) {
   return static_cast<size_t>(kGemvChunks) * M * N * sizeof(float);
 }
 
-hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
-                       size_t part_bytes, hipStream_t s) {
-  if (M < 1 || M > 8 || N % 8 != 0 || K < 1 || gemv_part_bytes(M, N, K) > part_bytes) return hipErrorInvalidValue;
+namespace {
+// Pass 1 of the GEMV; returns the number of K slices (0 on a launch error).
+int gemv_pass1(const void* x, const void* w, int M, int N, int K, float* part, hipStream_t s) {
   const int chunks = std::min(kGemvChunks, (K + 31) / 32);
   const int rows = (K + chunks - 1) / chunks;
   const dim3 grid((N + kGemvCols - 1) / kGemvCols, chunks);
@@ -434,11 +542,55 @@ hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int 
   else if (M == 2) gemv_partial_kernel<2><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
   else if (M <= 4) gemv_partial_kernel<4><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
   else gemv_partial_kernel<8><<<grid, 256, 0, s>>>(xx, ww, part, M, N, K, rows);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError() == hipSuccess ? chunks : 0;
+}
+
+bool gemv_args_ok(int M, int N, int K, size_t part_bytes) {
+  return M >= 1 && M <= 8 && N % 8 == 0 && K >= 1 && gemv_part_bytes(M, N, K) <= part_bytes;
+}
+}  // namespace
+
+hipError_t launch_gemv(const void* x, const void* w, void* y, int M, int N, int K, bool residual, float* part,
+                       size_t part_bytes, hipStream_t s) {
+  if (!gemv_args_ok(M, N, K, part_bytes)) return hipErrorInvalidValue;
+  const int chunks = gemv_pass1(x, w, M, N, K, part, s);
+  if (!chunks) return hipGetLastError();
   const int64_t items = static_cast<int64_t>(M) * N;
   gemv_reduce_kernel<<<static_cast<int>((items + 255) / 256), 256, 0, s>>>(part, chunks, M, N, static_cast<u16*>(y),
                                                                            residual);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_qkv(const void* x, const void* w, int M, int K, const int32_t* rows, int q_elems,
+                           int kv_elems, void* q, void* k, void* v, float* part, size_t part_bytes, hipStream_t s) {
+  const int N = q_elems + 2 * kv_elems;
+  if (!gemv_args_ok(M, N, K, part_bytes)) return hipErrorInvalidValue;
+  const int chunks = gemv_pass1(x, w, M, N, K, part, s);
+  if (!chunks) return hipGetLastError();
+  const int64_t items = static_cast<int64_t>(M) * N;
+  gemv_reduce_qkv_kernel<<<static_cast<int>((items + 255) / 256), 256, 0, s>>>(
+      part, chunks, M, N, rows, q_elems, kv_elems, static_cast<u16*>(q), static_cast<u16*>(k), static_cast<u16*>(v));
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_swiglu(const void* x, const void* w, void* act, int M, int ffn, int K, float* part,
+                              size_t part_bytes, hipStream_t s) {
+  if (!gemv_args_ok(M, 2 * ffn, K, part_bytes)) return hipErrorInvalidValue;
+  const int chunks = gemv_pass1(x, w, M, 2 * ffn, K, part, s);
+  if (!chunks) return hipGetLastError();
+  const int64_t items = static_cast<int64_t>(M) * ffn;
+  gemv_reduce_swiglu_kernel<<<static_cast<int>((items + 255) / 256), 256, 0, s>>>(part, chunks, M, ffn,
+                                                                                  static_cast<u16*>(act));
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_residual_norm(const void* x, const void* w, void* y, int M, int N, int K, const void* gain,
+                                     void* nout, float eps, float* part, size_t part_bytes, hipStream_t s) {
+  if (!gemv_args_ok(M, N, K, part_bytes) || N > kNormThreads * kNormVec * 8) return hipErrorInvalidValue;
+  const int chunks = gemv_pass1(x, w, M, N, K, part, s);
+  if (!chunks) return hipGetLastError();
+  gemv_reduce_norm_kernel<<<static_cast<unsigned>(M), kNormThreads, 0, s>>>(
+      part, chunks, M, N, static_cast<u16*>(y), static_cast<const uint4*>(gain), static_cast<uint4*>(nout), eps);
   return hipGetLastError();
 }
 
