@@ -32,6 +32,23 @@ __device__ __forceinline__ void store16(T* p, const Chunk16<T>& c) {
 
 constexpr int kPageWriteLds = 32768;
 
+// Eight LDS rows of four bf16 each (the slots of eight consecutive positions, dims
+// d .. d + 3) regrouped into four 16-byte chunks, chunk j holding dim d + j of the
+// eight positions in order.
+__device__ __forceinline__ void regroup_8x4(const uint2 (&in)[8], uint4 (&out)[4]) {
+  uint32_t w[4][4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint2 a = in[2 * k], b = in[2 * k + 1];
+    w[0][k] = (a.x & 0xffffu) | (b.x << 16);
+    w[1][k] = (a.x >> 16) | (b.x & 0xffff0000u);
+    w[2][k] = (a.y & 0xffffu) | (b.y << 16);
+    w[3][k] = (a.y >> 16) | (b.y & 0xffff0000u);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) out[j] = uint4{w[j][0], w[j][1], w[j][2], w[j][3]};
+}
+
 template <typename T, int D>
 __device__ __forceinline__ void write_page_heads(const NewPage& pg, int hb, int he, const T* __restrict__ k,
                                                  const T* __restrict__ v, T* __restrict__ pool, int64_t layer_off,
@@ -95,15 +112,33 @@ __device__ __forceinline__ void write_page_heads(const NewPage& pg, int hb, int 
     }
     __syncthreads();
     // row (head, d) holds 16 positions; position p carries slot v_pos(p) (an involution)
-    for (int e = tid; e < hn * D * (kPage / E); e += nth) {
-      const int pc = e % (kPage / E);
-      const int hd = e / (kPage / E);
-      const int d = hd % D;
-      const int hh = hd / D;
-      Chunk16<T> out;
+    if constexpr (sizeof(T) == 2) {
+      // item (head, four dims, half of the positions): eight 8-byte reads, four chunks out
+      for (int e = tid; e < hn * (D / 4) * 2; e += nth) {
+        const int pc = e & 1;
+        const int d4 = (e >> 1) % (D / 4);
+        const int hh = (e >> 1) / (D / 4);
+        uint2 in[8];
 #pragma unroll
-      for (int u = 0; u < E; ++u) out.x[u] = tile[(v_pos(pc * E + u) * HG + hh) * D + d];
-      store16(vp + (static_cast<int64_t>(h0 + hh) * D + d) * kPage + pc * E, out);
+        for (int u = 0; u < 8; ++u)
+          in[u] = *reinterpret_cast<const uint2*>(tile + (v_pos(8 * pc + u) * HG + hh) * D + 4 * d4);
+        uint4 out[4];
+        regroup_8x4(in, out);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<uint4*>(vp + (static_cast<int64_t>(h0 + hh) * D + 4 * d4 + j) * kPage + 8 * pc) = out[j];
+      }
+    } else {
+      for (int e = tid; e < hn * D * (kPage / E); e += nth) {
+        const int pc = e % (kPage / E);
+        const int hd = e / (kPage / E);
+        const int d = hd % D;
+        const int hh = hd / D;
+        Chunk16<T> out;
+#pragma unroll
+        for (int u = 0; u < E; ++u) out.x[u] = tile[(v_pos(pc * E + u) * HG + hh) * D + d];
+        store16(vp + (static_cast<int64_t>(h0 + hh) * D + d) * kPage + pc * E, out);
+      }
     }
     __syncthreads();
   }
@@ -174,15 +209,32 @@ __device__ __forceinline__ void write_pages_one_head(const NewPage* __restrict__
       store16(tile + ps * D + qd * E, val);
     }
     __syncthreads();
-    for (int e = tid; e < pn * D * (kPage / E); e += nth) {
-      const int pc = e % (kPage / E);
-      const int pd = e / (kPage / E);
-      const int d = pd % D;
-      const int pi = pd / D;
-      Chunk16<T> out;
+    if constexpr (sizeof(T) == 2) {
+      for (int e = tid; e < pn * (D / 4) * 2; e += nth) {
+        const int pc = e & 1;
+        const int d4 = (e >> 1) % (D / 4);
+        const int pi = (e >> 1) / (D / 4);
+        uint2 in[8];
 #pragma unroll
-      for (int u = 0; u < E; ++u) out.x[u] = tile[(pi * kPage + v_pos(pc * E + u)) * D + d];
-      store16(kbase(pages[p0 + pi]) + static_cast<int64_t>(hkv) * kPage * D + d * kPage + pc * E, out);
+        for (int u = 0; u < 8; ++u)
+          in[u] = *reinterpret_cast<const uint2*>(tile + (pi * kPage + v_pos(8 * pc + u)) * D + 4 * d4);
+        uint4 out[4];
+        regroup_8x4(in, out);
+        T* vrow = kbase(pages[p0 + pi]) + static_cast<int64_t>(hkv) * kPage * D;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(vrow + (4 * d4 + j) * kPage + 8 * pc) = out[j];
+      }
+    } else {
+      for (int e = tid; e < pn * D * (kPage / E); e += nth) {
+        const int pc = e % (kPage / E);
+        const int pd = e / (kPage / E);
+        const int d = pd % D;
+        const int pi = pd / D;
+        Chunk16<T> out;
+#pragma unroll
+        for (int u = 0; u < E; ++u) out.x[u] = tile[(pi * kPage + v_pos(pc * E + u)) * D + d];
+        store16(kbase(pages[p0 + pi]) + static_cast<int64_t>(hkv) * kPage * D + d * kPage + pc * E, out);
+      }
     }
     __syncthreads();
   }
