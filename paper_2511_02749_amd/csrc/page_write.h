@@ -61,36 +61,46 @@ __device__ __forceinline__ void write_page_heads(const NewPage& pg, int hb, int 
   T* kp = pool + layer_off + static_cast<int64_t>(pg.page_id) * page_elems;
   T* vp = kp + static_cast<int64_t>(hkv) * kPage * D;
 
-  // K: item (head, slot, chunk of E rotary pairs (i, i + H))
-  for (int e = tid; e < (he - hb) * kPage * (H / E); e += nth) {
+  // K: item (slot, chunk of E rotary pairs (i, i + H), group of up to KH heads): the
+  // pairs' (cos, sin) are read once for the item's heads
+  constexpr int KH = 4;
+  const int hgroups = (he - hb + KH - 1) / KH;
+  for (int e = tid; e < hgroups * kPage * (H / E); e += nth) {
     const int q = e % (H / E);
-    const int hs = e / (H / E);
-    const int s = hs % kPage;
-    const int h = hb + hs / kPage;
-    Chunk16<T> y0, y1;
+    const int s = (e / (H / E)) % kPage;
+    const int h0 = hb + KH * (e / (H / E * kPage));
+    const int h1 = min(he, h0 + KH);
+    float cs[E], sn[E];
     if (s < pg.n_valid) {
-      const T* src = k + (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + q * E;
-      const Chunk16<T> x0 = load16(src), x1 = load16(src + H);
       const float4* cs4 = reinterpret_cast<const float4*>(rope + static_cast<int64_t>(pg.pos0 + s) * H + q * E);
 #pragma unroll
       for (int u2 = 0; u2 < E / 2; ++u2) {
         const float4 w = cs4[u2];  // (cos, sin) of pairs q*E + 2u2 and + 1
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          const int u = 2 * u2 + b;
-          const float cs = b ? w.z : w.x, sn = b ? w.w : w.y;
-          const float a0 = to_f32(x0.x[u]), a1 = to_f32(x1.x[u]);
-          y0.x[u] = from_f32<T>(a0 * cs - a1 * sn);
-          y1.x[u] = from_f32<T>(a1 * cs + a0 * sn);
-        }
+        cs[2 * u2] = w.x;
+        sn[2 * u2] = w.y;
+        cs[2 * u2 + 1] = w.z;
+        sn[2 * u2 + 1] = w.w;
       }
-    } else {
-#pragma unroll
-      for (int u = 0; u < E; ++u) y0.x[u] = y1.x[u] = from_f32<T>(0.f);
     }
-    T* dst = kp + (static_cast<int64_t>(h) * kPage + s) * D + q * E;
-    store16(dst, y0);
-    store16(dst + H, y1);
+    for (int h = h0; h < h1; ++h) {
+      Chunk16<T> y0, y1;
+      if (s < pg.n_valid) {
+        const T* src = k + (static_cast<int64_t>(pg.src_row + s) * hkv + h) * D + q * E;
+        const Chunk16<T> x0 = load16(src), x1 = load16(src + H);
+#pragma unroll
+        for (int u = 0; u < E; ++u) {
+          const float a0 = to_f32(x0.x[u]), a1 = to_f32(x1.x[u]);
+          y0.x[u] = from_f32<T>(a0 * cs[u] - a1 * sn[u]);
+          y1.x[u] = from_f32<T>(a1 * cs[u] + a0 * sn[u]);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < E; ++u) y0.x[u] = y1.x[u] = from_f32<T>(0.f);
+      }
+      T* dst = kp + (static_cast<int64_t>(h) * kPage + s) * D + q * E;
+      store16(dst, y0);
+      store16(dst + H, y1);
+    }
   }
 
   // V: rows [slot][d] of a group of heads into LDS, then transposed rows out
