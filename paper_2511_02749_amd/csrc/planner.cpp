@@ -105,7 +105,38 @@ PoolIndex::PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode)
   reset();
 }
 
+size_t PoolIndex::ChainKeyHash::operator()(const ChainKey& k) const {
+  return static_cast<size_t>(mix64(reinterpret_cast<uintptr_t>(k.tok) ^ mix64(k.seed ^ static_cast<uint32_t>(k.n))));
+}
+
+const std::vector<uint64_t>* PoolIndex::cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const {
+  auto it = chain_cache_.find(ChainKey{tok, n, seed});
+  if (it == chain_cache_.end() || (n > 0 && std::memcmp(it->second.tok.data(), tok, sizeof(int32_t) * n) != 0))
+    return nullptr;
+  return &it->second.chain;
+}
+
+void PoolIndex::remember_chain(const int32_t* tok, int32_t n, uint64_t seed, const std::vector<uint64_t>& chain) {
+  const ChainKey key{tok, n, seed};
+  auto it = chain_cache_.find(key);
+  if (it != chain_cache_.end()) {
+    chain_cache_tokens_ -= it->second.tok.size();
+    chain_cache_.erase(it);
+  }
+  if (chain_cache_tokens_ + static_cast<size_t>(n) > kChainCacheTokens) {
+    chain_cache_.clear();
+    chain_cache_tokens_ = 0;
+    if (static_cast<size_t>(n) > kChainCacheTokens) return;
+  }
+  ChainEntry& e = chain_cache_[key];
+  e.tok.assign(tok, tok + n);
+  e.chain = chain;
+  chain_cache_tokens_ += static_cast<size_t>(n);
+}
+
 void PoolIndex::reset() {
+  chain_cache_.clear();
+  chain_cache_tokens_ = 0;
   // Records of ids >= watermark_ are rewritten when they are allocated again.
   for (int64_t i = 0; i < watermark_; ++i) pages_[i] = PageRec{};
   index_.clear();
@@ -289,6 +320,8 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   auto chain_of = [&](uint64_t seed, const SpanIn& in) -> const std::vector<uint64_t>& {
     auto it = memo.find(MemoKey{in.tok, in.n, seed});
     if (it != memo.end()) return it->second;
+    if (const std::vector<uint64_t>* c = cached_chain(in.tok, in.n, seed))
+      return memo.emplace(MemoKey{in.tok, in.n, seed}, *c).first->second;
     std::vector<uint64_t> hs;
     uint64_t h = seed;
     for (int32_t p = 0; p * ps < in.n; ++p) {
@@ -296,6 +329,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
       h = page_hash(h, in.tok + p * ps, n, p);
       hs.push_back(h);
     }
+    remember_chain(in.tok, in.n, seed, hs);
     return memo.emplace(MemoKey{in.tok, in.n, seed}, std::move(hs)).first->second;
   };
 
@@ -315,7 +349,11 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
       frag_seed[qi] = fs;
       for (const SpanIn& f : qs[qi].frags) {
         auto ins = memo.try_emplace(MemoKey{f.tok, f.n, fs});
-        if (ins.second) todo.push_back({&f, fs, &ins.first->second});  // node values stay put
+        if (!ins.second) continue;
+        if (const std::vector<uint64_t>* c = cached_chain(f.tok, f.n, fs))
+          ins.first->second = *c;
+        else
+          todo.push_back({&f, fs, &ins.first->second});  // node values stay put
       }
     }
     for (size_t i = 0; i < todo.size(); i += kLanes) {
@@ -329,6 +367,7 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
         out[c] = todo[i + c].out;
       }
       chains(seeds, in, k, ps, out);
+      for (int c = 0; c < k; ++c) remember_chain(in[c]->tok, in[c]->n, seeds[c], *out[c]);
     }
   }
   for (size_t qi = 0; qi < qs.size(); ++qi) {

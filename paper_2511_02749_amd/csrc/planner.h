@@ -184,6 +184,29 @@ class PoolIndex {
   void pending_begin(size_t n);
   int32_t pending_find(uint64_t h) const;
   void pending_insert(uint64_t h, int32_t v);  // keeps an existing entry
+  // Page-hash chains of spans planned before, by (tokens address, length, seed), each
+  // with a copy of its tokens: a span given again (same address, same tokens, checked
+  // in full) takes its chain from here instead of hashing its tokens again.  Part of
+  // the pool's state: cleared by reset(), and whenever it would hold more than
+  // kChainCacheTokens tokens.
+  struct ChainKey {
+    const int32_t* tok;
+    int32_t n;
+    uint64_t seed;
+    bool operator==(const ChainKey& o) const { return tok == o.tok && n == o.n && seed == o.seed; }
+  };
+  struct ChainKeyHash {
+    size_t operator()(const ChainKey& k) const;
+  };
+  struct ChainEntry {
+    std::vector<int32_t> tok;
+    std::vector<uint64_t> chain;
+  };
+  static constexpr size_t kChainCacheTokens = size_t{1} << 22;
+  std::unordered_map<ChainKey, ChainEntry, ChainKeyHash> chain_cache_;
+  size_t chain_cache_tokens_ = 0;
+  const std::vector<uint64_t>* cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const;
+  void remember_chain(const int32_t* tok, int32_t n, uint64_t seed, const std::vector<uint64_t>& chain);
   bool content_equal(int32_t pid, const Spec& s) const;
   bool spec_equal(const Spec& a, const Spec& b) const;
   int32_t pop_free();
