@@ -105,38 +105,66 @@ PoolIndex::PoolIndex(int64_t num_pages, int32_t page_size, int32_t hash_mode)
   reset();
 }
 
-size_t PoolIndex::ChainKeyHash::operator()(const ChainKey& k) const {
-  return static_cast<size_t>(mix64(reinterpret_cast<uintptr_t>(k.tok) ^ mix64(k.seed ^ static_cast<uint32_t>(k.n))));
+void PoolIndex::clear_chain_cache() {
+  chain_tok_.clear();
+  chain_hash_.clear();
+  chain_live_ = 0;
+  if (++chain_stamp_ == 0) {  // stamps wrapped: clear them all
+    for (ChainSlot& c : chain_slots_) c.stamp = 0;
+    chain_stamp_ = 1;
+  }
 }
 
-const std::vector<uint64_t>* PoolIndex::cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const {
-  auto it = chain_cache_.find(ChainKey{tok, n, seed});
-  if (it == chain_cache_.end() || (n > 0 && std::memcmp(it->second.tok.data(), tok, sizeof(int32_t) * n) != 0))
+size_t PoolIndex::chain_slot(const int32_t* tok, int32_t n, uint64_t seed) const {
+  const size_t mask = chain_slots_.size() - 1;
+  size_t i = static_cast<size_t>(mix64(reinterpret_cast<uintptr_t>(tok) ^ mix64(seed ^ static_cast<uint32_t>(n)))) & mask;
+  for (;; i = (i + 1) & mask) {
+    const ChainSlot& c = chain_slots_[i];
+    if (c.stamp != chain_stamp_ || (c.tok == tok && c.n == n && c.seed == seed)) return i;
+  }
+}
+
+const uint64_t* PoolIndex::cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const {
+  if (chain_live_ == 0) return nullptr;
+  const ChainSlot& c = chain_slots_[chain_slot(tok, n, seed)];
+  if (c.stamp != chain_stamp_ ||
+      (n > 0 && std::memcmp(chain_tok_.data() + c.tok_off, tok, sizeof(int32_t) * static_cast<size_t>(n)) != 0))
     return nullptr;
-  return &it->second.chain;
+  return chain_hash_.data() + c.chain_off;
 }
 
 void PoolIndex::remember_chain(const int32_t* tok, int32_t n, uint64_t seed, const std::vector<uint64_t>& chain) {
-  const ChainKey key{tok, n, seed};
-  auto it = chain_cache_.find(key);
-  if (it != chain_cache_.end()) {
-    chain_cache_tokens_ -= it->second.tok.size();
-    chain_cache_.erase(it);
+  if (static_cast<size_t>(n) > kChainCacheTokens) return;
+  if (chain_tok_.size() + static_cast<size_t>(n) > kChainCacheTokens) clear_chain_cache();
+  if (2 * (chain_live_ + 1) > chain_slots_.size()) {  // keep the table at most half full
+    std::vector<ChainSlot> old;
+    old.swap(chain_slots_);
+    chain_slots_.assign(std::max<size_t>(64, 2 * old.size()), ChainSlot{});
+    const uint32_t st = chain_stamp_;
+    chain_stamp_ = 1;
+    for (ChainSlot& c : chain_slots_) c.stamp = 0;
+    for (const ChainSlot& c : old)
+      if (c.stamp == st) {
+        ChainSlot d = c;
+        d.stamp = chain_stamp_;
+        chain_slots_[chain_slot(c.tok, c.n, c.seed)] = d;
+      }
   }
-  if (chain_cache_tokens_ + static_cast<size_t>(n) > kChainCacheTokens) {
-    chain_cache_.clear();
-    chain_cache_tokens_ = 0;
-    if (static_cast<size_t>(n) > kChainCacheTokens) return;
-  }
-  ChainEntry& e = chain_cache_[key];
-  e.tok.assign(tok, tok + n);
-  e.chain = chain;
-  chain_cache_tokens_ += static_cast<size_t>(n);
+  ChainSlot& c = chain_slots_[chain_slot(tok, n, seed)];
+  if (c.stamp != chain_stamp_) ++chain_live_;
+  c.tok = tok;
+  c.n = n;
+  c.seed = seed;
+  c.stamp = chain_stamp_;
+  c.tok_off = chain_tok_.size();
+  c.chain_off = chain_hash_.size();
+  c.chain_n = chain.size();
+  chain_tok_.insert(chain_tok_.end(), tok, tok + n);
+  chain_hash_.insert(chain_hash_.end(), chain.begin(), chain.end());
 }
 
 void PoolIndex::reset() {
-  chain_cache_.clear();
-  chain_cache_tokens_ = 0;
+  clear_chain_cache();
   // Records of ids >= watermark_ are rewritten when they are allocated again.
   for (int64_t i = 0; i < watermark_; ++i) pages_[i] = PageRec{};
   index_.clear();
@@ -320,8 +348,9 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
   auto chain_of = [&](uint64_t seed, const SpanIn& in) -> const std::vector<uint64_t>& {
     auto it = memo.find(MemoKey{in.tok, in.n, seed});
     if (it != memo.end()) return it->second;
-    if (const std::vector<uint64_t>* c = cached_chain(in.tok, in.n, seed))
-      return memo.emplace(MemoKey{in.tok, in.n, seed}, *c).first->second;
+    if (const uint64_t* c = cached_chain(in.tok, in.n, seed))
+      return memo.emplace(MemoKey{in.tok, in.n, seed}, std::vector<uint64_t>(c, c + (in.n + ps - 1) / ps))
+          .first->second;
     std::vector<uint64_t> hs;
     uint64_t h = seed;
     for (int32_t p = 0; p * ps < in.n; ++p) {
@@ -350,8 +379,8 @@ int PoolIndex::plan(const std::vector<QueryIn>& qs, bool build, const Tiling& ti
       for (const SpanIn& f : qs[qi].frags) {
         auto ins = memo.try_emplace(MemoKey{f.tok, f.n, fs});
         if (!ins.second) continue;
-        if (const std::vector<uint64_t>* c = cached_chain(f.tok, f.n, fs))
-          ins.first->second = *c;
+        if (const uint64_t* c = cached_chain(f.tok, f.n, fs))
+          ins.first->second.assign(c, c + (f.n + ps - 1) / ps);
         else
           todo.push_back({&f, fs, &ins.first->second});  // node values stay put
       }

@@ -188,24 +188,25 @@ class PoolIndex {
   // with a copy of its tokens: a span given again (same address, same tokens, checked
   // in full) takes its chain from here instead of hashing its tokens again.  Part of
   // the pool's state: cleared by reset(), and whenever it would hold more than
-  // kChainCacheTokens tokens.
-  struct ChainKey {
-    const int32_t* tok;
-    int32_t n;
-    uint64_t seed;
-    bool operator==(const ChainKey& o) const { return tok == o.tok && n == o.n && seed == o.seed; }
-  };
-  struct ChainKeyHash {
-    size_t operator()(const ChainKey& k) const;
-  };
-  struct ChainEntry {
-    std::vector<int32_t> tok;
-    std::vector<uint64_t> chain;
+  // kChainCacheTokens tokens.  Open addressing over flat arenas whose storage is kept
+  // when cleared (a slot is live iff its stamp is the current one), so that filling it
+  // again after a reset allocates nothing.
+  struct ChainSlot {
+    const int32_t* tok = nullptr;
+    int32_t n = 0;
+    uint64_t seed = 0;
+    uint32_t stamp = 0;
+    size_t tok_off = 0, chain_off = 0, chain_n = 0;
   };
   static constexpr size_t kChainCacheTokens = size_t{1} << 22;
-  std::unordered_map<ChainKey, ChainEntry, ChainKeyHash> chain_cache_;
-  size_t chain_cache_tokens_ = 0;
-  const std::vector<uint64_t>* cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const;
+  std::vector<ChainSlot> chain_slots_;
+  std::vector<int32_t> chain_tok_;
+  std::vector<uint64_t> chain_hash_;
+  uint32_t chain_stamp_ = 1;
+  size_t chain_live_ = 0;
+  void clear_chain_cache();
+  size_t chain_slot(const int32_t* tok, int32_t n, uint64_t seed) const;  // its slot or the empty one to use
+  const uint64_t* cached_chain(const int32_t* tok, int32_t n, uint64_t seed) const;
   void remember_chain(const int32_t* tok, int32_t n, uint64_t seed, const std::vector<uint64_t>& chain);
   bool content_equal(int32_t pid, const Spec& s) const;
   bool spec_equal(const Spec& a, const Spec& b) const;
