@@ -149,6 +149,42 @@ def _replay(seed, steps):
     pool.close()
 
 
+def test_planner_rehashes_tokens_changed_in_place(lib):
+    """The pool keeps the page-hash chains of spans it planned, keyed by the tokens'
+    address: the same arrays given again take their chains from there, and an array
+    whose tokens changed in place (same address) is hashed again.  Every plan against
+    the oracle replay, which hashes every span afresh (paper section 2: the cache key of
+    a block is a hash of its tokens and of everything before it)."""
+    rnd = random.Random(7)
+    vocab = 40
+    frags = [np.array([rnd.randrange(vocab) for _ in range(rnd.randrange(1, 70))], np.int32) for _ in range(6)]
+    prefix = np.array([rnd.randrange(vocab) for _ in range(20)], np.int32)
+    num_pages = 400
+    pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=num_pages, device=-1, dtype="f32")
+    ref = PoolReplay(num_pages=num_pages, page_size=16)
+    changed = 0
+    for step in range(120):
+        if step % 4 == 3:  # one token of one fragment changes in place
+            a = frags[rnd.randrange(len(frags))]
+            a[rnd.randrange(a.size)] = (a[0] + 1 + rnd.randrange(vocab - 1)) % vocab
+            changed += 1
+        chosen = rnd.sample(range(len(frags)), rnd.randrange(1, 4))
+        cross = np.array([rnd.randrange(vocab) for _ in range(rnd.randrange(0, 20))], np.int32)
+        qs = [(prefix.tolist(), [frags[i].tolist() for i in chosen], cross.tolist())]
+        res = ref.plan(qs)
+        q = SimpleNamespace(prefix=SimpleNamespace(tokens=prefix, row=0),
+                            frags=[SimpleNamespace(tokens=frags[i], row=0) for i in chosen],
+                            cross=SimpleNamespace(tokens=cross, row=0))
+        plan = pool.plan([q])
+        _compare(plan, res, qs)
+        plan.commit(); ref.commit(res); plan.destroy()
+        if step == 60:  # a reset empties the chain cache with the rest of the pool
+            pool.reset()
+            ref = PoolReplay(num_pages=num_pages, page_size=16)
+    assert changed >= 25
+    pool.close()
+
+
 def test_enomem_leaves_pool_unchanged(lib):
     pool = spanq.Pool(num_q_heads=2, num_kv_heads=1, head_dim=64, num_pages=4, device=-1, dtype="f32")
     a = pool.plan([_q(list(range(40)), [], [])])        # 3 pages
