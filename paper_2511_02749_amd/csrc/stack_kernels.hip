@@ -158,16 +158,25 @@ __global__ __launch_bounds__(kHeadThreads) void lm_head_kernel(const u16* __rest
     for (int t = 0; t < 8; ++t) acc[q][t] = 0.f;
   if (col0 < vocab) {
     const int vrow = vocab / 8;
-    for (int h = h0; h < h1; ++h) {
+    auto row = [&](int h, const uint4& wv) {  // weight row h into the sums
       float f[8];
-      unpack8(w[static_cast<int64_t>(h) * vrow + col0 / 8], f);
+      unpack8(wv, f);
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const float a = bf(n[static_cast<int64_t>(q) * hidden + h]);
 #pragma unroll
         for (int t = 0; t < 8; ++t) acc[q][t] = fmaf(a, f[t], acc[q][t]);
       }
+    };
+    int h = h0;
+    for (; h + 8 <= h1; h += 8) {  // eight rows of weights in flight, then their sums in row order
+      uint4 wv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) wv[u] = w[static_cast<int64_t>(h + u) * vrow + col0 / 8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) row(h + u, wv[u]);
     }
+    for (; h < h1; ++h) row(h, w[static_cast<int64_t>(h) * vrow + col0 / 8]);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       float* p = part + (static_cast<int64_t>(blockIdx.y) * NQ + q) * vocab + col0;
