@@ -412,8 +412,9 @@ typedef struct {
 } span_model_config;
 
 /* Bind a model to a bf16 device pool of the same layers and heads.  Allocates a
- * GEMM workspace and the transposed weight copies (waits for the transposition on
- * the null stream); activation buffers are allocated by the first forward call and
+ * GEMM workspace and the transposed weight copies (waits for the device, so that
+ * weights written on any stream are complete, then for the transposition);
+ * activation buffers are allocated by the first forward call and
  * grown when a later one needs more.  SPAN_EINVAL on a shape mismatch. */
 int span_model_create(span_pool* pool, const span_model_config* cfg, span_model** out);
 int span_model_destroy(span_model* model);

@@ -135,7 +135,8 @@ const uint64_t* PoolIndex::cached_chain(const int32_t* tok, int32_t n, uint64_t 
 
 void PoolIndex::remember_chain(const int32_t* tok, int32_t n, uint64_t seed, const std::vector<uint64_t>& chain) {
   if (static_cast<size_t>(n) > kChainCacheTokens) return;
-  if (chain_tok_.size() + static_cast<size_t>(n) > kChainCacheTokens) clear_chain_cache();
+  if (chain_tok_.size() + static_cast<size_t>(n) > kChainCacheTokens || chain_live_ >= kChainCacheSpans)
+    clear_chain_cache();
   if (2 * (chain_live_ + 1) > chain_slots_.size()) {  // keep the table at most half full
     std::vector<ChainSlot> old;
     old.swap(chain_slots_);

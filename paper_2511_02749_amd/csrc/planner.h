@@ -188,7 +188,7 @@ class PoolIndex {
   // with a copy of its tokens: a span given again (same address, same tokens, checked
   // in full) takes its chain from here instead of hashing its tokens again.  Part of
   // the pool's state: cleared by reset(), and whenever it would hold more than
-  // kChainCacheTokens tokens.  Open addressing over flat arenas whose storage is kept
+  // kChainCacheTokens tokens or kChainCacheSpans spans.  Open addressing over flat arenas whose storage is kept
   // when cleared (a slot is live iff its stamp is the current one), so that filling it
   // again after a reset allocates nothing.
   struct ChainSlot {
@@ -199,6 +199,7 @@ class PoolIndex {
     size_t tok_off = 0, chain_off = 0, chain_n = 0;
   };
   static constexpr size_t kChainCacheTokens = size_t{1} << 22;
+  static constexpr size_t kChainCacheSpans = size_t{1} << 16;
   std::vector<ChainSlot> chain_slots_;
   std::vector<int32_t> chain_tok_;
   std::vector<uint64_t> chain_hash_;

@@ -423,6 +423,9 @@ int make_transposed(span_model* m) {
                               {c.hidden, 2 * c.ffn},
                               {c.ffn, c.hidden}};  // K x N of W
   std::vector<const void*>* src[4] = {&m->w_qkv, &m->w_o, &m->w_gate_up, &m->w_down};
+  // the weights may have been written on any stream of the device: wait for all of them
+  hipError_t e0 = hipDeviceSynchronize();
+  if (e0 != hipSuccess) return hip_err(e0, "span_model_create: waiting for the weights");
   std::vector<const void*>* dst[4] = {&m->wt_qkv, &m->wt_o, &m->wt_gate_up, &m->wt_down};
   size_t total = 0;
   for (int i = 0; i < 4; ++i)
