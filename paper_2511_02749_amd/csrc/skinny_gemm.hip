@@ -242,11 +242,10 @@ size_t skinny_gemm_part_bytes(int M, int N, int K) {
   return s > 1 ? static_cast<size_t>(s) * M * N * sizeof(float) : 0;
 }
 
-hipError_t launch_skinny_gemm(const void* x, const void* wt, void* y, int M, int N, int K, bool residual, float* part,
-                              size_t part_bytes, hipStream_t s) {
-  if (!skinny_gemm_fits(M, N, K)) return hipErrorInvalidValue;
-  const int slices = skinny_gemm_slices(M, N, K);
-  if (slices > 1 && (!part || part_bytes < skinny_gemm_part_bytes(M, N, K))) return hipErrorInvalidValue;
+namespace {
+// The main kernel for `slices` K slices (partials to part when slices > 1).
+hipError_t skinny_main(const void* x, const void* wt, void* y, int M, int N, int K, int slices, bool residual,
+                       float* part, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(N / kSkN), static_cast<unsigned>(slices));
   const int nc = K / kSkKC / slices;
   const bf16_t *xb = static_cast<const bf16_t*>(x), *wb = static_cast<const bf16_t*>(wt);
@@ -261,12 +260,32 @@ hipError_t launch_skinny_gemm(const void* x, const void* wt, void* y, int M, int
     case 64: hipLaunchKernelGGL((skinny_gemm_kernel<kSkDepth, 64>), grid, dim3(kSkThreads), kSkLds, s, xb, wb, yb, pb, M, N, K, r); break;
     default: return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_skinny_gemm(const void* x, const void* wt, void* y, int M, int N, int K, bool residual, float* part,
+                              size_t part_bytes, hipStream_t s) {
+  if (!skinny_gemm_fits(M, N, K)) return hipErrorInvalidValue;
+  const int slices = skinny_gemm_slices(M, N, K);
+  if (slices > 1 && (!part || part_bytes < skinny_gemm_part_bytes(M, N, K))) return hipErrorInvalidValue;
+  hipError_t e = skinny_main(x, wt, y, M, N, K, slices, residual, part, s);
   if (e != hipSuccess || slices == 1) return e;
   const int64_t quads = static_cast<int64_t>(M) * N / 4;
   hipLaunchKernelGGL(skinny_reduce_kernel, dim3(static_cast<unsigned>((quads + 255) / 256)), dim3(256), 0, s, part,
-                     slices, M, N, yb, r);
+                     slices, M, N, static_cast<bf16_t*>(y), residual ? 1 : 0);
   return hipGetLastError();
+}
+
+hipError_t launch_skinny_gemm_norm(const void* x, const void* wt, void* y, int M, int N, int K, const void* gain,
+                                   void* nout, float eps, float* part, size_t part_bytes, hipStream_t s) {
+  if (!skinny_gemm_fits(M, N, K)) return hipErrorInvalidValue;
+  const int slices = skinny_gemm_slices(M, N, K);
+  if (slices == 1) return hipErrorNotSupported;
+  if (!part || part_bytes < skinny_gemm_part_bytes(M, N, K)) return hipErrorInvalidValue;
+  hipError_t e = skinny_main(x, wt, y, M, N, K, slices, true, part, s);
+  if (e != hipSuccess) return e;
+  return launch_reduce_residual_norm(part, slices, M, N, y, gain, nout, eps, s);
 }
 
 hipError_t launch_transpose_bf16(const void* in, void* out, int64_t R, int64_t C, hipStream_t s) {

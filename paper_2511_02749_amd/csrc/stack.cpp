@@ -135,6 +135,24 @@ struct Gemm {
            gemv_part_bytes(m, static_cast<int>(H), static_cast<int>(F)) <= gemv_part.cap;
   }
 
+  // y += x W, then nout = RMSNorm(y) * gain in the same second pass when the skinny
+  // kernel takes the shape with K split (bit for bit run + launch_rmsnorm); *fused
+  // tells whether it did (otherwise only y += x W was done).
+  int run_norm(const void* x, const void* w, const void* wt, void* y, int64_t M, int64_t N, int64_t K,
+               const void* gain, void* nout, float eps, bool* fused, hipStream_t s) {
+    *fused = false;
+    if (wt && skinny_gemm_fits(M, N, K) && skinny_gemm_slices(static_cast<int>(M), static_cast<int>(N),
+                                                              static_cast<int>(K)) > 1 &&
+        skinny_gemm_part_bytes(static_cast<int>(M), static_cast<int>(N), static_cast<int>(K)) <= sk_part.cap) {
+      hipError_t e = launch_skinny_gemm_norm(x, wt, y, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+                                             gain, nout, eps, sk_part.as<float>(), sk_part.cap, s);
+      if (e != hipSuccess) return hip_err(e, "skinny GEMM with norm");
+      *fused = true;
+      return SPAN_OK;
+    }
+    return run(x, w, wt, y, M, N, K, true, s);
+  }
+
   int run(const void* x, const void* w, const void* wt, void* y, int64_t M, int64_t N, int64_t K, bool residual,
           hipStream_t s) {
     if (M == 0) return SPAN_OK;
@@ -330,14 +348,17 @@ int run_layers(span_model* m, int64_t T, int n_layers, int64_t base, hipStream_t
     e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[0], m->n.p, T, H, c.rms_eps, s);
     if (e != hipSuccess) return hip_err(e, w + ": attention norm");
   }
+  bool normed = false;  // m->n already holds the attention norm of layer l
   for (int l = 0; l < n_layers; ++l) {
     int rc;
     if (gv) {
       e = launch_gemv_qkv(m->n.p, m->w_qkv[l], Ti, H, rows, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, gp, gcap, s);
       if (e != hipSuccess) return hip_err(e, w + ": q/k/v GEMV");
     } else {
-      e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
-      if (e != hipSuccess) return hip_err(e, w + ": attention norm");
+      if (!normed) {
+        e = launch_rmsnorm(m->x.p, nullptr, m->attn_norm[l], m->n.p, T, H, c.rms_eps, s);
+        if (e != hipSuccess) return hip_err(e, w + ": attention norm");
+      }
       rc = m->gemm.run(m->n.p, m->w_qkv[l], m->wt_qkv[l], m->qkv.p, T, qkv_w, H, false, s);
       if (rc) return rc;
       e = launch_scatter_qkv(m->qkv.p, rows, T, hq * d, hkv * d, m->q.p, m->k.p, m->v.p, s);
@@ -376,7 +397,12 @@ int run_layers(span_model* m, int64_t T, int n_layers, int64_t base, hipStream_t
     if (rc) return rc;
     e = launch_swiglu(m->gu.p, m->act.p, T, F, s);
     if (e != hipSuccess) return hip_err(e, w + ": swiglu");
-    rc = m->gemm.run(m->act.p, m->w_down[l], m->wt_down[l], m->x.p, T, H, F, true, s);
+    if (l + 1 < n_layers) {
+      rc = m->gemm.run_norm(m->act.p, m->w_down[l], m->wt_down[l], m->x.p, T, H, F, m->attn_norm[l + 1], m->n.p,
+                            c.rms_eps, &normed, s);
+    } else {
+      rc = m->gemm.run(m->act.p, m->w_down[l], m->wt_down[l], m->x.p, T, H, F, true, s);
+    }
     if (rc) return rc;
   }
   return SPAN_OK;

@@ -52,6 +52,16 @@ int skinny_gemm_slices(int M, int N, int K);
 size_t skinny_gemm_part_bytes(int M, int N, int K);
 hipError_t launch_skinny_gemm(const void* x, const void* wt, void* y, int M, int N, int K, bool residual, float* part,
                               size_t part_bytes, hipStream_t s);
+// The same with the second pass also forming nout = RMSNorm(y) * gain (N <= 8192),
+// bit for bit the plain launch followed by launch_rmsnorm, when the launch splits K
+// (skinny_gemm_slices > 1); returns hipErrorNotSupported, having done nothing, when it
+// does not.
+hipError_t launch_skinny_gemm_norm(const void* x, const void* wt, void* y, int M, int N, int K, const void* gain,
+                                   void* nout, float eps, float* part, size_t part_bytes, hipStream_t s);
+// Second pass over `slices` fp32 partial planes [slices][M][N]: y += their sum in plane
+// order (one rounding), then nout = RMSNorm(y) * gain, one work-group per row.
+hipError_t launch_reduce_residual_norm(const float* part, int slices, int M, int N, void* y, const void* gain,
+                                       void* nout, float eps, hipStream_t s);
 // out[c][r] = in[r][c] for an R x C bf16 matrix.
 hipError_t launch_transpose_bf16(const void* in, void* out, int64_t R, int64_t C, hipStream_t s);
 

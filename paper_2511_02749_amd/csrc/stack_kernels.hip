@@ -603,6 +603,14 @@ hipError_t launch_gemv_residual_norm(const void* x, const void* w, void* y, int 
   return hipGetLastError();
 }
 
+hipError_t launch_reduce_residual_norm(const float* part, int slices, int M, int N, void* y, const void* gain,
+                                       void* nout, float eps, hipStream_t s) {
+  if (M < 1 || N % 8 != 0 || N > kNormThreads * kNormVec * 8 || slices < 1) return hipErrorInvalidValue;
+  gemv_reduce_norm_kernel<<<static_cast<unsigned>(M), kNormThreads, 0, s>>>(
+      part, slices, M, N, static_cast<u16*>(y), static_cast<const uint4*>(gain), static_cast<uint4*>(nout), eps);
+  return hipGetLastError();
+}
+
 size_t argmax_scratch_bytes(int nq, int vocab) {
   return static_cast<size_t>(nq) * ((vocab + kArgCols - 1) / kArgCols) * (sizeof(float) + sizeof(int));
 }
