@@ -267,23 +267,30 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     return fmaxf(mx, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32_addr, __float_as_int(mx))));
   };
   // P = 2^(S - m) to bf16 (step g of the P.V contraction covers page g of the tile);
-  // returns this lane's sum of P
+  // returns this lane's sum of P, formed by v_dot2 over the packed bf16 values, i.e.
+  // over exactly the weights the P.V MFMAs take (two chains for independent adds)
   auto softmax_exp = [&](const f32x16_t (&sc)[2], bf16x8_t (&pk)[4]) -> float {
-    float psum = 0.f;
+    const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+    float ts0 = 0.f, ts1 = 0.f;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int kb = g >> 1, half = g & 1;
       u32x4_t w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e] - m);
-        const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e + 1] - m);
-        psum += p0 + p1;
-        w[e] = pack_bf16x2(p0, p1);
+        // the dot product takes the packed word itself (not w[e] read back, which
+        // hipcc at -O3 has been seen to feed from the vector's element 0)
+        const uint32_t pw = pack_bf16x2(__builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e] - m),
+                                        __builtin_amdgcn_exp2f(sc[kb][8 * half + 2 * e + 1] - m));
+        w[e] = pw;
+        if (e & 1)
+          ts1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts1, false);
+        else
+          ts0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts0, false);
       }
       pk[g] = __builtin_bit_cast(bf16x8_t, w);
     }
-    return psum;
+    return ts0 + ts1;
   };
   // P of a tile whose scores `scores(sc)` forms (QK and mask); the rare raise sets m
   // to the tile's row max, rescales O and l and takes P again, with the scores formed

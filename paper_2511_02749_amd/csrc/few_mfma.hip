@@ -373,8 +373,11 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         return row_max4(mx);
       };
       bf16x8_t pk[2];
+      // the lane's sum of P by v_dot2 over the packed bf16 values (the weights the
+      // P.V MFMAs take), as the 32-row kernel forms it
       auto exps = [&]() {
-        float psum = 0.f;
+        const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+        float ts0 = 0.f, ts1 = 0.f;
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {
           u32x4_t w;
@@ -382,14 +385,17 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           for (int h = 0; h < 2; ++h)  // block 2t2 + h: elements 4h .. 4h + 3 of the operand
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-              const float p0 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e] - m);
-              const float p1 = __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e + 1] - m);
-              psum += p0 + p1;
-              w[2 * h + e] = pack_bf16x2(p0, p1);
+              const uint32_t pw = pack_bf16x2(__builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e] - m),
+                                              __builtin_amdgcn_exp2f(sc[2 * t2 + h][2 * e + 1] - m));
+              w[2 * h + e] = pw;
+              if (e)
+                ts1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts1, false);
+              else
+                ts0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw), ones, ts0, false);
             }
           pk[t2] = __builtin_bit_cast(bf16x8_t, w);
         }
-        return psum;
+        return ts0 + ts1;
       };
       if (first) m = fmaxf(m, tile_max());
       first = false;
