@@ -227,12 +227,14 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < GE::KS; ++ks) {
       const bf16x8_t a0 = kop(ks, 0), a1 = kop(ks, 1);
       sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], sc[0], 0, 0, 0);
       sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], sc[1], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
     // instruction order: reads of two steps ahead, then per step its two MFMAs and
     // the reads of the step after next
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
@@ -324,11 +326,13 @@ __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     __asm__ volatile("" : "+v"(ln));
     const uint32_t vofs = 32u * (ln & 31) + 16u * ((ln >> 5) ^ ((ln >> 3) & 1));
     const bf16x8_t* a = reinterpret_cast<const bf16x8_t*>(stage + GE::KBYTES + vofs);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
       for (int db = 0; db < GE::DB; ++db)  // DB independent accumulator chains, interleaved
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(g * D * 32 + db * 1024) / 16], pk[g], o[db], 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
   };
   // query at (position - delta) = R(-delta) applied to the query at delta 0
   // The cos/sin row came with the tile's DMA, which the tile's wait and barrier
